@@ -1,0 +1,24 @@
+"""Oracle: a plain, slow CPU fp64 implementation of one generation of the
+spatial coevolutionary GAN training the paper describes (Section 3,
+"Coevolutionary GAN Training", steps 1-5).
+
+THIS IS TEST INFRASTRUCTURE.  Only the tests, the smoke check of the entry
+module and the CPU-baseline leg of the benchmark may import it.  It shares no
+code with the HIP path: the only inputs the two have in common are the seeded
+workloads and datasets of the ``synth`` package, and the random numbers both
+sides draw from their own implementations of Philox4x32-10.
+
+Modules
+  rng      Philox4x32-10 and the uniform / normal / index draws made from it
+  grid     toroidal grid and 5-cell von Neumann neighbourhoods
+  mlp      MLP forward / manual backward in fp64, flat parameter layout, init
+  coevo    state, evaluation, fitness, tournament, replacement, mutation,
+           training step (Adam), one generation
+  mixture  the (1+1)-ES over the generator-mixture weights and its score
+
+Pinned by tests/test_oracle_*.py against: published Philox known-answer
+vectors and rocRAND's host Philox, hand-enumerated neighbourhoods, BCE closed
+forms, finite differences and torch CPU fp64 autograd, Adam closed forms and
+torch.optim.Adam, brute-force tournament enumeration, the 1x1-grid reduction
+to plain alternating GAN training, and Frechet-distance closed forms.
+"""

@@ -1,0 +1,242 @@
+"""One generation of the grid coevolution, in fp64, in the order of Section 3
+("Coevolutionary GAN Training", steps 1-5):
+
+ 1. random initialisation of every cell's generator (u_i, delta_i) and
+    discriminator (v_j, gamma_j);                                   -> create
+ 2. every generator is evaluated against every discriminator of its
+    neighbourhood; the loss values of a discriminator are averaged and those
+    of a generator negative-averaged to give fitness;               -> evaluate
+ 3. tournament selection of one generator and one discriminator per
+    neighbourhood, Gaussian update of their hyper-parameters (learning rate),
+    gradient (Adam) training of the selected pair;        -> select_replace,
+                                                              train_step
+ 4. the generator-mixture weights w of each neighbourhood evolve by a
+    (1+1)-ES (module ``mixture``);
+ 5. repeat from 2.
+
+Readings where the paper is silent (each is a workload field):
+ * synchronous, double-buffered generations (state g is read, g+1 written);
+ * the loss L(u_i, v_j) is the discriminator's binary cross-entropy,
+   mean over the minibatch of softplus(-a_real) + mean of softplus(a_fake),
+   a = logit; lower fitness wins for both roles (fitness_mode 0);
+ * one evaluation minibatch per cell per generation, shared by its 25 pairs;
+ * tournament draws distinct slots; ties go to the first drawn; NaN loses;
+ * replacement is unconditional (population size 1 per cell): the winner's
+   parameters and Adam state (m, v, t) and learning rate are copied;
+ * learning-rate mutation after copying: with the given probability add
+   N(0, std^2), clamp at 0;
+ * training: per step one discriminator step (real vs detached fake), then
+   one non-saturating generator step against the updated discriminator on
+   the same latent batch; Adam with beta1, beta2, eps, bias-corrected.
+"""
+import numpy as np
+from scipy.special import expit
+
+from . import grid, mlp, rng
+
+
+def softplus(x):
+    return np.logaddexp(0.0, x)
+
+
+class Setup:
+    """Static description derived from a workload dict and the dataset."""
+
+    def __init__(self, wl, n_samples):
+        if wl["net"] != "mlp":
+            raise NotImplementedError("oracle: only the MLP networks are implemented")
+        self.wl = wl
+        self.rows, self.cols = wl["rows"], wl["cols"]
+        self.C = self.rows * self.cols
+        self.nbr = grid.neighbours(self.rows, self.cols)
+        self.B = wl["batch"]
+        self.zd, self.xd = wl["z_dim"], wl["x_dim"]
+        self.g_sizes = [self.zd] + list(wl["g_hidden"]) + [self.xd]
+        self.g_acts = [wl["g_hidden_act"]] * len(wl["g_hidden"]) + [wl["g_out_act"]]
+        self.d_sizes = [self.xd] + list(wl["d_hidden"]) + [1]
+        self.d_acts = [wl["d_hidden_act"]] * len(wl["d_hidden"]) + ["linear"]
+        self.slope = wl["lrelu_slope"]
+        self.seed = wl["seed"]
+        self.N = int(n_samples)
+        self.PG = mlp.layout(self.g_sizes)[1]
+        self.PD = mlp.layout(self.d_sizes)[1]
+
+
+class State:
+    """Per-cell individuals: params, Adam m, v, step t and learning rate per role; mixture w."""
+
+    FIELDS = ("Gp", "Gm", "Gv", "Gt", "Glr", "Dp", "Dm", "Dv", "Dt", "Dlr", "w")
+
+    def __init__(self, **kw):
+        for k in self.FIELDS:
+            setattr(self, k, kw[k])
+
+    def copy(self):
+        return State(**{k: np.array(getattr(self, k), copy=True) for k in self.FIELDS})
+
+
+def create(S):
+    """Step 1: random initial individuals, zero Adam state, initial learning rates, w = 1/5."""
+    wl = S.wl
+    Gp = np.stack([mlp.init(S.g_sizes, S.seed, c, "INIT_G") for c in range(S.C)])
+    Dp = np.stack([mlp.init(S.d_sizes, S.seed, c, "INIT_D") for c in range(S.C)])
+    return State(Gp=Gp, Gm=np.zeros_like(Gp), Gv=np.zeros_like(Gp),
+                 Gt=np.zeros(S.C, dtype=np.int64), Glr=np.full(S.C, float(wl["lr0_g"])),
+                 Dp=Dp, Dm=np.zeros_like(Dp), Dv=np.zeros_like(Dp),
+                 Dt=np.zeros(S.C, dtype=np.int64), Dlr=np.full(S.C, float(wl["lr0_d"])),
+                 w=np.full((S.C, grid.N_SLOTS), 1.0 / grid.N_SLOTS))
+
+
+def sample(S, data, cell, gen, step_field):
+    """Minibatch rows drawn uniformly with replacement and a latent batch z ~ N(0, 1)."""
+    idx = rng.indices(S.seed, S.B, S.N, cell, gen, step_field)
+    z = rng.normals(S.seed, S.B * S.zd, cell, gen, step_field, "Z").reshape(S.B, S.zd)
+    return idx, np.asarray(data[idx], dtype=np.float64), z
+
+
+def g_forward(S, p, z):
+    return mlp.forward(p, S.g_sizes, S.g_acts, z, S.slope)
+
+
+def d_logits(S, p, x):
+    pre, post = mlp.forward(p, S.d_sizes, S.d_acts, x, S.slope)
+    return pre, post, post[-1][:, 0]
+
+
+def evaluate(S, st, data, gen):
+    """Step 2: all 5x5 pairs of each neighbourhood, then fitness.
+
+    Returns L[C,5,5] (discriminator BCE), Lg[C,5,5] (non-saturating generator
+    loss), fit_g[C,5], fit_d[C,5].
+    """
+    C = S.C
+    L = np.zeros((C, 5, 5))
+    Lg = np.zeros((C, 5, 5))
+    for c in range(C):
+        _, x, z = sample(S, data, c, gen, 0)
+        fakes = [g_forward(S, st.Gp[S.nbr[c, i]], z)[1][-1] for i in range(5)]
+        for j in range(5):
+            dp = st.Dp[S.nbr[c, j]]
+            real_term = softplus(-d_logits(S, dp, x)[2]).mean()
+            for i in range(5):
+                a_f = d_logits(S, dp, fakes[i])[2]
+                L[c, i, j] = real_term + softplus(a_f).mean()
+                Lg[c, i, j] = softplus(-a_f).mean()
+    fit_d = L.mean(axis=1)
+    if S.wl["fitness_mode"] == 0:
+        fit_g = -L.mean(axis=2)
+    else:
+        fit_g = Lg.mean(axis=2)
+    return L, Lg, fit_g, fit_d
+
+
+def tournament_draw(S, cell, gen, tag):
+    """Distinct slots in draw order: draw j picks position floor(w_j * (5 - j) / 2^32)
+    among the slots not yet drawn (kept in slot order)."""
+    size = S.wl["tournament_size"]
+    w = rng.raw_words(S.seed, 4, cell, gen, 0, tag)
+    remaining = list(range(5))
+    drawn = []
+    for j in range(min(size, 4)):
+        pos = int((int(w[j]) * (5 - j)) >> 32)
+        drawn.append(remaining.pop(pos))
+    if size == 5:
+        drawn.append(remaining.pop(0))
+    return drawn
+
+
+def tournament_winner(fit_row, drawn):
+    """Lowest fitness wins; NaN counts as +inf; ties go to the earliest drawn slot."""
+    def key(f):
+        return np.inf if np.isnan(f) else f
+    best = drawn[0]
+    for k in drawn[1:]:
+        if key(fit_row[k]) < key(fit_row[best]):
+            best = k
+    return best
+
+
+def mutate_lr(S, lr, cell, gen, tag):
+    """Gaussian hyper-parameter update: with probability p, lr += std * n; clamp at 0."""
+    wl = S.wl
+    if not wl["lr_mutation"]:
+        return lr
+    u = rng.to_uniform(rng.raw_words(S.seed, 4, cell, gen, 0, tag))
+    if u[0] < wl["lr_mut_prob"]:
+        n = rng.box_muller(u)[2]
+        lr = max(lr + wl["lr_mut_std"] * n, 0.0)
+    return lr
+
+
+def select_replace(S, st, fit_g, fit_d, gen, forced=None):
+    """Step 3 (selection part): returns (state g+1, sel[C,2] source cells (G, D))."""
+    new = st.copy()
+    sel = np.zeros((S.C, 2), dtype=np.int64)
+    for c in range(S.C):
+        for r, (fit, ttag, mtag, pre) in enumerate(((fit_g, "TOURN_G", "LRMUT_G", "G"),
+                                                     (fit_d, "TOURN_D", "LRMUT_D", "D"))):
+            if forced is not None:
+                src = int(forced[c, r])
+            else:
+                src = int(S.nbr[c, tournament_winner(fit[c], tournament_draw(S, c, gen, ttag))])
+            sel[c, r] = src
+            for f in ("p", "m", "v", "t"):
+                getattr(new, pre + f)[c] = getattr(st, pre + f)[src]
+            getattr(new, pre + "lr")[c] = mutate_lr(S, getattr(st, pre + "lr")[src], c, gen, mtag)
+    return new, sel
+
+
+def adam(S, p, m, v, t, lr, g):
+    """One bias-corrected Adam step in place; returns the new step count."""
+    b1, b2, eps = S.wl["beta1"], S.wl["beta2"], S.wl["eps"]
+    t = t + 1
+    m *= b1
+    m += (1.0 - b1) * g
+    v *= b2
+    v += (1.0 - b2) * g * g
+    mhat = m / (1.0 - b1 ** t)
+    vhat = v / (1.0 - b2 ** t)
+    p -= lr * mhat / (np.sqrt(vhat) + eps)
+    return t
+
+
+def train_step(S, st, data, gen, step):
+    """Step 3 (training part): one discriminator and one generator Adam step for
+    every cell, in place.  Returns losses[C, 2] = (L_D, L_G) before the updates."""
+    B = S.B
+    losses = np.zeros((S.C, 2))
+    for c in range(S.C):
+        _, x, z = sample(S, data, c, gen, step + 1)
+        gpre, gpost = g_forward(S, st.Gp[c], z)
+        xf = gpost[-1]
+        # discriminator step on real and detached fake
+        pre_r, post_r, a_r = d_logits(S, st.Dp[c], x)
+        pre_f, post_f, a_f = d_logits(S, st.Dp[c], xf)
+        losses[c, 0] = softplus(-a_r).mean() + softplus(a_f).mean()
+        g_r, _ = mlp.backward(st.Dp[c], S.d_sizes, S.d_acts, pre_r, post_r,
+                              ((expit(a_r) - 1.0) / B)[:, None], S.slope)
+        g_f, _ = mlp.backward(st.Dp[c], S.d_sizes, S.d_acts, pre_f, post_f,
+                              (expit(a_f) / B)[:, None], S.slope)
+        st.Dt[c] = adam(S, st.Dp[c], st.Dm[c], st.Dv[c], st.Dt[c], st.Dlr[c], g_r + g_f)
+        # generator step (non-saturating) against the updated discriminator, same z
+        pre2, post2, a2 = d_logits(S, st.Dp[c], xf)
+        losses[c, 1] = softplus(-a2).mean()
+        _, dxf = mlp.backward(st.Dp[c], S.d_sizes, S.d_acts, pre2, post2,
+                              ((expit(a2) - 1.0) / B)[:, None], S.slope, want_input_grad=True)
+        gG, _ = mlp.backward(st.Gp[c], S.g_sizes, S.g_acts, gpre, gpost, dxf, S.slope)
+        st.Gt[c] = adam(S, st.Gp[c], st.Gm[c], st.Gv[c], st.Gt[c], st.Glr[c], gG)
+    return losses
+
+
+def generation(S, st, data, gen, mix_stats=None):
+    """Steps 2-4 for one generation; returns (new state, record dict)."""
+    from . import mixture
+    L, Lg, fg, fd = evaluate(S, st, data, gen)
+    st2, sel = select_replace(S, st, fg, fd, gen)
+    losses = [train_step(S, st2, data, gen, s) for s in range(S.wl["steps"])]
+    rec = dict(L=L, Lg=Lg, fit_g=fg, fit_d=fd, sel=sel, losses=np.array(losses))
+    if S.wl["mix_enable"]:
+        w, score, acc = mixture.update(S, st2, mix_stats, gen)
+        st2.w[...] = w
+        rec.update(w=w, score=score, accepted=acc)
+    return st2, rec
