@@ -1,0 +1,211 @@
+"""Throughput of one grid generation on one MI355X.
+
+A step is one generation of the 4x4 MNIST-shaped MLP grid with mixture
+weights: lipz_eval_neighborhoods (400 generator x discriminator pairings),
+lipz_select_replace, 100 x lipz_train_step, lipz_mixture_update.  Inputs
+(dataset, state) are resident in HBM before the timed region starts.
+
+Prints one JSON line:
+  value            grid generations per second (whole job, one GPU)
+  pair_evals_per_s pairings evaluated per second by lipz_eval_neighborhoods
+  mfma_frac        algorithmic GEMM FLOPs of a generation / time / fp32 MFMA peak
+  roofline         the grouped-GEMM kernel: algorithmic FLOPs per launch over its
+                   average launch time (HIP events on the grid's stream)
+  cpu_baseline     the oracle (fp64 NumPy) on this host's cores, on a bounded sample
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "G×D pair-evals/sec + grid generations/sec (4x4 MLP grid); % fp32 MFMA peak"
+FP32_MFMA_PEAK = 157.3e12  # MI355X dense fp32 matrix peak, FLOP/s
+
+
+def gemm_flops_per_generation(wl):
+    """Algorithmic GEMM FLOPs (2 per multiply-add, bias terms excluded) of one
+    generation: evaluation, S training steps, and the mixture step."""
+    C, B = wl["rows"] * wl["cols"], wl["batch"]
+    g = [wl["z_dim"]] + list(wl["g_hidden"]) + [wl["x_dim"]]
+    d = [wl["x_dim"]] + list(wl["d_hidden"]) + [1]
+    macs_g = sum(g[i] * g[i + 1] for i in range(len(g) - 1))
+    macs_d = sum(d[i] * d[i + 1] for i in range(len(d) - 1))
+    macs_d_in = macs_d - d[0] * d[1]  # D without its first layer's input gradient
+    # evaluation: 5 G forwards per cell, D forwards on B real + 5B fake rows per D slot
+    ev = C * (5 * B * macs_g + 5 * 6 * B * macs_d)
+    # D step: G fwd, D fwd (2B), D weight grads (2B), D input grads below layer 1 (2B)
+    d_step = B * macs_g + 2 * B * macs_d + 2 * B * macs_d + 2 * B * macs_d_in
+    # G step: D fwd (B), D input grads down to x (B), G weight grads, G input grads above z
+    g_step = B * macs_d + B * macs_d + B * macs_g + B * (macs_g - g[0] * g[1])
+    train = C * wl["steps"] * (d_step + g_step)
+    mix = 0
+    if wl["mix_enable"]:
+        mix = C * wl["mix_samples"] * (macs_g + wl["x_dim"] * wl["mix_feat_dim"])
+    return 2.0 * ev, 2.0 * train, 2.0 * mix
+
+
+def cpu_baseline(wl, data, budget_s=20.0):
+    """Time the oracle on a bounded sample of the same workload and scale it to
+    generations/s: one evaluation, k training steps (k chosen to fit the
+    budget), one mixture step; a generation = eval + S * mean step + mixture."""
+    import numpy as np
+    from oracle import coevo, mixture
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = int(os.environ.get("OMP_NUM_THREADS", "1"))
+    S = coevo.Setup(wl, len(data))
+    st = coevo.create(S)
+    t0 = time.perf_counter()
+    coevo.evaluate(S, st, data, 0)
+    t_eval = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    k = 0
+    while True:
+        coevo.train_step(S, st, data, 0, k)
+        k += 1
+        el = time.perf_counter() - t0
+        if el > budget_s * 0.5 or k >= wl["steps"]:
+            break
+    t_step = el / k
+    t_mix = 0.0
+    if wl["mix_enable"]:
+        stats = mixture.real_stats(S, data)
+        t0 = time.perf_counter()
+        mixture.update(S, st, stats, 0)
+        t_mix = time.perf_counter() - t0
+    t_gen = t_eval + wl["steps"] * t_step + t_mix
+    return {"value": 1.0 / t_gen, "unit": "generations/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"1 evaluation ({t_eval:.2f} s), {k} training steps ({t_step:.3f} s each)"
+                       + (f", 1 mixture step ({t_mix:.2f} s)" if wl["mix_enable"] else "")
+                       + f" of {wl['rows']}x{wl['cols']} grid; generation = eval + "
+                       f"{wl['steps']} x step + mixture"),
+            "pair_evals_per_s": S.C * 25 / t_eval}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5, help="timed generations")
+    ap.add_argument("--warmup", type=int, default=1, help="untimed generations")
+    ap.add_argument("--workload", default="mnist_mlp_4x4_mix")
+    ap.add_argument("--eval-reps", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU; the grid is not sharded across GPUs "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_1811_12843_amd as L
+    import synth
+
+    if not os.path.exists(L.LIB_PATH):
+        from paper_1811_12843_amd import build as _b
+        _b.build()
+    wl = synth.workload(args.workload)
+    data_np = synth.make_dataset(wl["data"])
+    dev = "cuda"
+    data = torch.from_numpy(data_np).to(dev)
+    cfg = L.config_from_dict(wl)
+    nb = L.lipz_workspace_bytes(cfg, len(data_np))
+    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    g = L.lipz_grid_create(cfg, ws.data_ptr(), nb, data.data_ptr(), len(data_np), stream.cuda_stream)
+    C = wl["rows"] * wl["cols"]
+    S = wl["steps"]
+
+    def generation(gen):
+        L.lipz_eval_neighborhoods(g, gen)
+        L.lipz_select_replace(g, gen)
+        L.lipz_train_step(g, gen, 0, S)
+        if wl["mix_enable"]:
+            L.lipz_mixture_update(g, gen)
+
+    gen = 0
+    for _ in range(args.warmup):
+        generation(gen)
+        gen += 1
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        generation(gen)
+        gen += 1
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert L.lipz_sync(g) in (L.LIPZ_OK, L.LIPZ_E_NONFINITE)
+    ms_per_gen = 1e3 * elapsed / args.steps
+
+    # evaluation alone
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for r in range(args.eval_reps):
+        L.lipz_eval_neighborhoods(g, gen + r)
+    torch.cuda.synchronize()
+    t_eval = (time.perf_counter() - t0) / args.eval_reps
+    pair_evals = C * 25 / t_eval
+
+    # grouped-GEMM kernel timing with HIP events on the grid's stream
+    L.lipz_set_gemm_timing(g, 1)
+    L.lipz_gemm_timing(g)  # reset
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        generation(gen)
+        gen += 1
+    torch.cuda.synchronize()
+    inst_ms = 1e3 * (time.perf_counter() - t0) / args.steps
+    gemm_ms, launches, gemm_flops = L.lipz_gemm_timing(g)
+    L.lipz_set_gemm_timing(g, 0)
+
+    f_ev, f_tr, f_mix = gemm_flops_per_generation(wl)
+    f_gen = f_ev + f_tr + f_mix
+    avg_ms = gemm_ms / max(launches, 1)
+    achieved = (gemm_flops / max(launches, 1)) / (avg_ms * 1e-3) if launches else 0.0
+    out = {
+        "metric": METRIC,
+        "value": 1e3 / ms_per_gen,
+        "unit": "generations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_gen,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded MNIST-shaped blobs, 60000 x 784); random-init MLPs",
+        "config": {"workload": args.workload, "grid": f"{wl['rows']}x{wl['cols']}", "cells": C,
+                   "pairings_per_eval": 25 * C, "batch": wl["batch"], "steps_per_generation": S,
+                   "g": [wl["z_dim"]] + wl["g_hidden"] + [wl["x_dim"]],
+                   "d": [wl["x_dim"]] + wl["d_hidden"] + [1], "mixture_es": bool(wl["mix_enable"])},
+        "pair_evals_per_s": pair_evals,
+        "eval_ms": t_eval * 1e3,
+        "gemm_gflop_per_generation": f_gen / 1e9,
+        "mfma_frac": f_gen / (ms_per_gen * 1e-3) / FP32_MFMA_PEAK,
+        "eval_mfma_frac": f_ev / t_eval / FP32_MFMA_PEAK,
+        "roofline": {"kernel": "gemm_grouped_kernel", "bound": "mfma", "achieved": achieved / 1e12,
+                     "peak": FP32_MFMA_PEAK / 1e12, "unit": "TFLOP/s",
+                     "frac": achieved / FP32_MFMA_PEAK, "traffic": None,
+                     "launches": launches, "avg_launch_us": avg_ms * 1e3,
+                     "flop_per_launch": gemm_flops / max(launches, 1),
+                     "instrumented_ms_per_step": inst_ms},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, data_np, args.cpu_budget)
+    L.lipz_grid_destroy(g)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

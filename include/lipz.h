@@ -1,0 +1,237 @@
+/*
+ * lipz.h -- C ABI of liblipz.so: one generation of spatial coevolutionary GAN
+ * training (Lipizzaner, arXiv 1811.12843) with every cell of the toroidal grid
+ * batched on one AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper Section 3, "Coevolutionary GAN Training", steps 1-5):
+ *   1. every cell holds one generator (params u, learning rate delta) and one
+ *      discriminator (params v, learning rate gamma), randomly initialised
+ *                                                       -> lipz_grid_create
+ *   2. each generator of a cell's 5-cell von Neumann neighbourhood (Section 2)
+ *      is evaluated against each discriminator of it; the losses of a
+ *      discriminator are averaged and those of a generator negative-averaged
+ *      to give fitness                                  -> lipz_eval_neighborhoods
+ *   3. tournament selection of one generator and one discriminator per
+ *      neighbourhood, Gaussian mutation of their learning rates
+ *                                                       -> lipz_select_replace
+ *      and gradient-based training of the selected pair -> lipz_train_step
+ *   4. the generator-mixture weights of each neighbourhood evolve by a
+ *      (1+1)-ES                                          -> lipz_mixture_update
+ *   5. go to 2.
+ * Hyper-parameter defaults follow the paper's experiment settings table
+ * (population size 1 per cell, tournament size 2, Adam, learning rate 2e-4,
+ * mutation rate 1e-4 with probability 0.5, mixture mutation scale 0.01).
+ *
+ * Readings where the paper is silent are fields of lipz_config; they are:
+ * synchronous double-buffered generations; BCE loss in logit form (mean over
+ * the minibatch), lower fitness wins; one evaluation minibatch per cell and
+ * generation; tournaments draw distinct slots, ties go to the first drawn,
+ * NaN fitness loses; the winner's parameters, Adam state and learning rate
+ * are copied, then the learning rate mutates; per training step one
+ * discriminator step then one non-saturating generator step on the same
+ * latent batch; the mixture score is a diagonal Frechet distance in a fixed
+ * random feature space (the paper's FID needs a pretrained network).
+ *
+ * Random numbers: Philox4x32-10 (Salmon et al., SC 2011) with key = seed and
+ * counter = (element / 4, cell, (gen << 16) | step_field, tag), word
+ * element % 4; step_field = 0 for evaluation, s + 1 for training step s.
+ * Uniform u = ((w >> 9) + 0.5) * 2^-23; normals by Box-Muller on (u0, u1) and
+ * (u2, u3); indices floor(w * n / 2^32).  Tags are the LIPZ_TAG_* values.
+ *
+ * Conventions for every call:
+ *  - Memory: the caller allocates ALL device memory (the workspace sized by
+ *    lipz_workspace_bytes, the dataset, every output).  The library never
+ *    allocates device memory; it owns only the small host handle.
+ *  - Pointers named d_* are device pointers, h_* host pointers.
+ *  - Streams: every call enqueues its kernels on the stream given at create
+ *    (a hipStream_t passed as void*) and returns without synchronising,
+ *    except create (which waits for its initialisation to finish), the state
+ *    layout queries and lipz_sync.  Outputs are valid after a stream sync.
+ *  - Errors: argument and call-order checks run on the host before anything
+ *    is enqueued and return a negative lipz_status.  HIP launch errors are
+ *    sticky on the handle and returned by the next call and by lipz_sync.
+ *    No C++ exception crosses this interface.
+ *  - A handle is not thread-safe; separate handles are independent.
+ */
+#ifndef LIPZ_H
+#define LIPZ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LIPZ_ABI_VERSION 1
+#define LIPZ_SLOTS 5          /* centre, north, south, west, east */
+#define LIPZ_MAX_HIDDEN 4
+
+typedef int32_t lipz_status;
+enum {
+  LIPZ_OK = 0,
+  LIPZ_E_INVAL = -1,        /* bad argument or configuration */
+  LIPZ_E_WORKSPACE = -2,    /* workspace too small or misaligned */
+  LIPZ_E_HIP = -3,          /* a HIP runtime call or kernel launch failed */
+  LIPZ_E_ORDER = -4,        /* call out of order (e.g. select before eval) */
+  LIPZ_E_NONFINITE = -5,    /* a loss or fitness value was NaN or Inf */
+  LIPZ_E_UNSUPPORTED = -6   /* configuration not implemented */
+};
+
+enum { LIPZ_NET_MLP = 0, LIPZ_NET_DCGAN = 1 };
+enum { LIPZ_ACT_LINEAR = 0, LIPZ_ACT_RELU = 1, LIPZ_ACT_LRELU = 2, LIPZ_ACT_TANH = 3 };
+enum { LIPZ_ROLE_G = 0, LIPZ_ROLE_D = 1 };
+enum {
+  LIPZ_TAG_IDX = 1, LIPZ_TAG_Z = 2, LIPZ_TAG_TOURN_G = 3, LIPZ_TAG_TOURN_D = 4,
+  LIPZ_TAG_LRMUT_G = 5, LIPZ_TAG_LRMUT_D = 6, LIPZ_TAG_MIXN = 7, LIPZ_TAG_MIXZ = 8,
+  LIPZ_TAG_PROJ = 9, LIPZ_TAG_INIT_G = 10, LIPZ_TAG_INIT_D = 11
+};
+
+/* Experiment configuration (the paper's single configuration file, Section 3,
+ * "Configuration").  Plain data; abi_version must be LIPZ_ABI_VERSION. */
+typedef struct {
+  int32_t abi_version;
+  int32_t rows, cols;               /* toroidal grid; cells = rows * cols, cell id = r * cols + c */
+  int32_t net;                      /* LIPZ_NET_MLP (LIPZ_NET_DCGAN: LIPZ_E_UNSUPPORTED) */
+  int32_t z_dim, x_dim;             /* latent width, flat sample width */
+  int32_t img_h, img_w, img_c;      /* DCGAN only; 0 for MLP */
+  int32_t n_g_hidden, g_hidden[LIPZ_MAX_HIDDEN];  /* G: z_dim -> g_hidden... -> x_dim */
+  int32_t n_d_hidden, d_hidden[LIPZ_MAX_HIDDEN];  /* D: x_dim -> d_hidden... -> 1 (logit) */
+  int32_t g_hidden_act, g_out_act, d_hidden_act;  /* LIPZ_ACT_* */
+  float lrelu_slope;
+  int32_t batch;                    /* minibatch rows for evaluation and training */
+  int32_t tournament_size;          /* 1..5 */
+  int32_t fitness_mode;             /* 0: fit_D = mean_i L, fit_G = -mean_j L (paper);
+                                       1: fit_G = mean_j Lg (non-saturating G loss) */
+  int32_t lr_mutation;              /* 1: mutate learning rates after replacement */
+  float lr0_g, lr0_d;               /* initial learning rates */
+  float beta1, beta2, eps;          /* Adam */
+  float lr_mut_std, lr_mut_prob;    /* Gaussian learning-rate mutation */
+  int32_t mix_enable;               /* 1: allocate and allow lipz_mixture_update */
+  int32_t mix_samples;              /* shared latents per generation for the mixture score */
+  int32_t mix_feat_dim;             /* random feature width F */
+  float mix_sigma;                  /* (1+1)-ES mutation scale */
+  uint64_t seed;
+} lipz_config;
+
+typedef struct lipz_grid lipz_grid;  /* opaque host handle */
+
+/* Bytes of device workspace a grid with this configuration and dataset size
+ * needs (0 if the configuration is invalid).  The workspace must be 256-byte
+ * aligned. */
+size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples);
+
+/* Step 1 (Section 3): carve the workspace, build the neighbour table, and
+ * initialise every cell on the device: MLP weights and biases of layer l are
+ * U(-1/sqrt(fan_in), 1/sqrt(fan_in)) from tag INIT_G / INIT_D, Adam m = v = 0,
+ * t = 0, learning rates lr0_g / lr0_d, mixture weights 1/5.  With mix_enable
+ * the projection P and the dataset's feature mean / std are computed here.
+ * d_dataset: [n_samples][x_dim] fp32 row-major, borrowed (must outlive the
+ * grid).  hip_stream: hipStream_t or NULL for the null stream.  Waits for
+ * the initialisation to finish. */
+lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t workspace_bytes,
+                             const float* d_dataset, int64_t n_samples, void* hip_stream,
+                             lipz_grid** out);
+lipz_status lipz_grid_destroy(lipz_grid* g);
+
+/* Step 2 (Section 3): for every cell c, draw one minibatch (B data rows,
+ * B latents; step_field 0) and evaluate each generator slot i against each
+ * discriminator slot j of its neighbourhood:
+ *   L [c][i][j] = mean_b softplus(-D_j(x_b)) + mean_b softplus(D_j(G_i(z_b)))
+ *   Lg[c][i][j] = mean_b softplus(-D_j(G_i(z_b)))
+ *   fit_d[c][j] = mean_i L[c][i][j];  fit_g[c][i] = -mean_j L[c][i][j]
+ *   (fitness_mode 1: fit_g[c][i] = mean_j Lg[c][i][j]).  Lower is better.
+ * Outputs fp32 [C][5][5] / [C][5]; any may be NULL.  A non-finite value sets
+ * the sticky LIPZ_E_NONFINITE flag reported by lipz_sync. */
+lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float* d_Lg,
+                                    float* d_fit_g, float* d_fit_d);
+
+/* Step 3, selection (Section 3): per cell and role, a tournament of
+ * tournament_size distinct slots on the fitness of the last evaluation
+ * (draw j picks position floor(w_j (5 - j) / 2^32) among the undrawn slots;
+ * lowest fitness wins, NaN loses, ties go to the first drawn).  The winner's
+ * parameters, Adam m, v, t and learning rate are copied into the cell (the
+ * next state buffer becomes current), then with probability lr_mut_prob the
+ * learning rate gets + N(0, lr_mut_std^2), clamped at 0 (words 0 / 2,3 of tag
+ * LRMUT_G / LRMUT_D).  d_forced [C][2] int32 (source cells for G, D) replaces
+ * the tournament when not NULL (an id outside [0, C) keeps the cell's own
+ * individual and is reported by lipz_sync).  d_sel [C][2] int32 receives the source cell
+ * ids, d_lr [C][2] fp32 the new learning rates; either may be NULL.
+ * Without d_forced, requires a preceding lipz_eval_neighborhoods since the
+ * last state change (else LIPZ_E_ORDER). */
+lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forced,
+                                int32_t* d_sel, float* d_lr);
+
+/* Step 3, training (Section 3): n_steps training steps s = step0 ..
+ * step0 + n_steps - 1 of every cell's own pair.  Per step: minibatch and
+ * latents from step_field s + 1; discriminator Adam step on
+ * mean softplus(-D(x)) + mean softplus(D(G(z))) with G(z) detached; then
+ * generator Adam step on mean softplus(-D'(G(z))) against the updated
+ * discriminator D' and the same z.  Adam: bias-corrected, per-cell learning
+ * rate and step count.  d_losses [n_steps][C][2] fp32 (L_D, L_G before each
+ * update) may be NULL. */
+lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_steps,
+                            float* d_losses);
+
+/* Step 4 (Section 3): one (1+1)-ES step on every cell's mixture weights over
+ * the generators of its neighbourhood (current state).  Features f = x P,
+ * P [x_dim][F] ~ N(0, 1/x_dim) (tag PROJ); generator moments over
+ * mix_samples shared latents (tag MIXZ, step_field 0);
+ *   score(w) = ||mu_w - mu_r||^2 + ||sqrt(max(s_w - mu_w^2, 0)) - sd_r||^2,
+ *   mu_w = sum_k w_k mean(f_k), s_w = sum_k w_k mean(f_k^2);
+ * proposal w' = max(w + mix_sigma n, 0) / sum (n: tag MIXN), accepted iff
+ * score(w') < score(w).  Outputs (any may be NULL): d_w [C][5] fp32,
+ * d_score [C] fp32 (score of the kept w), d_accepted [C] int32.
+ * LIPZ_E_ORDER if the grid was created with mix_enable = 0. */
+lipz_status lipz_mixture_update(lipz_grid* g, int32_t gen, float* d_w, float* d_score,
+                                int32_t* d_accepted);
+
+/* ---- inspection, checkpoint and teacher forcing ---- */
+
+/* Neighbour table [C][5] int32 into host memory. */
+lipz_status lipz_get_neighbors(const lipz_grid* g, int32_t* h_nbr);
+
+/* Parameter layout of one role's network: *h_n = number of layers; for
+ * layer l, h_offsets[3l + 0] = float offset of W_l in the cell's parameter
+ * row, [3l + 1] = fan_in, [3l + 2] = fan_out.  W_l is [fan_in][fan_out]
+ * row-major and its bias [fan_out] follows it directly.  h_offsets may be
+ * NULL to query *h_n; it must hold 3 * (LIPZ_MAX_HIDDEN + 1) entries. */
+lipz_status lipz_param_layout(const lipz_grid* g, int32_t role, int64_t* h_offsets, int32_t* h_n);
+
+/* State blob: the current population, in this layout (byte offsets written
+ * to h_offsets[0..11] by lipz_state_layout; h_offsets[11] = total bytes):
+ *   [0] Gp float [C][stride_G]  [1] Gm  [2] Gv
+ *   [3] Dp float [C][stride_D]  [4] Dm  [5] Dv
+ *   [6] Gt int32 [C]  [7] Dt int32 [C]  [8] Glr float [C]  [9] Dlr float [C]
+ *   [10] w float [C][5]
+ * h_strides[0] = stride_G, h_strides[1] = stride_D (floats per cell row,
+ * >= the role's parameter count; the padding is ignored). */
+lipz_status lipz_state_layout(const lipz_grid* g, int64_t* h_offsets, int64_t* h_strides);
+size_t lipz_state_bytes(const lipz_grid* g);
+/* Device-to-device copies of the current state, enqueued on the grid's
+ * stream.  lipz_load_state invalidates the last evaluation. */
+lipz_status lipz_save_state(lipz_grid* g, void* d_dst);
+lipz_status lipz_load_state(lipz_grid* g, const void* d_src);
+
+/* Synchronise the grid's stream; returns a sticky HIP error, then
+ * LIPZ_E_INVAL if a forced source cell of lipz_select_replace was outside
+ * [0, C) (that cell kept its own individual), then LIPZ_E_NONFINITE if any
+ * evaluation produced a non-finite value.  Both flags are sticky. */
+lipz_status lipz_sync(lipz_grid* g);
+const char* lipz_error_string(lipz_status s);
+/* Last error message of this handle ("" if none); valid until the next call. */
+const char* lipz_last_error(const lipz_grid* g);
+
+/* ---- kernel timing (for roofline measurement) ----
+ * When enabled, every launch of the grouped-GEMM kernel is bracketed by HIP
+ * events on the grid's stream.  lipz_gemm_timing (after a sync) returns the
+ * summed kernel milliseconds, the launch count and the algorithmic FLOPs
+ * (2 per multiply-add of the GEMM problems, bias rows excluded) since the
+ * last reset. */
+lipz_status lipz_set_gemm_timing(lipz_grid* g, int32_t enable);
+lipz_status lipz_gemm_timing(lipz_grid* g, double* h_ms, int64_t* h_launches, double* h_flops);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LIPZ_H */

@@ -1,0 +1,42 @@
+/*
+ * lipz_testing.h -- test hook of liblipz.so: runs the grouped fp32-MFMA GEMM
+ * kernel that every generation phase uses on ONE problem, so the kernel can
+ * be checked against a plain matrix product on ragged shapes.  Not needed to
+ * run the method (include/lipz.h).
+ *
+ *   C(i,j) <- epilogue( sum_k A(i,k) B(k,j) ),  0 <= i < M, 0 <= j < N, 0 <= k < K
+ *   A(i,k) = d_A[i*lda + k] (a_trans 0) or d_A[k*lda + i] (a_trans 1); with
+ *            ones_row >= 0 (a_trans 1 only) A has ones_row data rows and row
+ *            ones_row is all ones (appends a bias row to a weight gradient)
+ *   B(k,j) = d_B[k*ldb + j] (b_trans 0) or d_B[j*ldb + k] (b_trans 1)
+ *   epi 0: C = acc; 1: C = act(acc + bias[j]) (bias may be NULL);
+ *   epi 2: C = acc * act'(aux[i*ldc + j]) with act' taken from the output
+ *          value aux (relu: [aux > 0]; lrelu: 1 or slope; tanh: 1 - aux^2);
+ *   epi 3: acc is the gradient of parameter C[i*ldc + j]: one bias-corrected
+ *          Adam step with step count t = *d_t + step_local + 1 and learning
+ *          rate *d_lr on C, d_m, d_v (same indexing as C).
+ * d_desc: device scratch of at least 256 bytes for the problem descriptor
+ * (caller-owned).  The call copies the descriptor synchronously, enqueues the
+ * kernel on hip_stream and returns; LIPZ_E_INVAL on bad sizes.
+ */
+#ifndef LIPZ_TESTING_H
+#define LIPZ_TESTING_H
+
+#include "lipz.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M, int32_t N, int32_t K,
+                           const float* d_A, int32_t lda, int32_t a_trans, int32_t ones_row,
+                           const float* d_B, int32_t ldb, int32_t b_trans, float* d_C, int32_t ldc,
+                           int32_t epi, int32_t act, float slope, const float* d_bias,
+                           const float* d_aux, float* d_m, float* d_v, const float* d_lr,
+                           const int32_t* d_t, int32_t step_local, float beta1, float beta2,
+                           float eps);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LIPZ_TESTING_H */

@@ -1,0 +1,1005 @@
+// Host runtime of liblipz.so: configuration checks, workspace carving, the
+// per-phase grouped-GEMM problem tables, and the C ABI of include/lipz.h.
+//
+// A generation of the grid is a fixed sequence of dependent phases (paper
+// Section 3, steps 2-4).  Every phase is one kernel launch that covers all
+// cells of the grid.  The GEMM problems of every phase are built once at
+// create time, for both state buffers (generations are double-buffered), and
+// uploaded into the workspace; a call only enqueues launches.
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+#include <vector>
+
+#include "lipz_internal.h"
+
+using namespace lipz;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Bump allocator over the caller's workspace.  With base == nullptr it only
+// measures, so sizing and carving share one code path.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  template <class T>
+  T* take(size_t count) {
+    off = align_up(off, kAlign);
+    T* p = reinterpret_cast<T*>(base + off);
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+struct Net {
+  int nl = 0;            // layers, the last one is the output layer
+  int64_t off[LIPZ_MAX_HIDDEN + 1];
+  int fi[LIPZ_MAX_HIDDEN + 1], fo[LIPZ_MAX_HIDDEN + 1];
+  int act[LIPZ_MAX_HIDDEN + 1];
+  int64_t P = 0, stride = 0;
+  NetLayers layers() const {
+    NetLayers L{};
+    L.n = nl;
+    for (int l = 0; l < nl; ++l) {
+      L.off[l] = off[l];
+      L.fan_in[l] = fi[l];
+      L.fan_out[l] = fo[l];
+    }
+    return L;
+  }
+};
+
+struct StateBuf {
+  char* base;
+  float *Gp, *Gm, *Gv, *Dp, *Dm, *Dv;
+  int32_t *Gt, *Dt;
+  float *Glr, *Dlr, *w;
+};
+
+struct Phase {
+  int first = 0, count = 0, tiles = 0;
+  double flops = 0.0;
+};
+
+enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G };
+struct Op {
+  OpKind kind;
+  int phase;
+};
+
+}  // namespace
+
+struct lipz_grid {
+  lipz_config cfg;
+  int C = 0, B = 0, zd = 0, xd = 0, S = 0, F = 0;
+  Net G, D;
+  hipStream_t stream = nullptr;
+  const float* data = nullptr;
+  int64_t N = 0;
+  uint2 key;
+  float slope = 0.f;
+  AdamConsts ac;
+
+  StateBuf st[2];
+  int cur = 0;
+  size_t state_bytes = 0;
+  int64_t state_off[12];
+  std::vector<int32_t> nbr_h;
+
+  int32_t *nbr = nullptr, *sel = nullptr, *flags = nullptr;
+  float *L = nullptr, *Lg = nullptr, *fit_g = nullptr, *fit_d = nullptr;
+  // training buffers
+  float *z = nullptr, *Xtr = nullptr;
+  float *h[LIPZ_MAX_HIDDEN] = {}, *a[LIPZ_MAX_HIDDEN] = {}, *dD[LIPZ_MAX_HIDDEN] = {};
+  float *ag[LIPZ_MAX_HIDDEN] = {}, *dDg[LIPZ_MAX_HIDDEN] = {}, *dG[LIPZ_MAX_HIDDEN + 1] = {};
+  // evaluation buffers
+  float *ze = nullptr, *Xe = nullptr;
+  float *he[LIPZ_MAX_HIDDEN] = {}, *ae[LIPZ_MAX_HIDDEN] = {};
+  // mixture buffers
+  float *zeta = nullptr, *xm = nullptr, *fm = nullptr, *mu_k = nullptr, *s2_k = nullptr;
+  float *hm[LIPZ_MAX_HIDDEN] = {};
+  float *P = nullptr, *mu_r = nullptr, *sd_r = nullptr, *realfeat = nullptr;
+
+  GemmProb* probs_d = nullptr;
+  std::vector<GemmProb> probs_h;
+  std::vector<Phase> phases;
+  std::vector<Op> train_ops[2];
+  std::vector<int> eval_phases[2], mix_phases[2];
+  int real_phase = -1;
+
+  bool fitness_valid = false;
+  lipz_status sticky = LIPZ_OK;
+  std::string last_err;
+
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_live;
+  std::vector<double> ev_flops;
+  double gemm_ms = 0.0, gemm_flops = 0.0;
+  int64_t gemm_launches = 0;
+};
+
+namespace {
+
+lipz_status fail(lipz_grid* g, lipz_status s, const std::string& msg) {
+  if (g) g->last_err = msg;
+  return s;
+}
+
+lipz_status check_hip(lipz_grid* g, hipError_t e, const char* what) {
+  if (e == hipSuccess) return LIPZ_OK;
+  g->sticky = LIPZ_E_HIP;
+  g->last_err = std::string(what) + ": " + hipGetErrorString(e);
+  return LIPZ_E_HIP;
+}
+
+bool valid_act(int a) { return a >= LIPZ_ACT_LINEAR && a <= LIPZ_ACT_TANH; }
+
+// Validate a configuration; fills the network descriptions.  Returns "" if ok.
+std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) {
+  if (!c) return "null config";
+  if (c->abi_version != LIPZ_ABI_VERSION) return "abi_version mismatch";
+  if (c->net != LIPZ_NET_MLP) return "only LIPZ_NET_MLP is implemented";
+  if (c->rows < 1 || c->cols < 1 || (int64_t)c->rows * c->cols > 4096) return "grid size out of range";
+  if (c->z_dim < 1 || c->x_dim < 1 || c->z_dim > 65536 || c->x_dim > (1 << 20)) return "bad z_dim / x_dim";
+  if (c->batch < 1 || c->batch > 2048) return "batch must be in [1, 2048]";
+  if (c->n_g_hidden < 1 || c->n_g_hidden > LIPZ_MAX_HIDDEN) return "n_g_hidden must be in [1, 4]";
+  if (c->n_d_hidden < 1 || c->n_d_hidden > LIPZ_MAX_HIDDEN) return "n_d_hidden must be in [1, 4]";
+  for (int i = 0; i < c->n_g_hidden; ++i)
+    if (c->g_hidden[i] < 1 || c->g_hidden[i] > 65536) return "bad g_hidden width";
+  for (int i = 0; i < c->n_d_hidden; ++i)
+    if (c->d_hidden[i] < 1 || c->d_hidden[i] > 65536) return "bad d_hidden width";
+  if (!valid_act(c->g_hidden_act) || !valid_act(c->g_out_act) || !valid_act(c->d_hidden_act))
+    return "bad activation code";
+  if (!(c->lrelu_slope > 0.f) || c->lrelu_slope >= 1.f) return "lrelu_slope must be in (0, 1)";
+  if (c->tournament_size < 1 || c->tournament_size > 5) return "tournament_size must be in [1, 5]";
+  if (c->fitness_mode != 0 && c->fitness_mode != 1) return "fitness_mode must be 0 or 1";
+  if (!(c->beta1 >= 0.f && c->beta1 < 1.f && c->beta2 >= 0.f && c->beta2 < 1.f && c->eps > 0.f))
+    return "bad Adam constants";
+  if (!(c->lr0_g >= 0.f && c->lr0_d >= 0.f)) return "learning rates must be >= 0";
+  if (!(c->lr_mut_prob >= 0.f && c->lr_mut_prob <= 1.f && c->lr_mut_std >= 0.f))
+    return "bad learning-rate mutation";
+  if (c->mix_enable) {
+    if (c->mix_samples < 1 || c->mix_samples > (1 << 20)) return "bad mix_samples";
+    if (c->mix_feat_dim < 1 || c->mix_feat_dim > 4096) return "bad mix_feat_dim";
+    if (!(c->mix_sigma >= 0.f)) return "bad mix_sigma";
+  }
+  if (n_samples < 1 || n_samples > ((int64_t)1 << 31) - 1) return "n_samples must be in [1, 2^31)";
+  auto build = [](Net* n, int in, int nh, const int32_t* hid, int out, int hact, int oact) {
+    int64_t off = 0;
+    n->nl = nh + 1;
+    for (int l = 0; l <= nh; ++l) {
+      n->fi[l] = l == 0 ? in : hid[l - 1];
+      n->fo[l] = l == nh ? out : hid[l];
+      n->act[l] = l == nh ? oact : hact;
+      n->off[l] = off;
+      off += (int64_t)(n->fi[l] + 1) * n->fo[l];
+    }
+    n->P = off;
+    n->stride = (int64_t)align_up((size_t)off, 64);
+  };
+  build(Gn, c->z_dim, c->n_g_hidden, c->g_hidden, c->x_dim, c->g_hidden_act, c->g_out_act);
+  build(Dn, c->x_dim, c->n_d_hidden, c->d_hidden, 1, c->d_hidden_act, LIPZ_ACT_LINEAR);
+  return "";
+}
+
+// Carve every buffer; with base == nullptr only the size is computed.
+void carve(lipz_grid* g, char* base, size_t* total) {
+  Carver cv{base};
+  const int C = g->C, B = g->B, zd = g->zd, xd = g->xd;
+  const Net &G = g->G, &D = g->D;
+  // two state buffers in the documented blob layout
+  for (int b = 0; b < 2; ++b) {
+    StateBuf sb;
+    const size_t start = align_up(cv.off, kAlign);
+    cv.off = start;
+    int64_t* so = g->state_off;
+    auto take_f = [&](int k, size_t n) {
+      cv.off = align_up(cv.off, kAlign);
+      so[k] = (int64_t)(cv.off - start);
+      return cv.take<float>(n);
+    };
+    auto take_i = [&](int k, size_t n) {
+      cv.off = align_up(cv.off, kAlign);
+      so[k] = (int64_t)(cv.off - start);
+      return cv.take<int32_t>(n);
+    };
+    sb.base = base + start;
+    sb.Gp = take_f(0, (size_t)C * G.stride);
+    sb.Gm = take_f(1, (size_t)C * G.stride);
+    sb.Gv = take_f(2, (size_t)C * G.stride);
+    sb.Dp = take_f(3, (size_t)C * D.stride);
+    sb.Dm = take_f(4, (size_t)C * D.stride);
+    sb.Dv = take_f(5, (size_t)C * D.stride);
+    sb.Gt = take_i(6, C);
+    sb.Dt = take_i(7, C);
+    sb.Glr = take_f(8, C);
+    sb.Dlr = take_f(9, C);
+    sb.w = take_f(10, (size_t)C * LIPZ_SLOTS);
+    cv.off = align_up(cv.off, kAlign);
+    so[11] = (int64_t)(cv.off - start);
+    g->state_bytes = (size_t)so[11];
+    g->st[b] = sb;
+  }
+  g->nbr = cv.take<int32_t>((size_t)C * 5);
+  g->sel = cv.take<int32_t>((size_t)C * 2);
+  g->flags = cv.take<int32_t>(4);
+  g->L = cv.take<float>((size_t)C * 25);
+  g->Lg = cv.take<float>((size_t)C * 25);
+  g->fit_g = cv.take<float>((size_t)C * 5);
+  g->fit_d = cv.take<float>((size_t)C * 5);
+  // training
+  g->z = cv.take<float>((size_t)C * B * zd);
+  g->Xtr = cv.take<float>((size_t)C * 2 * B * xd);
+  for (int l = 0; l + 1 < G.nl; ++l) g->h[l] = cv.take<float>((size_t)C * B * G.fo[l]);
+  for (int l = 0; l < G.nl; ++l) g->dG[l] = cv.take<float>((size_t)C * B * G.fo[l]);
+  for (int l = 0; l + 1 < D.nl; ++l) {
+    g->a[l] = cv.take<float>((size_t)C * 2 * B * D.fo[l]);
+    g->dD[l] = cv.take<float>((size_t)C * 2 * B * D.fo[l]);
+    g->ag[l] = cv.take<float>((size_t)C * B * D.fo[l]);
+    g->dDg[l] = cv.take<float>((size_t)C * B * D.fo[l]);
+  }
+  // evaluation
+  g->ze = cv.take<float>((size_t)C * B * zd);
+  g->Xe = cv.take<float>((size_t)C * 6 * B * xd);
+  for (int l = 0; l + 1 < G.nl; ++l) g->he[l] = cv.take<float>((size_t)C * 5 * B * G.fo[l]);
+  for (int l = 0; l + 1 < D.nl; ++l) g->ae[l] = cv.take<float>((size_t)C * 5 * 6 * B * D.fo[l]);
+  // mixture
+  if (g->cfg.mix_enable) {
+    const int S = g->S, F = g->F;
+    g->zeta = cv.take<float>((size_t)S * zd);
+    for (int l = 0; l + 1 < G.nl; ++l) g->hm[l] = cv.take<float>((size_t)C * S * G.fo[l]);
+    g->xm = cv.take<float>((size_t)C * S * xd);
+    g->fm = cv.take<float>((size_t)C * S * F);
+    g->mu_k = cv.take<float>((size_t)C * F);
+    g->s2_k = cv.take<float>((size_t)C * F);
+    g->P = cv.take<float>((size_t)xd * F);
+    g->mu_r = cv.take<float>(F);
+    g->sd_r = cv.take<float>(F);
+    g->realfeat = cv.take<float>((size_t)g->N * F);
+  }
+  g->probs_d = cv.take<GemmProb>(g->probs_h.size());
+  *total = align_up(cv.off, kAlign);
+}
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+int vec_flag(const float* p, int ld) {
+  return (((uintptr_t)p & 15) == 0 && (ld & 3) == 0) ? 1 : 0;
+}
+
+GemmProb base_prob(const float* A, int lda, int a_trans, const float* Bm, int ldb, int b_trans,
+                   float* C, int ldc, int M, int N, int K) {
+  GemmProb p;
+  memset(&p, 0, sizeof(p));
+  p.A = A;
+  p.B = Bm;
+  p.C = C;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.lda = lda;
+  p.ldb = ldb;
+  p.ldc = ldc;
+  p.a_trans = a_trans;
+  p.b_trans = b_trans;
+  p.a_rows = M;
+  p.ones_row = -1;
+  p.vec = vec_flag(A, lda) | (vec_flag(Bm, ldb) << 1);
+  return p;
+}
+
+// y = act(x W + b): x [M][fi] (ld fi), Wb = W [fi][fo] then b [fo].
+GemmProb fwd_prob(const float* x, int M, const float* Wb, int fi, int fo, float* y, int act) {
+  GemmProb p = base_prob(x, fi, 0, Wb, fo, 0, y, fo, M, fo, fi);
+  p.bias = Wb + (size_t)fi * fo;
+  p.epi = EPI_BIAS_ACT;
+  p.act = act;
+  return p;
+}
+
+// dx = (dy W^T) * act'(xfwd): dy [M][fo], W [fi][fo], dx and xfwd [M][fi].
+GemmProb dgrad_prob(const float* dy, int M, const float* W, int fi, int fo, float* dx,
+                    const float* xfwd, int act) {
+  GemmProb p = base_prob(dy, fo, 0, W, fo, 1, dx, fi, M, fi, fo);
+  p.aux = xfwd;
+  p.epi = EPI_DACT;
+  p.act = act;
+  return p;
+}
+
+// (dW; db) = [x | 1]^T dy over `rows` samples, applied by Adam to (W; b).
+GemmProb wgrad_adam_prob(const float* x, int rows, int fi, const float* dy, int fo, float* Wb,
+                         float* m, float* v, const float* lr, const int32_t* t) {
+  GemmProb p = base_prob(x, fi, 1, dy, fo, 0, Wb, fo, fi + 1, fo, rows);
+  p.a_rows = fi;
+  p.ones_row = fi;
+  p.m = m;
+  p.v = v;
+  p.lr = lr;
+  p.t = t;
+  p.epi = EPI_ADAM;
+  return p;
+}
+
+double prob_flops(const GemmProb& p) {
+  const double rows = p.ones_row >= 0 ? (double)p.a_rows : (double)p.M;
+  return 2.0 * rows * p.N * p.K;
+}
+
+int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
+  Phase ph;
+  ph.first = (int)g->probs_h.size();
+  ph.count = (int)ps.size();
+  int tiles = 0;
+  for (GemmProb p : ps) {
+    p.tiles_n = ceil_div(p.N, GEMM_BN);
+    p.tile_begin = tiles;
+    tiles += ceil_div(p.M, GEMM_BM) * p.tiles_n;
+    ph.flops += prob_flops(p);
+    g->probs_h.push_back(p);
+  }
+  ph.tiles = tiles;
+  g->phases.push_back(ph);
+  return (int)g->phases.size() - 1;
+}
+
+// The backward schedule shared by both networks: the weight gradient of
+// layer l + 1 (which rewrites W_{l+1}) runs beside the input gradient of
+// layer l (which reads W_l), never beside the one of its own layer.
+template <class Dgrad, class Wgrad>
+void backward_phases(lipz_grid* g, int top, Dgrad dgrad, Wgrad wgrad, std::vector<Op>* ops) {
+  std::vector<GemmProb> pending;
+  for (int l = top; l >= 0; --l) {
+    std::vector<GemmProb> ph;
+    if (l >= 1) dgrad(l, &ph);
+    ph.insert(ph.end(), pending.begin(), pending.end());
+    pending.clear();
+    wgrad(l, &pending);
+    if (l == 0) ph.insert(ph.end(), pending.begin(), pending.end());
+    ops->push_back({OP_GEMM, add_phase(g, ph)});
+  }
+}
+
+void build_tables(lipz_grid* g) {
+  g->probs_h.clear();
+  g->phases.clear();
+  const int C = g->C, B = g->B, zd = g->zd, xd = g->xd;
+  const Net &G = g->G, &D = g->D;
+  const int LG = G.nl, LD = D.nl;
+  const size_t sG = G.stride, sD = D.stride;
+  for (int par = 0; par < 2; ++par) {
+    const StateBuf& S = g->st[par];
+    std::vector<Op>& ops = g->train_ops[par];
+    ops.clear();
+    // ---- training step ----
+    ops.push_back({OP_SAMPLE, -1});
+    for (int l = 0; l < LG; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c) {
+        const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
+        float* y = l + 1 < LG ? g->h[l] + (size_t)c * B * G.fo[l]
+                              : g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd;
+        ps.push_back(fwd_prob(x, B, S.Gp + c * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
+      }
+      ops.push_back({OP_GEMM, add_phase(g, ps)});
+    }
+    for (int l = 0; l + 1 < LD; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c) {
+        const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
+                                : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
+        ps.push_back(fwd_prob(x, 2 * B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
+                              g->a[l] + (size_t)c * 2 * B * D.fo[l], D.act[l]));
+      }
+      ops.push_back({OP_GEMM, add_phase(g, ps)});
+    }
+    ops.push_back({OP_HEAD_D, -1});
+    backward_phases(
+        g, LD - 2,
+        [&](int l, std::vector<GemmProb>* ph) {
+          for (int c = 0; c < C; ++c)
+            ph->push_back(dgrad_prob(g->dD[l] + (size_t)c * 2 * B * D.fo[l], 2 * B,
+                                     S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
+                                     g->dD[l - 1] + (size_t)c * 2 * B * D.fi[l],
+                                     g->a[l - 1] + (size_t)c * 2 * B * D.fi[l], D.act[l - 1]));
+        },
+        [&](int l, std::vector<GemmProb>* ph) {
+          for (int c = 0; c < C; ++c) {
+            const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
+                                    : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
+            const size_t o = c * sD + D.off[l];
+            ph->push_back(wgrad_adam_prob(x, 2 * B, D.fi[l], g->dD[l] + (size_t)c * 2 * B * D.fo[l],
+                                          D.fo[l], S.Dp + o, S.Dm + o, S.Dv + o, S.Dlr + c,
+                                          S.Dt + c));
+          }
+        },
+        &ops);
+    // generator step: D forward on the fake rows with the updated D
+    for (int l = 0; l + 1 < LD; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c) {
+        const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd
+                                : g->ag[l - 1] + (size_t)c * B * D.fi[l];
+        ps.push_back(fwd_prob(x, B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
+                              g->ag[l] + (size_t)c * B * D.fo[l], D.act[l]));
+      }
+      ops.push_back({OP_GEMM, add_phase(g, ps)});
+    }
+    ops.push_back({OP_HEAD_G, -1});
+    for (int l = LD - 2; l >= 0; --l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c) {
+        if (l >= 1) {
+          ps.push_back(dgrad_prob(g->dDg[l] + (size_t)c * B * D.fo[l], B, S.Dp + c * sD + D.off[l],
+                                  D.fi[l], D.fo[l], g->dDg[l - 1] + (size_t)c * B * D.fi[l],
+                                  g->ag[l - 1] + (size_t)c * B * D.fi[l], D.act[l - 1]));
+        } else {
+          // into the generator output: delta of G's last layer
+          ps.push_back(dgrad_prob(g->dDg[0] + (size_t)c * B * D.fo[0], B, S.Dp + c * sD + D.off[0],
+                                  D.fi[0], D.fo[0], g->dG[LG - 1] + (size_t)c * B * xd,
+                                  g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd, G.act[LG - 1]));
+        }
+      }
+      ops.push_back({OP_GEMM, add_phase(g, ps)});
+    }
+    backward_phases(
+        g, LG - 1,
+        [&](int l, std::vector<GemmProb>* ph) {
+          for (int c = 0; c < C; ++c)
+            ph->push_back(dgrad_prob(g->dG[l] + (size_t)c * B * G.fo[l], B, S.Gp + c * sG + G.off[l],
+                                     G.fi[l], G.fo[l], g->dG[l - 1] + (size_t)c * B * G.fi[l],
+                                     g->h[l - 1] + (size_t)c * B * G.fi[l], G.act[l - 1]));
+        },
+        [&](int l, std::vector<GemmProb>* ph) {
+          for (int c = 0; c < C; ++c) {
+            const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
+            const size_t o = c * sG + G.off[l];
+            ph->push_back(wgrad_adam_prob(x, B, G.fi[l], g->dG[l] + (size_t)c * B * G.fo[l], G.fo[l],
+                                          S.Gp + o, S.Gm + o, S.Gv + o, S.Glr + c, S.Gt + c));
+          }
+        },
+        &ops);
+
+    // ---- evaluation ----
+    std::vector<int>& ev = g->eval_phases[par];
+    ev.clear();
+    for (int l = 0; l < LG; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c)
+        for (int i = 0; i < 5; ++i) {
+          const int owner = g->nbr_h[c * 5 + i];
+          const float* x = l == 0 ? g->ze + (size_t)c * B * zd
+                                  : g->he[l - 1] + (size_t)(c * 5 + i) * B * G.fi[l];
+          float* y = l + 1 < LG ? g->he[l] + (size_t)(c * 5 + i) * B * G.fo[l]
+                                : g->Xe + (size_t)c * 6 * B * xd + (size_t)(1 + i) * B * xd;
+          ps.push_back(fwd_prob(x, B, S.Gp + owner * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
+        }
+      ev.push_back(add_phase(g, ps));
+    }
+    for (int l = 0; l + 1 < LD; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c)
+        for (int j = 0; j < 5; ++j) {
+          const int owner = g->nbr_h[c * 5 + j];
+          const float* x = l == 0 ? g->Xe + (size_t)c * 6 * B * xd
+                                  : g->ae[l - 1] + (size_t)(c * 5 + j) * 6 * B * D.fi[l];
+          ps.push_back(fwd_prob(x, 6 * B, S.Dp + owner * sD + D.off[l], D.fi[l], D.fo[l],
+                                g->ae[l] + (size_t)(c * 5 + j) * 6 * B * D.fo[l], D.act[l]));
+        }
+      ev.push_back(add_phase(g, ps));
+    }
+    // ---- mixture ----
+    std::vector<int>& mx = g->mix_phases[par];
+    mx.clear();
+    if (g->cfg.mix_enable) {
+      const int Sm = g->S, F = g->F;
+      for (int l = 0; l < LG; ++l) {
+        std::vector<GemmProb> ps;
+        for (int c = 0; c < C; ++c) {
+          const float* x = l == 0 ? g->zeta : g->hm[l - 1] + (size_t)c * Sm * G.fi[l];
+          float* y = l + 1 < LG ? g->hm[l] + (size_t)c * Sm * G.fo[l] : g->xm + (size_t)c * Sm * xd;
+          ps.push_back(fwd_prob(x, Sm, S.Gp + c * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
+        }
+        mx.push_back(add_phase(g, ps));
+      }
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c)
+        ps.push_back(base_prob(g->xm + (size_t)c * Sm * xd, xd, 0, g->P, F, 0,
+                               g->fm + (size_t)c * Sm * F, F, Sm, F, xd));
+      mx.push_back(add_phase(g, ps));
+    }
+  }
+  if (g->cfg.mix_enable) {
+    std::vector<GemmProb> ps;
+    ps.push_back(base_prob(g->data, g->xd, 0, g->P, g->F, 0, g->realfeat, g->F, (int)g->N, g->F, g->xd));
+    g->real_phase = add_phase(g, ps);
+  }
+}
+
+hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local) {
+  const Phase& ph = g->phases[phase];
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (g->timing) {
+    if (g->ev_pool.size() < 2) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return hipErrorOutOfMemory;
+      g->ev_pool.push_back(a);
+      g->ev_pool.push_back(b);
+    }
+    e1 = g->ev_pool.back();
+    g->ev_pool.pop_back();
+    e0 = g->ev_pool.back();
+    g->ev_pool.pop_back();
+    hipEventRecord(e0, g->stream);
+  }
+  hipError_t e = launch_gemm_grouped(g->probs_d + ph.first, ph.count, ph.tiles, step_local, g->slope,
+                                     g->ac, g->stream);
+  if (g->timing) {
+    hipEventRecord(e1, g->stream);
+    g->ev_live.push_back({e0, e1});
+    g->ev_flops.push_back(ph.flops);
+  }
+  return e;
+}
+
+lipz_status pre_call(lipz_grid* g) {
+  if (!g) return LIPZ_E_INVAL;
+  g->last_err.clear();
+  if (g->sticky != LIPZ_OK) {
+    g->last_err = "a previous HIP error is pending";
+    return g->sticky;
+  }
+  return LIPZ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples) {
+  Net Gn, Dn;
+  if (!validate(cfg, n_samples, &Gn, &Dn).empty()) return 0;
+  lipz_grid* g = new (std::nothrow) lipz_grid();
+  if (!g) return 0;
+  g->cfg = *cfg;
+  g->C = cfg->rows * cfg->cols;
+  g->B = cfg->batch;
+  g->zd = cfg->z_dim;
+  g->xd = cfg->x_dim;
+  g->S = cfg->mix_samples;
+  g->F = cfg->mix_feat_dim;
+  g->N = n_samples;
+  g->G = Gn;
+  g->D = Dn;
+  g->nbr_h.assign((size_t)g->C * 5, 0);
+  size_t total = 0;
+  carve(g, nullptr, &total);
+  build_tables(g);
+  carve(g, nullptr, &total);
+  delete g;
+  return total;
+}
+
+lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t workspace_bytes,
+                             const float* d_dataset, int64_t n_samples, void* hip_stream,
+                             lipz_grid** out) {
+  if (!out) return LIPZ_E_INVAL;
+  *out = nullptr;
+  Net Gn, Dn;
+  if (cfg && cfg->abi_version == LIPZ_ABI_VERSION && cfg->net == LIPZ_NET_DCGAN) return LIPZ_E_UNSUPPORTED;
+  if (!validate(cfg, n_samples, &Gn, &Dn).empty()) return LIPZ_E_INVAL;
+  if (!d_workspace || !d_dataset) return LIPZ_E_INVAL;
+  if (((uintptr_t)d_workspace & (kAlign - 1)) != 0) return LIPZ_E_WORKSPACE;
+  const size_t need = lipz_workspace_bytes(cfg, n_samples);
+  if (need == 0 || workspace_bytes < need) return LIPZ_E_WORKSPACE;
+
+  lipz_grid* g = new (std::nothrow) lipz_grid();
+  if (!g) return LIPZ_E_INVAL;
+  g->cfg = *cfg;
+  g->C = cfg->rows * cfg->cols;
+  g->B = cfg->batch;
+  g->zd = cfg->z_dim;
+  g->xd = cfg->x_dim;
+  g->S = cfg->mix_samples;
+  g->F = cfg->mix_feat_dim;
+  g->N = n_samples;
+  g->G = Gn;
+  g->D = Dn;
+  g->stream = (hipStream_t)hip_stream;
+  g->data = d_dataset;
+  g->key = make_uint2((uint32_t)(cfg->seed & 0xFFFFFFFFull), (uint32_t)(cfg->seed >> 32));
+  g->slope = cfg->lrelu_slope;
+  g->ac.beta1 = cfg->beta1;
+  g->ac.beta2 = cfg->beta2;
+  g->ac.one_minus_beta1 = (float)(1.0 - (double)cfg->beta1);
+  g->ac.one_minus_beta2 = (float)(1.0 - (double)cfg->beta2);
+  g->ac.eps = cfg->eps;
+
+  // neighbour table: slots centre, north, south, west, east on the torus
+  const int R = cfg->rows, Q = cfg->cols;
+  g->nbr_h.resize((size_t)g->C * 5);
+  for (int r = 0; r < R; ++r)
+    for (int q = 0; q < Q; ++q) {
+      int32_t* n = &g->nbr_h[(size_t)(r * Q + q) * 5];
+      n[0] = r * Q + q;
+      n[1] = ((r - 1 + R) % R) * Q + q;
+      n[2] = ((r + 1) % R) * Q + q;
+      n[3] = r * Q + (q - 1 + Q) % Q;
+      n[4] = r * Q + (q + 1) % Q;
+    }
+
+  // The GEMM tables are carved last, so building them after the first carve
+  // already sees the final buffer addresses; the second carve sizes them.
+  size_t total = 0;
+  carve(g, (char*)d_workspace, &total);
+  build_tables(g);
+  carve(g, (char*)d_workspace, &total);
+  if (total > workspace_bytes) {
+    delete g;
+    return LIPZ_E_WORKSPACE;
+  }
+
+  hipStream_t s = g->stream;
+  lipz_status st = LIPZ_OK;
+  auto ck = [&](hipError_t e, const char* what) {
+    if (st == LIPZ_OK) st = check_hip(g, e, what);
+  };
+  ck(hipMemcpyAsync(g->nbr, g->nbr_h.data(), g->nbr_h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s),
+     "upload neighbours");
+  ck(hipMemcpyAsync(g->probs_d, g->probs_h.data(), g->probs_h.size() * sizeof(GemmProb),
+                    hipMemcpyHostToDevice, s),
+     "upload GEMM tables");
+  const StateBuf& S0 = g->st[0];
+  const int C = g->C;
+  // both state buffers, padding included, start at zero so saved blobs are deterministic
+  for (int b = 0; b < 2; ++b)
+    ck(launch_fill_i32(reinterpret_cast<int32_t*>(g->st[b].base), (int64_t)(g->state_bytes / 4), 0, s),
+       "zero state");
+  ck(launch_init_params(S0.Gp, g->G.stride, g->G.P, C, g->G.layers(), g->key, LIPZ_TAG_INIT_G, s), "init G");
+  ck(launch_init_params(S0.Dp, g->D.stride, g->D.P, C, g->D.layers(), g->key, LIPZ_TAG_INIT_D, s), "init D");
+  ck(launch_fill_f32(S0.Gm, (int64_t)C * g->G.stride, 0.f, s), "zero");
+  ck(launch_fill_f32(S0.Gv, (int64_t)C * g->G.stride, 0.f, s), "zero");
+  ck(launch_fill_f32(S0.Dm, (int64_t)C * g->D.stride, 0.f, s), "zero");
+  ck(launch_fill_f32(S0.Dv, (int64_t)C * g->D.stride, 0.f, s), "zero");
+  ck(launch_fill_i32(S0.Gt, C, 0, s), "zero");
+  ck(launch_fill_i32(S0.Dt, C, 0, s), "zero");
+  ck(launch_fill_f32(S0.Glr, C, cfg->lr0_g, s), "fill");
+  ck(launch_fill_f32(S0.Dlr, C, cfg->lr0_d, s), "fill");
+  ck(launch_fill_f32(S0.w, (int64_t)C * 5, 1.f / 5.f, s), "fill");
+  ck(launch_fill_i32(g->flags, 4, 0, s), "zero");
+  if (cfg->mix_enable) {
+    ck(launch_normals(g->P, (int64_t)g->xd * g->F, 1.0 / sqrt((double)g->xd), g->key, 0, 0, 0,
+                      LIPZ_TAG_PROJ, s),
+       "projection");
+    ck(run_gemm_phase(g, g->real_phase, 0), "project dataset");
+    ck(launch_col_stats(g->realfeat, g->N, g->F, g->mu_r, g->sd_r, s), "dataset feature stats");
+  }
+  ck(hipStreamSynchronize(s), "create sync");
+  if (st != LIPZ_OK) {
+    std::string msg = g->last_err;
+    delete g;
+    (void)msg;
+    return st;
+  }
+  *out = g;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_grid_destroy(lipz_grid* g) {
+  if (!g) return LIPZ_E_INVAL;
+  for (auto& e : g->ev_pool) hipEventDestroy(e);
+  for (auto& p : g->ev_live) {
+    hipEventDestroy(p.first);
+    hipEventDestroy(p.second);
+  }
+  delete g;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float* d_Lg,
+                                    float* d_fit_g, float* d_fit_d) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (gen < 0 || gen > 65535) return fail(g, LIPZ_E_INVAL, "gen must be in [0, 65535]");
+  hipStream_t s = g->stream;
+  const int par = g->cur;
+  const int C = g->C, B = g->B;
+  hipError_t e = launch_sample(g->data, g->N, g->xd, g->zd, B, C, g->key, (uint32_t)gen, 0, g->Xe,
+                               (int64_t)6 * B * g->xd, g->ze, (int64_t)B * g->zd, s);
+  if ((st = check_hip(g, e, "eval sample"))) return st;
+  for (int ph : g->eval_phases[par])
+    if ((st = check_hip(g, run_gemm_phase(g, ph, 0), "eval forward"))) return st;
+  EvalHeadArgs ha;
+  const int LD = g->D.nl;
+  ha.act = g->ae[LD - 2];
+  ha.Dp = g->st[par].Dp;
+  ha.p_stride = g->D.stride;
+  ha.head_off = g->D.off[LD - 1];
+  ha.nbr = g->nbr;
+  ha.L = g->L;
+  ha.Lg = g->Lg;
+  ha.H = g->D.fi[LD - 1];
+  ha.B = B;
+  ha.C = C;
+  if ((st = check_hip(g, launch_head_eval(ha, s), "eval head"))) return st;
+  e = launch_fitness(g->L, g->Lg, C, g->cfg.fitness_mode, g->fit_g, g->fit_d, g->flags, d_L, d_Lg,
+                     d_fit_g, d_fit_d, s);
+  if ((st = check_hip(g, e, "fitness"))) return st;
+  g->fitness_valid = true;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forced, int32_t* d_sel,
+                                float* d_lr) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (gen < 0 || gen > 65535) return fail(g, LIPZ_E_INVAL, "gen must be in [0, 65535]");
+  if (!d_forced && !g->fitness_valid)
+    return fail(g, LIPZ_E_ORDER, "select_replace needs an evaluation of the current state");
+  hipStream_t s = g->stream;
+  const StateBuf& A = g->st[g->cur];
+  const StateBuf& Bn = g->st[1 - g->cur];
+  SelectArgs sa;
+  sa.fit_g = g->fit_g;
+  sa.fit_d = g->fit_d;
+  sa.nbr = g->nbr;
+  sa.forced = d_forced;
+  sa.sel = g->sel;
+  sa.flags = g->flags;
+  sa.sel_out = d_sel;
+  sa.lr_out = d_lr;
+  sa.t_src[0] = A.Gt;
+  sa.t_src[1] = A.Dt;
+  sa.lr_src[0] = A.Glr;
+  sa.lr_src[1] = A.Dlr;
+  sa.t_dst[0] = Bn.Gt;
+  sa.t_dst[1] = Bn.Dt;
+  sa.lr_dst[0] = Bn.Glr;
+  sa.lr_dst[1] = Bn.Dlr;
+  sa.C = g->C;
+  sa.tsize = g->cfg.tournament_size;
+  sa.mutate = g->cfg.lr_mutation;
+  sa.mut_std = g->cfg.lr_mut_std;
+  sa.mut_prob = g->cfg.lr_mut_prob;
+  sa.key = g->key;
+  sa.gen = (uint32_t)gen;
+  if ((st = check_hip(g, launch_select(sa, s), "tournament"))) return st;
+  CopyArgs ca;
+  ca.sel = g->sel;
+  ca.src[0][0] = A.Gp;
+  ca.src[0][1] = A.Gm;
+  ca.src[0][2] = A.Gv;
+  ca.src[1][0] = A.Dp;
+  ca.src[1][1] = A.Dm;
+  ca.src[1][2] = A.Dv;
+  ca.dst[0][0] = Bn.Gp;
+  ca.dst[0][1] = Bn.Gm;
+  ca.dst[0][2] = Bn.Gv;
+  ca.dst[1][0] = Bn.Dp;
+  ca.dst[1][1] = Bn.Dm;
+  ca.dst[1][2] = Bn.Dv;
+  ca.stride[0] = g->G.stride;
+  ca.stride[1] = g->D.stride;
+  ca.w_src = A.w;
+  ca.w_dst = Bn.w;
+  ca.C = g->C;
+  if ((st = check_hip(g, launch_copy_winners(ca, s), "replace"))) return st;
+  g->cur = 1 - g->cur;
+  g->fitness_valid = false;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_steps,
+                            float* d_losses) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (gen < 0 || gen > 65535) return fail(g, LIPZ_E_INVAL, "gen must be in [0, 65535]");
+  if (step0 < 0 || n_steps < 0 || (int64_t)step0 + n_steps > 65535)
+    return fail(g, LIPZ_E_INVAL, "steps must satisfy 0 <= step0, step0 + n_steps <= 65535");
+  if (n_steps == 0) return LIPZ_OK;
+  hipStream_t s = g->stream;
+  const int par = g->cur;
+  const StateBuf& S = g->st[par];
+  const int C = g->C, B = g->B, LD = g->D.nl;
+  HeadArgs hd;
+  hd.act = g->a[LD - 2];
+  hd.act_cell_stride = (int64_t)2 * B * g->D.fi[LD - 1];
+  hd.delta = g->dD[LD - 2];
+  hd.p = S.Dp;
+  hd.m = S.Dm;
+  hd.v = S.Dv;
+  hd.p_stride = g->D.stride;
+  hd.head_off = g->D.off[LD - 1];
+  hd.lr = S.Dlr;
+  hd.t = S.Dt;
+  hd.H = g->D.fi[LD - 1];
+  hd.B = B;
+  hd.C = C;
+  hd.hidden_act = g->D.act[LD - 2];
+  hd.slope = g->slope;
+  hd.ac = g->ac;
+  HeadArgs hg = hd;
+  hg.act = g->ag[LD - 2];
+  hg.act_cell_stride = (int64_t)B * g->D.fi[LD - 1];
+  hg.delta = g->dDg[LD - 2];
+  for (int k = 0; k < n_steps; ++k) {
+    const int step = step0 + k;
+    hd.step_local = hg.step_local = k;
+    hd.losses = hg.losses = d_losses ? d_losses + (size_t)k * C * 2 : nullptr;
+    for (const Op& op : g->train_ops[par]) {
+      hipError_t e = hipSuccess;
+      switch (op.kind) {
+        case OP_SAMPLE:
+          e = launch_sample(g->data, g->N, g->xd, g->zd, B, C, g->key, (uint32_t)gen,
+                            (uint32_t)(step + 1), g->Xtr, (int64_t)2 * B * g->xd, g->z,
+                            (int64_t)B * g->zd, s);
+          break;
+        case OP_GEMM: e = run_gemm_phase(g, op.phase, k); break;
+        case OP_HEAD_D: e = launch_head_d(hd, s); break;
+        case OP_HEAD_G: e = launch_head_g(hg, s); break;
+      }
+      if ((st = check_hip(g, e, "train step"))) return st;
+    }
+  }
+  hipError_t e = launch_add_i32(S.Gt, C, n_steps, s);
+  if (e == hipSuccess) e = launch_add_i32(S.Dt, C, n_steps, s);
+  if ((st = check_hip(g, e, "step count"))) return st;
+  g->fitness_valid = false;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_mixture_update(lipz_grid* g, int32_t gen, float* d_w, float* d_score,
+                                int32_t* d_accepted) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (!g->cfg.mix_enable) return fail(g, LIPZ_E_ORDER, "grid created with mix_enable = 0");
+  if (gen < 0 || gen > 65535) return fail(g, LIPZ_E_INVAL, "gen must be in [0, 65535]");
+  hipStream_t s = g->stream;
+  const int par = g->cur;
+  hipError_t e = launch_normals(g->zeta, (int64_t)g->S * g->zd, 1.0, g->key, 0, (uint32_t)gen, 0,
+                                LIPZ_TAG_MIXZ, s);
+  if ((st = check_hip(g, e, "mixture latents"))) return st;
+  for (int ph : g->mix_phases[par])
+    if ((st = check_hip(g, run_gemm_phase(g, ph, 0), "mixture forward"))) return st;
+  e = launch_moments(g->fm, g->C, g->S, g->F, g->mu_k, g->s2_k, s);
+  if ((st = check_hip(g, e, "mixture moments"))) return st;
+  EsArgs ea;
+  ea.mu = g->mu_k;
+  ea.s2 = g->s2_k;
+  ea.mu_r = g->mu_r;
+  ea.sd_r = g->sd_r;
+  ea.nbr = g->nbr;
+  ea.w = g->st[par].w;
+  ea.w_out = d_w;
+  ea.score_out = d_score;
+  ea.acc_out = d_accepted;
+  ea.C = g->C;
+  ea.F = g->F;
+  ea.sigma = g->cfg.mix_sigma;
+  ea.key = g->key;
+  ea.gen = (uint32_t)gen;
+  return check_hip(g, launch_es(ea, s), "mixture ES");
+}
+
+lipz_status lipz_get_neighbors(const lipz_grid* g, int32_t* h_nbr) {
+  if (!g || !h_nbr) return LIPZ_E_INVAL;
+  memcpy(h_nbr, g->nbr_h.data(), g->nbr_h.size() * sizeof(int32_t));
+  return LIPZ_OK;
+}
+
+lipz_status lipz_param_layout(const lipz_grid* g, int32_t role, int64_t* h_offsets, int32_t* h_n) {
+  if (!g || !h_n || (role != LIPZ_ROLE_G && role != LIPZ_ROLE_D)) return LIPZ_E_INVAL;
+  const Net& n = role == LIPZ_ROLE_G ? g->G : g->D;
+  *h_n = n.nl;
+  if (h_offsets)
+    for (int l = 0; l < n.nl; ++l) {
+      h_offsets[3 * l + 0] = n.off[l];
+      h_offsets[3 * l + 1] = n.fi[l];
+      h_offsets[3 * l + 2] = n.fo[l];
+    }
+  return LIPZ_OK;
+}
+
+lipz_status lipz_state_layout(const lipz_grid* g, int64_t* h_offsets, int64_t* h_strides) {
+  if (!g) return LIPZ_E_INVAL;
+  if (h_offsets) memcpy(h_offsets, g->state_off, sizeof(g->state_off));
+  if (h_strides) {
+    h_strides[0] = g->G.stride;
+    h_strides[1] = g->D.stride;
+  }
+  return LIPZ_OK;
+}
+
+size_t lipz_state_bytes(const lipz_grid* g) { return g ? g->state_bytes : 0; }
+
+lipz_status lipz_save_state(lipz_grid* g, void* d_dst) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (!d_dst) return fail(g, LIPZ_E_INVAL, "null destination");
+  return check_hip(g, hipMemcpyAsync(d_dst, g->st[g->cur].base, g->state_bytes, hipMemcpyDeviceToDevice,
+                                     g->stream),
+                   "save state");
+}
+
+lipz_status lipz_load_state(lipz_grid* g, const void* d_src) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (!d_src) return fail(g, LIPZ_E_INVAL, "null source");
+  g->fitness_valid = false;
+  return check_hip(g, hipMemcpyAsync(g->st[g->cur].base, d_src, g->state_bytes, hipMemcpyDeviceToDevice,
+                                     g->stream),
+                   "load state");
+}
+
+lipz_status lipz_sync(lipz_grid* g) {
+  if (!g) return LIPZ_E_INVAL;
+  if (g->sticky != LIPZ_OK) return g->sticky;
+  hipError_t e = hipStreamSynchronize(g->stream);
+  if (e != hipSuccess) return check_hip(g, e, "stream sync");
+  int32_t flags = 0;
+  e = hipMemcpy(&flags, g->flags, sizeof(flags), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return check_hip(g, e, "read flags");
+  if (flags & 2) {
+    g->last_err = "a forced source cell was out of range (the cell kept itself)";
+    return LIPZ_E_INVAL;
+  }
+  if (flags & 1) {
+    g->last_err = "non-finite loss or fitness";
+    return LIPZ_E_NONFINITE;
+  }
+  return LIPZ_OK;
+}
+
+const char* lipz_error_string(lipz_status s) {
+  switch (s) {
+    case LIPZ_OK: return "ok";
+    case LIPZ_E_INVAL: return "invalid argument";
+    case LIPZ_E_WORKSPACE: return "workspace too small or misaligned";
+    case LIPZ_E_HIP: return "HIP runtime error";
+    case LIPZ_E_ORDER: return "call out of order";
+    case LIPZ_E_NONFINITE: return "non-finite loss or fitness";
+    case LIPZ_E_UNSUPPORTED: return "unsupported configuration";
+    default: return "unknown status";
+  }
+}
+
+const char* lipz_last_error(const lipz_grid* g) { return g ? g->last_err.c_str() : ""; }
+
+lipz_status lipz_set_gemm_timing(lipz_grid* g, int32_t enable) {
+  if (!g) return LIPZ_E_INVAL;
+  g->timing = enable != 0;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_gemm_timing(lipz_grid* g, double* h_ms, int64_t* h_launches, double* h_flops) {
+  if (!g) return LIPZ_E_INVAL;
+  hipError_t e = hipStreamSynchronize(g->stream);
+  if (e != hipSuccess) return check_hip(g, e, "timing sync");
+  for (size_t i = 0; i < g->ev_live.size(); ++i) {
+    float ms = 0.f;
+    hipEventElapsedTime(&ms, g->ev_live[i].first, g->ev_live[i].second);
+    g->gemm_ms += ms;
+    g->gemm_flops += g->ev_flops[i];
+    g->gemm_launches += 1;
+    g->ev_pool.push_back(g->ev_live[i].first);
+    g->ev_pool.push_back(g->ev_live[i].second);
+  }
+  g->ev_live.clear();
+  g->ev_flops.clear();
+  if (h_ms) *h_ms = g->gemm_ms;
+  if (h_launches) *h_launches = g->gemm_launches;
+  if (h_flops) *h_flops = g->gemm_flops;
+  g->gemm_ms = 0.0;
+  g->gemm_flops = 0.0;
+  g->gemm_launches = 0;
+  return LIPZ_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,520 @@
+// Element-wise, sampling, loss-head, selection and mixture kernels of the grid
+// coevolution.  Every reduction runs in a fixed order, so results are
+// bit-reproducible run to run (no floating-point atomics).
+#include "lipz_internal.h"
+
+namespace lipz {
+
+namespace {
+
+constexpr int NT = 256;
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// Sum of one value per thread over a 256-thread block in a fixed order.
+__device__ float block_sum(float x, float* red) {
+  x = wave_sum(x);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = x;
+  __syncthreads();
+  const float r = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// Step 1 initialisation: element e of a cell's parameter row, in layer l,
+// is (2u - 1) / sqrt(fan_in_l) with u from word e of stream (cell, 0, 0, tag).
+// ---------------------------------------------------------------------------
+__global__ void init_params_kernel(float* p, int64_t stride, int64_t P, int C, NetLayers L,
+                                   uint2 key, uint32_t tag) {
+  const int64_t total = (int64_t)C * P;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(i / P);
+    const int64_t e = i - (int64_t)c * P;
+    int l = 0;
+    while (l + 1 < L.n && e >= L.off[l + 1]) ++l;
+    const uint4 w = stream_block(key, (uint32_t)(e >> 2), (uint32_t)c, 0, 0, tag);
+    const double u = uniform_of(word_of(w, (int)(e & 3)));
+    p[(int64_t)c * stride + e] = (float)((2.0 * u - 1.0) / sqrt((double)L.fan_in[l]));
+  }
+}
+
+__global__ void fill_f32_kernel(float* p, int64_t n, float v) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+__global__ void add_i32_kernel(int32_t* p, int n, int32_t v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] += v;
+}
+
+__global__ void normals_kernel(float* out, int64_t n, double scale, uint2 key, uint32_t cell,
+                               uint32_t gen, uint32_t sf, uint32_t tag) {
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const uint4 w = stream_block(key, (uint32_t)(e >> 2), cell, gen, sf, tag);
+    out[e] = (float)(scale * normal_of(w, (int)(e & 3)));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Minibatch sampling: block (b, c) draws data row floor(w_b N / 2^32) of
+// stream (c, gen, sf, IDX) and copies it to X[c][b]; it also writes the
+// latent row z[c][b][:] from stream (c, gen, sf, Z), element b * zd + k.
+// ---------------------------------------------------------------------------
+__global__ void sample_kernel(const float* __restrict__ data, int64_t N, int xd, int zd,
+                              uint2 key, uint32_t gen, uint32_t sf, float* __restrict__ X,
+                              int64_t x_cell_stride, float* __restrict__ Z, int64_t z_cell_stride) {
+  const int b = blockIdx.x, c = blockIdx.y;
+  const uint4 wi = stream_block(key, (uint32_t)(b >> 2), (uint32_t)c, gen, sf, LIPZ_TAG_IDX);
+  const int64_t row = (int64_t)(((uint64_t)word_of(wi, b & 3) * (uint64_t)N) >> 32);
+  const float* src = data + row * xd;
+  float* dst = X + c * x_cell_stride + (int64_t)b * xd;
+  if ((xd & 3) == 0) {
+    for (int q = threadIdx.x; q < (xd >> 2); q += blockDim.x)
+      reinterpret_cast<float4*>(dst)[q] = reinterpret_cast<const float4*>(src)[q];
+  } else {
+    for (int q = threadIdx.x; q < xd; q += blockDim.x) dst[q] = src[q];
+  }
+  for (int k = threadIdx.x; k < zd; k += blockDim.x) {
+    const int64_t e = (int64_t)b * zd + k;
+    const uint4 w = stream_block(key, (uint32_t)(e >> 2), (uint32_t)c, gen, sf, LIPZ_TAG_Z);
+    Z[c * z_cell_stride + e] = (float)normal_of(w, (int)(e & 3));
+  }
+}
+
+// Logit of row r: dot(act[r], w) + bias, one wave per row.
+__device__ void head_logits(const float* act, int rows, int H, const float* w, float bias,
+                            float* logit) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int r = wave; r < rows; r += NT / 64) {
+    const float* a = act + (int64_t)r * H;
+    float s = 0.f;
+    for (int n = lane; n < H; n += 64) s += a[n] * w[n];
+    s = wave_sum(s);
+    if (lane == 0) logit[r] = s + bias;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Discriminator-step head for cell blockIdx.x: logits of B real then B fake
+// rows, L_D = mean softplus(-a_real) + mean softplus(a_fake), dL/da =
+// (sigmoid(a) - y) / B, delta = dL/da * w * act'(act), gradient of (w, bias),
+// then Adam on (w, bias) after every read of the old w.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void head_d_kernel(HeadArgs A) {
+  extern __shared__ float sm[];
+  float* logit = sm;            // 2B
+  float* dl = sm + 2 * A.B;     // 2B
+  __shared__ float red[4];
+  const int c = blockIdx.x;
+  const int rows = 2 * A.B;
+  const float* act = A.act + c * A.act_cell_stride;
+  float* p = A.p + c * A.p_stride + A.head_off;
+  float* m = A.m + c * A.p_stride + A.head_off;
+  float* v = A.v + c * A.p_stride + A.head_off;
+  const int H = A.H;
+  head_logits(act, rows, H, p, p[H], logit);
+  __syncthreads();
+  const float invB = 1.f / (float)A.B;
+  float lsum_r = 0.f, lsum_f = 0.f;
+  for (int r = threadIdx.x; r < rows; r += NT) {
+    const float a = logit[r];
+    if (r < A.B) {
+      dl[r] = (sigmoid_f(a) - 1.f) * invB;
+      lsum_r += softplus_f(-a);
+    } else {
+      dl[r] = sigmoid_f(a) * invB;
+      lsum_f += softplus_f(a);
+    }
+  }
+  lsum_r = block_sum(lsum_r, red);
+  lsum_f = block_sum(lsum_f, red);
+  if (threadIdx.x == 0 && A.losses) A.losses[c * 2 + 0] = lsum_r * invB + lsum_f * invB;
+  // delta[r][n] = dl[r] * w[n] * act'(act[r][n])
+  float* delta = A.delta + c * A.act_cell_stride;
+  for (int r = 0; r < rows; ++r) {
+    const float d = dl[r];
+    for (int n = threadIdx.x; n < H; n += NT) {
+      const int64_t o = (int64_t)r * H + n;
+      delta[o] = d * p[n] * act_deriv_from_out(A.hidden_act, act[o], A.slope);
+    }
+  }
+  // gradient of the head weights (column sums, fixed row order) and bias
+  float gb = 0.f;
+  for (int r = threadIdx.x; r < rows; r += NT) gb += dl[r];
+  gb = block_sum(gb, red);
+  const int tt = *(A.t + c) + A.step_local + 1;
+  const float bc1 = (float)(1.0 - pow((double)A.ac.beta1, (double)tt));
+  const float bc2 = (float)(1.0 - pow((double)A.ac.beta2, (double)tt));
+  const float lr = A.lr[c];
+  __syncthreads();  // every read of the old head weights is done
+  for (int n = threadIdx.x; n <= H; n += NT) {
+    float g;
+    if (n < H) {
+      g = 0.f;
+      for (int r = 0; r < rows; ++r) g += act[(int64_t)r * H + n] * dl[r];
+    } else {
+      g = gb;
+    }
+    const float mm = A.ac.beta1 * m[n] + A.ac.one_minus_beta1 * g;
+    const float vv = A.ac.beta2 * v[n] + A.ac.one_minus_beta2 * g * g;
+    m[n] = mm;
+    v[n] = vv;
+    p[n] = p[n] - lr * (mm / bc1) / (sqrtf(vv / bc2) + A.ac.eps);
+  }
+}
+
+// Generator-step head: logits of B fake rows against the updated D,
+// L_G = mean softplus(-a), dL/da = (sigmoid(a) - 1) / B, delta as above.
+__global__ __launch_bounds__(NT) void head_g_kernel(HeadArgs A) {
+  extern __shared__ float sm[];
+  float* logit = sm;
+  float* dl = sm + A.B;
+  __shared__ float red[4];
+  const int c = blockIdx.x;
+  const int rows = A.B;
+  const float* act = A.act + c * A.act_cell_stride;
+  const float* p = A.p + c * A.p_stride + A.head_off;
+  const int H = A.H;
+  head_logits(act, rows, H, p, p[H], logit);
+  __syncthreads();
+  const float invB = 1.f / (float)A.B;
+  float ls = 0.f;
+  for (int r = threadIdx.x; r < rows; r += NT) {
+    const float a = logit[r];
+    dl[r] = (sigmoid_f(a) - 1.f) * invB;
+    ls += softplus_f(-a);
+  }
+  ls = block_sum(ls, red);
+  if (threadIdx.x == 0 && A.losses) A.losses[c * 2 + 1] = ls * invB;
+  float* delta = A.delta + c * A.act_cell_stride;
+  for (int r = 0; r < rows; ++r) {
+    const float d = dl[r];
+    for (int n = threadIdx.x; n < H; n += NT) {
+      const int64_t o = (int64_t)r * H + n;
+      delta[o] = d * p[n] * act_deriv_from_out(A.hidden_act, act[o], A.slope);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Evaluation head for block (j, c): logits of the 6B rows [x_c; G_0(z_c);
+// ...; G_4(z_c)] under discriminator slot j, then
+//   L[c][i][j] = mean softplus(-a_real) + mean softplus(a_fake_i)
+//   Lg[c][i][j] = mean softplus(-a_fake_i)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void head_eval_kernel(EvalHeadArgs A) {
+  extern __shared__ float logit[];
+  const int j = blockIdx.x, c = blockIdx.y;
+  const int rows = 6 * A.B;
+  const int owner = A.nbr[c * 5 + j];
+  const float* p = A.Dp + owner * A.p_stride + A.head_off;
+  const float* act = A.act + ((int64_t)(c * 5 + j) * rows) * A.H;
+  head_logits(act, rows, A.H, p, p[A.H], logit);
+  __syncthreads();
+  // thread 0: real term; threads 1..5: fake terms of slot i = tid - 1;
+  // threads 6..10: generator terms.  Each sums its B rows in order.
+  const int t = threadIdx.x;
+  if (t < 11) {
+    const int blk = t == 0 ? 0 : (t <= 5 ? t : t - 5);
+    const float sgn = (t == 0 || t > 5) ? -1.f : 1.f;
+    float s = 0.f;
+    for (int b = 0; b < A.B; ++b) s += softplus_f(sgn * logit[blk * A.B + b]);
+    logit[rows + t] = s / (float)A.B;
+  }
+  __syncthreads();
+  if (t < 5) {
+    const float real = logit[rows];
+    A.L[(c * 5 + t) * 5 + j] = real + logit[rows + 1 + t];
+    A.Lg[(c * 5 + t) * 5 + j] = logit[rows + 6 + t];
+  }
+}
+
+// fit_d[c][j] = mean_i L[c][i][j]; fit_g[c][i] = -mean_j L[c][i][j] (mode 0)
+// or mean_j Lg[c][i][j] (mode 1).  Flags bit 0 on any non-finite value.
+__global__ void fitness_kernel(const float* L, const float* Lg, int C, int mode, float* fit_g,
+                               float* fit_d, int32_t* flags, float* oL, float* oLg, float* ofg,
+                               float* ofd) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < C * 25) {
+    if (oL) oL[i] = L[i];
+    if (oLg) oLg[i] = Lg[i];
+    if (!isfinite(L[i]) || !isfinite(Lg[i])) atomicOr(flags, 1);
+  }
+  if (i >= C * 5) return;
+  const int c = i / 5, k = i % 5;
+  const float* Lc = L + c * 25;
+  float sd = 0.f;
+  for (int a = 0; a < 5; ++a) sd += Lc[a * 5 + k];
+  float sg = 0.f;
+  if (mode == 0) {
+    for (int b = 0; b < 5; ++b) sg += Lc[k * 5 + b];
+    sg = -(sg / 5.f);
+  } else {
+    for (int b = 0; b < 5; ++b) sg += Lg[c * 25 + k * 5 + b];
+    sg = sg / 5.f;
+  }
+  sd = sd / 5.f;
+  fit_d[i] = sd;
+  fit_g[i] = sg;
+  if (ofd) ofd[i] = sd;
+  if (ofg) ofg[i] = sg;
+}
+
+// ---------------------------------------------------------------------------
+// Tournament + learning-rate mutation, one thread per (cell, role).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float fit_key(float f) { return f != f ? INFINITY : f; }
+
+__global__ void select_kernel(SelectArgs A) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 2 * A.C) return;
+  const int c = i >> 1, role = i & 1;
+  int src;
+  if (A.forced) {
+    src = A.forced[c * 2 + role];
+    if (src < 0 || src >= A.C) {
+      atomicOr(A.flags, 2);
+      src = c;
+    }
+  } else {
+    const float* fit = (role == 0 ? A.fit_g : A.fit_d) + c * 5;
+    const uint4 w = stream_block(A.key, 0, (uint32_t)c, A.gen, 0,
+                                 role == 0 ? LIPZ_TAG_TOURN_G : LIPZ_TAG_TOURN_D);
+    int remaining[5] = {0, 1, 2, 3, 4};
+    int n_rem = 5;
+    int best = -1;
+    const int draws = A.tsize < 4 ? A.tsize : 4;
+    for (int j = 0; j < A.tsize; ++j) {
+      int pos = 0;
+      if (j < draws) pos = (int)(((uint64_t)word_of(w, j) * (uint64_t)(5 - j)) >> 32);
+      const int k = remaining[pos];
+      for (int q = pos; q + 1 < n_rem; ++q) remaining[q] = remaining[q + 1];
+      --n_rem;
+      if (best < 0 || fit_key(fit[k]) < fit_key(fit[best])) best = k;
+    }
+    src = A.nbr[c * 5 + best];
+  }
+  A.sel[c * 2 + role] = src;
+  if (A.sel_out) A.sel_out[c * 2 + role] = src;
+  A.t_dst[role][c] = A.t_src[role][src];
+  float lr = A.lr_src[role][src];
+  if (A.mutate) {
+    const uint4 w = stream_block(A.key, 0, (uint32_t)c, A.gen, 0,
+                                 role == 0 ? LIPZ_TAG_LRMUT_G : LIPZ_TAG_LRMUT_D);
+    if (uniform_of(w.x) < (double)A.mut_prob) {
+      const double nv = (double)lr + (double)A.mut_std * normal_of(w, 2);
+      lr = (float)(nv > 0.0 ? nv : 0.0);
+    }
+  }
+  A.lr_dst[role][c] = lr;
+  if (A.lr_out) A.lr_out[c * 2 + role] = lr;
+}
+
+// Copy every winner's parameters and Adam moments into its cell of the next
+// buffer: grid (chunks, C, 2 roles), float4 copies.
+__global__ void copy_winners_kernel(CopyArgs A) {
+  const int c = blockIdx.y, role = blockIdx.z;
+  const int src = A.sel[c * 2 + role];
+  const int64_t n4 = A.stride[role] >> 2;
+  for (int a = 0; a < 3; ++a) {
+    const float4* s = reinterpret_cast<const float4*>(A.src[role][a] + src * A.stride[role]);
+    float4* d = reinterpret_cast<float4*>(A.dst[role][a] + c * A.stride[role]);
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n4;
+         q += (int64_t)gridDim.x * blockDim.x)
+      d[q] = s[q];
+  }
+  if (role == 0 && blockIdx.x == 0 && threadIdx.x < 5)
+    A.w_dst[c * 5 + threadIdx.x] = A.w_src[c * 5 + threadIdx.x];
+}
+
+// Per-cell feature moments over S samples: mu = mean f, s2 = mean f^2.
+__global__ void moments_kernel(const float* feats, int S, int F, float* mu, float* s2) {
+  const int c = blockIdx.x;
+  for (int f = threadIdx.x; f < F; f += blockDim.x) {
+    float s = 0.f, q = 0.f;
+    const float* x = feats + (int64_t)c * S * F + f;
+    for (int r = 0; r < S; ++r) {
+      const float v = x[(int64_t)r * F];
+      s += v;
+      q += v * v;
+    }
+    mu[c * F + f] = s / (float)S;
+    s2[c * F + f] = q / (float)S;
+  }
+}
+
+// Column mean and (biased, two-pass) standard deviation over N rows.
+__global__ __launch_bounds__(NT) void col_stats_kernel(const float* feats, int64_t N, int F,
+                                                       float* mu, float* sd) {
+  __shared__ float red[4];
+  const int f = blockIdx.x;
+  double s = 0.0;
+  for (int64_t r = threadIdx.x; r < N; r += NT) s += feats[r * F + f];
+  const float mean = block_sum((float)(s / (double)N), red);
+  double q = 0.0;
+  for (int64_t r = threadIdx.x; r < N; r += NT) {
+    const double d = (double)feats[r * F + f] - (double)mean;
+    q += d * d;
+  }
+  const float var = block_sum((float)(q / (double)N), red);
+  if (threadIdx.x == 0) {
+    mu[f] = mean;
+    sd[f] = sqrtf(var);
+  }
+}
+
+__device__ float mixture_score(const float* w, const int32_t* ks, const float* mu, const float* s2,
+                               const float* mu_r, const float* sd_r, int F) {
+  float sc = 0.f;
+  for (int f = 0; f < F; ++f) {
+    float mw = 0.f, sw = 0.f;
+    for (int k = 0; k < 5; ++k) {
+      mw += w[k] * mu[ks[k] * F + f];
+      sw += w[k] * s2[ks[k] * F + f];
+    }
+    const float var = fmaxf(sw - mw * mw, 0.f);
+    const float dm = mw - mu_r[f], ds = sqrtf(var) - sd_r[f];
+    sc += dm * dm + ds * ds;
+  }
+  return sc;
+}
+
+// (1+1)-ES on the mixture weights of cell i.
+__global__ void es_kernel(EsArgs A) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= A.C) return;
+  const int32_t* ks = A.nbr + c * 5;
+  float w[5], wp[5];
+  for (int k = 0; k < 5; ++k) w[k] = A.w[c * 5 + k];
+  const uint4 w0 = stream_block(A.key, 0, (uint32_t)c, A.gen, 0, LIPZ_TAG_MIXN);
+  const uint4 w1 = stream_block(A.key, 1, (uint32_t)c, A.gen, 0, LIPZ_TAG_MIXN);
+  double tot = 0.0;
+  double wpd[5];
+  for (int k = 0; k < 5; ++k) {
+    const double n = k < 4 ? normal_of(w0, k) : normal_of(w1, 0);
+    const double x = (double)w[k] + (double)A.sigma * n;
+    wpd[k] = x > 0.0 ? x : 0.0;
+    tot += wpd[k];
+  }
+  float cur = mixture_score(w, ks, A.mu, A.s2, A.mu_r, A.sd_r, A.F);
+  int acc = 0;
+  if (tot > 0.0) {
+    for (int k = 0; k < 5; ++k) wp[k] = (float)(wpd[k] / tot);
+    const float nw = mixture_score(wp, ks, A.mu, A.s2, A.mu_r, A.sd_r, A.F);
+    if (nw < cur) {
+      cur = nw;
+      acc = 1;
+      for (int k = 0; k < 5; ++k) w[k] = wp[k];
+    }
+  }
+  for (int k = 0; k < 5; ++k) {
+    A.w[c * 5 + k] = w[k];
+    if (A.w_out) A.w_out[c * 5 + k] = w[k];
+  }
+  if (A.score_out) A.score_out[c] = cur;
+  if (A.acc_out) A.acc_out[c] = acc;
+}
+
+int grid_for(int64_t n, int threads = NT, int cap = 8192) {
+  int64_t b = (n + threads - 1) / threads;
+  if (b < 1) b = 1;
+  if (b > cap) b = cap;
+  return (int)b;
+}
+
+}  // namespace
+
+hipError_t launch_init_params(float* p, int64_t stride, int64_t P, int C, NetLayers L, uint2 key,
+                              uint32_t tag, hipStream_t s) {
+  hipLaunchKernelGGL(init_params_kernel, dim3(grid_for((int64_t)C * P)), dim3(NT), 0, s, p, stride,
+                     P, C, L, key, tag);
+  return hipGetLastError();
+}
+hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(n)), dim3(NT), 0, s, p, n, v);
+  return hipGetLastError();
+}
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(n)), dim3(NT), 0, s, p, n, v);
+  return hipGetLastError();
+}
+hipError_t launch_add_i32(int32_t* p, int n, int32_t v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(add_i32_kernel, dim3(grid_for(n)), dim3(NT), 0, s, p, n, v);
+  return hipGetLastError();
+}
+hipError_t launch_normals(float* out, int64_t n, double scale, uint2 key, uint32_t cell,
+                          uint32_t gen, uint32_t sf, uint32_t tag, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(normals_kernel, dim3(grid_for(n)), dim3(NT), 0, s, out, n, scale, key, cell,
+                     gen, sf, tag);
+  return hipGetLastError();
+}
+hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, int C, uint2 key,
+                         uint32_t gen, uint32_t sf, float* X, int64_t x_cell_stride, float* Z,
+                         int64_t z_cell_stride, hipStream_t s) {
+  hipLaunchKernelGGL(sample_kernel, dim3(B, C), dim3(NT), 0, s, data, N, xd, zd, key, gen, sf, X,
+                     x_cell_stride, Z, z_cell_stride);
+  return hipGetLastError();
+}
+hipError_t launch_head_d(const HeadArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(head_d_kernel, dim3(a.C), dim3(NT), 4 * a.B * sizeof(float), s, a);
+  return hipGetLastError();
+}
+hipError_t launch_head_g(const HeadArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(head_g_kernel, dim3(a.C), dim3(NT), 2 * a.B * sizeof(float), s, a);
+  return hipGetLastError();
+}
+hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(head_eval_kernel, dim3(5, a.C), dim3(NT), (6 * a.B + 11) * sizeof(float), s, a);
+  return hipGetLastError();
+}
+hipError_t launch_fitness(const float* L, const float* Lg, int C, int mode, float* fit_g,
+                          float* fit_d, int32_t* flags, float* oL, float* oLg, float* ofg,
+                          float* ofd, hipStream_t s) {
+  hipLaunchKernelGGL(fitness_kernel, dim3(grid_for((int64_t)C * 25)), dim3(NT), 0, s, L, Lg, C,
+                     mode, fit_g, fit_d, flags, oL, oLg, ofg, ofd);
+  return hipGetLastError();
+}
+hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(select_kernel, dim3(grid_for(2 * a.C)), dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_copy_winners(const CopyArgs& a, hipStream_t s) {
+  const int64_t n4 = (a.stride[0] > a.stride[1] ? a.stride[0] : a.stride[1]) >> 2;
+  hipLaunchKernelGGL(copy_winners_kernel, dim3(grid_for(n4, NT, 64), a.C, 2), dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_moments(const float* feats, int C, int S, int F, float* mu, float* s2,
+                          hipStream_t s) {
+  hipLaunchKernelGGL(moments_kernel, dim3(C), dim3(64), 0, s, feats, S, F, mu, s2);
+  return hipGetLastError();
+}
+hipError_t launch_col_stats(const float* feats, int64_t N, int F, float* mu, float* sd,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(col_stats_kernel, dim3(F), dim3(NT), 0, s, feats, N, F, mu, sd);
+  return hipGetLastError();
+}
+hipError_t launch_es(const EsArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(es_kernel, dim3(grid_for(a.C, 64)), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace lipz

@@ -1,0 +1,241 @@
+// Internal declarations shared by the HIP kernels and the host runtime of
+// liblipz.so.  Not part of the public interface (include/lipz.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "lipz.h"
+
+namespace lipz {
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon et al., SC 2011): ten rounds of
+//   (c0,c1,c2,c3) -> (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0))
+// with the key advanced by the Weyl constants between rounds.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint2 k) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k.x += 0x9E3779B9u;
+      k.y += 0xBB67AE85u;
+    }
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = make_uint4(hi1 ^ c.y ^ k.x, lo1, hi0 ^ c.w ^ k.y, lo0);
+  }
+  return c;
+}
+
+// Word `e % 4` of block e / 4 of the stream (cell, gen, step_field, tag).
+__device__ __forceinline__ uint4 stream_block(uint2 key, uint32_t blk, uint32_t cell, uint32_t gen,
+                                              uint32_t step_field, uint32_t tag) {
+  return philox4x32_10(make_uint4(blk, cell, (gen << 16) | step_field, tag), key);
+}
+
+__device__ __forceinline__ uint32_t word_of(uint4 w, int i) {
+  return i == 0 ? w.x : i == 1 ? w.y : i == 2 ? w.z : w.w;
+}
+
+// ((w >> 9) + 0.5) * 2^-23: exact in fp32, in (0, 1).
+__device__ __forceinline__ double uniform_of(uint32_t w) {
+  return ((double)(w >> 9) + 0.5) * (1.0 / 8388608.0);
+}
+
+// Normal number q (0..3) of a block by Box-Muller on (u0, u1) and (u2, u3), in fp64.
+__device__ __forceinline__ double normal_of(uint4 w, int q) {
+  const double ua = uniform_of(q < 2 ? w.x : w.z);
+  const double ub = uniform_of(q < 2 ? w.y : w.w);
+  const double r = sqrt(-2.0 * log(ua));
+  double s, c;
+  sincos(2.0 * 3.141592653589793 * ub, &s, &c);
+  return (q & 1) ? r * s : r * c;
+}
+
+// ---------------------------------------------------------------------------
+// Activations (LIPZ_ACT_*) and their derivatives expressed through the output
+// y = act(x): relu' = [y > 0], lrelu' = [y > 0] + slope [y <= 0], tanh' = 1 - y^2.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float act_fwd(int act, float x, float slope) {
+  switch (act) {
+    case 1: return x > 0.f ? x : 0.f;
+    case 2: return x > 0.f ? x : slope * x;
+    case 3: return tanhf(x);
+    default: return x;
+  }
+}
+__device__ __forceinline__ float act_deriv_from_out(int act, float y, float slope) {
+  switch (act) {
+    case 1: return y > 0.f ? 1.f : 0.f;
+    case 2: return y > 0.f ? 1.f : slope;
+    case 3: return 1.f - y * y;
+    default: return 1.f;
+  }
+}
+// softplus(x) = log(1 + e^x), stable form.
+__device__ __forceinline__ float softplus_f(float x) {
+  return fmaxf(x, 0.f) + log1pf(expf(-fabsf(x)));
+}
+__device__ __forceinline__ float sigmoid_f(float x) { return 1.f / (1.f + expf(-x)); }
+
+// ---------------------------------------------------------------------------
+// Grouped GEMM: one launch computes many independent problems
+//   C[M][N] (+)= epilogue( sum_k A(i,k) B(k,j) )
+// A(i,k) = A[i*lda + k] (a_trans 0) or A[k*lda + i] (a_trans 1);
+// rows i >= a_rows of A are zero, except row ones_row which is all ones (this
+// appends the bias row to a weight gradient: [X | 1]^T dY = (dW; db)).
+// B(k,j) = B[k*ldb + j] (b_trans 0) or B[j*ldb + k] (b_trans 1).
+// ---------------------------------------------------------------------------
+enum Epi : int32_t {
+  EPI_STORE = 0,     // C = acc
+  EPI_BIAS_ACT = 1,  // C = act(acc + bias[j])
+  EPI_DACT = 2,      // C = acc * act'(aux) with aux the forward output at the same index
+  EPI_ADAM = 3       // acc is the gradient of parameter C[i][j]; Adam update of C, m, v
+};
+
+struct GemmProb {
+  const float* A;
+  const float* B;
+  float* C;
+  const float* bias;
+  const float* aux;
+  float* m;
+  float* v;
+  const float* lr;     // EPI_ADAM: the cell's learning rate
+  const int32_t* t;    // EPI_ADAM: the cell's Adam step count before this call
+  int32_t M, N, K;
+  int32_t lda, ldb, ldc;
+  int32_t a_trans, b_trans;
+  int32_t a_rows, ones_row;
+  int32_t epi, act;
+  int32_t vec;         // bit 0: A rows 16-byte aligned; bit 1: B rows 16-byte aligned
+  int32_t tiles_n;
+  int32_t tile_begin;
+  int32_t reserved;
+};
+
+struct AdamConsts {
+  float beta1, beta2, one_minus_beta1, one_minus_beta2, eps;
+};
+
+constexpr int GEMM_BM = 64;
+constexpr int GEMM_BN = 64;
+
+// Launch the grouped GEMM over `nprob` problems stored at d_probs (device),
+// covering `total_tiles` 64x64 output tiles.
+hipError_t launch_gemm_grouped(const GemmProb* d_probs, int nprob, int total_tiles, int step_local,
+                               float slope, AdamConsts ac, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Other kernels (kernels.hip)
+// ---------------------------------------------------------------------------
+struct NetLayers {
+  int32_t n;             // number of layers
+  int64_t off[8];        // offset of W_l in the parameter row
+  int32_t fan_in[8];
+  int32_t fan_out[8];
+};
+
+hipError_t launch_init_params(float* p, int64_t stride, int64_t P, int C, NetLayers L, uint2 key,
+                              uint32_t tag, hipStream_t s);
+hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+hipError_t launch_normals(float* out, int64_t n, double scale, uint2 key, uint32_t cell, uint32_t gen,
+                          uint32_t step_field, uint32_t tag, hipStream_t s);
+hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, int C, uint2 key,
+                         uint32_t gen, uint32_t step_field, float* X, int64_t x_cell_stride,
+                         float* Z, int64_t z_cell_stride, hipStream_t s);
+
+struct HeadArgs {
+  const float* act;      // last hidden activations [C][rows][H] (cell stride act_cell_stride)
+  int64_t act_cell_stride;
+  float* delta;          // out: gradient w.r.t. the last hidden pre-activation, same layout
+  float* p;              // D parameter rows (current state), stride p_stride
+  float* m;
+  float* v;
+  int64_t p_stride;
+  int64_t head_off;      // offset of the head weight vector w (H floats) then bias
+  const float* lr;       // [C]
+  const int32_t* t;      // [C]
+  float* losses;         // [C][2] slice for this step, or null
+  int H, B, C;
+  int hidden_act;
+  float slope;
+  AdamConsts ac;
+  int step_local;
+};
+// Discriminator step head: logits of 2B rows (B real then B fake), BCE, its
+// gradient into delta, Adam update of the head weights.
+hipError_t launch_head_d(const HeadArgs& a, hipStream_t s);
+// Generator step head: logits of B fake rows, non-saturating loss, delta.
+hipError_t launch_head_g(const HeadArgs& a, hipStream_t s);
+
+struct EvalHeadArgs {
+  const float* act;      // [C][5][6B][H]
+  const float* Dp;       // [cells][stride]
+  int64_t p_stride, head_off;
+  const int32_t* nbr;    // [C][5]
+  float* L;              // [C][5][5]
+  float* Lg;
+  int H, B, C;
+};
+hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s);
+hipError_t launch_fitness(const float* L, const float* Lg, int C, int mode, float* fit_g, float* fit_d,
+                          int32_t* flags, float* out_L, float* out_Lg, float* out_fg, float* out_fd,
+                          hipStream_t s);
+
+struct SelectArgs {
+  const float* fit_g;
+  const float* fit_d;
+  const int32_t* nbr;
+  const int32_t* forced;   // or null
+  int32_t* sel;            // internal [C][2]
+  int32_t* flags;          // bit 1 set when a forced source cell is out of range
+  int32_t* sel_out;        // or null
+  float* lr_out;           // or null
+  const int32_t* t_src[2]; // current buffer Gt, Dt
+  const float* lr_src[2];
+  int32_t* t_dst[2];       // next buffer
+  float* lr_dst[2];
+  int C, tsize, mutate;
+  float mut_std, mut_prob;
+  uint2 key;
+  uint32_t gen;
+};
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+
+struct CopyArgs {
+  const int32_t* sel;      // [C][2]
+  const float* src[2][3];  // role, (p, m, v)
+  float* dst[2][3];
+  int64_t stride[2];       // floats per row, multiple of 4
+  const float* w_src;
+  float* w_dst;
+  int C;
+};
+hipError_t launch_copy_winners(const CopyArgs& a, hipStream_t s);
+hipError_t launch_add_i32(int32_t* p, int n, int32_t v, hipStream_t s);
+
+hipError_t launch_moments(const float* feats, int C, int S, int F, float* mu, float* s2, hipStream_t s);
+hipError_t launch_col_stats(const float* feats, int64_t N, int F, float* mu, float* sd, hipStream_t s);
+
+struct EsArgs {
+  const float* mu;        // [cells][F]
+  const float* s2;
+  const float* mu_r;
+  const float* sd_r;
+  const int32_t* nbr;
+  float* w;               // [C][5] in place
+  float* w_out;
+  float* score_out;
+  int32_t* acc_out;
+  int C, F;
+  float sigma;
+  uint2 key;
+  uint32_t gen;
+};
+hipError_t launch_es(const EsArgs& a, hipStream_t s);
+
+}  // namespace lipz

@@ -1,0 +1,64 @@
+// Test hook of include/lipz_testing.h: one grouped-GEMM problem.
+#include <string.h>
+
+#include "lipz_internal.h"
+#include "lipz_testing.h"
+
+using namespace lipz;
+
+extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M, int32_t N,
+                                      int32_t K, const float* d_A, int32_t lda, int32_t a_trans,
+                                      int32_t ones_row, const float* d_B, int32_t ldb,
+                                      int32_t b_trans, float* d_C, int32_t ldc, int32_t epi,
+                                      int32_t act, float slope, const float* d_bias,
+                                      const float* d_aux, float* d_m, float* d_v,
+                                      const float* d_lr, const int32_t* d_t, int32_t step_local,
+                                      float beta1, float beta2, float eps) {
+  if (!d_desc || !d_A || !d_B || !d_C || M < 1 || N < 1 || K < 1) return LIPZ_E_INVAL;
+  if (epi < EPI_STORE || epi > EPI_ADAM || act < LIPZ_ACT_LINEAR || act > LIPZ_ACT_TANH)
+    return LIPZ_E_INVAL;
+  if (ones_row >= 0 && (!a_trans || ones_row != M - 1)) return LIPZ_E_INVAL;
+  if (epi == EPI_DACT && !d_aux) return LIPZ_E_INVAL;
+  if (epi == EPI_ADAM && (!d_m || !d_v || !d_lr || !d_t)) return LIPZ_E_INVAL;
+  const int a_rows = ones_row >= 0 ? ones_row : M;
+  if (lda < (a_trans ? a_rows : K) || ldb < (b_trans ? K : N) || ldc < N) return LIPZ_E_INVAL;
+  GemmProb p;
+  memset(&p, 0, sizeof(p));
+  p.A = d_A;
+  p.B = d_B;
+  p.C = d_C;
+  p.bias = d_bias;
+  p.aux = d_aux;
+  p.m = d_m;
+  p.v = d_v;
+  p.lr = d_lr;
+  p.t = d_t;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.lda = lda;
+  p.ldb = ldb;
+  p.ldc = ldc;
+  p.a_trans = a_trans;
+  p.b_trans = b_trans;
+  p.a_rows = a_rows;
+  p.ones_row = ones_row;
+  p.epi = epi;
+  p.act = act;
+  p.vec = ((((uintptr_t)d_A & 15) == 0 && (lda & 3) == 0) ? 1 : 0) |
+          ((((uintptr_t)d_B & 15) == 0 && (ldb & 3) == 0) ? 2 : 0);
+  p.tiles_n = (N + GEMM_BN - 1) / GEMM_BN;
+  p.tile_begin = 0;
+  const int tiles = ((M + GEMM_BM - 1) / GEMM_BM) * p.tiles_n;
+  if (hipMemcpy(d_desc, &p, sizeof(p), hipMemcpyHostToDevice) != hipSuccess) return LIPZ_E_HIP;
+  AdamConsts ac;
+  ac.beta1 = beta1;
+  ac.beta2 = beta2;
+  ac.one_minus_beta1 = (float)(1.0 - (double)beta1);
+  ac.one_minus_beta2 = (float)(1.0 - (double)beta2);
+  ac.eps = eps;
+  if (launch_gemm_grouped((const GemmProb*)d_desc, 1, tiles, step_local, slope, ac,
+                          (hipStream_t)hip_stream) != hipSuccess)
+    return LIPZ_E_HIP;
+  return LIPZ_OK;
+}

@@ -1,0 +1,168 @@
+"""Test infrastructure shared by the GPU parity tests: a torch-backed wrapper
+around one grid of liblipz.so, and conversion between the library's state
+blob and the oracle's State.  Imports the oracle (tests may)."""
+import numpy as np
+import torch
+
+import paper_1811_12843_amd as L
+from oracle import coevo
+
+
+def fp32_state(st):
+    """The oracle state with every float rounded to fp32 (what the GPU can hold)."""
+    s = st.copy()
+    for f in ("Gp", "Gm", "Gv", "Glr", "Dp", "Dm", "Dv", "Dlr", "w"):
+        setattr(s, f, getattr(s, f).astype(np.float32).astype(np.float64))
+    return s
+
+
+class GpuGrid:
+    def __init__(self, wl, data_np, device="cuda"):
+        self.wl = wl
+        self.cfg = L.config_from_dict(wl)
+        self.N = int(len(data_np))
+        self.C = wl["rows"] * wl["cols"]
+        self.device = device
+        self.data = torch.from_numpy(np.ascontiguousarray(data_np, dtype=np.float32)).to(device)
+        nb = L.lipz_workspace_bytes(self.cfg, self.N)
+        assert nb > 0
+        self.ws = torch.empty(nb, dtype=torch.uint8, device=device)
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.g = L.lipz_grid_create(self.cfg, self.ws.data_ptr(), nb, self.data.data_ptr(), self.N,
+                                    self.stream)
+        self.offs, self.strides = L.lipz_state_layout(self.g)
+        self.state_bytes = L.lipz_state_bytes(self.g)
+        self.S = coevo.Setup(wl, self.N)
+
+    def close(self):
+        if self.g:
+            L.lipz_grid_destroy(self.g)
+            self.g = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def sync(self):
+        return L.lipz_sync(self.g)
+
+    # ---- state ----
+    def save_blob(self):
+        buf = torch.empty(self.state_bytes, dtype=torch.uint8, device=self.device)
+        L.lipz_save_state(self.g, buf.data_ptr())
+        assert self.sync() in (L.LIPZ_OK, L.LIPZ_E_NONFINITE)
+        return buf.cpu().numpy()
+
+    def load_blob(self, blob):
+        buf = torch.from_numpy(np.ascontiguousarray(blob)).to(self.device)
+        L.lipz_load_state(self.g, buf.data_ptr())
+        assert self.sync() in (L.LIPZ_OK, L.LIPZ_E_NONFINITE)
+
+    def get_state(self):
+        return blob_to_state(self.save_blob(), self.S, self.offs, self.strides)
+
+    def set_state(self, st):
+        self.load_blob(state_to_blob(st, self.S, self.offs, self.strides, self.state_bytes))
+
+    # ---- calls ----
+    def _f(self, *shape):
+        return torch.zeros(*shape, dtype=torch.float32, device=self.device)
+
+    def _i(self, *shape):
+        return torch.zeros(*shape, dtype=torch.int32, device=self.device)
+
+    def eval(self, gen):
+        Lm, Lg, fg, fd = self._f(self.C, 5, 5), self._f(self.C, 5, 5), self._f(self.C, 5), self._f(self.C, 5)
+        L.lipz_eval_neighborhoods(self.g, gen, Lm.data_ptr(), Lg.data_ptr(), fg.data_ptr(), fd.data_ptr())
+        self.sync()
+        return [t.cpu().numpy().astype(np.float64) for t in (Lm, Lg, fg, fd)]
+
+    def select(self, gen, forced=None):
+        sel, lr = self._i(self.C, 2), self._f(self.C, 2)
+        fp = None
+        if forced is not None:
+            ft = torch.from_numpy(np.ascontiguousarray(forced, dtype=np.int32)).to(self.device)
+            fp = ft.data_ptr()
+        L.lipz_select_replace(self.g, gen, fp, sel.data_ptr(), lr.data_ptr())
+        self.sync()
+        return sel.cpu().numpy().astype(np.int64), lr.cpu().numpy().astype(np.float64)
+
+    def train(self, gen, step0, n):
+        losses = self._f(max(n, 1), self.C, 2)
+        L.lipz_train_step(self.g, gen, step0, n, losses.data_ptr())
+        self.sync()
+        return losses.cpu().numpy().astype(np.float64)[:n]
+
+    def mixture(self, gen):
+        w, sc, acc = self._f(self.C, 5), self._f(self.C), self._i(self.C)
+        L.lipz_mixture_update(self.g, gen, w.data_ptr(), sc.data_ptr(), acc.data_ptr())
+        self.sync()
+        return (w.cpu().numpy().astype(np.float64), sc.cpu().numpy().astype(np.float64),
+                acc.cpu().numpy().astype(np.int64))
+
+
+def state_to_blob(st, S, offs, strides, nbytes):
+    blob = np.zeros(nbytes, dtype=np.uint8)
+    C = S.C
+
+    def put(k, arr, dtype):
+        a = np.ascontiguousarray(arr, dtype=dtype).view(np.uint8).ravel()
+        blob[offs[k]:offs[k] + a.size] = a
+
+    for k, (name, P, stride) in enumerate((("G", S.PG, strides[0]), ("D", S.PD, strides[1]))):
+        for j, f in enumerate(("p", "m", "v")):
+            full = np.zeros((C, stride), dtype=np.float32)
+            full[:, :P] = getattr(st, name + f)
+            put(3 * k + j, full, np.float32)
+    put(6, st.Gt, np.int32)
+    put(7, st.Dt, np.int32)
+    put(8, st.Glr, np.float32)
+    put(9, st.Dlr, np.float32)
+    put(10, st.w, np.float32)
+    return blob
+
+
+def blob_to_state(blob, S, offs, strides):
+    C = S.C
+
+    def get(k, n, dtype):
+        return np.frombuffer(blob[offs[k]:offs[k] + n * np.dtype(dtype).itemsize].tobytes(), dtype=dtype)
+
+    kw = {}
+    for k, (name, P, stride) in enumerate((("G", S.PG, strides[0]), ("D", S.PD, strides[1]))):
+        for j, f in enumerate(("p", "m", "v")):
+            kw[name + f] = get(3 * k + j, C * stride, np.float32).reshape(C, stride)[:, :P].astype(np.float64)
+    kw["Gt"] = get(6, C, np.int32).astype(np.int64)
+    kw["Dt"] = get(7, C, np.int32).astype(np.int64)
+    kw["Glr"] = get(8, C, np.float32).astype(np.float64)
+    kw["Dlr"] = get(9, C, np.float32).astype(np.float64)
+    kw["w"] = get(10, C * 5, np.float32).reshape(C, 5).astype(np.float64)
+    return coevo.State(**kw)
+
+
+def rel_err(a, b):
+    """Per-array ||a - b|| / ||b||."""
+    a, b = np.asarray(a, dtype=np.float64), np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (nb if nb > 0 else 1.0))
+
+
+def per_tensor_rel(Pa, Pb, sizes):
+    """Worst per-tensor relative error over cells and layers (W and b separately)."""
+    from oracle import mlp
+    worst = 0.0
+    for off, fi, fo in mlp.layout(sizes)[0]:
+        for lo, hi in ((off, off + fi * fo), (off + fi * fo, off + (fi + 1) * fo)):
+            for c in range(Pa.shape[0]):
+                worst = max(worst, rel_err(Pa[c, lo:hi], Pb[c, lo:hi]))
+    return worst
+
+
+def decisive(f, k1, k2, tol=1e-4):
+    """True when the fitness margin between two slots exceeds the tolerance."""
+    a, b = f[k1], f[k2]
+    if np.isnan(a) or np.isnan(b):
+        return not (np.isnan(a) and np.isnan(b))
+    return abs(a - b) > tol * max(abs(a), abs(b))
