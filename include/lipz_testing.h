@@ -15,6 +15,8 @@
  *   epi 3: acc is the gradient of parameter C[i*ldc + j]: one bias-corrected
  *          Adam step with step count t = *d_t + step_local + 1 and learning
  *          rate *d_lr on C, d_m, d_v (same indexing as C).
+ * tile_rows: 32 or 64 output rows per workgroup tile, 0 = the choice the
+ * library makes for a phase of this size.
  * d_desc: device scratch of at least 256 bytes for the problem descriptor
  * (caller-owned).  The call copies the descriptor synchronously, enqueues the
  * kernel on hip_stream and returns; LIPZ_E_INVAL on bad sizes.
@@ -34,7 +36,7 @@ lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M, int32_t N,
                            int32_t epi, int32_t act, float slope, const float* d_bias,
                            const float* d_aux, float* d_m, float* d_v, const float* d_lr,
                            const int32_t* d_t, int32_t step_local, float beta1, float beta2,
-                           float eps);
+                           float eps, int32_t tile_rows);
 
 #ifdef __cplusplus
 }

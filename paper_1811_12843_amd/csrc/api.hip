@@ -7,6 +7,7 @@
 // create time, for both state buffers (generations are double-buffered), and
 // uploaded into the workspace; a call only enqueues launches.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <new>
@@ -63,7 +64,9 @@ struct StateBuf {
 };
 
 struct Phase {
-  int first = 0, count = 0, tiles = 0;
+  int first = 0, count = 0, tiles = 0, tile_rows = 64;
+  bool fast = true;
+  GemmGroups grp;
   double flops = 0.0;
 };
 
@@ -98,6 +101,8 @@ struct lipz_grid {
   float *z = nullptr, *Xtr = nullptr;
   float *h[LIPZ_MAX_HIDDEN] = {}, *a[LIPZ_MAX_HIDDEN] = {}, *dD[LIPZ_MAX_HIDDEN] = {};
   float *ag[LIPZ_MAX_HIDDEN] = {}, *dDg[LIPZ_MAX_HIDDEN] = {}, *dG[LIPZ_MAX_HIDDEN + 1] = {};
+  float *part_tr = nullptr, *part_g = nullptr, *part_e = nullptr;  // partial logits
+  int tn = 1;  // column tiles of D's last hidden layer
   // evaluation buffers
   float *ze = nullptr, *Xe = nullptr;
   float *he[LIPZ_MAX_HIDDEN] = {}, *ae[LIPZ_MAX_HIDDEN] = {};
@@ -239,6 +244,9 @@ void carve(lipz_grid* g, char* base, size_t* total) {
   g->Xtr = cv.take<float>((size_t)C * 2 * B * xd);
   for (int l = 0; l + 1 < G.nl; ++l) g->h[l] = cv.take<float>((size_t)C * B * G.fo[l]);
   for (int l = 0; l < G.nl; ++l) g->dG[l] = cv.take<float>((size_t)C * B * G.fo[l]);
+  g->part_tr = cv.take<float>((size_t)C * 2 * B * g->tn);
+  g->part_g = cv.take<float>((size_t)C * B * g->tn);
+  g->part_e = cv.take<float>((size_t)C * 5 * 6 * B * g->tn);
   for (int l = 0; l + 1 < D.nl; ++l) {
     g->a[l] = cv.take<float>((size_t)C * 2 * B * D.fo[l]);
     g->dD[l] = cv.take<float>((size_t)C * 2 * B * D.fo[l]);
@@ -304,6 +312,16 @@ GemmProb fwd_prob(const float* x, int M, const float* Wb, int fi, int fo, float*
   return p;
 }
 
+// Attach D's output layer (H -> 1, weights w then bias) to the forward
+// problem of its last hidden layer: per-tile partial logits into part [M][tn].
+GemmProb with_head(GemmProb p, const float* head, float* part, int tn) {
+  p.dotw = head;
+  p.dot_bias = head + p.N;
+  p.dot_out = part;
+  p.dot_ld = tn;
+  return p;
+}
+
 // dx = (dy W^T) * act'(xfwd): dy [M][fo], W [fi][fo], dx and xfwd [M][fi].
 GemmProb dgrad_prob(const float* dy, int M, const float* W, int fi, int fo, float* dx,
                     const float* xfwd, int act) {
@@ -337,11 +355,29 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
   Phase ph;
   ph.first = (int)g->probs_h.size();
   ph.count = (int)ps.size();
+  int tiles64 = 0;
+  for (const GemmProb& p : ps) tiles64 += ceil_div(p.M, 64) * ceil_div(p.N, GEMM_BN);
+  ph.tile_rows = gemm_tile_rows(tiles64);
   int tiles = 0;
-  for (GemmProb p : ps) {
+  memset(&ph.grp, 0, sizeof(ph.grp));
+  int prev_tpp = -1;
+  for (size_t k = 0; k < ps.size(); ++k) {
+    GemmProb p = ps[k];
+    gemm_set_extents(p);
+    ph.fast = ph.fast && gemm_fast_ok(p);
     p.tiles_n = ceil_div(p.N, GEMM_BN);
     p.tile_begin = tiles;
-    tiles += ceil_div(p.M, GEMM_BM) * p.tiles_n;
+    const int tpp = ceil_div(p.M, ph.tile_rows) * p.tiles_n;
+    if (tpp != prev_tpp) {
+      // a new group; the problem lists built here have at most 2 shapes per phase
+      if (ph.grp.n == GEMM_MAX_GROUPS) abort();
+      ph.grp.first_tile[ph.grp.n] = tiles;
+      ph.grp.first_prob[ph.grp.n] = (int)k;
+      ph.grp.tiles_per_prob[ph.grp.n] = tpp;
+      ++ph.grp.n;
+      prev_tpp = tpp;
+    }
+    tiles += tpp;
     ph.flops += prob_flops(p);
     g->probs_h.push_back(p);
   }
@@ -395,8 +431,10 @@ void build_tables(lipz_grid* g) {
       for (int c = 0; c < C; ++c) {
         const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
                                 : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
-        ps.push_back(fwd_prob(x, 2 * B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
-                              g->a[l] + (size_t)c * 2 * B * D.fo[l], D.act[l]));
+        GemmProb p = fwd_prob(x, 2 * B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
+                              g->a[l] + (size_t)c * 2 * B * D.fo[l], D.act[l]);
+        if (l == LD - 2) p = with_head(p, S.Dp + c * sD + D.off[LD - 1], g->part_tr + (size_t)c * 2 * B * g->tn, g->tn);
+        ps.push_back(p);
       }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
     }
@@ -427,8 +465,10 @@ void build_tables(lipz_grid* g) {
       for (int c = 0; c < C; ++c) {
         const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd
                                 : g->ag[l - 1] + (size_t)c * B * D.fi[l];
-        ps.push_back(fwd_prob(x, B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
-                              g->ag[l] + (size_t)c * B * D.fo[l], D.act[l]));
+        GemmProb p = fwd_prob(x, B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
+                              g->ag[l] + (size_t)c * B * D.fo[l], D.act[l]);
+        if (l == LD - 2) p = with_head(p, S.Dp + c * sD + D.off[LD - 1], g->part_g + (size_t)c * B * g->tn, g->tn);
+        ps.push_back(p);
       }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
     }
@@ -490,8 +530,12 @@ void build_tables(lipz_grid* g) {
           const int owner = g->nbr_h[c * 5 + j];
           const float* x = l == 0 ? g->Xe + (size_t)c * 6 * B * xd
                                   : g->ae[l - 1] + (size_t)(c * 5 + j) * 6 * B * D.fi[l];
-          ps.push_back(fwd_prob(x, 6 * B, S.Dp + owner * sD + D.off[l], D.fi[l], D.fo[l],
-                                g->ae[l] + (size_t)(c * 5 + j) * 6 * B * D.fo[l], D.act[l]));
+          GemmProb p = fwd_prob(x, 6 * B, S.Dp + owner * sD + D.off[l], D.fi[l], D.fo[l],
+                                g->ae[l] + (size_t)(c * 5 + j) * 6 * B * D.fo[l], D.act[l]);
+          if (l == LD - 2)
+            p = with_head(p, S.Dp + owner * sD + D.off[LD - 1],
+                          g->part_e + (size_t)(c * 5 + j) * 6 * B * g->tn, g->tn);
+          ps.push_back(p);
         }
       ev.push_back(add_phase(g, ps));
     }
@@ -539,8 +583,8 @@ hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local) {
     g->ev_pool.pop_back();
     hipEventRecord(e0, g->stream);
   }
-  hipError_t e = launch_gemm_grouped(g->probs_d + ph.first, ph.count, ph.tiles, step_local, g->slope,
-                                     g->ac, g->stream);
+  hipError_t e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.fast,
+                                     step_local, g->slope, g->ac, g->stream);
   if (g->timing) {
     hipEventRecord(e1, g->stream);
     g->ev_live.push_back({e0, e1});
@@ -578,6 +622,7 @@ size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples) {
   g->N = n_samples;
   g->G = Gn;
   g->D = Dn;
+  g->tn = ceil_div(Dn.fi[Dn.nl - 1], GEMM_BN);
   g->nbr_h.assign((size_t)g->C * 5, 0);
   size_t total = 0;
   carve(g, nullptr, &total);
@@ -612,6 +657,7 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
   g->N = n_samples;
   g->G = Gn;
   g->D = Dn;
+  g->tn = ceil_div(Dn.fi[Dn.nl - 1], GEMM_BN);
   g->stream = (hipStream_t)hip_stream;
   g->data = d_dataset;
   g->key = make_uint2((uint32_t)(cfg->seed & 0xFFFFFFFFull), (uint32_t)(cfg->seed >> 32));
@@ -717,15 +763,10 @@ lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float
   for (int ph : g->eval_phases[par])
     if ((st = check_hip(g, run_gemm_phase(g, ph, 0), "eval forward"))) return st;
   EvalHeadArgs ha;
-  const int LD = g->D.nl;
-  ha.act = g->ae[LD - 2];
-  ha.Dp = g->st[par].Dp;
-  ha.p_stride = g->D.stride;
-  ha.head_off = g->D.off[LD - 1];
-  ha.nbr = g->nbr;
+  ha.part = g->part_e;
+  ha.tn = g->tn;
   ha.L = g->L;
   ha.Lg = g->Lg;
-  ha.H = g->D.fi[LD - 1];
   ha.B = B;
   ha.C = C;
   if ((st = check_hip(g, launch_head_eval(ha, s), "eval head"))) return st;
@@ -809,6 +850,8 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   const StateBuf& S = g->st[par];
   const int C = g->C, B = g->B, LD = g->D.nl;
   HeadArgs hd;
+  hd.part = g->part_tr;
+  hd.tn = g->tn;
   hd.act = g->a[LD - 2];
   hd.act_cell_stride = (int64_t)2 * B * g->D.fi[LD - 1];
   hd.delta = g->dD[LD - 2];
@@ -826,6 +869,7 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   hd.slope = g->slope;
   hd.ac = g->ac;
   HeadArgs hg = hd;
+  hg.part = g->part_g;
   hg.act = g->ag[LD - 2];
   hg.act_cell_stride = (int64_t)B * g->D.fi[LD - 1];
   hg.delta = g->dDg[LD - 2];

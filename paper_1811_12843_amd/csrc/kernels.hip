@@ -96,124 +96,106 @@ __global__ void sample_kernel(const float* __restrict__ data, int64_t N, int xd,
   }
 }
 
-// Logit of row r: dot(act[r], w) + bias, one wave per row.
-__device__ void head_logits(const float* act, int rows, int H, const float* w, float bias,
-                            float* logit) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int r = wave; r < rows; r += NT / 64) {
-    const float* a = act + (int64_t)r * H;
-    float s = 0.f;
-    for (int n = lane; n < H; n += 64) s += a[n] * w[n];
-    s = wave_sum(s);
-    if (lane == 0) logit[r] = s + bias;
+// Logits of `rows` rows from the per-tile partial sums (bias included), in a
+// fixed order; also dL/da into dl[] and the loss sums.
+//   d_step: rows < B are real (target 1), the rest fake (target 0)
+//   else:   all rows fake, non-saturating generator target 1
+__device__ void head_logits_and_dl(const float* part, int tn, int rows, int B, bool d_step, float* dl,
+                                   float* red, float* loss_real, float* loss_fake, float* dl_sum) {
+  const float invB = 1.f / (float)B;
+  float lr_ = 0.f, lf = 0.f, ds = 0.f;
+  for (int r = threadIdx.x; r < rows; r += NT) {
+    float a = 0.f;
+    for (int t = 0; t < tn; ++t) a += part[(int64_t)r * tn + t];
+    float d;
+    if (d_step && r >= B) {
+      d = sigmoid_f(a) * invB;
+      lf += softplus_f(a);
+    } else {
+      d = (sigmoid_f(a) - 1.f) * invB;
+      lr_ += softplus_f(-a);
+    }
+    dl[r] = d;
+    ds += d;
   }
+  *loss_real = block_sum(lr_, red);
+  *loss_fake = block_sum(lf, red);
+  *dl_sum = block_sum(ds, red);
 }
 
 // ---------------------------------------------------------------------------
-// Discriminator-step head for cell blockIdx.x: logits of B real then B fake
-// rows, L_D = mean softplus(-a_real) + mean softplus(a_fake), dL/da =
-// (sigmoid(a) - y) / B, delta = dL/da * w * act'(act), gradient of (w, bias),
-// then Adam on (w, bias) after every read of the old w.
+// Output layer of D (H -> 1) for block (cell, 64-column block cb):
+//   logits, BCE (D step: mean softplus(-a_real) + mean softplus(a_fake);
+//   G step: mean softplus(-a_fake)), dL/da = (sigmoid(a) - target) / B,
+//   delta[r][n] = dL/da_r * w_n * act'(act[r][n]) for the block's columns,
+//   and in the D step the gradient of w_n and Adam on the block's columns
+//   (the bias by block 0).  Each block owns its columns of w, so reading
+//   w_n for delta and then updating it cannot race with another block; the
+//   bias is not read here (it is inside the partial sums).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) void head_d_kernel(HeadArgs A) {
-  extern __shared__ float sm[];
-  float* logit = sm;            // 2B
-  float* dl = sm + 2 * A.B;     // 2B
+template <bool D_STEP>
+__global__ __launch_bounds__(NT) void head_kernel(HeadArgs A) {
+  extern __shared__ float dl[];
   __shared__ float red[4];
-  const int c = blockIdx.x;
-  const int rows = 2 * A.B;
-  const float* act = A.act + c * A.act_cell_stride;
-  float* p = A.p + c * A.p_stride + A.head_off;
-  float* m = A.m + c * A.p_stride + A.head_off;
-  float* v = A.v + c * A.p_stride + A.head_off;
+  __shared__ float gpart[4][64];
+  const int c = blockIdx.x, cb = blockIdx.y;
+  const int rows = D_STEP ? 2 * A.B : A.B;
   const int H = A.H;
-  head_logits(act, rows, H, p, p[H], logit);
+  float lreal, lfake, dsum;
+  head_logits_and_dl(A.part + (int64_t)c * rows * A.tn, A.tn, rows, A.B, D_STEP, dl, red, &lreal,
+                     &lfake, &dsum);
+  if (cb == 0 && threadIdx.x == 0 && A.losses) {
+    const float invB = 1.f / (float)A.B;
+    A.losses[c * 2 + (D_STEP ? 0 : 1)] = D_STEP ? lreal * invB + lfake * invB : lreal * invB;
+  }
   __syncthreads();
-  const float invB = 1.f / (float)A.B;
-  float lsum_r = 0.f, lsum_f = 0.f;
-  for (int r = threadIdx.x; r < rows; r += NT) {
-    const float a = logit[r];
-    if (r < A.B) {
-      dl[r] = (sigmoid_f(a) - 1.f) * invB;
-      lsum_r += softplus_f(-a);
-    } else {
-      dl[r] = sigmoid_f(a) * invB;
-      lsum_f += softplus_f(a);
-    }
-  }
-  lsum_r = block_sum(lsum_r, red);
-  lsum_f = block_sum(lsum_f, red);
-  if (threadIdx.x == 0 && A.losses) A.losses[c * 2 + 0] = lsum_r * invB + lsum_f * invB;
-  // delta[r][n] = dl[r] * w[n] * act'(act[r][n])
+  float* p = A.p + c * A.p_stride + A.head_off;
+  const float* act = A.act + c * A.act_cell_stride;
   float* delta = A.delta + c * A.act_cell_stride;
-  for (int r = 0; r < rows; ++r) {
-    const float d = dl[r];
-    for (int n = threadIdx.x; n < H; n += NT) {
+  const int n = cb * 64 + (threadIdx.x & 63);
+  const int rg = threadIdx.x >> 6;
+  const bool valid = n < H;
+  const float w = valid ? p[n] : 0.f;
+  float g = 0.f;
+  if (valid) {
+    for (int r = rg; r < rows; r += 4) {
       const int64_t o = (int64_t)r * H + n;
-      delta[o] = d * p[n] * act_deriv_from_out(A.hidden_act, act[o], A.slope);
+      const float y = act[o];
+      delta[o] = dl[r] * w * act_deriv_from_out(A.hidden_act, y, A.slope);
+      g += y * dl[r];
     }
   }
-  // gradient of the head weights (column sums, fixed row order) and bias
-  float gb = 0.f;
-  for (int r = threadIdx.x; r < rows; r += NT) gb += dl[r];
-  gb = block_sum(gb, red);
-  const int tt = *(A.t + c) + A.step_local + 1;
+  if (!D_STEP) return;
+  gpart[rg][threadIdx.x & 63] = g;
+  __syncthreads();
+  const int tt = A.t[c] + A.step_local + 1;
   const float bc1 = (float)(1.0 - pow((double)A.ac.beta1, (double)tt));
   const float bc2 = (float)(1.0 - pow((double)A.ac.beta2, (double)tt));
   const float lr = A.lr[c];
-  __syncthreads();  // every read of the old head weights is done
-  for (int n = threadIdx.x; n <= H; n += NT) {
-    float g;
-    if (n < H) {
-      g = 0.f;
-      for (int r = 0; r < rows; ++r) g += act[(int64_t)r * H + n] * dl[r];
-    } else {
-      g = gb;
-    }
-    const float mm = A.ac.beta1 * m[n] + A.ac.one_minus_beta1 * g;
-    const float vv = A.ac.beta2 * v[n] + A.ac.one_minus_beta2 * g * g;
-    m[n] = mm;
-    v[n] = vv;
-    p[n] = p[n] - lr * (mm / bc1) / (sqrtf(vv / bc2) + A.ac.eps);
+  float* m = A.m + c * A.p_stride + A.head_off;
+  float* v = A.v + c * A.p_stride + A.head_off;
+  int k = -1;
+  float gk = 0.f;
+  if (threadIdx.x < 64 && valid) {
+    k = n;
+    const int q = threadIdx.x;
+    gk = (gpart[0][q] + gpart[1][q]) + (gpart[2][q] + gpart[3][q]);
+  } else if (cb == 0 && threadIdx.x == 64) {
+    k = H;
+    gk = dsum;
   }
-}
-
-// Generator-step head: logits of B fake rows against the updated D,
-// L_G = mean softplus(-a), dL/da = (sigmoid(a) - 1) / B, delta as above.
-__global__ __launch_bounds__(NT) void head_g_kernel(HeadArgs A) {
-  extern __shared__ float sm[];
-  float* logit = sm;
-  float* dl = sm + A.B;
-  __shared__ float red[4];
-  const int c = blockIdx.x;
-  const int rows = A.B;
-  const float* act = A.act + c * A.act_cell_stride;
-  const float* p = A.p + c * A.p_stride + A.head_off;
-  const int H = A.H;
-  head_logits(act, rows, H, p, p[H], logit);
-  __syncthreads();
-  const float invB = 1.f / (float)A.B;
-  float ls = 0.f;
-  for (int r = threadIdx.x; r < rows; r += NT) {
-    const float a = logit[r];
-    dl[r] = (sigmoid_f(a) - 1.f) * invB;
-    ls += softplus_f(-a);
-  }
-  ls = block_sum(ls, red);
-  if (threadIdx.x == 0 && A.losses) A.losses[c * 2 + 1] = ls * invB;
-  float* delta = A.delta + c * A.act_cell_stride;
-  for (int r = 0; r < rows; ++r) {
-    const float d = dl[r];
-    for (int n = threadIdx.x; n < H; n += NT) {
-      const int64_t o = (int64_t)r * H + n;
-      delta[o] = d * p[n] * act_deriv_from_out(A.hidden_act, act[o], A.slope);
-    }
+  if (k >= 0) {
+    const float mm = A.ac.beta1 * m[k] + A.ac.one_minus_beta1 * gk;
+    const float vv = A.ac.beta2 * v[k] + A.ac.one_minus_beta2 * gk * gk;
+    m[k] = mm;
+    v[k] = vv;
+    p[k] = p[k] - lr * (mm / bc1) / (sqrtf(vv / bc2) + A.ac.eps);
   }
 }
 
 // ---------------------------------------------------------------------------
 // Evaluation head for block (j, c): logits of the 6B rows [x_c; G_0(z_c);
-// ...; G_4(z_c)] under discriminator slot j, then
+// ...; G_4(z_c)] under discriminator slot j (from the partial sums), then
 //   L[c][i][j] = mean softplus(-a_real) + mean softplus(a_fake_i)
 //   Lg[c][i][j] = mean softplus(-a_fake_i)
 // ---------------------------------------------------------------------------
@@ -221,25 +203,29 @@ __global__ __launch_bounds__(NT) void head_eval_kernel(EvalHeadArgs A) {
   extern __shared__ float logit[];
   const int j = blockIdx.x, c = blockIdx.y;
   const int rows = 6 * A.B;
-  const int owner = A.nbr[c * 5 + j];
-  const float* p = A.Dp + owner * A.p_stride + A.head_off;
-  const float* act = A.act + ((int64_t)(c * 5 + j) * rows) * A.H;
-  head_logits(act, rows, A.H, p, p[A.H], logit);
-  __syncthreads();
-  // thread 0: real term; threads 1..5: fake terms of slot i = tid - 1;
-  // threads 6..10: generator terms.  Each sums its B rows in order.
-  const int t = threadIdx.x;
-  if (t < 11) {
-    const int blk = t == 0 ? 0 : (t <= 5 ? t : t - 5);
-    const float sgn = (t == 0 || t > 5) ? -1.f : 1.f;
-    float s = 0.f;
-    for (int b = 0; b < A.B; ++b) s += softplus_f(sgn * logit[blk * A.B + b]);
-    logit[rows + t] = s / (float)A.B;
+  const float* part = A.part + (int64_t)(c * 5 + j) * rows * A.tn;
+  for (int r = threadIdx.x; r < rows; r += NT) {
+    float a = 0.f;
+    for (int t = 0; t < A.tn; ++t) a += part[(int64_t)r * A.tn + t];
+    logit[r] = a;
   }
   __syncthreads();
-  if (t < 5) {
-    const float real = logit[rows];
-    A.L[(c * 5 + t) * 5 + j] = real + logit[rows + 1 + t];
+  // one wave per mean: wave w < 11 sums its B terms (lane-strided, then a
+  // fixed shuffle tree).  Mean 0: real rows; 1..5: fake slot i = w - 1;
+  // 6..10: generator terms of slot w - 6.
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int q = wave; q < 11; q += NT / 64) {
+    const int blk = q == 0 ? 0 : (q <= 5 ? q : q - 5);
+    const float sgn = (q == 0 || q > 5) ? -1.f : 1.f;
+    float s = 0.f;
+    for (int b = lane; b < A.B; b += 64) s += softplus_f(sgn * logit[blk * A.B + b]);
+    s = wave_sum(s);
+    if (lane == 0) logit[rows + q] = s / (float)A.B;
+  }
+  __syncthreads();
+  if (threadIdx.x < 5) {
+    const int t = threadIdx.x;
+    A.L[(c * 5 + t) * 5 + j] = logit[rows] + logit[rows + 1 + t];
     A.Lg[(c * 5 + t) * 5 + j] = logit[rows + 6 + t];
   }
 }
@@ -475,11 +461,13 @@ hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, in
   return hipGetLastError();
 }
 hipError_t launch_head_d(const HeadArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(head_d_kernel, dim3(a.C), dim3(NT), 4 * a.B * sizeof(float), s, a);
+  hipLaunchKernelGGL(head_kernel<true>, dim3(a.C, (a.H + 63) / 64), dim3(NT), 2 * a.B * sizeof(float), s,
+                     a);
   return hipGetLastError();
 }
 hipError_t launch_head_g(const HeadArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(head_g_kernel, dim3(a.C), dim3(NT), 2 * a.B * sizeof(float), s, a);
+  hipLaunchKernelGGL(head_kernel<false>, dim3(a.C, (a.H + 63) / 64), dim3(NT), a.B * sizeof(float), s,
+                     a);
   return hipGetLastError();
 }
 hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s) {

@@ -10,6 +10,16 @@
 
 namespace lipz {
 
+// Pointers read from a descriptor in memory have no known address space, so
+// the compiler would access them with flat instructions, which share the
+// LDS wait counter and serialise a prefetch behind every LDS read.  Device
+// code casts them to the global address space before use.
+#define LIPZ_GLOBAL __attribute__((address_space(1)))
+template <class T>
+__device__ __forceinline__ LIPZ_GLOBAL T* as_global(T* p) {
+  return (LIPZ_GLOBAL T*)p;
+}
+
 // ---------------------------------------------------------------------------
 // Philox4x32-10 (Salmon et al., SC 2011): ten rounds of
 //   (c0,c1,c2,c3) -> (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0))
@@ -105,6 +115,13 @@ struct GemmProb {
   float* v;
   const float* lr;     // EPI_ADAM: the cell's learning rate
   const int32_t* t;    // EPI_ADAM: the cell's Adam step count before this call
+  // EPI_BIAS_ACT only: when dot_out is set, the tile also writes
+  //   dot_out[i*dot_ld + tile_n] = sum over its columns j of C[i][j] * dotw[j]
+  // (+ *dot_bias in tile column 0): the next layer's 1-wide output, split
+  // into per-tile partial sums that a later kernel adds in a fixed order.
+  const float* dotw;
+  const float* dot_bias;
+  float* dot_out;
   int32_t M, N, K;
   int32_t lda, ldb, ldc;
   int32_t a_trans, b_trans;
@@ -113,20 +130,44 @@ struct GemmProb {
   int32_t vec;         // bit 0: A rows 16-byte aligned; bit 1: B rows 16-byte aligned
   int32_t tiles_n;
   int32_t tile_begin;
-  int32_t reserved;
+  int32_t dot_ld;
+  uint32_t a_bytes;    // extent of A from its base: a_rows * lda (a_trans 0) or K * lda floats
+  uint32_t b_bytes;    // extent of B: K * ldb (b_trans 0) or N * ldb floats
 };
 
 struct AdamConsts {
   float beta1, beta2, one_minus_beta1, one_minus_beta2, eps;
 };
 
-constexpr int GEMM_BM = 64;
 constexpr int GEMM_BN = 64;
+constexpr int GEMM_MAX_GROUPS = 4;
 
-// Launch the grouped GEMM over `nprob` problems stored at d_probs (device),
-// covering `total_tiles` 64x64 output tiles.
-hipError_t launch_gemm_grouped(const GemmProb* d_probs, int nprob, int total_tiles, int step_local,
-                               float slope, AdamConsts ac, hipStream_t s);
+// A phase's problems form up to 4 groups of consecutive problems with the
+// same tile count, so a workgroup finds its problem from kernel arguments
+// alone: group g covers tiles [first_tile[g], first_tile[g+1]) and problem
+// first_prob[g] + (tile - first_tile[g]) / tiles_per_prob[g].
+struct GemmGroups {
+  int32_t n;
+  int32_t first_tile[GEMM_MAX_GROUPS];
+  int32_t first_prob[GEMM_MAX_GROUPS];
+  int32_t tiles_per_prob[GEMM_MAX_GROUPS];
+};
+
+// Tile height (32 or 64 rows) for a phase that has `tiles64` tiles of 64x64.
+int gemm_tile_rows(int tiles64);
+
+// True when a problem can use the fast kernel: one of the three operand
+// layouts it instantiates, 16-byte aligned rows of both operands and extents
+// below 2 GiB (buffer-load offsets are 32-bit).
+bool gemm_fast_ok(const GemmProb& p);
+// Fill a_bytes / b_bytes from the problem's shape (0 if they do not fit 32 bits).
+void gemm_set_extents(GemmProb& p);
+
+// Launch the grouped GEMM over the problems stored at d_probs (device),
+// covering `total_tiles` tiles of tile_rows x 64 outputs.
+hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
+                               int tile_rows, bool fast, int step_local, float slope, AdamConsts ac,
+                               hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Other kernels (kernels.hip)
@@ -149,6 +190,8 @@ hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, in
                          float* Z, int64_t z_cell_stride, hipStream_t s);
 
 struct HeadArgs {
+  const float* part;     // per-tile partial logits [C][rows][tn] (bias included)
+  int tn;
   const float* act;      // last hidden activations [C][rows][H] (cell stride act_cell_stride)
   int64_t act_cell_stride;
   float* delta;          // out: gradient w.r.t. the last hidden pre-activation, same layout
@@ -173,13 +216,11 @@ hipError_t launch_head_d(const HeadArgs& a, hipStream_t s);
 hipError_t launch_head_g(const HeadArgs& a, hipStream_t s);
 
 struct EvalHeadArgs {
-  const float* act;      // [C][5][6B][H]
-  const float* Dp;       // [cells][stride]
-  int64_t p_stride, head_off;
-  const int32_t* nbr;    // [C][5]
+  const float* part;     // partial logits [C][5][6B][tn] (bias included)
+  int tn;
   float* L;              // [C][5][5]
   float* Lg;
-  int H, B, C;
+  int B, C;
 };
 hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s);
 hipError_t launch_fitness(const float* L, const float* Lg, int C, int mode, float* fit_g, float* fit_d,

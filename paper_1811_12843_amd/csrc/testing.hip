@@ -13,12 +13,13 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
                                       int32_t act, float slope, const float* d_bias,
                                       const float* d_aux, float* d_m, float* d_v,
                                       const float* d_lr, const int32_t* d_t, int32_t step_local,
-                                      float beta1, float beta2, float eps) {
+                                      float beta1, float beta2, float eps, int32_t tile_rows) {
   if (!d_desc || !d_A || !d_B || !d_C || M < 1 || N < 1 || K < 1) return LIPZ_E_INVAL;
   if (epi < EPI_STORE || epi > EPI_ADAM || act < LIPZ_ACT_LINEAR || act > LIPZ_ACT_TANH)
     return LIPZ_E_INVAL;
   if (ones_row >= 0 && (!a_trans || ones_row != M - 1)) return LIPZ_E_INVAL;
   if (epi == EPI_DACT && !d_aux) return LIPZ_E_INVAL;
+  if (tile_rows != 0 && tile_rows != 32 && tile_rows != 64) return LIPZ_E_INVAL;
   if (epi == EPI_ADAM && (!d_m || !d_v || !d_lr || !d_t)) return LIPZ_E_INVAL;
   const int a_rows = ones_row >= 0 ? ones_row : M;
   if (lda < (a_trans ? a_rows : K) || ldb < (b_trans ? K : N) || ldc < N) return LIPZ_E_INVAL;
@@ -49,7 +50,8 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
           ((((uintptr_t)d_B & 15) == 0 && (ldb & 3) == 0) ? 2 : 0);
   p.tiles_n = (N + GEMM_BN - 1) / GEMM_BN;
   p.tile_begin = 0;
-  const int tiles = ((M + GEMM_BM - 1) / GEMM_BM) * p.tiles_n;
+  if (tile_rows == 0) tile_rows = gemm_tile_rows(((M + 63) / 64) * p.tiles_n);
+  const int tiles = ((M + tile_rows - 1) / tile_rows) * p.tiles_n;
   if (hipMemcpy(d_desc, &p, sizeof(p), hipMemcpyHostToDevice) != hipSuccess) return LIPZ_E_HIP;
   AdamConsts ac;
   ac.beta1 = beta1;
@@ -57,7 +59,13 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
   ac.one_minus_beta1 = (float)(1.0 - (double)beta1);
   ac.one_minus_beta2 = (float)(1.0 - (double)beta2);
   ac.eps = eps;
-  if (launch_gemm_grouped((const GemmProb*)d_desc, 1, tiles, step_local, slope, ac,
+  GemmGroups grp;
+  memset(&grp, 0, sizeof(grp));
+  grp.n = 1;
+  grp.tiles_per_prob[0] = tiles;
+  gemm_set_extents(p);
+  if (hipMemcpy(d_desc, &p, sizeof(p), hipMemcpyHostToDevice) != hipSuccess) return LIPZ_E_HIP;
+  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, gemm_fast_ok(p), step_local, slope, ac,
                           (hipStream_t)hip_stream) != hipSuccess)
     return LIPZ_E_HIP;
   return LIPZ_OK;

@@ -89,11 +89,12 @@ def test_gemm_kernel_against_matmul():
     stream = torch.cuda.current_stream().cuda_stream
     shapes = [(1, 1, 1), (64, 64, 16), (37, 53, 19), (129, 65, 33), (100, 256, 64), (200, 256, 784),
               (257, 784, 100)]
-    for (M, N, K) in shapes:
+    for (M, N, K), tile_rows in [(s, tr) for s in shapes for tr in (32, 64)]:
         for a_trans in (0, 1):
             for b_trans in (0, 1):
                 for epi, act in ((0, 0), (1, 1), (1, 2), (1, 3), (2, 2), (2, 3)):
-                    _print_case("gemm", M=M, N=N, K=K, at=a_trans, bt=b_trans, epi=epi, act=act)
+                    _print_case("gemm", M=M, N=N, K=K, at=a_trans, bt=b_trans, epi=epi, act=act,
+                                tile_rows=tile_rows)
                     A = g.normal(size=(M, K)).astype(np.float32)
                     Bm = g.normal(size=(K, N)).astype(np.float32)
                     bias = g.normal(size=N).astype(np.float32)
@@ -106,7 +107,7 @@ def test_gemm_kernel_against_matmul():
                     L.lipz_test_gemm(stream, desc.data_ptr(), M, N, K, dA.data_ptr(),
                                      M if a_trans else K, a_trans, -1, dB.data_ptr(),
                                      K if b_trans else N, b_trans, dC.data_ptr(), N, epi, act, 0.2,
-                                     d_bias=db.data_ptr(), d_aux=daux.data_ptr())
+                                     d_bias=db.data_ptr(), d_aux=daux.data_ptr(), tile_rows=tile_rows)
                     torch.cuda.synchronize()
                     acc = A.astype(np.float64) @ Bm.astype(np.float64)
                     scale = np.abs(A).astype(np.float64) @ np.abs(Bm).astype(np.float64)
@@ -131,8 +132,9 @@ def test_gemm_weight_gradient_with_bias_row_and_adam():
     dev = "cuda"
     desc = torch.zeros(256, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream().cuda_stream
-    for (rows, fi, fo) in [(200, 784, 256), (100, 256, 784), (19, 37, 45), (64, 2, 64), (100, 64, 256)]:
-        _print_case("wgrad_adam", rows=rows, fi=fi, fo=fo)
+    for (rows, fi, fo), tile_rows in [(s, tr) for s in [(200, 784, 256), (100, 256, 784), (19, 37, 45),
+                                                        (64, 2, 64), (100, 64, 256)] for tr in (32, 64)]:
+        _print_case("wgrad_adam", rows=rows, fi=fi, fo=fo, tile_rows=tile_rows)
         X = g.normal(size=(rows, fi)).astype(np.float32)
         dY = (g.normal(size=(rows, fo)) * 1e-2).astype(np.float32)
         P0 = g.normal(size=(fi + 1, fo)).astype(np.float32)
@@ -148,7 +150,8 @@ def test_gemm_weight_gradient_with_bias_row_and_adam():
         dt = torch.tensor([t0], dtype=torch.int32, device=dev)
         L.lipz_test_gemm(stream, desc.data_ptr(), fi + 1, fo, rows, dX.data_ptr(), fi, 1, fi,
                          ddY.data_ptr(), fo, 0, dP.data_ptr(), fo, 3, 0, 0.2, d_m=dm.data_ptr(),
-                         d_v=dv.data_ptr(), d_lr=dlr.data_ptr(), d_t=dt.data_ptr(), step_local=step_local)
+                         d_v=dv.data_ptr(), d_lr=dlr.data_ptr(), d_t=dt.data_ptr(), step_local=step_local,
+                         tile_rows=tile_rows)
         torch.cuda.synchronize()
         Xe = np.concatenate([X, np.ones((rows, 1), np.float32)], axis=1).astype(np.float64)
         grad = Xe.T @ dY.astype(np.float64)
