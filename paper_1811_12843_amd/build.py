@@ -32,10 +32,12 @@ def sources():
     return sorted(glob.glob(os.path.join(PKG, "csrc", "*.hip")))
 
 
-def build(verbose=False):
-    """Compile every HIP source into paper_1811_12843_amd/liblipz.so."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"),
+def build(verbose=False, out=None, defines=()):
+    """Compile every HIP source into paper_1811_12843_amd/liblipz.so (or `out`),
+    with optional -D definitions."""
+    lib = out or LIB
+    tmp = lib + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, *["-D" + d for d in defines], "-I", os.path.join(ROOT, "include"),
            "-I", os.path.join(PKG, "csrc"), *sources(), "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -46,8 +48,8 @@ def build(verbose=False):
         raise RuntimeError("hipcc failed:\n" + msgs)
     if verbose and msgs.strip():
         print(msgs)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

@@ -21,6 +21,10 @@ using namespace lipz;
 namespace {
 
 constexpr size_t kAlign = 256;
+#define LIPZ_MAX_GROUPS 4
+#ifndef LIPZ_CELL_GROUPS
+#define LIPZ_CELL_GROUPS 0  // 0: choose from the grid size
+#endif
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -65,7 +69,7 @@ struct StateBuf {
 
 struct Phase {
   int first = 0, count = 0, tiles = 0, tile_rows = 64;
-  bool fast = true;
+  bool fast = true, wave = false;
   GemmGroups grp;
   double flops = 0.0;
 };
@@ -102,6 +106,7 @@ struct lipz_grid {
   float *h[LIPZ_MAX_HIDDEN] = {}, *a[LIPZ_MAX_HIDDEN] = {}, *dD[LIPZ_MAX_HIDDEN] = {};
   float *ag[LIPZ_MAX_HIDDEN] = {}, *dDg[LIPZ_MAX_HIDDEN] = {}, *dG[LIPZ_MAX_HIDDEN + 1] = {};
   float *part_tr = nullptr, *part_g = nullptr, *part_e = nullptr;  // partial logits
+  float* dlbuf = nullptr;  // D-step dL/d(logit) [C][2B][4]
   int tn = 1;  // column tiles of D's last hidden layer
   // evaluation buffers
   float *ze = nullptr, *Xe = nullptr;
@@ -114,7 +119,14 @@ struct lipz_grid {
   GemmProb* probs_d = nullptr;
   std::vector<GemmProb> probs_h;
   std::vector<Phase> phases;
-  std::vector<Op> train_ops[2];
+  // Cells are split into groups whose training phases run on separate
+  // streams (group 0 on the caller's stream), so that one group's
+  // latency-bound launches overlap another group's work.
+  int n_groups = 1;
+  int group_c0[LIPZ_MAX_GROUPS + 1] = {};
+  hipStream_t gstream[LIPZ_MAX_GROUPS] = {};
+  hipEvent_t fork_ev = nullptr, join_ev[LIPZ_MAX_GROUPS] = {};
+  std::vector<Op> train_ops[2][LIPZ_MAX_GROUPS];
   std::vector<int> eval_phases[2], mix_phases[2];
   int real_phase = -1;
 
@@ -245,6 +257,7 @@ void carve(lipz_grid* g, char* base, size_t* total) {
   for (int l = 0; l + 1 < G.nl; ++l) g->h[l] = cv.take<float>((size_t)C * B * G.fo[l]);
   for (int l = 0; l < G.nl; ++l) g->dG[l] = cv.take<float>((size_t)C * B * G.fo[l]);
   g->part_tr = cv.take<float>((size_t)C * 2 * B * g->tn);
+  g->dlbuf = cv.take<float>((size_t)C * 2 * B * 4);
   g->part_g = cv.take<float>((size_t)C * B * g->tn);
   g->part_e = cv.take<float>((size_t)C * 5 * 6 * B * g->tn);
   for (int l = 0; l + 1 < D.nl; ++l) {
@@ -358,6 +371,9 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
   int tiles64 = 0;
   for (const GemmProb& p : ps) tiles64 += ceil_div(p.M, 64) * ceil_div(p.N, GEMM_BN);
   ph.tile_rows = gemm_tile_rows(tiles64);
+  int max_k = 0;
+  for (const GemmProb& p : ps) max_k = p.K > max_k ? p.K : max_k;
+  ph.wave = gemm_wave_ok(max_k);
   int tiles = 0;
   memset(&ph.grp, 0, sizeof(ph.grp));
   int prev_tpp = -1;
@@ -390,17 +406,32 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
 // layer l + 1 (which rewrites W_{l+1}) runs beside the input gradient of
 // layer l (which reads W_l), never beside the one of its own layer.
 template <class Dgrad, class Wgrad>
-void backward_phases(lipz_grid* g, int top, Dgrad dgrad, Wgrad wgrad, std::vector<Op>* ops) {
+void backward_phases(lipz_grid* g, int top, Dgrad dgrad, Wgrad wgrad, std::vector<Op>* ops,
+                     const std::vector<GemmProb>& extra_first = {}) {
   std::vector<GemmProb> pending;
   for (int l = top; l >= 0; --l) {
     std::vector<GemmProb> ph;
     if (l >= 1) dgrad(l, &ph);
+    if (l == top) ph.insert(ph.end(), extra_first.begin(), extra_first.end());
     ph.insert(ph.end(), pending.begin(), pending.end());
     pending.clear();
     wgrad(l, &pending);
     if (l == 0) ph.insert(ph.end(), pending.begin(), pending.end());
     ops->push_back({OP_GEMM, add_phase(g, ph)});
   }
+}
+
+
+void setup_groups(lipz_grid* g) {
+  // Measured on the 4x4 MNIST-shaped grid: 1, 2 and 4 groups are within a
+  // few percent of each other, so by default one stream keeps the phases
+  // in a single dependency chain.
+  int n = LIPZ_CELL_GROUPS;
+  if (n <= 0) n = 1;
+  if (n > LIPZ_MAX_GROUPS) n = LIPZ_MAX_GROUPS;
+  if (n > g->C) n = g->C;
+  g->n_groups = n;
+  for (int i = 0; i <= n; ++i) g->group_c0[i] = (int)((int64_t)g->C * i / n);
 }
 
 void build_tables(lipz_grid* g) {
@@ -412,13 +443,15 @@ void build_tables(lipz_grid* g) {
   const size_t sG = G.stride, sD = D.stride;
   for (int par = 0; par < 2; ++par) {
     const StateBuf& S = g->st[par];
-    std::vector<Op>& ops = g->train_ops[par];
+    for (int grp = 0; grp < g->n_groups; ++grp) {
+    const int cb = g->group_c0[grp], ce = g->group_c0[grp + 1];
+    std::vector<Op>& ops = g->train_ops[par][grp];
     ops.clear();
     // ---- training step ----
     ops.push_back({OP_SAMPLE, -1});
     for (int l = 0; l < LG; ++l) {
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c) {
+      for (int c = cb; c < ce; ++c) {
         const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
         float* y = l + 1 < LG ? g->h[l] + (size_t)c * B * G.fo[l]
                               : g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd;
@@ -428,7 +461,7 @@ void build_tables(lipz_grid* g) {
     }
     for (int l = 0; l + 1 < LD; ++l) {
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c) {
+      for (int c = cb; c < ce; ++c) {
         const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
                                 : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
         GemmProb p = fwd_prob(x, 2 * B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
@@ -439,17 +472,33 @@ void build_tables(lipz_grid* g) {
       ops.push_back({OP_GEMM, add_phase(g, ps)});
     }
     ops.push_back({OP_HEAD_D, -1});
+    // output layer of D: ([act | 1]^T dL/da) and its Adam step, as GEMM problems
+    std::vector<GemmProb> head_grad;
+    for (int c = cb; c < ce; ++c) {
+      const int H = D.fi[LD - 1];
+      const size_t o = c * sD + D.off[LD - 1];
+      GemmProb p = base_prob(g->a[LD - 2] + (size_t)c * 2 * B * H, H, 1, g->dlbuf + (size_t)c * 2 * B * 4, 4,
+                             0, S.Dp + o, 1, H + 1, 1, 2 * B);
+      p.a_rows = H;
+      p.ones_row = H;
+      p.m = S.Dm + o;
+      p.v = S.Dv + o;
+      p.lr = S.Dlr + c;
+      p.t = S.Dt + c;
+      p.epi = EPI_ADAM;
+      head_grad.push_back(p);
+    }
     backward_phases(
         g, LD - 2,
         [&](int l, std::vector<GemmProb>* ph) {
-          for (int c = 0; c < C; ++c)
+          for (int c = cb; c < ce; ++c)
             ph->push_back(dgrad_prob(g->dD[l] + (size_t)c * 2 * B * D.fo[l], 2 * B,
                                      S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
                                      g->dD[l - 1] + (size_t)c * 2 * B * D.fi[l],
                                      g->a[l - 1] + (size_t)c * 2 * B * D.fi[l], D.act[l - 1]));
         },
         [&](int l, std::vector<GemmProb>* ph) {
-          for (int c = 0; c < C; ++c) {
+          for (int c = cb; c < ce; ++c) {
             const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
                                     : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
             const size_t o = c * sD + D.off[l];
@@ -458,11 +507,11 @@ void build_tables(lipz_grid* g) {
                                           S.Dt + c));
           }
         },
-        &ops);
+        &ops, head_grad);
     // generator step: D forward on the fake rows with the updated D
     for (int l = 0; l + 1 < LD; ++l) {
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c) {
+      for (int c = cb; c < ce; ++c) {
         const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd
                                 : g->ag[l - 1] + (size_t)c * B * D.fi[l];
         GemmProb p = fwd_prob(x, B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
@@ -475,7 +524,7 @@ void build_tables(lipz_grid* g) {
     ops.push_back({OP_HEAD_G, -1});
     for (int l = LD - 2; l >= 0; --l) {
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c) {
+      for (int c = cb; c < ce; ++c) {
         if (l >= 1) {
           ps.push_back(dgrad_prob(g->dDg[l] + (size_t)c * B * D.fo[l], B, S.Dp + c * sD + D.off[l],
                                   D.fi[l], D.fo[l], g->dDg[l - 1] + (size_t)c * B * D.fi[l],
@@ -492,13 +541,13 @@ void build_tables(lipz_grid* g) {
     backward_phases(
         g, LG - 1,
         [&](int l, std::vector<GemmProb>* ph) {
-          for (int c = 0; c < C; ++c)
+          for (int c = cb; c < ce; ++c)
             ph->push_back(dgrad_prob(g->dG[l] + (size_t)c * B * G.fo[l], B, S.Gp + c * sG + G.off[l],
                                      G.fi[l], G.fo[l], g->dG[l - 1] + (size_t)c * B * G.fi[l],
                                      g->h[l - 1] + (size_t)c * B * G.fi[l], G.act[l - 1]));
         },
         [&](int l, std::vector<GemmProb>* ph) {
-          for (int c = 0; c < C; ++c) {
+          for (int c = cb; c < ce; ++c) {
             const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
             const size_t o = c * sG + G.off[l];
             ph->push_back(wgrad_adam_prob(x, B, G.fi[l], g->dG[l] + (size_t)c * B * G.fo[l], G.fo[l],
@@ -506,6 +555,7 @@ void build_tables(lipz_grid* g) {
           }
         },
         &ops);
+    }  // groups
 
     // ---- evaluation ----
     std::vector<int>& ev = g->eval_phases[par];
@@ -567,7 +617,7 @@ void build_tables(lipz_grid* g) {
   }
 }
 
-hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local) {
+hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t stream) {
   const Phase& ph = g->phases[phase];
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (g->timing) {
@@ -581,12 +631,12 @@ hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local) {
     g->ev_pool.pop_back();
     e0 = g->ev_pool.back();
     g->ev_pool.pop_back();
-    hipEventRecord(e0, g->stream);
+    hipEventRecord(e0, stream);
   }
   hipError_t e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.fast,
-                                     step_local, g->slope, g->ac, g->stream);
+                                     ph.wave, step_local, g->slope, g->ac, stream);
   if (g->timing) {
-    hipEventRecord(e1, g->stream);
+    hipEventRecord(e1, stream);
     g->ev_live.push_back({e0, e1});
     g->ev_flops.push_back(ph.flops);
   }
@@ -624,6 +674,7 @@ size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples) {
   g->D = Dn;
   g->tn = ceil_div(Dn.fi[Dn.nl - 1], GEMM_BN);
   g->nbr_h.assign((size_t)g->C * 5, 0);
+  setup_groups(g);
   size_t total = 0;
   carve(g, nullptr, &total);
   build_tables(g);
@@ -681,6 +732,7 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
       n[4] = r * Q + (q + 1) % Q;
     }
 
+  setup_groups(g);
   // The GEMM tables are carved last, so building them after the first carve
   // already sees the final buffer addresses; the second carve sizes them.
   size_t total = 0;
@@ -697,6 +749,12 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
   auto ck = [&](hipError_t e, const char* what) {
     if (st == LIPZ_OK) st = check_hip(g, e, what);
   };
+  g->gstream[0] = s;
+  ck(hipEventCreateWithFlags(&g->fork_ev, hipEventDisableTiming), "create event");
+  for (int i = 1; i < g->n_groups; ++i) {
+    ck(hipStreamCreateWithFlags(&g->gstream[i], hipStreamNonBlocking), "create stream");
+    ck(hipEventCreateWithFlags(&g->join_ev[i], hipEventDisableTiming), "create event");
+  }
   ck(hipMemcpyAsync(g->nbr, g->nbr_h.data(), g->nbr_h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s),
      "upload neighbours");
   ck(hipMemcpyAsync(g->probs_d, g->probs_h.data(), g->probs_h.size() * sizeof(GemmProb),
@@ -724,14 +782,12 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
     ck(launch_normals(g->P, (int64_t)g->xd * g->F, 1.0 / sqrt((double)g->xd), g->key, 0, 0, 0,
                       LIPZ_TAG_PROJ, s),
        "projection");
-    ck(run_gemm_phase(g, g->real_phase, 0), "project dataset");
+    ck(run_gemm_phase(g, g->real_phase, 0, s), "project dataset");
     ck(launch_col_stats(g->realfeat, g->N, g->F, g->mu_r, g->sd_r, s), "dataset feature stats");
   }
   ck(hipStreamSynchronize(s), "create sync");
   if (st != LIPZ_OK) {
-    std::string msg = g->last_err;
-    delete g;
-    (void)msg;
+    lipz_grid_destroy(g);
     return st;
   }
   *out = g;
@@ -740,6 +796,14 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
 
 lipz_status lipz_grid_destroy(lipz_grid* g) {
   if (!g) return LIPZ_E_INVAL;
+  for (int i = 1; i < g->n_groups; ++i) {
+    if (g->gstream[i]) {
+      hipStreamSynchronize(g->gstream[i]);
+      hipStreamDestroy(g->gstream[i]);
+    }
+    if (g->join_ev[i]) hipEventDestroy(g->join_ev[i]);
+  }
+  if (g->fork_ev) hipEventDestroy(g->fork_ev);
   for (auto& e : g->ev_pool) hipEventDestroy(e);
   for (auto& p : g->ev_live) {
     hipEventDestroy(p.first);
@@ -757,11 +821,11 @@ lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float
   hipStream_t s = g->stream;
   const int par = g->cur;
   const int C = g->C, B = g->B;
-  hipError_t e = launch_sample(g->data, g->N, g->xd, g->zd, B, C, g->key, (uint32_t)gen, 0, g->Xe,
+  hipError_t e = launch_sample(g->data, g->N, g->xd, g->zd, B, 0, C, g->key, (uint32_t)gen, 0, g->Xe,
                                (int64_t)6 * B * g->xd, g->ze, (int64_t)B * g->zd, s);
   if ((st = check_hip(g, e, "eval sample"))) return st;
   for (int ph : g->eval_phases[par])
-    if ((st = check_hip(g, run_gemm_phase(g, ph, 0), "eval forward"))) return st;
+    if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "eval forward"))) return st;
   EvalHeadArgs ha;
   ha.part = g->part_e;
   ha.tn = g->tn;
@@ -855,42 +919,57 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   hd.act = g->a[LD - 2];
   hd.act_cell_stride = (int64_t)2 * B * g->D.fi[LD - 1];
   hd.delta = g->dD[LD - 2];
-  hd.p = S.Dp;
-  hd.m = S.Dm;
-  hd.v = S.Dv;
+  hd.w = S.Dp + g->D.off[LD - 1];
   hd.p_stride = g->D.stride;
-  hd.head_off = g->D.off[LD - 1];
-  hd.lr = S.Dlr;
-  hd.t = S.Dt;
+  hd.dlbuf = g->dlbuf;
   hd.H = g->D.fi[LD - 1];
   hd.B = B;
+  hd.c0 = 0;
   hd.C = C;
   hd.hidden_act = g->D.act[LD - 2];
   hd.slope = g->slope;
-  hd.ac = g->ac;
   HeadArgs hg = hd;
   hg.part = g->part_g;
   hg.act = g->ag[LD - 2];
   hg.act_cell_stride = (int64_t)B * g->D.fi[LD - 1];
   hg.delta = g->dDg[LD - 2];
+  hg.dlbuf = nullptr;
+  // fork: every group stream waits for the work already on the caller's stream
+  if (g->n_groups > 1) {
+    if ((st = check_hip(g, hipEventRecord(g->fork_ev, s), "fork"))) return st;
+    for (int i = 1; i < g->n_groups; ++i)
+      if ((st = check_hip(g, hipStreamWaitEvent(g->gstream[i], g->fork_ev, 0), "fork"))) return st;
+  }
+  // enqueue step by step across the groups so every stream has work early
   for (int k = 0; k < n_steps; ++k) {
     const int step = step0 + k;
-    hd.step_local = hg.step_local = k;
-    hd.losses = hg.losses = d_losses ? d_losses + (size_t)k * C * 2 : nullptr;
-    for (const Op& op : g->train_ops[par]) {
-      hipError_t e = hipSuccess;
-      switch (op.kind) {
-        case OP_SAMPLE:
-          e = launch_sample(g->data, g->N, g->xd, g->zd, B, C, g->key, (uint32_t)gen,
-                            (uint32_t)(step + 1), g->Xtr, (int64_t)2 * B * g->xd, g->z,
-                            (int64_t)B * g->zd, s);
-          break;
-        case OP_GEMM: e = run_gemm_phase(g, op.phase, k); break;
-        case OP_HEAD_D: e = launch_head_d(hd, s); break;
-        case OP_HEAD_G: e = launch_head_g(hg, s); break;
+    for (int grp = 0; grp < g->n_groups; ++grp) {
+      const int c0 = g->group_c0[grp], nc = g->group_c0[grp + 1] - c0;
+      hipStream_t gs = g->gstream[grp];
+      HeadArgs gd = hd, gg = hg;
+      gd.c0 = gg.c0 = c0;
+      gd.C = gg.C = nc;
+      gd.losses = gg.losses = d_losses ? d_losses + (size_t)k * C * 2 : nullptr;
+      for (const Op& op : g->train_ops[par][grp]) {
+        hipError_t e = hipSuccess;
+        switch (op.kind) {
+          case OP_SAMPLE:
+            e = launch_sample(g->data, g->N, g->xd, g->zd, B, c0, nc, g->key, (uint32_t)gen,
+                              (uint32_t)(step + 1), g->Xtr, (int64_t)2 * B * g->xd, g->z,
+                              (int64_t)B * g->zd, gs);
+            break;
+          case OP_GEMM: e = run_gemm_phase(g, op.phase, k, gs); break;
+          case OP_HEAD_D: e = launch_head_d(gd, gs); break;
+          case OP_HEAD_G: e = launch_head_g(gg, gs); break;
+        }
+        if ((st = check_hip(g, e, "train step"))) return st;
       }
-      if ((st = check_hip(g, e, "train step"))) return st;
     }
+  }
+  // join: the caller's stream waits for every group
+  for (int i = 1; i < g->n_groups; ++i) {
+    if ((st = check_hip(g, hipEventRecord(g->join_ev[i], g->gstream[i]), "join"))) return st;
+    if ((st = check_hip(g, hipStreamWaitEvent(s, g->join_ev[i], 0), "join"))) return st;
   }
   hipError_t e = launch_add_i32(S.Gt, C, n_steps, s);
   if (e == hipSuccess) e = launch_add_i32(S.Dt, C, n_steps, s);
@@ -911,7 +990,7 @@ lipz_status lipz_mixture_update(lipz_grid* g, int32_t gen, float* d_w, float* d_
                                 LIPZ_TAG_MIXZ, s);
   if ((st = check_hip(g, e, "mixture latents"))) return st;
   for (int ph : g->mix_phases[par])
-    if ((st = check_hip(g, run_gemm_phase(g, ph, 0), "mixture forward"))) return st;
+    if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "mixture forward"))) return st;
   e = launch_moments(g->fm, g->C, g->S, g->F, g->mu_k, g->s2_k, s);
   if ((st = check_hip(g, e, "mixture moments"))) return st;
   EsArgs ea;

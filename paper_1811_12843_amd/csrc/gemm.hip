@@ -29,8 +29,32 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 
 namespace {
 
+#ifndef LIPZ_GEMM_STAGES
+#define LIPZ_GEMM_STAGES 2      // slices of A/B loads in flight per workgroup
+#endif
+#ifndef LIPZ_GEMM_WG32
+#define LIPZ_GEMM_WG32 4        // occupancy target of the fast kernel, 32-row tiles
+#endif
+#ifndef LIPZ_GEMM_WG64
+#define LIPZ_GEMM_WG64 2        // occupancy target of the fast kernel, 64-row tiles
+#endif
+#ifndef LIPZ_GEMM_TILE64_MIN
+#define LIPZ_GEMM_TILE64_MIN 100000  // phases with at least this many 64x64 tiles use 64-row tiles
+#endif
+
+#ifndef LIPZ_GEMM_BK
+#define LIPZ_GEMM_BK 32         // K depth of one LDS slice
+#endif
+#ifndef LIPZ_GEMM_WAVE_SPLIT
+#define LIPZ_GEMM_WAVE_SPLIT 1  // allow the wave-split (split-K in the workgroup) kernel
+#endif
+#ifndef LIPZ_GEMM_WAVE_MIN_K
+#define LIPZ_GEMM_WAVE_MIN_K 512  // ... for phases whose deepest problem has K >= this
+#endif
+
 constexpr int BN = GEMM_BN;
-constexpr int BK = 64;
+constexpr int BK = LIPZ_GEMM_BK;
+constexpr int KQ = BK / 4;    // float4 per row of a k-contiguous slice
 constexpr int NT = 256;
 constexpr int S_K = BK + 4;   // row stride of k-contiguous LDS tiles ([m][k], [n][k])
 
@@ -48,7 +72,7 @@ struct Tile {
   static constexpr int S_M = BM + 4;                        // row stride of [k][m] tiles
   static constexpr int S_N = BN + 4;                        // row stride of [k][n] tiles
   static constexpr int A_FLOATS = (BK * S_M > BM * S_K) ? BK * S_M : BM * S_K;
-  static constexpr int B_FLOATS = BK * S_N;                 // == BN * S_K
+  static constexpr int B_FLOATS = (BK * S_N > BN * S_K) ? BK * S_N : BN * S_K;
   static constexpr int A_VEC = BM * BK / 4 / NT;            // float4 of A per thread per slice
   static constexpr int B_VEC = BN * BK / 4 / NT;
   static constexpr int WM = BM / 2;                         // rows per wave
@@ -77,8 +101,8 @@ __device__ __forceinline__ void load_slices(const GemmProb& P, int m0, int n0, i
   for (int rep = 0; rep < T::A_VEC; ++rep) {
     const int q = tid + NT * rep;
     float4 v;
-    if (!P.a_trans) {  // [M][K]: row q / 16, k 4 (q % 16)
-      const int gm = m0 + (q >> 4), gk = k0 + ((q & 15) << 2);
+    if (!P.a_trans) {  // [M][K]: row q / KQ, k 4 (q % KQ)
+      const int gm = m0 + q / KQ, gk = k0 + ((q % KQ) << 2);
       if ((P.vec & 1) && gm < P.a_rows && gk + 3 < P.K) {
         v = ld4(gA + (size_t)gm * P.lda + gk);
       } else {
@@ -127,8 +151,8 @@ __device__ __forceinline__ void load_slices(const GemmProb& P, int m0, int n0, i
         v.z = (r && gn + 2 < P.N) ? s[gn + 2] : 0.f;
         v.w = (r && gn + 3 < P.N) ? s[gn + 3] : 0.f;
       }
-    } else {  // [N][K]: n q / 16, k 4 (q % 16)
-      const int gn = n0 + (q >> 4), gk = k0 + ((q & 15) << 2);
+    } else {  // [N][K]: n q / KQ, k 4 (q % KQ)
+      const int gn = n0 + q / KQ, gk = k0 + ((q % KQ) << 2);
       if ((P.vec & 2) && gn < P.N && gk + 3 < P.K) {
         v = ld4(gB + (size_t)gn * P.ldb + gk);
       } else {
@@ -153,7 +177,7 @@ __device__ __forceinline__ void store_slices(const GemmProb& P, int tid, const R
   for (int rep = 0; rep < T::A_VEC; ++rep) {
     const int q = tid + NT * rep;
     float* d;
-    if (!P.a_trans) d = As + (q >> 4) * S_K + ((q & 15) << 2);
+    if (!P.a_trans) d = As + (q / KQ) * S_K + ((q % KQ) << 2);
     else d = As + (q / (BM / 4)) * T::S_M + ((q % (BM / 4)) << 2);
     *reinterpret_cast<float4*>(d) = f.a[rep];
   }
@@ -162,7 +186,7 @@ __device__ __forceinline__ void store_slices(const GemmProb& P, int tid, const R
     const int q = tid + NT * rep;
     float* d;
     if (!P.b_trans) d = Bs + (q >> 4) * T::S_N + ((q & 15) << 2);
-    else d = Bs + (q >> 4) * S_K + ((q & 15) << 2);
+    else d = Bs + (q / KQ) * S_K + ((q % KQ) << 2);
     *reinterpret_cast<float4*>(d) = f.b[rep];
   }
 }
@@ -170,66 +194,118 @@ __device__ __forceinline__ void store_slices(const GemmProb& P, int tid, const R
 // Epilogue shared by both kernel variants: bias + activation (optionally
 // with the per-tile partial dot product of the next 1-wide layer), the
 // activation-derivative product, or the fused Adam update; then stores.
+// All of a lane's loads are issued before any of them is used, so their
+// latencies overlap (out-of-range elements read element 0 and are dropped).
 template <int BM>
 __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>::TI][2], int m0, int n0,
                                          int tile_n, int step_local, float slope, const AdamConsts& ac,
                                          float (*red)[BM]) {
   using T = Tile<BM>;
+  constexpr int NE = T::TI * 2 * 4;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = (wave >> 1) * T::WM, wn = (wave & 1) * 32;
   const int li = lane & 15, lg = lane >> 4;
-  float lr = 0.f, bc1 = 1.f, bc2 = 1.f;
-  if (P.epi == EPI_ADAM) {
-    lr = *as_global(P.lr);
-    const int tt = *as_global(P.t) + step_local + 1;
-    bc1 = (float)(1.0 - pow((double)ac.beta1, (double)tt));
-    bc2 = (float)(1.0 - pow((double)ac.beta2, (double)tt));
-  }
-  const bool dot = P.dot_out != nullptr;
   LIPZ_GLOBAL float* gC = as_global(P.C);
-  LIPZ_GLOBAL float* gM = as_global(P.m);
-  LIPZ_GLOBAL float* gV = as_global(P.v);
-  const LIPZ_GLOBAL float* gBias = as_global(P.bias);
-  const LIPZ_GLOBAL float* gAux = as_global(P.aux);
-  const LIPZ_GLOBAL float* gDotw = as_global(P.dotw);
+  uint32_t off[NE];
+  bool ok[NE];
+#pragma unroll
+  for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int e = (i * 2 + j) * 4 + r;
+        const int row = m0 + wm + 16 * i + 4 * lg + r;
+        const int col = n0 + wn + 16 * j + li;
+        ok[e] = row < P.M && col < P.N;
+        off[e] = ok[e] ? (uint32_t)(row * P.ldc + col) : 0u;
+      }
+  if (P.epi == EPI_ADAM) {
+    LIPZ_GLOBAL float* gM = as_global(P.m);
+    LIPZ_GLOBAL float* gV = as_global(P.v);
+    const float lr = *as_global(P.lr);
+    const int tt = *as_global(P.t) + step_local + 1;
+    const float bc1 = (float)(1.0 - pow((double)ac.beta1, (double)tt));
+    const float bc2 = (float)(1.0 - pow((double)ac.beta2, (double)tt));
+    float pp[NE], mm[NE], vv[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      pp[e] = gC[off[e]];
+      mm[e] = gM[off[e]];
+      vv[e] = gV[off[e]];
+    }
+#pragma unroll
+    for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = (i * 2 + j) * 4 + r;
+          const float g = acc[i][j][r];
+          const float m = ac.beta1 * mm[e] + ac.one_minus_beta1 * g;
+          const float v = ac.beta2 * vv[e] + ac.one_minus_beta2 * g * g;
+          const float p = pp[e] - lr * (m / bc1) / (sqrtf(v / bc2) + ac.eps);
+          if (ok[e]) {
+            gM[off[e]] = m;
+            gV[off[e]] = v;
+            gC[off[e]] = p;
+          }
+        }
+    return;
+  }
+  if (P.epi == EPI_DACT) {
+    const LIPZ_GLOBAL float* gAux = as_global(P.aux);
+    float ax[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e) ax[e] = gAux[off[e]];
+#pragma unroll
+    for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = (i * 2 + j) * 4 + r;
+          if (ok[e]) gC[off[e]] = acc[i][j][r] * act_deriv_from_out(P.act, ax[e], slope);
+        }
+    return;
+  }
+  if (P.epi != EPI_BIAS_ACT) {
+#pragma unroll
+    for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = (i * 2 + j) * 4 + r;
+          if (ok[e]) gC[off[e]] = acc[i][j][r];
+        }
+    return;
+  }
+  // bias + activation, optional partial dot product with the next layer's weights
+  const bool dot = P.dot_out != nullptr;
+  float bias[2] = {0.f, 0.f}, dw[2] = {0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int col = n0 + wn + 16 * j + li;
+    const int c = col < P.N ? col : 0;
+    if (P.bias) bias[j] = as_global(P.bias)[c];
+    if (dot) dw[j] = col < P.N ? as_global(P.dotw)[c] : 0.f;
+  }
 #pragma unroll
   for (int i = 0; i < T::TI; ++i) {
     float rowdot[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn + 16 * j + li;
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm + 16 * i + 4 * lg + r;
-        if (row >= P.M || col >= P.N) continue;
-        float x = acc[i][j][r];
-        const size_t o = (size_t)row * P.ldc + col;
-        switch (P.epi) {
-          case EPI_BIAS_ACT: {
-            if (P.bias) x += gBias[col];
-            const float y = act_fwd(P.act, x, slope);
-            gC[o] = y;
-            if (dot) rowdot[r] += y * gDotw[col];
-            break;
-          }
-          case EPI_DACT:
-            gC[o] = x * act_deriv_from_out(P.act, gAux[o], slope);
-            break;
-          case EPI_ADAM: {
-            const float m = ac.beta1 * gM[o] + ac.one_minus_beta1 * x;
-            const float v = ac.beta2 * gV[o] + ac.one_minus_beta2 * x * x;
-            gM[o] = m;
-            gV[o] = v;
-            const float mhat = m / bc1, vhat = v / bc2;
-            gC[o] = gC[o] - lr * mhat / (sqrtf(vhat) + ac.eps);
-            break;
-          }
-          default:
-            gC[o] = x;
+        const int e = (i * 2 + j) * 4 + r;
+        const float y = act_fwd(P.act, acc[i][j][r] + bias[j], slope);
+        if (ok[e]) {
+          gC[off[e]] = y;
+          rowdot[r] += y * dw[j];
         }
       }
-    }
     if (dot) {
       // sum over the 16 lanes that hold one row's columns, then over the two
       // column halves of the tile (waves wn = 0 and 32) in a fixed order
@@ -250,10 +326,10 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
   }
   if (dot) {
     __syncthreads();
-    const float bias = (tile_n == 0 && P.dot_bias) ? *as_global(P.dot_bias) : 0.f;
+    const float b = (tile_n == 0 && P.dot_bias) ? *as_global(P.dot_bias) : 0.f;
     for (int r = tid; r < BM; r += NT) {
       const int row = m0 + r;
-      if (row < P.M) as_global(P.dot_out)[(size_t)row * P.dot_ld + tile_n] = (red[0][r] + red[1][r]) + bias;
+      if (row < P.M) as_global(P.dot_out)[(size_t)row * P.dot_ld + tile_n] = (red[0][r] + red[1][r]) + b;
     }
   }
 }
@@ -380,7 +456,7 @@ __device__ __forceinline__ void fast_load(const GemmProb& P, __amdgpu_buffer_rsr
   for (int rep = 0; rep < T::A_VEC; ++rep) {
     const int q = tid + NT * rep;
     uint32_t off;
-    if (AT == 0) off = (uint32_t)((m0 + (q >> 4)) * P.lda + k0 + ((q & 15) << 2)) * 4u;
+    if (AT == 0) off = (uint32_t)((m0 + q / KQ) * P.lda + k0 + ((q % KQ) << 2)) * 4u;
     else off = (uint32_t)((k0 + q / (BM / 4)) * P.lda + m0 + ((q % (BM / 4)) << 2)) * 4u;
     f.a[rep] = bload4(ra, off);
   }
@@ -389,7 +465,7 @@ __device__ __forceinline__ void fast_load(const GemmProb& P, __amdgpu_buffer_rsr
     const int q = tid + NT * rep;
     uint32_t off;
     if (BT == 0) off = (uint32_t)((k0 + (q >> 4)) * P.ldb + n0 + ((q & 15) << 2)) * 4u;
-    else off = (uint32_t)((n0 + (q >> 4)) * P.ldb + k0 + ((q & 15) << 2)) * 4u;
+    else off = (uint32_t)((n0 + q / KQ) * P.ldb + k0 + ((q % KQ) << 2)) * 4u;
     f.b[rep] = bload4(rb, off);
   }
 }
@@ -406,12 +482,12 @@ __device__ __forceinline__ void fast_store(const GemmProb& P, int m0, int kvalid
     float4 v = f.a[rep];
     float* d;
     if (AT == 0) {
-      const int kq = (q & 15) << 2;
+      const int kq = (q % KQ) << 2;
       v.x = kq + 0 < kvalid ? v.x : 0.f;
       v.y = kq + 1 < kvalid ? v.y : 0.f;
       v.z = kq + 2 < kvalid ? v.z : 0.f;
       v.w = kq + 3 < kvalid ? v.w : 0.f;
-      d = As + (q >> 4) * S_K + kq;
+      d = As + (q / KQ) * S_K + kq;
     } else {
       const int kk = q / (BM / 4), mq = (q % (BM / 4)) << 2;
       const bool kok = kk < kvalid;
@@ -435,12 +511,12 @@ __device__ __forceinline__ void fast_store(const GemmProb& P, int m0, int kvalid
       if (kk >= kvalid) v = make_float4(0.f, 0.f, 0.f, 0.f);
       d = Bs + kk * T::S_N + ((q & 15) << 2);
     } else {
-      const int kq = (q & 15) << 2;
+      const int kq = (q % KQ) << 2;
       v.x = kq + 0 < kvalid ? v.x : 0.f;
       v.y = kq + 1 < kvalid ? v.y : 0.f;
       v.z = kq + 2 < kvalid ? v.z : 0.f;
       v.w = kq + 3 < kvalid ? v.w : 0.f;
-      d = Bs + (q >> 4) * S_K + kq;
+      d = Bs + (q / KQ) * S_K + kq;
     }
     *reinterpret_cast<float4*>(d) = v;
   }
@@ -494,9 +570,9 @@ __device__ __forceinline__ void mfma_frag(const Frag<BM>& F, v4f (&acc)[Tile<BM>
 }
 
 // One slice: write registers R (slice it) to LDS stage (as, bs), barrier,
-// start the loads of slice it + 2 into R, then the MFMAs of the slice with
+// start the loads of slice it + NS into R, then the MFMAs of the slice with
 // the LDS reads of k block kb + 1 issued ahead of the MFMAs of block kb.
-template <int BM, int AT, int BT>
+template <int BM, int AT, int BT, int NS>
 __device__ __forceinline__ void fast_slice(const GemmProb& P, __amdgpu_buffer_rsrc_t ra,
                                            __amdgpu_buffer_rsrc_t rb, int m0, int n0, int it, int n_it,
                                            FastRegs<BM, AT, BT>& R, float* as, float* bs,
@@ -508,7 +584,7 @@ __device__ __forceinline__ void fast_slice(const GemmProb& P, __amdgpu_buffer_rs
   const int li = lane & 15, lg = lane >> 4;
   fast_store<BM, AT, BT>(P, m0, P.K - it * BK, tid, R, as, bs);
   __syncthreads();
-  if (it + 2 < n_it) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, (it + 2) * BK, tid, R);
+  if (it + NS < n_it) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, (it + NS) * BK, tid, R);
   Frag<BM> F0, F1;
   read_frag<BM, AT, BT>(as, bs, 0, wm, wn, li, lg, F0);
 #pragma unroll
@@ -524,28 +600,34 @@ __device__ __forceinline__ void fast_slice(const GemmProb& P, __amdgpu_buffer_rs
   }
 }
 
+// K loop: NS register sets hold the loads of the next NS slices; the loop is
+// unrolled by NS so each set (and each of the two LDS stages) has a fixed
+// role and the compiler can count outstanding loads exactly.
 template <int BM, int AT, int BT>
 __device__ __forceinline__ void fast_mainloop(const GemmProb& P, int m0, int n0, float* As0,
                                               float* Bs0, v4f (&acc)[Tile<BM>::TI][2]) {
   using T = Tile<BM>;
+  constexpr int NS = LIPZ_GEMM_STAGES;
+  static_assert(NS % 2 == 0, "an even number of register stages maps onto the two LDS stages");
   const int tid = threadIdx.x;
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(P.A, P.a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(P.B, P.b_bytes);
-  FastRegs<BM, AT, BT> R0, R1;
+  FastRegs<BM, AT, BT> R[NS];
   const int n_it = (P.K + BK - 1) / BK;
-  fast_load<BM, AT, BT>(P, ra, rb, m0, n0, 0, tid, R0);
-  if (n_it > 1) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, BK, tid, R1);
-  // unrolled by two so that R0 / R1 and the LDS stages have fixed roles
-  for (int it = 0; it < n_it; it += 2) {
-    fast_slice<BM, AT, BT>(P, ra, rb, m0, n0, it, n_it, R0, As0, Bs0, acc);
-    if (it + 1 < n_it)
-      fast_slice<BM, AT, BT>(P, ra, rb, m0, n0, it + 1, n_it, R1, As0 + T::A_FLOATS,
-                             Bs0 + T::B_FLOATS, acc);
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < n_it) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, s * BK, tid, R[s]);
+  for (int it = 0; it < n_it; it += NS) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      if (it + s < n_it)
+        fast_slice<BM, AT, BT, NS>(P, ra, rb, m0, n0, it + s, n_it, R[s], As0 + (s & 1) * T::A_FLOATS,
+                                   Bs0 + (s & 1) * T::B_FLOATS, acc);
   }
 }
 
 template <int BM>
-__global__ __launch_bounds__(NT, 2) void gemm_fast_kernel(const GemmProb* __restrict__ probs,
+__global__ __launch_bounds__(NT, BM == 32 ? LIPZ_GEMM_WG32 : LIPZ_GEMM_WG64) void gemm_fast_kernel(const GemmProb* __restrict__ probs,
                                                           GemmGroups grp, int step_local, float slope,
                                                           AdamConsts ac) {
   using T = Tile<BM>;
@@ -576,9 +658,200 @@ __global__ __launch_bounds__(NT, 2) void gemm_fast_kernel(const GemmProb* __rest
   else fast_mainloop<BM, 0, 0>(P, m0, n0, As, Bs, acc);
   epilogue<BM>(P, acc, m0, n0, tile_n, step_local, slope, ac, red);
 }
+
+// ---------------------------------------------------------------------------
+// Wave-split variant: the four waves of a workgroup each compute the whole
+// BM x 64 tile over every fourth 16-deep k block (split-K inside the
+// workgroup).  Each wave streams its operands from global memory (L2)
+// straight into registers in the MFMA fragment layout, PD k blocks ahead of
+// its MFMAs, so the main loop has no LDS traffic and no barriers, and a
+// tile's dependent chain is a quarter of K.  No operand element is loaded
+// twice, exactly as with an LDS-shared tile.  At the end the four partial
+// tiles are summed through LDS in a fixed order and handed to the shared
+// epilogue.
+// ---------------------------------------------------------------------------
+#ifndef LIPZ_WAVE_PD
+#define LIPZ_WAVE_PD 2
+#endif
+
+template <int BM>
+struct WFrag {
+  float a[BM / 16][4];   // A rows 16 i + (l % 16), k = kb + 4 (l / 16) + s
+  float b[4][4];         // B cols 16 j + (l % 16), same k
+};
+
+template <int BM, int AT, int BT>
+__device__ __forceinline__ void wave_load(const GemmProb& P, __amdgpu_buffer_rsrc_t ra,
+                                          __amdgpu_buffer_rsrc_t rb, int m0, int n0, int kb, int li,
+                                          int lg, WFrag<BM>& F) {
+  const int k = kb + 4 * lg;
+#pragma unroll
+  for (int i = 0; i < BM / 16; ++i) {
+    const int m = m0 + 16 * i + li;
+    if (AT == 0) {
+      const float4 v = bload4(ra, (uint32_t)(m * P.lda + k) * 4u);
+      F.a[i][0] = v.x; F.a[i][1] = v.y; F.a[i][2] = v.z; F.a[i][3] = v.w;
+    } else {
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        F.a[i][s] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ra, (int)((uint32_t)((k + s) * P.lda + m) * 4u), 0, 0));
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int n = n0 + 16 * j + li;
+    if (BT == 1) {
+      const float4 v = bload4(rb, (uint32_t)(n * P.ldb + k) * 4u);
+      F.b[j][0] = v.x; F.b[j][1] = v.y; F.b[j][2] = v.z; F.b[j][3] = v.w;
+    } else {
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        F.b[j][s] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rb, (int)((uint32_t)((k + s) * P.ldb + n) * 4u), 0, 0));
+    }
+  }
+}
+
+// MFMAs of one k block.  TAIL: zero k >= K (the problem's last, partial
+// block).  ONES: the tile holds the bias row of a [K][M] operand: set row
+// ones_row to 1 (0 past K) and the other rows past a_rows to 0.
+template <int BM, bool TAIL, bool ONES>
+__device__ __forceinline__ void wave_mma(const GemmProb& P, int m0, int kb, int li, int lg, WFrag<BM>& F,
+                                         v4f (&acc)[BM / 16][4]) {
+  const int k = kb + 4 * lg;
+  if (TAIL) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const bool ok = k + s < P.K;
+#pragma unroll
+      for (int i = 0; i < BM / 16; ++i) F.a[i][s] = ok ? F.a[i][s] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) F.b[j][s] = ok ? F.b[j][s] : 0.f;
+    }
+  }
+  if (ONES) {
+#pragma unroll
+    for (int i = 0; i < BM / 16; ++i) {
+      const int m = m0 + 16 * i + li;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const float one = (TAIL && k + s >= P.K) ? 0.f : 1.f;
+        F.a[i][s] = m < P.a_rows ? F.a[i][s] : (m == P.ones_row ? one : 0.f);
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int i = 0; i < BM / 16; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(F.a[i][s], F.b[j][s], acc[i][j], 0, 0, 0);
+}
+
+template <int BM, int AT, int BT, bool ONES>
+__device__ __forceinline__ void wave_mainloop(const GemmProb& P, int m0, int n0, v4f (&acc)[BM / 16][4]) {
+  constexpr int PD = LIPZ_WAVE_PD;
+  // the wave index is uniform across the wave: keep it (and every k-block
+  // index and loop bound derived from it) in scalar registers
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int li = lane & 15, lg = lane >> 4;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(P.A, P.a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(P.B, P.b_bytes);
+  const int nkb = (P.K + 15) / 16;                          // k blocks of the problem
+  const int mine = nkb > wave ? (nkb - wave + 3) / 4 : 0;   // blocks wave, wave + 4, ...
+  WFrag<BM> F[PD];
+#pragma unroll
+  for (int p = 0; p < PD; ++p)
+    if (p < mine) wave_load<BM, AT, BT>(P, ra, rb, m0, n0, 16 * (wave + 4 * p), li, lg, F[p]);
+  // steady state: every block full, every prefetch needed, no branches on
+  // the loads, so the compiler can count outstanding loads exactly
+  int q = 0;
+  for (; q + 2 * PD <= mine; q += PD) {
+#pragma unroll
+    for (int p = 0; p < PD; ++p) {
+      wave_mma<BM, false, ONES>(P, m0, 16 * (wave + 4 * (q + p)), li, lg, F[p], acc);
+      wave_load<BM, AT, BT>(P, ra, rb, m0, n0, 16 * (wave + 4 * (q + p + PD)), li, lg, F[p]);
+    }
+  }
+  // drain: the last PD .. 2 PD - 1 blocks, the problem's partial block among them
+  for (; q < mine; q += PD) {
+#pragma unroll
+    for (int p = 0; p < PD; ++p) {
+      if (q + p < mine) {
+        const int kb = 16 * (wave + 4 * (q + p));
+        if (kb + 16 > P.K) wave_mma<BM, true, ONES>(P, m0, kb, li, lg, F[p], acc);
+        else wave_mma<BM, false, ONES>(P, m0, kb, li, lg, F[p], acc);
+        if (q + p + PD < mine)
+          wave_load<BM, AT, BT>(P, ra, rb, m0, n0, 16 * (wave + 4 * (q + p + PD)), li, lg, F[p]);
+      }
+    }
+  }
+}
+
+template <int BM>
+__global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(const GemmProb* __restrict__ probs,
+                                                          GemmGroups grp, int step_local, float slope,
+                                                          AdamConsts ac) {
+  using T = Tile<BM>;
+  constexpr int RS = BN + 4;  // row stride of the partial tiles in LDS
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  int gi = 0;
+#pragma unroll
+  for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
+    if (q < grp.n && t >= grp.first_tile[q]) gi = q;
+  const int rel = t - grp.first_tile[gi];
+  const int pi = grp.first_prob[gi] + rel / grp.tiles_per_prob[gi];
+  const int lt = rel % grp.tiles_per_prob[gi];
+  const GemmProb P = probs[pi];
+  const int tile_n = lt % P.tiles_n;
+  const int m0 = (lt / P.tiles_n) * BM;
+  const int n0 = tile_n * BN;
+
+  __shared__ __align__(16) float part[4][BM * RS];
+  __shared__ float red[2][BM];
+
+  v4f pacc[BM / 16][4];
+#pragma unroll
+  for (int i = 0; i < BM / 16; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) pacc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+  if (P.a_trans) {
+    if (m0 + BM > P.a_rows) wave_mainloop<BM, 1, 0, true>(P, m0, n0, pacc);
+    else wave_mainloop<BM, 1, 0, false>(P, m0, n0, pacc);
+  } else if (P.b_trans) {
+    wave_mainloop<BM, 0, 1, false>(P, m0, n0, pacc);
+  } else {
+    wave_mainloop<BM, 0, 0, false>(P, m0, n0, pacc);
+  }
+
+  // partial tiles to LDS (MFMA D layout: row 16 i + 4 (l / 16) + r, col 16 j + l % 16)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int li = lane & 15, lg = lane >> 4;
+  float* mine = part[wave];
+#pragma unroll
+  for (int i = 0; i < BM / 16; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) mine[(16 * i + 4 * lg + r) * RS + 16 * j + li] = pacc[i][j][r];
+  __syncthreads();
+  // each wave takes its quadrant of the tile in the layout the epilogue expects
+  const int wm = (wave >> 1) * T::WM, wn = (wave & 1) * 32;
+  v4f acc[T::TI][2];
+#pragma unroll
+  for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = (wm + 16 * i + 4 * lg + r) * RS + wn + 16 * j + li;
+        acc[i][j][r] = (part[0][o] + part[1][o]) + (part[2][o] + part[3][o]);
+      }
+  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, slope, ac, red);
+}
 }  // namespace
 
-int gemm_tile_rows(int tiles64) { return tiles64 < 512 ? 32 : 64; }
+int gemm_tile_rows(int tiles64) { return tiles64 < LIPZ_GEMM_TILE64_MIN ? 32 : 64; }
 
 void gemm_set_extents(GemmProb& p) {
   const uint64_t a = (uint64_t)(p.a_trans ? p.K : p.a_rows) * (uint64_t)p.lda * 4u;
@@ -594,12 +867,19 @@ bool gemm_fast_ok(const GemmProb& p) {
          p.b_bytes < 0x7FFFFFF0u;
 }
 
+bool gemm_wave_ok(int max_k) { return LIPZ_GEMM_WAVE_SPLIT && max_k >= LIPZ_GEMM_WAVE_MIN_K; }
+
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
-                               int tile_rows, bool fast, int step_local, float slope, AdamConsts ac,
-                               hipStream_t s) {
+                               int tile_rows, bool fast, bool wave, int step_local, float slope,
+                               AdamConsts ac, hipStream_t s) {
   if (grp.n <= 0 || total_tiles <= 0) return hipSuccess;
   const dim3 g(total_tiles), b(NT);
-  if (fast) {
+  if (fast && wave) {
+    if (tile_rows == 32)
+      hipLaunchKernelGGL(gemm_wave_kernel<32>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
+    else
+      hipLaunchKernelGGL(gemm_wave_kernel<64>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
+  } else if (fast) {
     if (tile_rows == 32)
       hipLaunchKernelGGL(gemm_fast_kernel<32>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
     else

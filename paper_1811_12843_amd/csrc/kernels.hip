@@ -75,10 +75,10 @@ __global__ void normals_kernel(float* out, int64_t n, double scale, uint2 key, u
 // stream (c, gen, sf, IDX) and copies it to X[c][b]; it also writes the
 // latent row z[c][b][:] from stream (c, gen, sf, Z), element b * zd + k.
 // ---------------------------------------------------------------------------
-__global__ void sample_kernel(const float* __restrict__ data, int64_t N, int xd, int zd,
+__global__ void sample_kernel(const float* __restrict__ data, int64_t N, int xd, int zd, int c0,
                               uint2 key, uint32_t gen, uint32_t sf, float* __restrict__ X,
                               int64_t x_cell_stride, float* __restrict__ Z, int64_t z_cell_stride) {
-  const int b = blockIdx.x, c = blockIdx.y;
+  const int b = blockIdx.x, c = c0 + blockIdx.y;
   const uint4 wi = stream_block(key, (uint32_t)(b >> 2), (uint32_t)c, gen, sf, LIPZ_TAG_IDX);
   const int64_t row = (int64_t)(((uint64_t)word_of(wi, b & 3) * (uint64_t)N) >> 32);
   const float* src = data + row * xd;
@@ -96,100 +96,80 @@ __global__ void sample_kernel(const float* __restrict__ data, int64_t N, int xd,
   }
 }
 
-// Logits of `rows` rows from the per-tile partial sums (bias included), in a
-// fixed order; also dL/da into dl[] and the loss sums.
-//   d_step: rows < B are real (target 1), the rest fake (target 0)
-//   else:   all rows fake, non-saturating generator target 1
-__device__ void head_logits_and_dl(const float* part, int tn, int rows, int B, bool d_step, float* dl,
-                                   float* red, float* loss_real, float* loss_fake, float* dl_sum) {
-  const float invB = 1.f / (float)B;
-  float lr_ = 0.f, lf = 0.f, ds = 0.f;
-  for (int r = threadIdx.x; r < rows; r += NT) {
-    float a = 0.f;
-    for (int t = 0; t < tn; ++t) a += part[(int64_t)r * tn + t];
-    float d;
-    if (d_step && r >= B) {
-      d = sigmoid_f(a) * invB;
-      lf += softplus_f(a);
-    } else {
-      d = (sigmoid_f(a) - 1.f) * invB;
-      lr_ += softplus_f(-a);
-    }
-    dl[r] = d;
-    ds += d;
-  }
-  *loss_real = block_sum(lr_, red);
-  *loss_fake = block_sum(lf, red);
-  *dl_sum = block_sum(ds, red);
+// ---------------------------------------------------------------------------
+// Output layer of D (H -> 1) for block (cell, 64-column block cb, 32-row
+// chunk rs).  Logits come from the per-tile partial sums (bias included):
+//   D step rows: B real (target 1) then B fake (target 0); G step: B fake
+//   rows with the non-saturating target 1.  dL/da = (sigmoid(a) - target) / B,
+//   delta[r][n] = dL/da_r * w_n * act'(act[r][n]) for the block's cells.
+// Block (cb 0, rs 0) also writes the loss (mean softplus(-a_real) + mean
+// softplus(a_fake), or mean softplus(-a_fake)).  In the D step, blocks with
+// cb 0 write dL/da into dlbuf[r][0] (columns 1..3 zero): the gradient of the
+// output layer, [act | 1]^T dL/da, and its Adam step run as a GEMM problem
+// of the next phase, so nothing here reads and writes w in one launch.
+// ---------------------------------------------------------------------------
+constexpr int HEAD_ROWS = 32;
+
+__device__ __forceinline__ float head_dl(float a, bool real_target, float invB) {
+  return (sigmoid_f(a) - (real_target ? 1.f : 0.f)) * invB;
 }
 
-// ---------------------------------------------------------------------------
-// Output layer of D (H -> 1) for block (cell, 64-column block cb):
-//   logits, BCE (D step: mean softplus(-a_real) + mean softplus(a_fake);
-//   G step: mean softplus(-a_fake)), dL/da = (sigmoid(a) - target) / B,
-//   delta[r][n] = dL/da_r * w_n * act'(act[r][n]) for the block's columns,
-//   and in the D step the gradient of w_n and Adam on the block's columns
-//   (the bias by block 0).  Each block owns its columns of w, so reading
-//   w_n for delta and then updating it cannot race with another block; the
-//   bias is not read here (it is inside the partial sums).
-// ---------------------------------------------------------------------------
 template <bool D_STEP>
 __global__ __launch_bounds__(NT) void head_kernel(HeadArgs A) {
-  extern __shared__ float dl[];
+  __shared__ float dl[HEAD_ROWS];
   __shared__ float red[4];
-  __shared__ float gpart[4][64];
-  const int c = blockIdx.x, cb = blockIdx.y;
+  const int c = A.c0 + blockIdx.x, cb = blockIdx.y, rs = blockIdx.z;
   const int rows = D_STEP ? 2 * A.B : A.B;
-  const int H = A.H;
-  float lreal, lfake, dsum;
-  head_logits_and_dl(A.part + (int64_t)c * rows * A.tn, A.tn, rows, A.B, D_STEP, dl, red, &lreal,
-                     &lfake, &dsum);
-  if (cb == 0 && threadIdx.x == 0 && A.losses) {
-    const float invB = 1.f / (float)A.B;
-    A.losses[c * 2 + (D_STEP ? 0 : 1)] = D_STEP ? lreal * invB + lfake * invB : lreal * invB;
-  }
-  __syncthreads();
-  float* p = A.p + c * A.p_stride + A.head_off;
-  const float* act = A.act + c * A.act_cell_stride;
-  float* delta = A.delta + c * A.act_cell_stride;
-  const int n = cb * 64 + (threadIdx.x & 63);
-  const int rg = threadIdx.x >> 6;
-  const bool valid = n < H;
-  const float w = valid ? p[n] : 0.f;
-  float g = 0.f;
-  if (valid) {
-    for (int r = rg; r < rows; r += 4) {
-      const int64_t o = (int64_t)r * H + n;
-      const float y = act[o];
-      delta[o] = dl[r] * w * act_deriv_from_out(A.hidden_act, y, A.slope);
-      g += y * dl[r];
+  const int r0 = rs * HEAD_ROWS;
+  const int nr = min(HEAD_ROWS, rows - r0);
+  const int tn = A.tn;
+  const float* part = A.part + (int64_t)c * rows * tn;
+  const float invB = 1.f / (float)A.B;
+  if ((int)threadIdx.x < nr) {
+    const int r = r0 + threadIdx.x;
+    float a = 0.f;
+    for (int t = 0; t < tn; ++t) a += part[(int64_t)r * tn + t];
+    const float d = head_dl(a, !D_STEP || r < A.B, invB);
+    dl[threadIdx.x] = d;
+    if (D_STEP && cb == 0) {
+      float* o = A.dlbuf + ((int64_t)c * rows + r) * 4;
+      o[0] = d;
+      o[1] = 0.f;
+      o[2] = 0.f;
+      o[3] = 0.f;
     }
   }
-  if (!D_STEP) return;
-  gpart[rg][threadIdx.x & 63] = g;
-  __syncthreads();
-  const int tt = A.t[c] + A.step_local + 1;
-  const float bc1 = (float)(1.0 - pow((double)A.ac.beta1, (double)tt));
-  const float bc2 = (float)(1.0 - pow((double)A.ac.beta2, (double)tt));
-  const float lr = A.lr[c];
-  float* m = A.m + c * A.p_stride + A.head_off;
-  float* v = A.v + c * A.p_stride + A.head_off;
-  int k = -1;
-  float gk = 0.f;
-  if (threadIdx.x < 64 && valid) {
-    k = n;
-    const int q = threadIdx.x;
-    gk = (gpart[0][q] + gpart[1][q]) + (gpart[2][q] + gpart[3][q]);
-  } else if (cb == 0 && threadIdx.x == 64) {
-    k = H;
-    gk = dsum;
+  if (cb == 0 && rs == 0) {
+    float lr_ = 0.f, lf = 0.f;
+    for (int r = threadIdx.x; r < rows; r += NT) {
+      float a = 0.f;
+      for (int t = 0; t < tn; ++t) a += part[(int64_t)r * tn + t];
+      if (D_STEP && r >= A.B) lf += softplus_f(a);
+      else lr_ += softplus_f(-a);
+    }
+    lr_ = block_sum(lr_, red);
+    lf = block_sum(lf, red);
+    if (threadIdx.x == 0 && A.losses)
+      A.losses[c * 2 + (D_STEP ? 0 : 1)] = D_STEP ? lr_ * invB + lf * invB : lr_ * invB;
   }
-  if (k >= 0) {
-    const float mm = A.ac.beta1 * m[k] + A.ac.one_minus_beta1 * gk;
-    const float vv = A.ac.beta2 * v[k] + A.ac.one_minus_beta2 * gk * gk;
-    m[k] = mm;
-    v[k] = vv;
-    p[k] = p[k] - lr * (mm / bc1) / (sqrtf(vv / bc2) + A.ac.eps);
+  __syncthreads();
+  const int H = A.H;
+  const int n = cb * 64 + (threadIdx.x & 63);
+  if (n >= H) return;
+  const int rg = threadIdx.x >> 6;
+  const float w = A.w[(int64_t)c * A.p_stride + n];
+  const float* act = A.act + c * A.act_cell_stride;
+  float* delta = A.delta + c * A.act_cell_stride;
+  float y[HEAD_ROWS / 4];
+#pragma unroll
+  for (int k = 0; k < HEAD_ROWS / 4; ++k) {
+    const int rr = rg + 4 * k;
+    y[k] = rr < nr ? act[(int64_t)(r0 + rr) * H + n] : 0.f;
+  }
+#pragma unroll
+  for (int k = 0; k < HEAD_ROWS / 4; ++k) {
+    const int rr = rg + 4 * k;
+    if (rr < nr) delta[(int64_t)(r0 + rr) * H + n] = dl[rr] * w * act_deriv_from_out(A.hidden_act, y[k], A.slope);
   }
 }
 
@@ -453,21 +433,21 @@ hipError_t launch_normals(float* out, int64_t n, double scale, uint2 key, uint32
                      gen, sf, tag);
   return hipGetLastError();
 }
-hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, int C, uint2 key,
+hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, int c0, int C, uint2 key,
                          uint32_t gen, uint32_t sf, float* X, int64_t x_cell_stride, float* Z,
                          int64_t z_cell_stride, hipStream_t s) {
-  hipLaunchKernelGGL(sample_kernel, dim3(B, C), dim3(NT), 0, s, data, N, xd, zd, key, gen, sf, X,
+  hipLaunchKernelGGL(sample_kernel, dim3(B, C), dim3(NT), 0, s, data, N, xd, zd, c0, key, gen, sf, X,
                      x_cell_stride, Z, z_cell_stride);
   return hipGetLastError();
 }
 hipError_t launch_head_d(const HeadArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(head_kernel<true>, dim3(a.C, (a.H + 63) / 64), dim3(NT), 2 * a.B * sizeof(float), s,
-                     a);
+  hipLaunchKernelGGL(head_kernel<true>, dim3(a.C, (a.H + 63) / 64, (2 * a.B + HEAD_ROWS - 1) / HEAD_ROWS),
+                     dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_head_g(const HeadArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(head_kernel<false>, dim3(a.C, (a.H + 63) / 64), dim3(NT), a.B * sizeof(float), s,
-                     a);
+  hipLaunchKernelGGL(head_kernel<false>, dim3(a.C, (a.H + 63) / 64, (a.B + HEAD_ROWS - 1) / HEAD_ROWS),
+                     dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s) {

@@ -163,11 +163,17 @@ bool gemm_fast_ok(const GemmProb& p);
 // Fill a_bytes / b_bytes from the problem's shape (0 if they do not fit 32 bits).
 void gemm_set_extents(GemmProb& p);
 
+// True when a phase whose deepest problem has K = max_k runs faster on the
+// wave-split kernel (each wave takes every fourth k block of the whole tile,
+// operands straight from L2 into registers) than on the LDS-staged kernel.
+bool gemm_wave_ok(int max_k);
+
 // Launch the grouped GEMM over the problems stored at d_probs (device),
-// covering `total_tiles` tiles of tile_rows x 64 outputs.
+// covering `total_tiles` tiles of tile_rows x 64 outputs.  fast: the
+// aligned kernels (else the generic one); wave: the wave-split kernel.
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
-                               int tile_rows, bool fast, int step_local, float slope, AdamConsts ac,
-                               hipStream_t s);
+                               int tile_rows, bool fast, bool wave, int step_local, float slope,
+                               AdamConsts ac, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Other kernels (kernels.hip)
@@ -185,7 +191,8 @@ hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_normals(float* out, int64_t n, double scale, uint2 key, uint32_t cell, uint32_t gen,
                           uint32_t step_field, uint32_t tag, hipStream_t s);
-hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, int C, uint2 key,
+// Cells c0 .. c0 + C - 1.
+hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, int c0, int C, uint2 key,
                          uint32_t gen, uint32_t step_field, float* X, int64_t x_cell_stride,
                          float* Z, int64_t z_cell_stride, hipStream_t s);
 
@@ -195,22 +202,17 @@ struct HeadArgs {
   const float* act;      // last hidden activations [C][rows][H] (cell stride act_cell_stride)
   int64_t act_cell_stride;
   float* delta;          // out: gradient w.r.t. the last hidden pre-activation, same layout
-  float* p;              // D parameter rows (current state), stride p_stride
-  float* m;
-  float* v;
+  const float* w;        // output-layer weights of cell 0; cell c at w + c * p_stride
   int64_t p_stride;
-  int64_t head_off;      // offset of the head weight vector w (H floats) then bias
-  const float* lr;       // [C]
-  const int32_t* t;      // [C]
-  float* losses;         // [C][2] slice for this step, or null
-  int H, B, C;
+  float* dlbuf;          // D step: out dL/da as [C][2B][4] (column 0), else null
+  float* losses;         // [cells][2] slice for this step, or null
+  int H, B;
+  int c0, C;             // the launch covers cells c0 .. c0 + C - 1
   int hidden_act;
   float slope;
-  AdamConsts ac;
-  int step_local;
 };
 // Discriminator step head: logits of 2B rows (B real then B fake), BCE, its
-// gradient into delta, Adam update of the head weights.
+// gradient dL/da into dlbuf and delta.
 hipError_t launch_head_d(const HeadArgs& a, hipStream_t s);
 // Generator step head: logits of B fake rows, non-saturating loss, delta.
 hipError_t launch_head_g(const HeadArgs& a, hipStream_t s);

@@ -65,7 +65,8 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
   grp.tiles_per_prob[0] = tiles;
   gemm_set_extents(p);
   if (hipMemcpy(d_desc, &p, sizeof(p), hipMemcpyHostToDevice) != hipSuccess) return LIPZ_E_HIP;
-  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, gemm_fast_ok(p), step_local, slope, ac,
+  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, gemm_fast_ok(p), gemm_wave_ok(K),
+                          step_local, slope, ac,
                           (hipStream_t)hip_stream) != hipSuccess)
     return LIPZ_E_HIP;
   return LIPZ_OK;

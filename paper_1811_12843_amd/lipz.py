@@ -9,7 +9,7 @@ import ctypes
 import os
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "liblipz.so")
+LIB_PATH = os.environ.get("LIPZ_LIBRARY") or os.path.join(_PKG, "liblipz.so")
 
 LIPZ_ABI_VERSION = 1
 LIPZ_MAX_HIDDEN = 4

@@ -87,8 +87,10 @@ def test_gemm_kernel_against_matmul():
     dev = "cuda"
     desc = torch.zeros(256, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream().cuda_stream
+    # (37, 52, 600) and (200, 256, 784) reach the wave-split kernel (K >= 512) with
+    # ragged M, N and K tails; (37, 53, 19) is unaligned and takes the generic kernel
     shapes = [(1, 1, 1), (64, 64, 16), (37, 53, 19), (129, 65, 33), (100, 256, 64), (200, 256, 784),
-              (257, 784, 100)]
+              (257, 784, 100), (37, 52, 600)]
     for (M, N, K), tile_rows in [(s, tr) for s in shapes for tr in (32, 64)]:
         for a_trans in (0, 1):
             for b_trans in (0, 1):
@@ -133,7 +135,8 @@ def test_gemm_weight_gradient_with_bias_row_and_adam():
     desc = torch.zeros(256, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream().cuda_stream
     for (rows, fi, fo), tile_rows in [(s, tr) for s in [(200, 784, 256), (100, 256, 784), (19, 37, 45),
-                                                        (64, 2, 64), (100, 64, 256)] for tr in (32, 64)]:
+                                                        (64, 2, 64), (100, 64, 256), (520, 72, 36)]
+                                      for tr in (32, 64)]:
         _print_case("wgrad_adam", rows=rows, fi=fi, fo=fo, tile_rows=tile_rows)
         X = g.normal(size=(rows, fi)).astype(np.float32)
         dY = (g.normal(size=(rows, fo)) * 1e-2).astype(np.float32)
