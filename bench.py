@@ -10,7 +10,9 @@ Prints one JSON line:
   pair_evals_per_s pairings evaluated per second by lipz_eval_neighborhoods
   mfma_frac        algorithmic GEMM FLOPs of a generation / time / fp32 MFMA peak
   roofline         the grouped-GEMM kernel: algorithmic FLOPs per launch over its
-                   average launch time (HIP events on the grid's stream)
+                   average launch time (HIP events stamped by each GEMM dispatch);
+                   traffic = HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE
+                   passes stored in profiles/ (null once the GEMM source changed)
   cpu_baseline     the oracle (fp64 NumPy) on this host's cores, on a bounded sample
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
@@ -48,6 +50,28 @@ def gemm_flops_per_generation(wl):
     if wl["mix_enable"]:
         mix = C * wl["mix_samples"] * (macs_g + wl["x_dim"] * wl["mix_feat_dim"])
     return 2.0 * ev, 2.0 * train, 2.0 * mix
+
+
+def gemm_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("gemm.hip", "lipz_internal.h"):
+        with open(os.path.join(ROOT, "paper_1811_12843_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def stored_gemm_traffic(workload):
+    """HBM bytes per grouped-GEMM launch from the FETCH_SIZE / WRITE_SIZE passes
+    recorded in profiles/, or None when the GEMM source changed since."""
+    path = os.path.join(ROOT, "profiles", f"gemm_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("gemm_source_sha256") != gemm_source_digest():
+        return None
+    return rec.get("traffic_bytes_per_launch")
 
 
 def cpu_baseline(wl, data, budget_s=20.0):
@@ -99,7 +123,19 @@ def main():
     ap.add_argument("--eval-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (calibrates HBM byte counters)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration * 1024 * 1024 // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n}), flush=True)
+        return
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU; the grid is not sharded across GPUs "
               "(--gpus must be 1)", file=sys.stderr)
@@ -165,9 +201,10 @@ def main():
         gen += 1
     torch.cuda.synchronize()
     inst_ms = 1e3 * (time.perf_counter() - t0) / args.steps
-    gemm_ms, launches, gemm_flops = L.lipz_gemm_timing(g)
+    gemm_ms, launches, gemm_flops, gemm_bytes = L.lipz_gemm_timing(g)
     L.lipz_set_gemm_timing(g, 0)
 
+    traffic = stored_gemm_traffic(args.workload)
     f_ev, f_tr, f_mix = gemm_flops_per_generation(wl)
     f_gen = f_ev + f_tr + f_mix
     avg_ms = gemm_ms / max(launches, 1)
@@ -196,9 +233,10 @@ def main():
         "eval_mfma_frac": f_ev / t_eval / FP32_MFMA_PEAK,
         "roofline": {"kernel": "gemm_grouped_kernel", "bound": "mfma", "achieved": achieved / 1e12,
                      "peak": FP32_MFMA_PEAK / 1e12, "unit": "TFLOP/s",
-                     "frac": achieved / FP32_MFMA_PEAK, "traffic": None,
+                     "frac": achieved / FP32_MFMA_PEAK, "traffic": traffic,
                      "launches": launches, "avg_launch_us": avg_ms * 1e3,
                      "flop_per_launch": gemm_flops / max(launches, 1),
+                     "algorithmic_bytes_per_launch": gemm_bytes / max(launches, 1),
                      "instrumented_ms_per_step": inst_ms},
     }
     if not args.no_cpu_baseline:

@@ -72,6 +72,7 @@ struct Phase {
   bool fast = true, wave = false;
   GemmGroups grp;
   double flops = 0.0;
+  double bytes = 0.0;  // algorithmic: each operand read once, each output written once
 };
 
 enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G };
@@ -137,8 +138,8 @@ struct lipz_grid {
   bool timing = false;
   std::vector<hipEvent_t> ev_pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_live;
-  std::vector<double> ev_flops;
-  double gemm_ms = 0.0, gemm_flops = 0.0;
+  std::vector<double> ev_flops, ev_bytes;
+  double gemm_ms = 0.0, gemm_flops = 0.0, gemm_bytes = 0.0;
   int64_t gemm_launches = 0;
 };
 
@@ -359,6 +360,17 @@ GemmProb wgrad_adam_prob(const float* x, int rows, int fi, const float* dy, int 
   return p;
 }
 
+double prob_bytes(const GemmProb& p) {
+  const double mn = (double)p.M * p.N;
+  double b = (double)p.a_rows * p.K + (double)p.K * p.N;  // operands
+  if (p.epi == EPI_ADAM) b += 6.0 * mn;                    // read p, m, v; write p, m, v
+  else b += mn;                                            // write C
+  if (p.epi == EPI_DACT) b += mn;                          // read the forward output
+  if (p.epi == EPI_BIAS_ACT && p.bias) b += p.N;
+  if (p.dot_out) b += (double)p.M * ((p.N + GEMM_BN - 1) / GEMM_BN) + p.N;
+  return 4.0 * b;
+}
+
 double prob_flops(const GemmProb& p) {
   const double rows = p.ones_row >= 0 ? (double)p.a_rows : (double)p.M;
   return 2.0 * rows * p.N * p.K;
@@ -395,6 +407,7 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
     }
     tiles += tpp;
     ph.flops += prob_flops(p);
+    ph.bytes += prob_bytes(p);
     g->probs_h.push_back(p);
   }
   ph.tiles = tiles;
@@ -631,14 +644,13 @@ hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t s
     g->ev_pool.pop_back();
     e0 = g->ev_pool.back();
     g->ev_pool.pop_back();
-    hipEventRecord(e0, stream);
   }
   hipError_t e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.fast,
-                                     ph.wave, step_local, g->slope, g->ac, stream);
+                                     ph.wave, step_local, g->slope, g->ac, stream, e0, e1);
   if (g->timing) {
-    hipEventRecord(e1, stream);
     g->ev_live.push_back({e0, e1});
     g->ev_flops.push_back(ph.flops);
+    g->ev_bytes.push_back(ph.bytes);
   }
   return e;
 }
@@ -1101,7 +1113,8 @@ lipz_status lipz_set_gemm_timing(lipz_grid* g, int32_t enable) {
   return LIPZ_OK;
 }
 
-lipz_status lipz_gemm_timing(lipz_grid* g, double* h_ms, int64_t* h_launches, double* h_flops) {
+lipz_status lipz_gemm_timing(lipz_grid* g, double* h_ms, int64_t* h_launches, double* h_flops,
+                             double* h_bytes) {
   if (!g) return LIPZ_E_INVAL;
   hipError_t e = hipStreamSynchronize(g->stream);
   if (e != hipSuccess) return check_hip(g, e, "timing sync");
@@ -1110,17 +1123,21 @@ lipz_status lipz_gemm_timing(lipz_grid* g, double* h_ms, int64_t* h_launches, do
     hipEventElapsedTime(&ms, g->ev_live[i].first, g->ev_live[i].second);
     g->gemm_ms += ms;
     g->gemm_flops += g->ev_flops[i];
+    g->gemm_bytes += g->ev_bytes[i];
     g->gemm_launches += 1;
     g->ev_pool.push_back(g->ev_live[i].first);
     g->ev_pool.push_back(g->ev_live[i].second);
   }
   g->ev_live.clear();
   g->ev_flops.clear();
+  g->ev_bytes.clear();
   if (h_ms) *h_ms = g->gemm_ms;
   if (h_launches) *h_launches = g->gemm_launches;
   if (h_flops) *h_flops = g->gemm_flops;
+  if (h_bytes) *h_bytes = g->gemm_bytes;
   g->gemm_ms = 0.0;
   g->gemm_flops = 0.0;
+  g->gemm_bytes = 0.0;
   g->gemm_launches = 0;
   return LIPZ_OK;
 }

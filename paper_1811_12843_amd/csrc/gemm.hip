@@ -2,25 +2,38 @@
 // epilogues.  One launch computes every (cell, slot) problem of one dependent
 // phase of a generation: each cell's networks are small (M = 100..600 rows,
 // K = 64..784), so they are only worth a GPU when all of them run side by side.
+// Problems of one launch are described in device memory (GemmProb) and grouped
+// by shape (GemmGroups, kernel arguments); blockIdx is remapped so that the
+// tiles of one problem land on one XCD and share its L2.
 //
 // Tiling: a 256-thread workgroup (4 wave64) owns a BM x 64 output tile
-// (BM = 64 or 32, chosen per phase so that small phases still spread over the
-// 256 CUs).  Wave w owns the (BM/2) x 32 block (w / 2, w % 2) as (BM/32) x 2
-// MFMA 16x16 accumulators.  K advances in 64-deep slices through a
-// double-buffered LDS ring: the global loads of slice k+1 are in flight while
-// the MFMAs of slice k run, one barrier per slice.
+// (BM = 32 or 64).  Three kernels share the tile and the epilogue:
 //
-// Each operand keeps its global layout in LDS (no transposing stores):
+// * gemm_fast_kernel (16-byte aligned operands): wave w owns the (BM/2) x 32
+//   block (w / 2, w % 2) as (BM/32) x 2 MFMA 16x16 accumulators.  K advances
+//   in BK-deep slices through an LDS ring: buffer loads (bounded by the
+//   operand's extent, so no branches on the edges) of the next slices are in
+//   registers while the MFMAs of the current one run, one barrier per slice.
+//   Each operand keeps its global layout in LDS (no transposing stores):
 //   k-contiguous operands (A row-major, B = W^T) are read as 4 consecutive k
 //   per lane with ds_read_b128; m/n-contiguous operands are read one k per
 //   MFMA.  Within a 16-deep k block, MFMA sub-step s of lane group g = l / 16
 //   uses k = 4 g + s for both operands, so the two layouts mix freely.  Row
 //   strides are padded to 4 (mod 16) floats, which puts the four lane groups
 //   of one read on disjoint LDS banks.
+// * gemm_wave_kernel (deep K): split-K across the four waves, no LDS in the
+//   main loop (described at its definition).
+// * gemm_generic_kernel: any alignment, per-element bounds checks.
+//
+// Epilogues: plain store; bias + activation (forward), optionally with the
+// tile's partial dot product against a 1-wide output layer; activation
+// derivative (input gradient); Adam on the weight gradient in registers.
 //
 // MFMA 16x16x4 f32 operand layout (wave64): lane l supplies A[l % 16][l / 16]
 // and B[l / 16][l % 16]; accumulator register r of lane l is
 // D[4 (l / 16) + r][l % 16].
+#include <hip/hip_ext.h>
+
 #include "lipz_internal.h"
 
 namespace lipz {
@@ -871,25 +884,23 @@ bool gemm_wave_ok(int max_k) { return LIPZ_GEMM_WAVE_SPLIT && max_k >= LIPZ_GEMM
 
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
                                int tile_rows, bool fast, bool wave, int step_local, float slope,
-                               AdamConsts ac, hipStream_t s) {
+                               AdamConsts ac, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (grp.n <= 0 || total_tiles <= 0) return hipSuccess;
   const dim3 g(total_tiles), b(NT);
+  // the events (may be null) are stamped by the kernel's own dispatch packet,
+  // so their difference is the kernel's execution time alone
+#define LIPZ_LAUNCH(K) hipExtLaunchKernelGGL(K, g, b, 0, s, ev_start, ev_stop, 0, d_probs, grp, step_local, slope, ac)
   if (fast && wave) {
-    if (tile_rows == 32)
-      hipLaunchKernelGGL(gemm_wave_kernel<32>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
-    else
-      hipLaunchKernelGGL(gemm_wave_kernel<64>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
+    if (tile_rows == 32) LIPZ_LAUNCH(gemm_wave_kernel<32>);
+    else LIPZ_LAUNCH(gemm_wave_kernel<64>);
   } else if (fast) {
-    if (tile_rows == 32)
-      hipLaunchKernelGGL(gemm_fast_kernel<32>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
-    else
-      hipLaunchKernelGGL(gemm_fast_kernel<64>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
+    if (tile_rows == 32) LIPZ_LAUNCH(gemm_fast_kernel<32>);
+    else LIPZ_LAUNCH(gemm_fast_kernel<64>);
   } else {
-    if (tile_rows == 32)
-      hipLaunchKernelGGL(gemm_generic_kernel<32>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
-    else
-      hipLaunchKernelGGL(gemm_generic_kernel<64>, g, b, 0, s, d_probs, grp, step_local, slope, ac);
+    if (tile_rows == 32) LIPZ_LAUNCH(gemm_generic_kernel<32>);
+    else LIPZ_LAUNCH(gemm_generic_kernel<64>);
   }
+#undef LIPZ_LAUNCH
   return hipGetLastError();
 }
 

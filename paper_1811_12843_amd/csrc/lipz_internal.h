@@ -171,9 +171,11 @@ bool gemm_wave_ok(int max_k);
 // Launch the grouped GEMM over the problems stored at d_probs (device),
 // covering `total_tiles` tiles of tile_rows x 64 outputs.  fast: the
 // aligned kernels (else the generic one); wave: the wave-split kernel.
+// ev_start / ev_stop (or null) are recorded around the kernel itself.
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
                                int tile_rows, bool fast, bool wave, int step_local, float slope,
-                               AdamConsts ac, hipStream_t s);
+                               AdamConsts ac, hipStream_t s, hipEvent_t ev_start = nullptr,
+                               hipEvent_t ev_stop = nullptr);
 
 // ---------------------------------------------------------------------------
 // Other kernels (kernels.hip)

@@ -95,7 +95,7 @@ _SIGS = {
     "lipz_last_error": (ctypes.c_char_p, [_vp]),
     "lipz_set_gemm_timing": (_i32, [_vp, _i32]),
     "lipz_gemm_timing": (_i32, [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64),
-                                ctypes.POINTER(ctypes.c_double)]),
+                                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     "lipz_test_gemm": (_i32, [_vp, _vp, _i32, _i32, _i32, _vp, _i32, _i32, _i32, _vp, _i32, _i32,
                               _vp, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                               _f32, _f32, _f32, _i32]),
@@ -234,10 +234,12 @@ def lipz_set_gemm_timing(g, enable):
 
 
 def lipz_gemm_timing(g):
-    ms, n, fl = ctypes.c_double(), _i64(), ctypes.c_double()
-    _check(load_library().lipz_gemm_timing(_p(g), ctypes.byref(ms), ctypes.byref(n), ctypes.byref(fl)),
+    """(milliseconds, launches, algorithmic FLOPs, algorithmic bytes) since the last call."""
+    ms, n, fl, by = ctypes.c_double(), _i64(), ctypes.c_double(), ctypes.c_double()
+    _check(load_library().lipz_gemm_timing(_p(g), ctypes.byref(ms), ctypes.byref(n), ctypes.byref(fl),
+                                           ctypes.byref(by)),
            "lipz_gemm_timing", g)
-    return ms.value, n.value, fl.value
+    return ms.value, n.value, fl.value, by.value
 
 
 def lipz_test_gemm(stream, d_desc, M, N, K, d_A, lda, a_trans, ones_row, d_B, ldb, b_trans, d_C, ldc,
