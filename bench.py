@@ -231,7 +231,7 @@ def main():
         "gemm_gflop_per_generation": f_gen / 1e9,
         "mfma_frac": f_gen / (ms_per_gen * 1e-3) / FP32_MFMA_PEAK,
         "eval_mfma_frac": f_ev / t_eval / FP32_MFMA_PEAK,
-        "roofline": {"kernel": "gemm_grouped_kernel", "bound": "mfma", "achieved": achieved / 1e12,
+        "roofline": {"kernel": "grouped GEMM (gemm_fast_kernel + gemm_wave_kernel)", "bound": "mfma", "achieved": achieved / 1e12,
                      "peak": FP32_MFMA_PEAK / 1e12, "unit": "TFLOP/s",
                      "frac": achieved / FP32_MFMA_PEAK, "traffic": traffic,
                      "launches": launches, "avg_launch_us": avg_ms * 1e3,
