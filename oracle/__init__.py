@@ -12,13 +12,15 @@ Modules
   rng      Philox4x32-10 and the uniform / normal / index draws made from it
   grid     toroidal grid and 5-cell von Neumann neighbourhoods
   mlp      MLP forward / manual backward in fp64, flat parameter layout, init
+  dcgan    DCGAN-style conv / transposed-conv / batch-norm networks, forward
+           and manual backward in fp64, flat parameter layout, init
   coevo    state, evaluation, fitness, tournament, replacement, mutation,
            training step (Adam), one generation
   mixture  the (1+1)-ES over the generator-mixture weights and its score
 
 Pinned by tests/test_oracle_*.py against: published Philox known-answer
 vectors and rocRAND's host Philox, hand-enumerated neighbourhoods, BCE closed
-forms, finite differences and torch CPU fp64 autograd, Adam closed forms and
+forms, finite differences, torch CPU fp64 convolutions, batch norm and autograd, Adam closed forms and
 torch.optim.Adam, brute-force tournament enumeration, the 1x1-grid reduction
 to plain alternating GAN training, and Frechet-distance closed forms.
 """

@@ -32,19 +32,57 @@ Readings where the paper is silent (each is a workload field):
 import numpy as np
 from scipy.special import expit
 
-from . import grid, mlp, rng
+from . import dcgan, grid, mlp, rng
 
 
 def softplus(x):
     return np.logaddexp(0.0, x)
 
 
+class MlpNet:
+    """One role's fully connected network (module ``mlp``)."""
+
+    def __init__(self, role, sizes, acts, slope):
+        self.role, self.sizes, self.acts, self.slope = role, sizes, acts, slope
+        self.P = mlp.layout(sizes)[1]
+
+    def init(self, seed, cell, tag):
+        return mlp.init(self.sizes, seed, cell, tag)
+
+    def forward(self, p, x):
+        """(cache, out): out = G's samples [N, x_dim] or D's logits [N]."""
+        pre, post = mlp.forward(p, self.sizes, self.acts, x, self.slope)
+        return (pre, post), (post[-1] if self.role == "G" else post[-1][:, 0])
+
+    def backward(self, p, cache, d_out, want_input_grad=False):
+        d = d_out if self.role == "G" else d_out[:, None]
+        return mlp.backward(p, self.sizes, self.acts, cache[0], cache[1], d, self.slope,
+                            want_input_grad)
+
+
+class ConvNet:
+    """One role's DCGAN-style network (module ``dcgan``)."""
+
+    def __init__(self, role, wl):
+        self.arch = dcgan.Arch(role, wl["z_dim"], tuple(wl["img"]), wl["g_hidden"], wl["d_hidden"])
+        self.role, self.slope, self.P = role, wl["lrelu_slope"], self.arch.P
+
+    def init(self, seed, cell, tag):
+        return dcgan.init(self.arch, seed, cell, tag)
+
+    def forward(self, p, x):
+        return dcgan.forward(self.arch, p, x, self.slope)
+
+    def backward(self, p, cache, d_out, want_input_grad=False):
+        return dcgan.backward(self.arch, p, cache, d_out, self.slope, want_input_grad)
+
+
 class Setup:
     """Static description derived from a workload dict and the dataset."""
 
     def __init__(self, wl, n_samples):
-        if wl["net"] != "mlp":
-            raise NotImplementedError("oracle: only the MLP networks are implemented")
+        if wl["net"] not in ("mlp", "dcgan"):
+            raise ValueError(f"unknown network kind {wl['net']!r}")
         self.wl = wl
         self.rows, self.cols = wl["rows"], wl["cols"]
         self.C = self.rows * self.cols
@@ -58,8 +96,14 @@ class Setup:
         self.slope = wl["lrelu_slope"]
         self.seed = wl["seed"]
         self.N = int(n_samples)
-        self.PG = mlp.layout(self.g_sizes)[1]
-        self.PD = mlp.layout(self.d_sizes)[1]
+        if wl["net"] == "mlp":
+            self.Gnet = MlpNet("G", self.g_sizes, self.g_acts, self.slope)
+            self.Dnet = MlpNet("D", self.d_sizes, self.d_acts, self.slope)
+        else:
+            if wl["mix_enable"]:
+                raise ValueError("the mixture step is defined for the MLP workloads only")
+            self.Gnet, self.Dnet = ConvNet("G", wl), ConvNet("D", wl)
+        self.PG, self.PD = self.Gnet.P, self.Dnet.P
 
 
 class State:
@@ -78,8 +122,8 @@ class State:
 def create(S):
     """Step 1: random initial individuals, zero Adam state, initial learning rates, w = 1/5."""
     wl = S.wl
-    Gp = np.stack([mlp.init(S.g_sizes, S.seed, c, "INIT_G") for c in range(S.C)])
-    Dp = np.stack([mlp.init(S.d_sizes, S.seed, c, "INIT_D") for c in range(S.C)])
+    Gp = np.stack([S.Gnet.init(S.seed, c, "INIT_G") for c in range(S.C)])
+    Dp = np.stack([S.Dnet.init(S.seed, c, "INIT_D") for c in range(S.C)])
     return State(Gp=Gp, Gm=np.zeros_like(Gp), Gv=np.zeros_like(Gp),
                  Gt=np.zeros(S.C, dtype=np.int64), Glr=np.full(S.C, float(wl["lr0_g"])),
                  Dp=Dp, Dm=np.zeros_like(Dp), Dv=np.zeros_like(Dp),
@@ -95,12 +139,13 @@ def sample(S, data, cell, gen, step_field):
 
 
 def g_forward(S, p, z):
-    return mlp.forward(p, S.g_sizes, S.g_acts, z, S.slope)
+    """(cache, G(z)) with G(z) [N, x_dim]."""
+    return S.Gnet.forward(p, z)
 
 
 def d_logits(S, p, x):
-    pre, post = mlp.forward(p, S.d_sizes, S.d_acts, x, S.slope)
-    return pre, post, post[-1][:, 0]
+    """(cache, logits [N])."""
+    return S.Dnet.forward(p, x)
 
 
 def evaluate(S, st, data, gen):
@@ -114,12 +159,12 @@ def evaluate(S, st, data, gen):
     Lg = np.zeros((C, 5, 5))
     for c in range(C):
         _, x, z = sample(S, data, c, gen, 0)
-        fakes = [g_forward(S, st.Gp[S.nbr[c, i]], z)[1][-1] for i in range(5)]
+        fakes = [g_forward(S, st.Gp[S.nbr[c, i]], z)[1] for i in range(5)]
         for j in range(5):
             dp = st.Dp[S.nbr[c, j]]
-            real_term = softplus(-d_logits(S, dp, x)[2]).mean()
+            real_term = softplus(-d_logits(S, dp, x)[1]).mean()
             for i in range(5):
-                a_f = d_logits(S, dp, fakes[i])[2]
+                a_f = d_logits(S, dp, fakes[i])[1]
                 L[c, i, j] = real_term + softplus(a_f).mean()
                 Lg[c, i, j] = softplus(-a_f).mean()
     fit_d = L.mean(axis=1)
@@ -207,23 +252,19 @@ def train_step(S, st, data, gen, step):
     losses = np.zeros((S.C, 2))
     for c in range(S.C):
         _, x, z = sample(S, data, c, gen, step + 1)
-        gpre, gpost = g_forward(S, st.Gp[c], z)
-        xf = gpost[-1]
+        gcache, xf = g_forward(S, st.Gp[c], z)
         # discriminator step on real and detached fake
-        pre_r, post_r, a_r = d_logits(S, st.Dp[c], x)
-        pre_f, post_f, a_f = d_logits(S, st.Dp[c], xf)
+        cache_r, a_r = d_logits(S, st.Dp[c], x)
+        cache_f, a_f = d_logits(S, st.Dp[c], xf)
         losses[c, 0] = softplus(-a_r).mean() + softplus(a_f).mean()
-        g_r, _ = mlp.backward(st.Dp[c], S.d_sizes, S.d_acts, pre_r, post_r,
-                              ((expit(a_r) - 1.0) / B)[:, None], S.slope)
-        g_f, _ = mlp.backward(st.Dp[c], S.d_sizes, S.d_acts, pre_f, post_f,
-                              (expit(a_f) / B)[:, None], S.slope)
+        g_r, _ = S.Dnet.backward(st.Dp[c], cache_r, (expit(a_r) - 1.0) / B)
+        g_f, _ = S.Dnet.backward(st.Dp[c], cache_f, expit(a_f) / B)
         st.Dt[c] = adam(S, st.Dp[c], st.Dm[c], st.Dv[c], st.Dt[c], st.Dlr[c], g_r + g_f)
         # generator step (non-saturating) against the updated discriminator, same z
-        pre2, post2, a2 = d_logits(S, st.Dp[c], xf)
+        cache2, a2 = d_logits(S, st.Dp[c], xf)
         losses[c, 1] = softplus(-a2).mean()
-        _, dxf = mlp.backward(st.Dp[c], S.d_sizes, S.d_acts, pre2, post2,
-                              ((expit(a2) - 1.0) / B)[:, None], S.slope, want_input_grad=True)
-        gG, _ = mlp.backward(st.Gp[c], S.g_sizes, S.g_acts, gpre, gpost, dxf, S.slope)
+        _, dxf = S.Dnet.backward(st.Dp[c], cache2, (expit(a2) - 1.0) / B, want_input_grad=True)
+        gG, _ = S.Gnet.backward(st.Gp[c], gcache, dxf)
         st.Gt[c] = adam(S, st.Gp[c], st.Gm[c], st.Gv[c], st.Gt[c], st.Glr[c], gG)
     return losses
 

@@ -18,7 +18,7 @@ rejected if the sum is 0; accepted iff score(w') < score(w).
 """
 import numpy as np
 
-from . import mlp, rng
+from . import rng
 
 
 def projection(S):
@@ -42,7 +42,7 @@ def generator_moments(S, st, P, gen):
     mu = np.zeros((S.C, P.shape[1]))
     s2 = np.zeros((S.C, P.shape[1]))
     for k in range(S.C):
-        out = mlp.forward(st.Gp[k], S.g_sizes, S.g_acts, zeta, S.slope)[1][-1]
+        out = S.Gnet.forward(st.Gp[k], zeta)[1]
         f = out @ P
         mu[k] = f.mean(axis=0)
         s2[k] = (f * f).mean(axis=0)

@@ -82,5 +82,6 @@ def make_dataset(recipe):
     if kind == "mnist_like":
         return mnist_like(n, seed)
     if kind == "celeba_like":
-        return celeba_like(n, seed)
+        return celeba_like(n, seed, h=int(recipe.get("h", 64)), w=int(recipe.get("w", 64)),
+                           c=int(recipe.get("c", 3)))
     raise ValueError(f"unknown dataset kind {kind!r}")
