@@ -92,11 +92,26 @@ enum {
 typedef struct {
   int32_t abi_version;
   int32_t rows, cols;               /* toroidal grid; cells = rows * cols, cell id = r * cols + c */
-  int32_t net;                      /* LIPZ_NET_MLP (LIPZ_NET_DCGAN: LIPZ_E_UNSUPPORTED) */
+  int32_t net;                      /* LIPZ_NET_MLP or LIPZ_NET_DCGAN (see below) */
   int32_t z_dim, x_dim;             /* latent width, flat sample width */
   int32_t img_h, img_w, img_c;      /* DCGAN only; 0 for MLP */
   int32_t n_g_hidden, g_hidden[LIPZ_MAX_HIDDEN];  /* G: z_dim -> g_hidden... -> x_dim */
   int32_t n_d_hidden, d_hidden[LIPZ_MAX_HIDDEN];  /* D: x_dim -> d_hidden... -> 1 (logit) */
+  /* LIPZ_NET_DCGAN (Section 4's CelebA network): n = n_g_hidden = n_d_hidden
+   * stride-2 stages, square NHWC images of side img_h = img_w = 4 * 2^n,
+   * x_dim = img_h * img_w * img_c; g_hidden / d_hidden are channel widths
+   * (multiples of 4, at most 1024).
+   *   G: dense z -> 4x4 x g_hidden[0] (no bias), batch norm, g_hidden_act;
+   *      n - 1 x [4x4 transposed conv, stride 2, pad 1 (no bias), batch
+   *      norm, g_hidden_act]; 4x4 transposed conv to img_c + bias, g_out_act.
+   *   D: n x [4x4 conv, stride 2, pad 1 + bias, d_hidden_act]; dense over
+   *      the 4x4 x d_hidden[n-1] map to 1 logit + bias.
+   * Batch norm uses the statistics of the batch it normalises (biased
+   * variance, eps 1e-5).  Parameter row of a layer: the weight block
+   * [(taps * c_in)][c_out] with rows (kh, kw, c_in) (taps = 16; 1 for the
+   * dense layers), the bias [c_out] if any, then gamma and beta [c_out].
+   * Init: weights N(0, 0.02^2), gamma N(1, 0.02^2), biases and betas 0.
+   * mix_enable must be 0. */
   int32_t g_hidden_act, g_out_act, d_hidden_act;  /* LIPZ_ACT_* */
   float lrelu_slope;
   int32_t batch;                    /* minibatch rows for evaluation and training */
@@ -194,7 +209,9 @@ lipz_status lipz_get_neighbors(const lipz_grid* g, int32_t* h_nbr);
 /* Parameter layout of one role's network: *h_n = number of layers; for
  * layer l, h_offsets[3l + 0] = float offset of W_l in the cell's parameter
  * row, [3l + 1] = fan_in, [3l + 2] = fan_out.  W_l is [fan_in][fan_out]
- * row-major and its bias [fan_out] follows it directly.  h_offsets may be
+ * row-major and its bias [fan_out] follows it directly (DCGAN: fan_in =
+ * taps * c_in, and a layer without bias is followed by its batch-norm gamma
+ * and beta instead).  h_offsets may be
  * NULL to query *h_n; it must hold 3 * (LIPZ_MAX_HIDDEN + 1) entries. */
 lipz_status lipz_param_layout(const lipz_grid* g, int32_t role, int64_t* h_offsets, int32_t* h_n);
 

@@ -38,6 +38,19 @@ lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M, int32_t N,
                            const int32_t* d_t, int32_t step_local, float beta1, float beta2,
                            float eps, int32_t tile_rows);
 
+/*
+ * Host-only check of a configuration's launch plan (no GPU, no device
+ * memory): the library lays the plan out over placeholder addresses and
+ * recomputes, for every GEMM, convolution, batch-norm, reduction and dot
+ * descriptor, the first and last element each kernel can read or write,
+ * using the kernels' own index formulas.  *n_bad = the number of accesses
+ * that fall outside the workspace or the dataset; msg (msg_len bytes,
+ * NUL-terminated, may be NULL) names the first of them.  LIPZ_E_INVAL for an
+ * invalid configuration.
+ */
+lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, char* msg, int32_t msg_len,
+                                  int32_t* n_bad);
+
 #ifdef __cplusplus
 }
 #endif

@@ -14,136 +14,12 @@
 #include <string>
 #include <vector>
 
-#include "lipz_internal.h"
+#include "grid.h"
+#include "lipz_testing.h"
 
 using namespace lipz;
 
-namespace {
-
-constexpr size_t kAlign = 256;
-#define LIPZ_MAX_GROUPS 4
-#ifndef LIPZ_CELL_GROUPS
-#define LIPZ_CELL_GROUPS 0  // 0: choose from the grid size
-#endif
-
-size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
-
-// Bump allocator over the caller's workspace.  With base == nullptr it only
-// measures, so sizing and carving share one code path.
-struct Carver {
-  char* base;
-  size_t off = 0;
-  template <class T>
-  T* take(size_t count) {
-    off = align_up(off, kAlign);
-    T* p = reinterpret_cast<T*>(base + off);
-    off += count * sizeof(T);
-    return p;
-  }
-};
-
-struct Net {
-  int nl = 0;            // layers, the last one is the output layer
-  int64_t off[LIPZ_MAX_HIDDEN + 1];
-  int fi[LIPZ_MAX_HIDDEN + 1], fo[LIPZ_MAX_HIDDEN + 1];
-  int act[LIPZ_MAX_HIDDEN + 1];
-  int64_t P = 0, stride = 0;
-  NetLayers layers() const {
-    NetLayers L{};
-    L.n = nl;
-    for (int l = 0; l < nl; ++l) {
-      L.off[l] = off[l];
-      L.fan_in[l] = fi[l];
-      L.fan_out[l] = fo[l];
-    }
-    return L;
-  }
-};
-
-struct StateBuf {
-  char* base;
-  float *Gp, *Gm, *Gv, *Dp, *Dm, *Dv;
-  int32_t *Gt, *Dt;
-  float *Glr, *Dlr, *w;
-};
-
-struct Phase {
-  int first = 0, count = 0, tiles = 0, tile_rows = 64;
-  bool fast = true, wave = false;
-  GemmGroups grp;
-  double flops = 0.0;
-  double bytes = 0.0;  // algorithmic: each operand read once, each output written once
-};
-
-enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G };
-struct Op {
-  OpKind kind;
-  int phase;
-};
-
-}  // namespace
-
-struct lipz_grid {
-  lipz_config cfg;
-  int C = 0, B = 0, zd = 0, xd = 0, S = 0, F = 0;
-  Net G, D;
-  hipStream_t stream = nullptr;
-  const float* data = nullptr;
-  int64_t N = 0;
-  uint2 key;
-  float slope = 0.f;
-  AdamConsts ac;
-
-  StateBuf st[2];
-  int cur = 0;
-  size_t state_bytes = 0;
-  int64_t state_off[12];
-  std::vector<int32_t> nbr_h;
-
-  int32_t *nbr = nullptr, *sel = nullptr, *flags = nullptr;
-  float *L = nullptr, *Lg = nullptr, *fit_g = nullptr, *fit_d = nullptr;
-  // training buffers
-  float *z = nullptr, *Xtr = nullptr;
-  float *h[LIPZ_MAX_HIDDEN] = {}, *a[LIPZ_MAX_HIDDEN] = {}, *dD[LIPZ_MAX_HIDDEN] = {};
-  float *ag[LIPZ_MAX_HIDDEN] = {}, *dDg[LIPZ_MAX_HIDDEN] = {}, *dG[LIPZ_MAX_HIDDEN + 1] = {};
-  float *part_tr = nullptr, *part_g = nullptr, *part_e = nullptr;  // partial logits
-  float* dlbuf = nullptr;  // D-step dL/d(logit) [C][2B][4]
-  int tn = 1;  // column tiles of D's last hidden layer
-  // evaluation buffers
-  float *ze = nullptr, *Xe = nullptr;
-  float *he[LIPZ_MAX_HIDDEN] = {}, *ae[LIPZ_MAX_HIDDEN] = {};
-  // mixture buffers
-  float *zeta = nullptr, *xm = nullptr, *fm = nullptr, *mu_k = nullptr, *s2_k = nullptr;
-  float *hm[LIPZ_MAX_HIDDEN] = {};
-  float *P = nullptr, *mu_r = nullptr, *sd_r = nullptr, *realfeat = nullptr;
-
-  GemmProb* probs_d = nullptr;
-  std::vector<GemmProb> probs_h;
-  std::vector<Phase> phases;
-  // Cells are split into groups whose training phases run on separate
-  // streams (group 0 on the caller's stream), so that one group's
-  // latency-bound launches overlap another group's work.
-  int n_groups = 1;
-  int group_c0[LIPZ_MAX_GROUPS + 1] = {};
-  hipStream_t gstream[LIPZ_MAX_GROUPS] = {};
-  hipEvent_t fork_ev = nullptr, join_ev[LIPZ_MAX_GROUPS] = {};
-  std::vector<Op> train_ops[2][LIPZ_MAX_GROUPS];
-  std::vector<int> eval_phases[2], mix_phases[2];
-  int real_phase = -1;
-
-  bool fitness_valid = false;
-  lipz_status sticky = LIPZ_OK;
-  std::string last_err;
-
-  bool timing = false;
-  std::vector<hipEvent_t> ev_pool;
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_live;
-  std::vector<double> ev_flops, ev_bytes;
-  double gemm_ms = 0.0, gemm_flops = 0.0, gemm_bytes = 0.0;
-  int64_t gemm_launches = 0;
-};
-
-namespace {
+namespace lipz {
 
 lipz_status fail(lipz_grid* g, lipz_status s, const std::string& msg) {
   if (g) g->last_err = msg;
@@ -163,7 +39,7 @@ bool valid_act(int a) { return a >= LIPZ_ACT_LINEAR && a <= LIPZ_ACT_TANH; }
 std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) {
   if (!c) return "null config";
   if (c->abi_version != LIPZ_ABI_VERSION) return "abi_version mismatch";
-  if (c->net != LIPZ_NET_MLP) return "only LIPZ_NET_MLP is implemented";
+  if (c->net != LIPZ_NET_MLP && c->net != LIPZ_NET_DCGAN) return "unknown net";
   if (c->rows < 1 || c->cols < 1 || (int64_t)c->rows * c->cols > 4096) return "grid size out of range";
   if (c->z_dim < 1 || c->x_dim < 1 || c->z_dim > 65536 || c->x_dim > (1 << 20)) return "bad z_dim / x_dim";
   if (c->batch < 1 || c->batch > 2048) return "batch must be in [1, 2048]";
@@ -189,6 +65,7 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
     if (!(c->mix_sigma >= 0.f)) return "bad mix_sigma";
   }
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31) - 1) return "n_samples must be in [1, 2^31)";
+  if (c->net == LIPZ_NET_DCGAN) return dc_validate(c, Gn, Dn);
   auto build = [](Net* n, int in, int nh, const int32_t* hid, int out, int hact, int oact) {
     int64_t off = 0;
     n->nl = nh + 1;
@@ -207,12 +84,10 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
   return "";
 }
 
-// Carve every buffer; with base == nullptr only the size is computed.
-void carve(lipz_grid* g, char* base, size_t* total) {
-  Carver cv{base};
-  const int C = g->C, B = g->B, zd = g->zd, xd = g->xd;
+// The two state buffers in the documented blob layout.
+void carve_state(lipz_grid* g, Carver& cv, char* base) {
+  const int C = g->C;
   const Net &G = g->G, &D = g->D;
-  // two state buffers in the documented blob layout
   for (int b = 0; b < 2; ++b) {
     StateBuf sb;
     const size_t start = align_up(cv.off, kAlign);
@@ -244,6 +119,29 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     so[11] = (int64_t)(cv.off - start);
     g->state_bytes = (size_t)so[11];
     g->st[b] = sb;
+  }
+}
+
+// Carve every buffer; with base == nullptr only the size is computed.
+void carve(lipz_grid* g, char* base, size_t* total) {
+  Carver cv{base};
+  const int C = g->C, B = g->B, zd = g->zd, xd = g->xd;
+  const Net &G = g->G, &D = g->D;
+  carve_state(g, cv, base);
+  if (g->dc) {
+    // grid-level buffers shared with the MLP path
+    g->nbr = cv.take<int32_t>((size_t)C * 5);
+    g->sel = cv.take<int32_t>((size_t)C * 2);
+    g->flags = cv.take<int32_t>(4);
+    g->L = cv.take<float>((size_t)C * 25);
+    g->Lg = cv.take<float>((size_t)C * 25);
+    g->fit_g = cv.take<float>((size_t)C * 5);
+    g->fit_d = cv.take<float>((size_t)C * 5);
+    dc_carve(g, cv);
+    g->probs_d = cv.take<GemmProb>(g->probs_h.size());
+    dc_carve_tables(g, cv);
+    *total = align_up(cv.off, kAlign);
+    return;
   }
   g->nbr = cv.take<int32_t>((size_t)C * 5);
   g->sel = cv.take<int32_t>((size_t)C * 2);
@@ -665,15 +563,13 @@ lipz_status pre_call(lipz_grid* g) {
   return LIPZ_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples) {
+// A grid handle with its configuration, neighbour table, carved buffers
+// (from `base`; nullptr only sizes them) and plan tables; no HIP calls.
+lipz_grid* plan_grid(const lipz_config* cfg, int64_t n_samples, char* base, const float* data, size_t* total) {
   Net Gn, Dn;
-  if (!validate(cfg, n_samples, &Gn, &Dn).empty()) return 0;
+  if (!validate(cfg, n_samples, &Gn, &Dn).empty()) return nullptr;
   lipz_grid* g = new (std::nothrow) lipz_grid();
-  if (!g) return 0;
+  if (!g) return nullptr;
   g->cfg = *cfg;
   g->C = cfg->rows * cfg->cols;
   g->B = cfg->batch;
@@ -684,45 +580,16 @@ size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples) {
   g->N = n_samples;
   g->G = Gn;
   g->D = Dn;
-  g->tn = ceil_div(Dn.fi[Dn.nl - 1], GEMM_BN);
-  g->nbr_h.assign((size_t)g->C * 5, 0);
-  setup_groups(g);
-  size_t total = 0;
-  carve(g, nullptr, &total);
-  build_tables(g);
-  carve(g, nullptr, &total);
-  delete g;
-  return total;
-}
-
-lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t workspace_bytes,
-                             const float* d_dataset, int64_t n_samples, void* hip_stream,
-                             lipz_grid** out) {
-  if (!out) return LIPZ_E_INVAL;
-  *out = nullptr;
-  Net Gn, Dn;
-  if (cfg && cfg->abi_version == LIPZ_ABI_VERSION && cfg->net == LIPZ_NET_DCGAN) return LIPZ_E_UNSUPPORTED;
-  if (!validate(cfg, n_samples, &Gn, &Dn).empty()) return LIPZ_E_INVAL;
-  if (!d_workspace || !d_dataset) return LIPZ_E_INVAL;
-  if (((uintptr_t)d_workspace & (kAlign - 1)) != 0) return LIPZ_E_WORKSPACE;
-  const size_t need = lipz_workspace_bytes(cfg, n_samples);
-  if (need == 0 || workspace_bytes < need) return LIPZ_E_WORKSPACE;
-
-  lipz_grid* g = new (std::nothrow) lipz_grid();
-  if (!g) return LIPZ_E_INVAL;
-  g->cfg = *cfg;
-  g->C = cfg->rows * cfg->cols;
-  g->B = cfg->batch;
-  g->zd = cfg->z_dim;
-  g->xd = cfg->x_dim;
-  g->S = cfg->mix_samples;
-  g->F = cfg->mix_feat_dim;
-  g->N = n_samples;
-  g->G = Gn;
-  g->D = Dn;
-  g->tn = ceil_div(Dn.fi[Dn.nl - 1], GEMM_BN);
-  g->stream = (hipStream_t)hip_stream;
-  g->data = d_dataset;
+  if (cfg->net == LIPZ_NET_DCGAN) {
+    g->dc = dc_new(cfg);
+    if (!g->dc) {
+      delete g;
+      return nullptr;
+    }
+  } else {
+    g->tn = ceil_div(Dn.fi[Dn.nl - 1], GEMM_BN);
+  }
+  g->data = data;
   g->key = make_uint2((uint32_t)(cfg->seed & 0xFFFFFFFFull), (uint32_t)(cfg->seed >> 32));
   g->slope = cfg->lrelu_slope;
   g->ac.beta1 = cfg->beta1;
@@ -745,16 +612,48 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
     }
 
   setup_groups(g);
-  // The GEMM tables are carved last, so building them after the first carve
+  // The plan tables are carved last, so building them after the first carve
   // already sees the final buffer addresses; the second carve sizes them.
+  carve(g, base, total);
+  if (g->dc) dc_build(g);
+  else build_tables(g);
+  carve(g, base, total);
+  return g;
+}
+
+}  // namespace lipz
+
+extern "C" {
+
+size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples) {
   size_t total = 0;
-  carve(g, (char*)d_workspace, &total);
-  build_tables(g);
-  carve(g, (char*)d_workspace, &total);
+  lipz_grid* g = plan_grid(cfg, n_samples, nullptr, nullptr, &total);
+  if (!g) return 0;
+  dc_delete(g->dc);
+  delete g;
+  return total;
+}
+
+lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t workspace_bytes,
+                             const float* d_dataset, int64_t n_samples, void* hip_stream,
+                             lipz_grid** out) {
+  if (!out) return LIPZ_E_INVAL;
+  *out = nullptr;
+  Net Gn, Dn;
+  if (!validate(cfg, n_samples, &Gn, &Dn).empty()) return LIPZ_E_INVAL;
+  if (!d_workspace || !d_dataset) return LIPZ_E_INVAL;
+  if (((uintptr_t)d_workspace & (kAlign - 1)) != 0) return LIPZ_E_WORKSPACE;
+  const size_t need = lipz_workspace_bytes(cfg, n_samples);
+  if (need == 0 || workspace_bytes < need) return LIPZ_E_WORKSPACE;
+  size_t total = 0;
+  lipz_grid* g = plan_grid(cfg, n_samples, (char*)d_workspace, d_dataset, &total);
+  if (!g) return LIPZ_E_INVAL;
   if (total > workspace_bytes) {
+    dc_delete(g->dc);
     delete g;
     return LIPZ_E_WORKSPACE;
   }
+  g->stream = (hipStream_t)hip_stream;
 
   hipStream_t s = g->stream;
   lipz_status st = LIPZ_OK;
@@ -772,14 +671,19 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
   ck(hipMemcpyAsync(g->probs_d, g->probs_h.data(), g->probs_h.size() * sizeof(GemmProb),
                     hipMemcpyHostToDevice, s),
      "upload GEMM tables");
+  if (g->dc) ck(dc_upload_tables(g, s), "upload convolution tables");
   const StateBuf& S0 = g->st[0];
   const int C = g->C;
   // both state buffers, padding included, start at zero so saved blobs are deterministic
   for (int b = 0; b < 2; ++b)
     ck(launch_fill_i32(reinterpret_cast<int32_t*>(g->st[b].base), (int64_t)(g->state_bytes / 4), 0, s),
        "zero state");
-  ck(launch_init_params(S0.Gp, g->G.stride, g->G.P, C, g->G.layers(), g->key, LIPZ_TAG_INIT_G, s), "init G");
-  ck(launch_init_params(S0.Dp, g->D.stride, g->D.P, C, g->D.layers(), g->key, LIPZ_TAG_INIT_D, s), "init D");
+  if (g->dc) {
+    ck(dc_init_params(g, S0, s), "init");
+  } else {
+    ck(launch_init_params(S0.Gp, g->G.stride, g->G.P, C, g->G.layers(), g->key, LIPZ_TAG_INIT_G, s), "init G");
+    ck(launch_init_params(S0.Dp, g->D.stride, g->D.P, C, g->D.layers(), g->key, LIPZ_TAG_INIT_D, s), "init D");
+  }
   ck(launch_fill_f32(S0.Gm, (int64_t)C * g->G.stride, 0.f, s), "zero");
   ck(launch_fill_f32(S0.Gv, (int64_t)C * g->G.stride, 0.f, s), "zero");
   ck(launch_fill_f32(S0.Dm, (int64_t)C * g->D.stride, 0.f, s), "zero");
@@ -821,6 +725,7 @@ lipz_status lipz_grid_destroy(lipz_grid* g) {
     hipEventDestroy(p.first);
     hipEventDestroy(p.second);
   }
+  dc_delete(g->dc);
   delete g;
   return LIPZ_OK;
 }
@@ -833,19 +738,24 @@ lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float
   hipStream_t s = g->stream;
   const int par = g->cur;
   const int C = g->C, B = g->B;
-  hipError_t e = launch_sample(g->data, g->N, g->xd, g->zd, B, 0, C, g->key, (uint32_t)gen, 0, g->Xe,
-                               (int64_t)6 * B * g->xd, g->ze, (int64_t)B * g->zd, s);
-  if ((st = check_hip(g, e, "eval sample"))) return st;
-  for (int ph : g->eval_phases[par])
-    if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "eval forward"))) return st;
-  EvalHeadArgs ha;
-  ha.part = g->part_e;
-  ha.tn = g->tn;
-  ha.L = g->L;
-  ha.Lg = g->Lg;
-  ha.B = B;
-  ha.C = C;
-  if ((st = check_hip(g, launch_head_eval(ha, s), "eval head"))) return st;
+  hipError_t e;
+  if (g->dc) {
+    if ((st = dc_eval(g, gen))) return st;
+  } else {
+    e = launch_sample(g->data, g->N, g->xd, g->zd, B, 0, C, g->key, (uint32_t)gen, 0, g->Xe,
+                      (int64_t)6 * B * g->xd, g->ze, (int64_t)B * g->zd, s);
+    if ((st = check_hip(g, e, "eval sample"))) return st;
+    for (int ph : g->eval_phases[par])
+      if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "eval forward"))) return st;
+    EvalHeadArgs ha;
+    ha.part = g->part_e;
+    ha.tn = g->tn;
+    ha.L = g->L;
+    ha.Lg = g->Lg;
+    ha.B = B;
+    ha.C = C;
+    if ((st = check_hip(g, launch_head_eval(ha, s), "eval head"))) return st;
+  }
   e = launch_fitness(g->L, g->Lg, C, g->cfg.fitness_mode, g->fit_g, g->fit_d, g->flags, d_L, d_Lg,
                      d_fit_g, d_fit_d, s);
   if ((st = check_hip(g, e, "fitness"))) return st;
@@ -922,6 +832,15 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
     return fail(g, LIPZ_E_INVAL, "steps must satisfy 0 <= step0, step0 + n_steps <= 65535");
   if (n_steps == 0) return LIPZ_OK;
   hipStream_t s = g->stream;
+  if (g->dc) {
+    if ((st = dc_train(g, gen, step0, n_steps, d_losses))) return st;
+    const StateBuf& S = g->st[g->cur];
+    hipError_t e = launch_add_i32(S.Gt, g->C, n_steps, s);
+    if (e == hipSuccess) e = launch_add_i32(S.Dt, g->C, n_steps, s);
+    if ((st = check_hip(g, e, "step count"))) return st;
+    g->fitness_valid = false;
+    return LIPZ_OK;
+  }
   const int par = g->cur;
   const StateBuf& S = g->st[par];
   const int C = g->C, B = g->B, LD = g->D.nl;
@@ -1031,6 +950,7 @@ lipz_status lipz_get_neighbors(const lipz_grid* g, int32_t* h_nbr) {
 
 lipz_status lipz_param_layout(const lipz_grid* g, int32_t role, int64_t* h_offsets, int32_t* h_n) {
   if (!g || !h_n || (role != LIPZ_ROLE_G && role != LIPZ_ROLE_D)) return LIPZ_E_INVAL;
+  if (g->dc) return dc_param_layout(g, role, h_offsets, h_n);
   const Net& n = role == LIPZ_ROLE_G ? g->G : g->D;
   *h_n = n.nl;
   if (h_offsets)
@@ -1139,6 +1059,61 @@ lipz_status lipz_gemm_timing(lipz_grid* g, double* h_ms, int64_t* h_launches, do
   g->gemm_flops = 0.0;
   g->gemm_bytes = 0.0;
   g->gemm_launches = 0;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, char* msg, int32_t msg_len,
+                                  int32_t* n_bad) {
+  if (!n_bad) return LIPZ_E_INVAL;
+  *n_bad = 0;
+  // Placeholder addresses, never dereferenced: the plan is only inspected.
+  char* const base = reinterpret_cast<char*>((uintptr_t)1 << 40);
+  const float* const data = reinterpret_cast<const float*>((uintptr_t)1 << 44);
+  size_t total = 0;
+  lipz_grid* g = plan_grid(cfg, n_samples, base, data, &total);
+  if (!g) return LIPZ_E_INVAL;
+  const char* lo[2] = {base, (const char*)data};
+  const char* hi[2] = {base + total, (const char*)data + (size_t)n_samples * g->xd * 4};
+  std::string text;
+  int bad = 0;
+  auto inside = [&](const void* p, int64_t first, int64_t last) {
+    if (!p || first < 0) return false;
+    const char* a = (const char*)p + 4 * first;
+    const char* b = (const char*)p + 4 * (last + 1);
+    for (int i = 0; i < 2; ++i)
+      if (a >= lo[i] && b <= hi[i]) return true;
+    return false;
+  };
+  auto note = [&](const char* what, size_t i) {
+    ++bad;
+    if (text.size() < 2000) text += std::string(what) + " #" + std::to_string(i) + "; ";
+  };
+  for (size_t i = 0; i < g->probs_h.size(); ++i) {
+    const GemmProb& p = g->probs_h[i];
+    const int64_t a_last = p.a_trans ? (int64_t)(p.K - 1) * p.lda + p.a_rows - 1 : (int64_t)(p.a_rows - 1) * p.lda + p.K - 1;
+    const int64_t b_last = p.b_trans ? (int64_t)(p.N - 1) * p.ldb + p.K - 1 : (int64_t)(p.K - 1) * p.ldb + p.N - 1;
+    const int64_t c_last = (int64_t)(p.M - 1) * p.ldc + p.N - 1;
+    if (!inside(p.A, 0, a_last)) note("gemm A", i);
+    if (!inside(p.B, 0, b_last)) note("gemm B", i);
+    if (!inside(p.C, 0, c_last)) note("gemm C", i);
+    if (p.epi == EPI_ADAM && (!inside(p.m, 0, c_last) || !inside(p.v, 0, c_last) || !inside(p.lr, 0, 0) ||
+                              !inside(p.t, 0, 0)))
+      note("gemm Adam state", i);
+    if (p.epi == EPI_DACT && !inside(p.aux, 0, c_last)) note("gemm aux", i);
+    if (p.epi == EPI_BIAS_ACT && p.bias && !inside(p.bias, 0, p.N - 1)) note("gemm bias", i);
+    if (p.dot_out && (!inside(p.dot_out, 0, (int64_t)(p.M - 1) * p.dot_ld + (p.N + GEMM_BN - 1) / GEMM_BN - 1) ||
+                      !inside(p.dotw, 0, p.N - 1)))
+      note("gemm dot", i);
+  }
+  if (g->dc) bad += dc_check_bounds(g, lo, hi, 2, &text);
+  *n_bad = bad;
+  if (msg && msg_len > 0) {
+    const size_t n = text.size() < (size_t)msg_len - 1 ? text.size() : (size_t)msg_len - 1;
+    memcpy(msg, text.data(), n);
+    msg[n] = 0;
+  }
+  dc_delete(g->dc);
+  delete g;
   return LIPZ_OK;
 }
 

@@ -1,0 +1,173 @@
+// The grid handle and the host-side helpers shared by the runtime files of
+// liblipz.so (api.hip: configuration, workspace, MLP plans and the C ABI;
+// dcgan.hip: the plans of the convolutional networks).
+#pragma once
+
+#include <string>
+#include <vector>
+
+#include "lipz_internal.h"
+
+namespace lipz {
+
+constexpr size_t kAlign = 256;
+#define LIPZ_MAX_GROUPS 4
+#ifndef LIPZ_CELL_GROUPS
+#define LIPZ_CELL_GROUPS 0  // 0: choose from the grid size
+#endif
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Bump allocator over the caller's workspace.  With base == nullptr it only
+// measures, so sizing and carving share one code path.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  template <class T>
+  T* take(size_t count) {
+    off = align_up(off, kAlign);
+    T* p = reinterpret_cast<T*>(base + off);
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+struct Net {
+  int nl = 0;            // layers, the last one is the output layer
+  int64_t off[LIPZ_MAX_HIDDEN + 1];
+  int fi[LIPZ_MAX_HIDDEN + 1], fo[LIPZ_MAX_HIDDEN + 1];
+  int act[LIPZ_MAX_HIDDEN + 1];
+  int64_t P = 0, stride = 0;
+  NetLayers layers() const {
+    NetLayers L{};
+    L.n = nl;
+    for (int l = 0; l < nl; ++l) {
+      L.off[l] = off[l];
+      L.fan_in[l] = fi[l];
+      L.fan_out[l] = fo[l];
+    }
+    return L;
+  }
+};
+
+struct StateBuf {
+  char* base;
+  float *Gp, *Gm, *Gv, *Dp, *Dm, *Dv;
+  int32_t *Gt, *Dt;
+  float *Glr, *Dlr, *w;
+};
+
+struct Phase {
+  int first = 0, count = 0, tiles = 0, tile_rows = 64;
+  bool fast = true, wave = false;
+  GemmGroups grp;
+  double flops = 0.0;
+  double bytes = 0.0;  // algorithmic: each operand read once, each output written once
+};
+
+enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G };
+struct Op {
+  OpKind kind;
+  int phase;
+};
+
+struct DcPlan;  // the convolutional networks' plan (dcgan.hip)
+
+}  // namespace lipz
+
+// The opaque handle of include/lipz.h.
+struct lipz_grid {
+  typedef lipz::Net Net;
+  typedef lipz::StateBuf StateBuf;
+  typedef lipz::Op Op;
+  typedef lipz::Phase Phase;
+  typedef lipz::AdamConsts AdamConsts;
+  typedef lipz::GemmProb GemmProb;
+  lipz_config cfg;
+  int C = 0, B = 0, zd = 0, xd = 0, S = 0, F = 0;
+  Net G, D;
+  hipStream_t stream = nullptr;
+  const float* data = nullptr;
+  int64_t N = 0;
+  uint2 key;
+  float slope = 0.f;
+  AdamConsts ac;
+
+  StateBuf st[2];
+  int cur = 0;
+  size_t state_bytes = 0;
+  int64_t state_off[12];
+  std::vector<int32_t> nbr_h;
+
+  int32_t *nbr = nullptr, *sel = nullptr, *flags = nullptr;
+  float *L = nullptr, *Lg = nullptr, *fit_g = nullptr, *fit_d = nullptr;
+  // training buffers
+  float *z = nullptr, *Xtr = nullptr;
+  float *h[LIPZ_MAX_HIDDEN] = {}, *a[LIPZ_MAX_HIDDEN] = {}, *dD[LIPZ_MAX_HIDDEN] = {};
+  float *ag[LIPZ_MAX_HIDDEN] = {}, *dDg[LIPZ_MAX_HIDDEN] = {}, *dG[LIPZ_MAX_HIDDEN + 1] = {};
+  float *part_tr = nullptr, *part_g = nullptr, *part_e = nullptr;  // partial logits
+  float* dlbuf = nullptr;  // D-step dL/d(logit) [C][2B][4]
+  int tn = 1;  // column tiles of D's last hidden layer
+  // evaluation buffers
+  float *ze = nullptr, *Xe = nullptr;
+  float *he[LIPZ_MAX_HIDDEN] = {}, *ae[LIPZ_MAX_HIDDEN] = {};
+  // mixture buffers
+  float *zeta = nullptr, *xm = nullptr, *fm = nullptr, *mu_k = nullptr, *s2_k = nullptr;
+  float *hm[LIPZ_MAX_HIDDEN] = {};
+  float *P = nullptr, *mu_r = nullptr, *sd_r = nullptr, *realfeat = nullptr;
+
+  GemmProb* probs_d = nullptr;
+  std::vector<GemmProb> probs_h;
+  std::vector<Phase> phases;
+  // Cells are split into groups whose training phases run on separate
+  // streams (group 0 on the caller's stream), so that one group's
+  // latency-bound launches overlap another group's work.
+  int n_groups = 1;
+  int group_c0[LIPZ_MAX_GROUPS + 1] = {};
+  hipStream_t gstream[LIPZ_MAX_GROUPS] = {};
+  hipEvent_t fork_ev = nullptr, join_ev[LIPZ_MAX_GROUPS] = {};
+  std::vector<Op> train_ops[2][LIPZ_MAX_GROUPS];
+  std::vector<int> eval_phases[2], mix_phases[2];
+  int real_phase = -1;
+
+  bool fitness_valid = false;
+  lipz_status sticky = LIPZ_OK;
+  std::string last_err;
+
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_live;
+  std::vector<double> ev_flops, ev_bytes;
+  double gemm_ms = 0.0, gemm_flops = 0.0, gemm_bytes = 0.0;
+  int64_t gemm_launches = 0;
+
+  lipz::DcPlan* dc = nullptr;  // set for LIPZ_NET_DCGAN
+};
+
+namespace lipz {
+
+// api.hip
+lipz_status fail(lipz_grid* g, lipz_status s, const std::string& msg);
+lipz_status check_hip(lipz_grid* g, hipError_t e, const char* what);
+void carve_state(lipz_grid* g, Carver& cv, char* base);
+GemmProb base_prob(const float* A, int lda, int a_trans, const float* Bm, int ldb, int b_trans, float* C, int ldc,
+                   int M, int N, int K);
+int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps);
+hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t stream);
+int ceil_div(int a, int b);
+
+// dcgan.hip
+std::string dc_validate(const lipz_config* c, Net* Gn, Net* Dn);
+DcPlan* dc_new(const lipz_config* c);
+void dc_delete(DcPlan* p);
+void dc_carve(lipz_grid* g, Carver& cv);
+void dc_build(lipz_grid* g);
+void dc_carve_tables(lipz_grid* g, Carver& cv);
+hipError_t dc_upload_tables(lipz_grid* g, hipStream_t s);
+hipError_t dc_init_params(lipz_grid* g, const StateBuf& S, hipStream_t s);
+lipz_status dc_eval(lipz_grid* g, int gen);
+lipz_status dc_train(lipz_grid* g, int gen, int step0, int n_steps, float* d_losses);
+lipz_status dc_param_layout(const lipz_grid* g, int role, int64_t* h_offsets, int32_t* h_n);
+int dc_check_bounds(const lipz_grid* g, const char* const* lo, const char* const* hi, int nreg, std::string* msg);
+
+}  // namespace lipz

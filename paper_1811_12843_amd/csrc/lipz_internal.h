@@ -178,6 +178,145 @@ hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, i
                                hipEvent_t ev_stop = nullptr);
 
 // ---------------------------------------------------------------------------
+// Convolutions as implicit GEMMs (conv.hip)
+//
+// Activations are NHWC.  A "position" is p = (img, y, x) of a grid
+// [NI][2^gh][2^gw]; p = (img << (gh + gw)) | (y << gw) | x.  A position map
+// sends p to the element ((img * 2^h + y * sy + y0) * 2^w + x * sx + x0) * ld
+// of a tensor [NI][2^h][2^w][ld].  A tap t = (a, b) of a tw x tw tap grid
+// (tw = 2^tw_log, t = a * tw + b) shifts the source row by a * tys + ty0 and the column by
+// b * tys + tx0; it uses the weight tap (kh, kw) = (a * khs + kh0,
+// b * khs + kw0) of a kw_full-wide kernel.  Source positions outside the
+// tensor read 0 (zero padding).
+//
+// CONV_FWD: rows are the grid positions, columns the output channels:
+//   C(p, n) = sum over taps t and channels c < cs of
+//             S[map(p) shifted by t][c] * W[(tap(t) * cs + c) * wsc + n * wsn]
+//   (wsc, wsn) = (N, 1): forward weights [taps][cs][N];
+//   (wsc, wsn) = (1, cs): the transposed weights of an input gradient.
+//   The output goes through the output position map; epilogues EPI_STORE,
+//   EPI_BIAS_ACT and EPI_DACT (aux at the output's own address).
+// CONV_WG: weight gradient, rows m = (t, c) of the tap-expanded input,
+//   columns the output channels, reduced over the grid positions:
+//   C(m, n) = sum over p of S[map(p) shifted by t][c] * P[pmap(p)][n],
+//   plus row ones_row (if >= 0) = sum over p of P[pmap(p)][n] (a bias).
+//   Row m = (t, c) is stored at weight-block row tap(t) * cs + c, the ones
+//   row at brow.  K (positions) is cut into splits of ksplit positions;
+//   split s writes its partial sums to C + s * split_stride.
+// ---------------------------------------------------------------------------
+enum ConvMode : int32_t { CONV_FWD = 0, CONV_WG = 1 };
+
+struct PosMap {
+  int32_t h_log, w_log;    // target spatial size (log2)
+  int32_t sy, y0, sx, x0;  // grid -> target coordinates
+  int32_t ld;              // floats per target position
+};
+
+struct ConvProb {
+  int32_t mode;
+  int32_t M, N, K;
+  int32_t gh_log, gw_log;  // grid of positions (per image)
+  int32_t taps, tw_log, cs;  // taps = 4^tw_log (0 for a bias-only problem), channels per tap
+  int32_t cs_log;          // log2 cs, or -1 when taps == 1 (then k = c)
+  int32_t tys, ty0, tx0;   // tap shifts
+  int32_t khs, kh0, kw0, kw_full;
+  int32_t gen;             // 1: element-wise (unaligned) operand loads
+  const float* S;          // the tap-gathered operand
+  PosMap smap;             // grid -> S (before the tap shift; sy/sx are the strides)
+  uint32_t s_bytes;        // extent of S
+  // CONV_FWD
+  const float* W;
+  int32_t wsc, wsn;
+  uint32_t w_bytes;
+  PosMap omap;             // grid -> C
+  // CONV_WG
+  const float* P;          // the plain operand (output gradient)
+  PosMap pmap;
+  uint32_t p_bytes;
+  int32_t ones_row, brow;
+  int32_t ksplit, splits;
+  int64_t split_stride;
+  int32_t ldc;             // CONV_WG: floats per partial row
+  // output
+  float* C;
+  int32_t epi, act;
+  const float* bias;
+  const float* aux;
+  int32_t tiles_m, tiles_n, tile_begin;
+};
+
+// Launch every problem of one phase (problems in device memory, grouped as
+// for the GEMM); tile counts per problem = tiles_m * tiles_n * splits.
+hipError_t launch_conv_grouped(const ConvProb* d_probs, const GemmGroups& grp, int total_tiles, float slope,
+                               hipStream_t s, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+
+// Sum of the split partial sums of a weight gradient, in split order, then
+// the Adam step of the parameters (W and its bias row laid out as the
+// partial rows).  One descriptor per (cell, layer).
+struct RedProb {
+  const float* part;
+  int64_t split_stride;
+  int32_t splits;
+  int64_t n;               // parameters (rows * cols)
+  int64_t first;           // prefix sum of n over the preceding descriptors
+  float* p;
+  float* m;
+  float* v;
+  const float* lr;
+  const int32_t* t;
+};
+hipError_t launch_reduce_adam(const RedProb* d_probs, int n_probs, int64_t total, int step_local, AdamConsts ac,
+                              hipStream_t s);
+
+// Batch norm over the rows of x [rows][ch] of each instance, statistics of
+// the batch itself (biased variance, eps), in a fixed order: per chunk of
+// BN_CHUNK rows a two-pass mean and sum of squared deviations, then the
+// chunks merged in order (Chan, Golub and LeVeque's pairwise update).
+constexpr int BN_CHUNK = 256;
+struct BnProb {
+  const float* x;          // conv output [rows][ch]
+  float* y;                // forward: act(gamma xhat + beta); backward: gradient in / out
+  const float* aux;        // backward: unused
+  int64_t rows;
+  int32_t ch;
+  float* part;             // [chunks][2][ch] scratch
+  float* stats;            // [2][ch]: mean, rstd  (backward: + [3][ch] coefficients)
+  float* gamma;            // parameters of the cell; beta = gamma + ch
+  float* gm;               // Adam m, v of gamma (beta follows)
+  float* gv;
+  const float* lr;
+  const int32_t* t;
+  int32_t act;
+  int32_t first_block;     // prefix of chunks * channel groups over preceding instances
+};
+hipError_t launch_bn_stats(const BnProb* d_probs, int n_probs, int total_blocks, float eps, hipStream_t s);
+hipError_t launch_bn_apply(const BnProb* d_probs, int n_probs, int64_t max_elems, float slope, hipStream_t s);
+// Backward: y holds dL/d(bn output); becomes dL/dx.  gamma, beta take an Adam step.
+hipError_t launch_bn_backward(const BnProb* d_probs, int n_probs, int total_blocks, int64_t max_elems,
+                              int step_local, AdamConsts ac, hipStream_t s);
+
+// out[r * ld_out] = dot(x[r][0..H), w) + *bias for each row r of each instance.
+struct DotProb {
+  const float* x;
+  const float* w;          // weights, bias at w[H]
+  float* out;
+  int32_t rows, H, ld_out;
+  int32_t first_row;       // prefix of rows over preceding instances
+};
+hipError_t launch_dot_rows(const DotProb* d_probs, int n_probs, int total_rows, hipStream_t s);
+
+// Initial DCGAN parameters of C cells (rows of `stride` floats): element e of
+// a row is normal number e of the stream (cell, 0, 0, tag); weights get
+// 0.02 n, batch-norm gammas 1 + 0.02 n, biases and betas 0.
+struct ConvInitLayout {
+  int32_t n;
+  int64_t off_w[8], n_w[8], off_b[8], off_g[8];
+  int32_t n_b[8], n_g[8];
+};
+hipError_t launch_init_conv_params(float* p, int64_t stride, int64_t P, int C, const ConvInitLayout& L, uint2 key,
+                                   uint32_t tag, hipStream_t s);
+
+// ---------------------------------------------------------------------------
 // Other kernels (kernels.hip)
 // ---------------------------------------------------------------------------
 struct NetLayers {

@@ -96,6 +96,8 @@ _SIGS = {
     "lipz_set_gemm_timing": (_i32, [_vp, _i32]),
     "lipz_gemm_timing": (_i32, [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64),
                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
+    "lipz_test_plan_bounds": (_i32, [ctypes.POINTER(lipz_config), _i64, ctypes.c_char_p, _i32,
+                                     ctypes.POINTER(_i32)]),
     "lipz_test_gemm": (_i32, [_vp, _vp, _i32, _i32, _i32, _vp, _i32, _i32, _i32, _vp, _i32, _i32,
                               _vp, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                               _f32, _f32, _f32, _i32]),
@@ -250,3 +252,12 @@ def lipz_test_gemm(stream, d_desc, M, N, K, d_A, lda, a_trans, ones_row, d_B, ld
                                                 slope, _p(d_bias), _p(d_aux), _p(d_m), _p(d_v), _p(d_lr),
                                                 _p(d_t), step_local, beta1, beta2, eps, tile_rows),
                   "lipz_test_gemm")
+
+
+def lipz_test_plan_bounds(cfg, n_samples):
+    """(number of out-of-bounds accesses in the launch plan, message)."""
+    buf = ctypes.create_string_buffer(4096)
+    bad = _i32()
+    _check(load_library().lipz_test_plan_bounds(ctypes.byref(cfg), n_samples, buf, 4096, ctypes.byref(bad)),
+           "lipz_test_plan_bounds")
+    return bad.value, buf.value.decode()

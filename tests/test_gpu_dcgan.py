@@ -1,0 +1,222 @@
+"""GPU parity of the DCGAN-style networks: every C-ABI call against the oracle
+from an identical state (the oracle state rounded to fp32 and loaded into the
+library), with the tolerances of the MLP parity tests:
+  losses and fitness        |gpu - oracle| <= 1e-4 |oracle| elementwise
+  parameters after steps    per-tensor ||gpu - oracle|| / ||oracle|| <= 1e-3
+  parameter updates         per-tensor relative error of (p_after - p_before) <= 5e-2
+  copies, indices, counts   bit-exact
+Small grids cover several tiles, ragged tails, multi-split weight gradients
+and the element-wise (3-channel image) paths; the 64x64 test runs the 4x4
+workload's own shapes and checks sampled outputs one by one."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import coevo, dcgan
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - collected on CPU, skipped there
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_1811_12843_amd as L  # noqa: E402
+from harness import GpuGrid, fp32_state, rel_err  # noqa: E402
+
+RTOL = 1e-4
+
+
+def _wl(**kw):
+    return synth.small_workload("celeba_dcgan_4x4", **kw)
+
+
+WORKLOADS = {
+    # 16x16 images, two stages, duplicate neighbours
+    "dc16_2x2": lambda: _wl(rows=2, cols=2, img=(16, 16, 3), x_dim=768, z_dim=8, g_hidden=[32, 16],
+                            d_hidden=[16, 32], batch=5, lr0_g=2e-3, lr0_d=2e-3,
+                            data=dict(n=512, h=16, w=16)),
+    # 32x32 images, three stages, multi-split weight gradients, 3x3 torus
+    "dc32_3x3": lambda: _wl(rows=3, cols=3, img=(32, 32, 3), x_dim=3072, z_dim=12, g_hidden=[64, 32, 16],
+                            d_hidden=[16, 32, 64], batch=6, lr0_g=2e-3, lr0_d=2e-3,
+                            data=dict(n=512, h=32, w=32)),
+}
+_CACHE = {}
+
+
+def _setup(key):
+    wl = WORKLOADS[key]()
+    dk = (wl["data"]["n"], wl["data"]["h"])
+    if dk not in _CACHE:
+        _CACHE[dk] = synth.make_dataset(wl["data"])
+    data = _CACHE[dk]
+    return wl, data, coevo.Setup(wl, len(data))
+
+
+def _warm_state(S, data, seed=1):
+    """An oracle state with non-zero biases and betas, Adam moments and step counts."""
+    st = coevo.create(S)
+    r = np.random.default_rng(seed)
+    st.Gp += 0.01 * r.normal(size=st.Gp.shape)
+    st.Dp += 0.01 * r.normal(size=st.Dp.shape)
+    coevo.train_step(S, st, data, 0, 40)
+    return fp32_state(st)
+
+
+def _sections(arch):
+    out = []
+    for l, Ly in enumerate(arch.layers):
+        out.append((f"L{l}.W", Ly["off_w"], Ly["off_w"] + Ly["n_w"]))
+        if Ly["bias"]:
+            out.append((f"L{l}.b", Ly["off_b"], Ly["off_b"] + Ly["cout"]))
+        if Ly["bn"]:
+            nb = dcgan.bn_channels(Ly)
+            out.append((f"L{l}.gamma", Ly["off_g"], Ly["off_g"] + nb))
+            out.append((f"L{l}.beta", Ly["off_be"], Ly["off_be"] + nb))
+    return out
+
+
+def _worst(Pa, Pb, arch, cells=None):
+    worst, where = 0.0, ""
+    for name, lo, hi in _sections(arch):
+        for c in (range(Pa.shape[0]) if cells is None else cells):
+            e = rel_err(Pa[c, lo:hi], Pb[c, lo:hi])
+            if e > worst:
+                worst, where = e, f"cell {c} {name}"
+    return worst, where
+
+
+def _print_case(name, **kw):
+    print(f"[case] {name} " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+@pytest.mark.parametrize("key", list(WORKLOADS))
+def test_plan_and_create_match_oracle_init(key):
+    wl, data, S = _setup(key)
+    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), len(data))
+    assert n_bad == 0, msg
+    _print_case("dcgan create", key=key)
+    with GpuGrid(wl, data) as gg:
+        assert gg.sync() == L.LIPZ_OK
+        got = gg.get_state()
+        ref = fp32_state(coevo.create(S))
+        for f in ("Gp", "Dp"):
+            a, b = getattr(got, f), getattr(ref, f)
+            ulp = np.spacing(np.abs(b).astype(np.float32)).astype(np.float64)
+            assert np.all(np.abs(a - b) <= ulp), f
+        for f in ("Gm", "Gv", "Dm", "Dv", "Gt", "Dt", "Glr", "Dlr", "w"):
+            assert np.array_equal(getattr(got, f), getattr(ref, f)), f
+        for role, net in ((L.LIPZ_ROLE_G, S.Gnet), (L.LIPZ_ROLE_D, S.Dnet)):
+            lay = L.lipz_param_layout(gg.g, role)
+            assert [x[0] for x in lay] == [Ly["off_w"] for Ly in net.arch.layers]
+
+
+@pytest.mark.parametrize("key", list(WORKLOADS))
+def test_eval_matches_oracle(key):
+    wl, data, S = _setup(key)
+    st = _warm_state(S, data)
+    _print_case("dcgan eval", key=key)
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        for gen in (0, 2):
+            Lm, Lg, fg, fd = gg.eval(gen)
+            oL, oLg, ofg, ofd = coevo.evaluate(S, st, data, gen)
+            for a, b in ((Lm, oL), (Lg, oLg), (fg, ofg), (fd, ofd)):
+                err = np.max(np.abs(a - b) / np.abs(b))
+                print(f"  gen {gen}: max rel err {err:.2e}")
+                assert np.all(np.abs(a - b) <= RTOL * np.abs(b)), err
+            if wl["rows"] == 2 and wl["cols"] == 2:
+                assert np.array_equal(Lm[:, 1], Lm[:, 2]) and np.array_equal(Lm[:, :, 3], Lm[:, :, 4])
+
+
+@pytest.mark.parametrize("key,steps", [("dc16_2x2", 1), ("dc16_2x2", 3), ("dc32_3x3", 2)])
+def test_train_step_matches_oracle(key, steps):
+    wl, data, S = _setup(key)
+    st = _warm_state(S, data)
+    gen, step0 = 1, 4
+    _print_case("dcgan train", key=key, steps=steps)
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        glosses = gg.train(gen, step0, steps)
+        ref = st.copy()
+        olosses = np.array([coevo.train_step(S, ref, data, gen, step0 + k) for k in range(steps)])
+        got = gg.get_state()
+        print(f"  losses max rel err {np.max(np.abs(glosses - olosses) / np.abs(olosses)):.2e}")
+        assert np.all(np.abs(glosses[0] - olosses[0]) <= RTOL * np.abs(olosses[0]))
+        assert np.all(np.abs(glosses - olosses) <= 1e-3 * np.abs(olosses))
+        assert np.array_equal(got.Gt, ref.Gt) and np.array_equal(got.Dt, ref.Dt)
+        for p, net in (("G", S.Gnet), ("D", S.Dnet)):
+            e, where = _worst(getattr(got, p + "p"), getattr(ref, p + "p"), net.arch)
+            du, wdu = _worst(getattr(got, p + "p") - getattr(st, p + "p"), getattr(ref, p + "p") - getattr(st, p + "p"),
+                             net.arch)
+            print(f"  {p}: params rel {e:.2e} ({where}), updates rel {du:.2e} ({wdu})")
+            assert e <= 1e-3 and du <= 5e-2
+
+
+def test_select_replace_copies_individuals_bit_exactly():
+    wl, data, S = _setup("dc16_2x2")
+    st = _warm_state(S, data)
+    _print_case("dcgan select", key="dc16_2x2")
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        gg.eval(0)
+        forced = np.array([[S.nbr[c, (c + 1) % 5], S.nbr[c, (c + 3) % 5]] for c in range(S.C)])
+        sel, _ = gg.select(0, forced=forced)
+        assert np.array_equal(sel, forced)
+        got = gg.get_state()
+        new, _ = coevo.select_replace(S, st, np.zeros((S.C, 5)), np.zeros((S.C, 5)), 0, forced=forced)
+        for f in ("Gp", "Gm", "Gv", "Dp", "Dm", "Dv", "Gt", "Dt"):
+            assert np.array_equal(getattr(got, f), getattr(new, f)), f
+
+
+def test_full_size_64x64_4x4_sampled():
+    """The 4x4 workload's shapes (64x64x3 images, G 100-512-256-128-64-3, D
+    3-64-128-256-512-1, batch 64): sampled pair losses of one evaluation and
+    cell 0's losses and parameters after one training step, each computed by
+    the oracle on its own."""
+    wl = synth.workload("celeba_dcgan_4x4")
+    wl["data"] = dict(wl["data"], n=2048)
+    data = synth.make_dataset(wl["data"])
+    S = coevo.Setup(wl, len(data))
+    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), len(data))
+    assert n_bad == 0, msg
+    st = coevo.create(S)
+    # Adam moments of a trained individual, so one step is not just lr * sign(g)
+    r = np.random.default_rng(3)
+    for f in ("G", "D"):
+        m = getattr(st, f + "m")
+        m[...] = 1e-3 * r.normal(size=m.shape)
+        getattr(st, f + "v")[...] = m * m + 1e-7 * r.uniform(0.5, 1.5, size=m.shape)
+    st.Gt[:] = 20
+    st.Dt[:] = 20
+    st = fp32_state(st)
+    _print_case("dcgan full size", grid="4x4", img=64, batch=64)
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        Lm, Lg, fg, fd = gg.eval(0)
+        assert np.all(np.isfinite(Lm))
+        for c, i, j in ((0, 0, 0), (5, 2, 3), (15, 4, 1)):
+            _, x, z = coevo.sample(S, data, c, 0, 0)
+            xf = coevo.g_forward(S, st.Gp[S.nbr[c, i]], z)[1]
+            dp = st.Dp[S.nbr[c, j]]
+            ar = coevo.d_logits(S, dp, x)[1]
+            af = coevo.d_logits(S, dp, xf)[1]
+            oL = coevo.softplus(-ar).mean() + coevo.softplus(af).mean()
+            oLg = coevo.softplus(-af).mean()
+            print(f"  L[{c},{i},{j}] gpu {Lm[c, i, j]:.7f} oracle {oL:.7f}")
+            assert abs(Lm[c, i, j] - oL) <= RTOL * abs(oL)
+            assert abs(Lg[c, i, j] - oLg) <= RTOL * abs(oLg)
+        glosses = gg.train(0, 0, 1)
+        got = gg.get_state()
+    # cell 0 alone: a 1x1 grid draws the same samples (cell id 0) from the same state
+    wl1 = dict(wl, rows=1, cols=1)
+    S1 = coevo.Setup(wl1, len(data))
+    st1 = coevo.State(**{f: np.array(getattr(st, f)[:1]) for f in coevo.State.FIELDS})
+    ol = coevo.train_step(S1, st1, data, 0, 0)
+    print(f"  cell 0 losses gpu {glosses[0, 0]} oracle {ol[0]}")
+    assert np.all(np.abs(glosses[0, 0] - ol[0]) <= RTOL * np.abs(ol[0]))
+    for p, net in (("G", S.Gnet), ("D", S.Dnet)):
+        e, where = _worst(getattr(got, p + "p")[:1], getattr(st1, p + "p"), net.arch)
+        du, wdu = _worst(getattr(got, p + "p")[:1] - getattr(st, p + "p")[:1],
+                         getattr(st1, p + "p") - getattr(st, p + "p")[:1], net.arch)
+        print(f"  {p}: params rel {e:.2e} ({where}), updates rel {du:.2e} ({wdu})")
+        assert e <= 1e-3 and du <= 5e-2

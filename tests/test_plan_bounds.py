@@ -1,0 +1,48 @@
+"""Host-only check of every launch plan (no GPU): each GEMM, convolution,
+batch-norm, reduction and dot descriptor the library builds for a workload
+stays inside the workspace and the dataset, with the kernels' own index
+formulas (lipz_test_plan_bounds)."""
+import pytest
+
+import paper_1811_12843_amd as L
+import synth
+
+SMALL_DCGAN = [
+    dict(rows=2, cols=2, img=(16, 16, 3), x_dim=768, z_dim=8, g_hidden=[32, 16], d_hidden=[16, 32], batch=5,
+         data=dict(n=512, h=16, w=16)),
+    dict(rows=3, cols=3, img=(32, 32, 3), x_dim=3072, z_dim=12, g_hidden=[64, 32, 16], d_hidden=[16, 32, 64],
+         batch=6, data=dict(n=512, h=32, w=32)),
+    dict(rows=1, cols=3, img=(8, 8, 1), x_dim=64, z_dim=5, g_hidden=[8], d_hidden=[12], batch=3,
+         data=dict(n=100, h=8, w=8, c=1)),
+]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    try:
+        L.load_library()
+    except RuntimeError as e:  # pragma: no cover
+        pytest.skip(str(e))
+
+
+@pytest.mark.parametrize("name", sorted(synth.WORKLOADS))
+def test_workload_plans_stay_in_bounds(name):
+    wl = synth.workload(name)
+    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
+    assert n_bad == 0, msg
+
+
+@pytest.mark.parametrize("i", range(len(SMALL_DCGAN)))
+def test_small_dcgan_plans_stay_in_bounds(i):
+    wl = synth.small_workload("celeba_dcgan_4x4", **SMALL_DCGAN[i])
+    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
+    assert n_bad == 0, msg
+
+
+def test_invalid_dcgan_shapes_are_rejected():
+    wl = synth.small_workload("celeba_dcgan_4x4", img=(48, 48, 3), x_dim=48 * 48 * 3)
+    assert L.lipz_workspace_bytes(L.config_from_dict(wl), 100) == 0
+    wl = synth.small_workload("celeba_dcgan_4x4", g_hidden=[512, 256, 128, 66])
+    assert L.lipz_workspace_bytes(L.config_from_dict(wl), 100) == 0
+    wl = synth.small_workload("celeba_dcgan_4x4", mix_enable=1)
+    assert L.lipz_workspace_bytes(L.config_from_dict(wl), 100) == 0
