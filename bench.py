@@ -16,6 +16,10 @@ Prints one JSON line:
   cpu_baseline     the oracle (fp64 NumPy) on this host's cores, on a bounded sample
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Other workloads (--workload): ring8_mlp_2x2, mnist_mlp_3x3, mnist_mlp_8x8 and
+celeba_dcgan_4x4 (the 64x64 DCGAN grid; its roofline kernel is the
+implicit-GEMM convolution together with the grouped GEMM).
 """
 import argparse
 import json
@@ -30,21 +34,38 @@ METRIC = "G×D pair-evals/sec + grid generations/sec (4x4 MLP grid); % fp32 MFMA
 FP32_MFMA_PEAK = 157.3e12  # MI355X dense fp32 matrix peak, FLOP/s
 
 
+def macs_per_sample(wl):
+    """Multiply-adds per sample of one forward pass: (G, G's first layer, D,
+    D's first layer).  Convolutions count their real taps only (a stride-2
+    transposed convolution: 16 taps per input pixel)."""
+    if wl["net"] == "mlp":
+        g = [wl["z_dim"]] + list(wl["g_hidden"]) + [wl["x_dim"]]
+        d = [wl["x_dim"]] + list(wl["d_hidden"]) + [1]
+        gl = [g[i] * g[i + 1] for i in range(len(g) - 1)]
+        dl = [d[i] * d[i + 1] for i in range(len(d) - 1)]
+    else:
+        h, _, c = wl["img"]
+        gc, dc = list(wl["g_hidden"]), list(wl["d_hidden"])
+        n = len(gc)
+        gl = [wl["z_dim"] * 16 * gc[0]]
+        gl += [16 * (4 << (k - 1)) ** 2 * gc[k - 1] * gc[k] for k in range(1, n)]
+        gl += [16 * (h // 2) ** 2 * gc[n - 1] * c]
+        cin = [c] + dc[:-1]
+        dl = [16 * (h >> (k + 1)) ** 2 * cin[k] * dc[k] for k in range(n)] + [16 * dc[-1]]
+    return sum(gl), gl[0], sum(dl), dl[0]
+
+
 def gemm_flops_per_generation(wl):
-    """Algorithmic GEMM FLOPs (2 per multiply-add, bias terms excluded) of one
-    generation: evaluation, S training steps, and the mixture step."""
+    """Algorithmic matrix-core FLOPs (2 per multiply-add, bias terms excluded)
+    of one generation: evaluation, S training steps, and the mixture step."""
     C, B = wl["rows"] * wl["cols"], wl["batch"]
-    g = [wl["z_dim"]] + list(wl["g_hidden"]) + [wl["x_dim"]]
-    d = [wl["x_dim"]] + list(wl["d_hidden"]) + [1]
-    macs_g = sum(g[i] * g[i + 1] for i in range(len(g) - 1))
-    macs_d = sum(d[i] * d[i + 1] for i in range(len(d) - 1))
-    macs_d_in = macs_d - d[0] * d[1]  # D without its first layer's input gradient
+    macs_g, g_first, macs_d, d_first = macs_per_sample(wl)
     # evaluation: 5 G forwards per cell, D forwards on B real + 5B fake rows per D slot
     ev = C * (5 * B * macs_g + 5 * 6 * B * macs_d)
     # D step: G fwd, D fwd (2B), D weight grads (2B), D input grads below layer 1 (2B)
-    d_step = B * macs_g + 2 * B * macs_d + 2 * B * macs_d + 2 * B * macs_d_in
+    d_step = B * macs_g + 2 * B * macs_d + 2 * B * macs_d + 2 * B * (macs_d - d_first)
     # G step: D fwd (B), D input grads down to x (B), G weight grads, G input grads above z
-    g_step = B * macs_d + B * macs_d + B * macs_g + B * (macs_g - g[0] * g[1])
+    g_step = B * macs_d + B * macs_d + B * macs_g + B * (macs_g - g_first)
     train = C * wl["steps"] * (d_step + g_step)
     mix = 0
     if wl["mix_enable"]:
@@ -74,19 +95,48 @@ def stored_gemm_traffic(workload):
     return rec.get("traffic_bytes_per_launch")
 
 
-def cpu_baseline(wl, data, budget_s=20.0):
-    """Time the oracle on a bounded sample of the same workload and scale it to
-    generations/s: one evaluation, k training steps (k chosen to fit the
-    budget), one mixture step; a generation = eval + S * mean step + mixture."""
-    import numpy as np
-    from oracle import coevo, mixture
+def _oracle_cores():
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        cores = int(os.environ.get("OMP_NUM_THREADS", "1"))
+        return int(os.environ.get("OMP_NUM_THREADS", "1"))
+
+
+def cpu_baseline(wl, data, budget_s=20.0):
+    """Time the oracle on a bounded sample of the same workload and scale it to
+    generations/s.  MLP: one whole evaluation, k training steps (k chosen to
+    fit the budget), one mixture step; a generation = eval + S * mean step +
+    mixture.  DCGAN: one cell's evaluation (5 generator and 30 discriminator
+    forwards) and one cell's training step (a 1x1 grid draws cell 0's samples),
+    each scaled by the number of cells."""
+    import numpy as np
+    from oracle import coevo, mixture
+    cores = _oracle_cores()
     S = coevo.Setup(wl, len(data))
     st = coevo.create(S)
+    if wl["net"] != "mlp":
+        t0 = time.perf_counter()
+        _, x, z = coevo.sample(S, data, 0, 0, 0)
+        fakes = [coevo.g_forward(S, st.Gp[S.nbr[0, i]], z)[1] for i in range(5)]
+        for j in range(5):
+            dp = st.Dp[S.nbr[0, j]]
+            coevo.d_logits(S, dp, x)
+            for i in range(5):
+                coevo.d_logits(S, dp, fakes[i])
+        t_cell_eval = time.perf_counter() - t0
+        S1 = coevo.Setup(dict(wl, rows=1, cols=1), len(data))
+        st1 = coevo.State(**{f: np.array(getattr(st, f)[:1]) for f in coevo.State.FIELDS})
+        t0 = time.perf_counter()
+        coevo.train_step(S1, st1, data, 0, 0)
+        t_cell_step = time.perf_counter() - t0
+        t_eval = S.C * t_cell_eval
+        t_gen = t_eval + wl["steps"] * S.C * t_cell_step
+        return {"value": 1.0 / t_gen, "unit": "generations/s", "cores": int(cores), "kind": "oracle",
+                "sample": (f"cell 0's evaluation ({t_cell_eval:.2f} s) and one training step of cell 0 "
+                           f"({t_cell_step:.2f} s) of the {wl['rows']}x{wl['cols']} grid; generation = "
+                           f"{S.C} x eval + {wl['steps']} x {S.C} x step (extrapolated from one cell)"),
+                "pair_evals_per_s": S.C * 25 / t_eval}
     t0 = time.perf_counter()
     coevo.evaluate(S, st, data, 0)
     t_eval = time.perf_counter() - t0
@@ -120,6 +170,10 @@ def main():
     ap.add_argument("--steps", type=int, default=5, help="timed generations")
     ap.add_argument("--warmup", type=int, default=1, help="untimed generations")
     ap.add_argument("--workload", default="mnist_mlp_4x4_mix")
+    ap.add_argument("--data-n", type=int, default=0,
+                    help="dataset rows (default: the workload's; 8192 for the 64x64 image workload, "
+                         "whose 200000 rows take minutes to synthesise; minibatches are drawn "
+                         "uniformly, so the work per step does not depend on it)")
     ap.add_argument("--eval-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
@@ -150,6 +204,8 @@ def main():
         from paper_1811_12843_amd import build as _b
         _b.build()
     wl = synth.workload(args.workload)
+    n_data = args.data_n or (8192 if wl["net"] == "dcgan" else wl["data"]["n"])
+    wl["data"] = dict(wl["data"], n=n_data)
     data_np = synth.make_dataset(wl["data"])
     dev = "cuda"
     data = torch.from_numpy(data_np).to(dev)
@@ -205,6 +261,20 @@ def main():
     L.lipz_set_gemm_timing(g, 0)
 
     traffic = stored_gemm_traffic(args.workload)
+    cfg_desc = {"workload": args.workload, "grid": f"{wl['rows']}x{wl['cols']}", "cells": C,
+                "pairings_per_eval": 25 * C, "batch": wl["batch"], "steps_per_generation": S,
+                "mixture_es": bool(wl["mix_enable"])}
+    if wl["net"] == "mlp":
+        cfg_desc.update(g=[wl["z_dim"]] + wl["g_hidden"] + [wl["x_dim"]], d=[wl["x_dim"]] + wl["d_hidden"] + [1])
+        data_desc = (f"synthetic (seeded MNIST-shaped blobs, {len(data_np)} x {wl['x_dim']}); "
+                     "random-init MLPs")
+        kernel = "grouped GEMM (gemm_fast_kernel + gemm_wave_kernel)"
+    else:
+        cfg_desc.update(image=list(wl["img"]), z=wl["z_dim"], g_channels=wl["g_hidden"],
+                        d_channels=wl["d_hidden"], net="dcgan")
+        data_desc = (f"synthetic (seeded colour fields + blobs, {len(data_np)} x {wl['img'][0]}x{wl['img'][1]}"
+                     f"x{wl['img'][2]} NHWC); random-init DCGAN-style conv nets")
+        kernel = "implicit-GEMM convolution (conv_kernel) + grouped GEMM"
     f_ev, f_tr, f_mix = gemm_flops_per_generation(wl)
     f_gen = f_ev + f_tr + f_mix
     avg_ms = gemm_ms / max(launches, 1)
@@ -221,17 +291,14 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
-        "data": "synthetic (seeded MNIST-shaped blobs, 60000 x 784); random-init MLPs",
-        "config": {"workload": args.workload, "grid": f"{wl['rows']}x{wl['cols']}", "cells": C,
-                   "pairings_per_eval": 25 * C, "batch": wl["batch"], "steps_per_generation": S,
-                   "g": [wl["z_dim"]] + wl["g_hidden"] + [wl["x_dim"]],
-                   "d": [wl["x_dim"]] + wl["d_hidden"] + [1], "mixture_es": bool(wl["mix_enable"])},
+        "data": data_desc,
+        "config": cfg_desc,
         "pair_evals_per_s": pair_evals,
         "eval_ms": t_eval * 1e3,
         "gemm_gflop_per_generation": f_gen / 1e9,
         "mfma_frac": f_gen / (ms_per_gen * 1e-3) / FP32_MFMA_PEAK,
         "eval_mfma_frac": f_ev / t_eval / FP32_MFMA_PEAK,
-        "roofline": {"kernel": "grouped GEMM (gemm_fast_kernel + gemm_wave_kernel)", "bound": "mfma", "achieved": achieved / 1e12,
+        "roofline": {"kernel": kernel, "bound": "mfma", "achieved": achieved / 1e12,
                      "peak": FP32_MFMA_PEAK / 1e12, "unit": "TFLOP/s",
                      "frac": achieved / FP32_MFMA_PEAK, "traffic": traffic,
                      "launches": launches, "avg_launch_us": avg_ms * 1e3,

@@ -240,13 +240,15 @@ const char* lipz_error_string(lipz_status s);
 const char* lipz_last_error(const lipz_grid* g);
 
 /* ---- kernel timing (for roofline measurement) ----
- * When enabled, every launch of the grouped-GEMM kernel is bracketed by HIP
- * events on the stream it runs on.  lipz_gemm_timing synchronises and returns,
- * since the previous call: the summed kernel milliseconds, the launch count,
- * the algorithmic FLOPs (2 per multiply-add of the GEMM problems, bias rows
- * excluded) and the algorithmic bytes (each operand element read once, each
- * output element written once, Adam's p, m, v read and written).  Any output
- * pointer may be NULL. */
+ * When enabled, every launch of the matrix-core kernels (the grouped GEMM
+ * and, for LIPZ_NET_DCGAN, the implicit-GEMM convolution) is bracketed by
+ * HIP events that the launch's own dispatch stamps.  lipz_gemm_timing
+ * synchronises and returns, since the previous call: the summed kernel
+ * milliseconds, the launch count, the algorithmic FLOPs (2 per multiply-add
+ * of the GEMM and convolution problems, bias rows excluded) and the
+ * algorithmic bytes (each operand element read once, each output element
+ * written once, Adam's p, m, v read and written).  Any output pointer may be
+ * NULL. */
 lipz_status lipz_set_gemm_timing(lipz_grid* g, int32_t enable);
 lipz_status lipz_gemm_timing(lipz_grid* g, double* h_ms, int64_t* h_launches, double* h_flops,
                              double* h_bytes);

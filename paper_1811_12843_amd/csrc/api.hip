@@ -528,28 +528,38 @@ void build_tables(lipz_grid* g) {
   }
 }
 
+// With timing on: a start / stop event pair for the next matrix-core launch.
+hipError_t timing_events(lipz_grid* g, hipEvent_t* e0, hipEvent_t* e1) {
+  *e0 = *e1 = nullptr;
+  if (!g->timing) return hipSuccess;
+  if (g->ev_pool.size() < 2) {
+    hipEvent_t a, b;
+    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return hipErrorOutOfMemory;
+    g->ev_pool.push_back(a);
+    g->ev_pool.push_back(b);
+  }
+  *e1 = g->ev_pool.back();
+  g->ev_pool.pop_back();
+  *e0 = g->ev_pool.back();
+  g->ev_pool.pop_back();
+  return hipSuccess;
+}
+
+void timing_record(lipz_grid* g, hipEvent_t e0, hipEvent_t e1, double flops, double bytes) {
+  if (!g->timing) return;
+  g->ev_live.push_back({e0, e1});
+  g->ev_flops.push_back(flops);
+  g->ev_bytes.push_back(bytes);
+}
+
 hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t stream) {
   const Phase& ph = g->phases[phase];
-  hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (g->timing) {
-    if (g->ev_pool.size() < 2) {
-      hipEvent_t a, b;
-      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return hipErrorOutOfMemory;
-      g->ev_pool.push_back(a);
-      g->ev_pool.push_back(b);
-    }
-    e1 = g->ev_pool.back();
-    g->ev_pool.pop_back();
-    e0 = g->ev_pool.back();
-    g->ev_pool.pop_back();
-  }
-  hipError_t e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.fast,
-                                     ph.wave, step_local, g->slope, g->ac, stream, e0, e1);
-  if (g->timing) {
-    g->ev_live.push_back({e0, e1});
-    g->ev_flops.push_back(ph.flops);
-    g->ev_bytes.push_back(ph.bytes);
-  }
+  hipEvent_t e0, e1;
+  hipError_t e = timing_events(g, &e0, &e1);
+  if (e != hipSuccess) return e;
+  e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.fast, ph.wave, step_local,
+                          g->slope, g->ac, stream, e0, e1);
+  timing_record(g, e0, e1, ph.flops, ph.bytes);
   return e;
 }
 

@@ -467,16 +467,6 @@ __global__ __launch_bounds__(NT, 2) void conv_kernel(const ConvProb* __restrict_
 // Split-K sums + Adam: thread e of descriptor d sums the splits of its
 // gradient element in split order and takes the Adam step of the parameter.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int find_prob_i64(const RedProb* probs, int n, int64_t i) {
-  int lo = 0, hi = n - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (probs[mid].first <= i) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
-
 __device__ __forceinline__ void adam_at(float* p, float* m, float* v, float g, float lr, float bc1, float bc2,
                                         const AdamConsts& ac) {
   const float mm = ac.beta1 * *m + ac.one_minus_beta1 * g;
@@ -486,18 +476,18 @@ __device__ __forceinline__ void adam_at(float* p, float* m, float* v, float g, f
   *p = *p - lr * (mm / bc1) / (sqrtf(vv / bc2) + ac.eps);
 }
 
-__global__ void reduce_adam_kernel(const RedProb* __restrict__ probs, int n_probs, int64_t total, int step_local,
-                                   AdamConsts ac) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const RedProb& R = probs[find_prob_i64(probs, n_probs, i)];
-    const int64_t e = i - R.first;
+// Grid (x, problem): the Adam bias corrections are computed once per thread,
+// not per element.
+__global__ void reduce_adam_kernel(const RedProb* __restrict__ probs, int step_local, AdamConsts ac) {
+  const RedProb& R = probs[blockIdx.y];
+  const int tt = *R.t + step_local + 1;
+  const float bc1 = (float)(1.0 - pow((double)ac.beta1, (double)tt));
+  const float bc2 = (float)(1.0 - pow((double)ac.beta2, (double)tt));
+  const float lr = *R.lr;
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < R.n; e += (int64_t)gridDim.x * blockDim.x) {
     float g = 0.f;
     for (int s = 0; s < R.splits; ++s) g += R.part[(int64_t)s * R.split_stride + e];
-    const int tt = *R.t + step_local + 1;
-    const float bc1 = (float)(1.0 - pow((double)ac.beta1, (double)tt));
-    const float bc2 = (float)(1.0 - pow((double)ac.beta2, (double)tt));
-    adam_at(R.p + e, R.m + e, R.v + e, g, *R.lr, bc1, bc2, ac);
+    adam_at(R.p + e, R.m + e, R.v + e, g, lr, bc1, bc2, ac);
   }
 }
 
@@ -749,11 +739,11 @@ hipError_t launch_conv_grouped(const ConvProb* d_probs, const GemmGroups& grp, i
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_adam(const RedProb* d_probs, int n_probs, int64_t total, int step_local, AdamConsts ac,
+hipError_t launch_reduce_adam(const RedProb* d_probs, int n_probs, int64_t max_n, int step_local, AdamConsts ac,
                               hipStream_t s) {
-  if (n_probs <= 0 || total <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_adam_kernel, dim3(blocks_for(total, 65536)), dim3(NT), 0, s, d_probs, n_probs, total,
-                     step_local, ac);
+  if (n_probs <= 0 || max_n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_adam_kernel, dim3(blocks_for(max_n, 2048), n_probs), dim3(NT), 0, s, d_probs, step_local,
+                     ac);
   return hipGetLastError();
 }
 

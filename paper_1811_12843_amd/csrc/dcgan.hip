@@ -49,6 +49,7 @@ struct ConvPhase {
   int first = 0, count = 0, tiles = 0;
   GemmGroups grp;
   double flops = 0.0;
+  double bytes = 0.0;  // algorithmic: each tensor read or written once
 };
 struct BnOp {
   int first, count, blocks;
@@ -56,7 +57,7 @@ struct BnOp {
 };
 struct RedOp {
   int first, count;
-  int64_t total;
+  int64_t max_n;
 };
 struct DotOp {
   int first, count, rows;
@@ -307,6 +308,23 @@ double conv_flops(const ConvProb& p) {
   return 2.0 * rows * p.N * p.K;
 }
 
+// Each input tensor element read once, each output element written once
+// (weight-gradient partial sums: written once per split).
+double conv_bytes(const ConvProb& p) {
+  if (p.mode == CONV_FWD) {
+    const int NI = p.M >> (p.gh_log + p.gw_log);
+    double b = (double)(((int64_t)NI << p.smap.h_log) << p.smap.w_log) * p.smap.ld;  // source
+    b += (double)p.taps * p.cs * p.N;                                              // weights
+    b += (double)p.M * p.N * (p.epi == EPI_DACT ? 2.0 : 1.0);                      // output (+ aux)
+    return 4.0 * b;
+  }
+  const int NI = p.K >> (p.gh_log + p.gw_log);
+  double b = p.taps ? (double)(((int64_t)NI << p.smap.h_log) << p.smap.w_log) * p.smap.ld : 0.0;
+  b += (double)p.K * p.N;                                 // output gradient at the grid positions
+  b += (double)p.splits * p.M * p.N;                      // partial sums
+  return 4.0 * b;
+}
+
 }  // namespace
 
 struct DcPlan {
@@ -520,6 +538,7 @@ int add_conv_phase(DcPlan& P, const std::vector<ConvProb>& ps) {
     }
     tiles += tpp;
     ph.flops += conv_flops(p);
+    ph.bytes += conv_bytes(p);
     P.conv_h.push_back(p);
   }
   ph.tiles = tiles;
@@ -548,10 +567,9 @@ int add_red_op(DcPlan& P, const std::vector<RedProb>& rs) {
   RedOp op;
   op.first = (int)P.red_h.size();
   op.count = (int)rs.size();
-  op.total = 0;
-  for (RedProb r : rs) {
-    r.first = op.total;
-    op.total += r.n;
+  op.max_n = 0;
+  for (const RedProb& r : rs) {
+    if (r.n > op.max_n) op.max_n = r.n;
     P.red_h.push_back(r);
   }
   P.redops.push_back(op);
@@ -954,7 +972,12 @@ namespace {
 hipError_t run_conv_phase(lipz_grid* g, int idx, hipStream_t s) {
   DcPlan& P = *g->dc;
   const ConvPhase& ph = P.cph[idx];
-  return launch_conv_grouped(P.conv_d + ph.first, ph.grp, ph.tiles, g->slope, s);
+  hipEvent_t e0, e1;
+  hipError_t e = timing_events(g, &e0, &e1);
+  if (e != hipSuccess) return e;
+  e = launch_conv_grouped(P.conv_d + ph.first, ph.grp, ph.tiles, g->slope, s, e0, e1);
+  timing_record(g, e0, e1, ph.flops, ph.bytes);
+  return e;
 }
 
 hipError_t run_op(lipz_grid* g, const DcOp& op, int step_local, hipStream_t s) {
@@ -974,7 +997,7 @@ hipError_t run_op(lipz_grid* g, const DcOp& op, int step_local, hipStream_t s) {
     }
     case DC_REDUCE: {
       const RedOp& r = P.redops[op.idx];
-      return launch_reduce_adam(P.red_d + r.first, r.count, r.total, step_local, g->ac, s);
+      return launch_reduce_adam(P.red_d + r.first, r.count, r.max_n, step_local, g->ac, s);
     }
     case DC_DOT: {
       const DotOp& d = P.dotops[op.idx];

@@ -154,6 +154,8 @@ GemmProb base_prob(const float* A, int lda, int a_trans, const float* Bm, int ld
                    int M, int N, int K);
 int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps);
 hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t stream);
+hipError_t timing_events(lipz_grid* g, hipEvent_t* e0, hipEvent_t* e1);
+void timing_record(lipz_grid* g, hipEvent_t e0, hipEvent_t e1, double flops, double bytes);
 int ceil_div(int a, int b);
 
 // dcgan.hip

@@ -258,14 +258,13 @@ struct RedProb {
   int64_t split_stride;
   int32_t splits;
   int64_t n;               // parameters (rows * cols)
-  int64_t first;           // prefix sum of n over the preceding descriptors
   float* p;
   float* m;
   float* v;
   const float* lr;
   const int32_t* t;
 };
-hipError_t launch_reduce_adam(const RedProb* d_probs, int n_probs, int64_t total, int step_local, AdamConsts ac,
+hipError_t launch_reduce_adam(const RedProb* d_probs, int n_probs, int64_t max_n, int step_local, AdamConsts ac,
                               hipStream_t s);
 
 // Batch norm over the rows of x [rows][ch] of each instance, statistics of
