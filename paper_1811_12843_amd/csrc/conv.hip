@@ -4,7 +4,8 @@
 // statistics, and the logits of the 1-wide output layer.
 //
 // The convolution kernel never materialises an im2col matrix.  A workgroup
-// (4 wave64) owns a 64 x 64 output tile; K advances in 32-deep slices staged
+// (4 wave64) owns a 64 x 64 output tile (64 x 16 for outputs at most 16
+// wide); K advances in 32-deep slices staged
 // through a double-buffered LDS ring, the next slice's global loads in
 // registers while the current one feeds the MFMAs.  Every operand element
 // comes from a position map plus a tap shift (ConvProb, lipz_internal.h);
@@ -33,10 +34,9 @@ typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 namespace {
 
 constexpr int NT = 256;
-constexpr int TM = 64, TN = 64, TK = 32;  // tile rows, tile columns, K slice
+constexpr int TM = 64, TK = 32;           // tile rows, K slice (tile columns: ConvProb::tn)
 constexpr int SK = TK + 4;                // row stride of [row][k] LDS tiles
 constexpr int SM = TM + 4;                // row stride of [k][m] tiles
-constexpr int SN = TN + 4;                // row stride of [k][n] tiles
 constexpr int TILE_FLOATS = (TM * SK > TK * SM) ? TM * SK : TK * SM;
 // A byte offset past every operand extent the host accepts: such a buffer
 // load returns 0.
@@ -160,7 +160,45 @@ __device__ __forceinline__ void setup_ctx(const ConvProb& P, int m0, Ctx& X) {
   }
 }
 
-template <int MODE, int BT, int GEN>
+// Wave layout of a TM x TN_ tile.  TN_ = 64: 2 x 2 waves of 32 x 32 (2 x 2
+// MFMA tiles each); TN_ = 16 (outputs at most 16 wide, such as 3 image
+// channels): 4 waves of 16 x 16 (one MFMA tile each).
+template <int TN_>
+struct TW {
+  static constexpr int TI = TN_ == 64 ? 2 : 1;  // MFMA tiles along m per wave
+  static constexpr int TJ = TN_ == 64 ? 2 : 1;  // MFMA tiles along n per wave
+  static constexpr int SN = TN_ + 4;            // row stride of [k][n] B tiles
+  __device__ static int wm(int wave) { return TN_ == 64 ? (wave >> 1) * 32 : wave * 16; }
+  __device__ static int wn(int wave) { return TN_ == 64 ? (wave & 1) * 32 : 0; }
+};
+
+// B group h of thread tid: (k row, first n) of a [k][n] slice, or (n row,
+// first k) of an [n][k] slice; false when the thread has no such group
+// (a 32 x 16 slice is 128 float4).
+template <int TN_>
+__device__ __forceinline__ bool b_kn(int h, int tid, int& kk, int& nq) {
+  if (TN_ == 64) {
+    kk = 16 * h + (tid >> 4);
+    nq = (tid & 15) << 2;
+    return true;
+  }
+  kk = tid >> 2;
+  nq = (tid & 3) << 2;
+  return h == 0 && tid < 128;
+}
+template <int TN_>
+__device__ __forceinline__ bool b_nk(int h, int tid, int& nn, int& kq) {
+  if (TN_ == 64) {
+    nn = 32 * h + (tid >> 3);
+    kq = (tid & 7) << 2;
+    return true;
+  }
+  nn = tid >> 3;
+  kq = (tid & 7) << 2;
+  return h == 0 && tid < 128;
+}
+
+template <int MODE, int BT, int GEN, int TN_>
 __device__ __forceinline__ void load_slice(const ConvProb& P, const Ctx& X, int n0, int k0, int kend,
                                            float4 (&ra)[2], float4 (&rb)[2]) {
   const int tid = threadIdx.x;
@@ -195,11 +233,13 @@ __device__ __forceinline__ void load_slice(const ConvProb& P, const Ctx& X, int 
     }
     // B: weights
     const int wtap = P.cs * P.N;
-    if (BT == 0) {
-      const int n = n0 + ((tid & 15) << 2);
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int kk = k0 + 16 * h + (tid >> 4);
+    for (int h = 0; h < 2; ++h) {
+      rb[h] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (BT == 0) {
+        int kr, nq;
+        if (!b_kn<TN_>(h, tid, kr, nq)) continue;
+        const int kk = k0 + kr, n = n0 + nq;
         int t = 0, c = 0;
         if (kk < kend) split_k(P, kk, t, c);
         const int base = tap_of(P, t).wt * wtap + c * P.wsc;
@@ -213,12 +253,10 @@ __device__ __forceinline__ void load_slice(const ConvProb& P, const Ctx& X, int 
             e4[e] = ld1(X.rw, (kk < kend && n + e < P.N) ? (uint32_t)(base + (n + e) * P.wsn) * 4u : OOB);
           rb[h] = make_float4(e4[0], e4[1], e4[2], e4[3]);
         }
-      }
-    } else {
-      const int kq = k0 + ((tid & 7) << 2);
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int n = n0 + 32 * h + (tid >> 3);
+      } else {
+        int nr, kr;
+        if (!b_nk<TN_>(h, tid, nr, kr)) continue;
+        const int n = n0 + nr, kq = k0 + kr;
         if (!GEN) {
           uint32_t off = OOB;
           if (kq < kend && n < P.N) {
@@ -244,7 +282,7 @@ __device__ __forceinline__ void load_slice(const ConvProb& P, const Ctx& X, int 
       }
     }
   } else {
-    // A [k = position][m = (tap, channel)]; B [k = position][n]
+    // A [k = position][m = (tap, channel)]
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int p = k0 + 16 * h + (tid >> 4);
@@ -268,8 +306,16 @@ __device__ __forceinline__ void load_slice(const ConvProb& P, const Ctx& X, int 
         }
         ra[h] = make_float4(e4[0], e4[1], e4[2], e4[3]);
       }
-      const int n = n0 + ((tid & 15) << 2);
-      const int base = pok ? map_off(P.pmap, q) : 0;
+    }
+    // B [k = position][n]
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      rb[h] = make_float4(0.f, 0.f, 0.f, 0.f);
+      int kr, nq;
+      if (!b_kn<TN_>(h, tid, kr, nq)) continue;
+      const int p = k0 + kr, n = n0 + nq;
+      const bool pok = p < kend;
+      const int base = pok ? map_off(P.pmap, grid_pos(p, P.gh_log, P.gw_log)) : 0;
       if (!GEN) {
         rb[h] = ld4(X.rp, (pok && n < P.N) ? (uint32_t)(base + n) * 4u : OOB);
       } else {
@@ -282,7 +328,7 @@ __device__ __forceinline__ void load_slice(const ConvProb& P, const Ctx& X, int 
   }
 }
 
-template <int MODE, int BT>
+template <int MODE, int BT, int TN_>
 __device__ __forceinline__ void store_slice(const float4 (&ra)[2], const float4 (&rb)[2], float* as, float* bs) {
   const int tid = threadIdx.x;
 #pragma unroll
@@ -290,26 +336,31 @@ __device__ __forceinline__ void store_slice(const float4 (&ra)[2], const float4 
     float* da = MODE == CONV_FWD ? as + (32 * h + (tid >> 3)) * SK + ((tid & 7) << 2)
                                  : as + (16 * h + (tid >> 4)) * SM + ((tid & 15) << 2);
     *reinterpret_cast<float4*>(da) = ra[h];
-    float* db = (MODE == CONV_FWD && BT == 1) ? bs + (32 * h + (tid >> 3)) * SK + ((tid & 7) << 2)
-                                              : bs + (16 * h + (tid >> 4)) * SN + ((tid & 15) << 2);
-    *reinterpret_cast<float4*>(db) = rb[h];
+    if (MODE == CONV_FWD && BT == 1) {
+      int nr, kr;
+      if (b_nk<TN_>(h, tid, nr, kr)) *reinterpret_cast<float4*>(bs + nr * SK + kr) = rb[h];
+    } else {
+      int kr, nq;
+      if (b_kn<TN_>(h, tid, kr, nq)) *reinterpret_cast<float4*>(bs + kr * TW<TN_>::SN + nq) = rb[h];
+    }
   }
 }
 
 // MFMAs of one slice in LDS: two 16-deep k blocks; in block kb, sub-step u
 // of lane group g = l / 16 uses k = 16 kb + 4 g + u for both operands.
-template <int MODE, int BT>
+template <int MODE, int BT, int TN_>
 __device__ __forceinline__ void mma_slice(const float* as, const float* bs, v4f (&acc)[2][2]) {
+  using W = TW<TN_>;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int wm = W::wm(wave), wn = W::wn(wave);
   const int li = lane & 15, lg = lane >> 4;
 #pragma unroll
   for (int kb = 0; kb < TK / 16; ++kb) {
     const int kq = 16 * kb + 4 * lg;
-    float a[2][4], b[2][4];
+    float a[W::TI][4], b[W::TJ][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < W::TI; ++i) {
       const int m = wm + 16 * i + li;
       if (MODE == CONV_FWD) {
         const float4 v = *reinterpret_cast<const float4*>(as + m * SK + kq);
@@ -320,55 +371,57 @@ __device__ __forceinline__ void mma_slice(const float* as, const float* bs, v4f 
       }
     }
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < W::TJ; ++j) {
       const int n = wn + 16 * j + li;
       if (MODE == CONV_FWD && BT == 1) {
         const float4 v = *reinterpret_cast<const float4*>(bs + n * SK + kq);
         b[j][0] = v.x; b[j][1] = v.y; b[j][2] = v.z; b[j][3] = v.w;
       } else {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) b[j][u] = bs[(kq + u) * SN + n];
+        for (int u = 0; u < 4; ++u) b[j][u] = bs[(kq + u) * W::SN + n];
       }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][u], b[0][u], acc[i][0], 0, 0, 0);
-        acc[i][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][u], b[1][u], acc[i][1], 0, 0, 0);
-      }
+      for (int i = 0; i < W::TI; ++i)
+#pragma unroll
+        for (int j = 0; j < W::TJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][u], b[j][u], acc[i][j], 0, 0, 0);
   }
 }
 
-template <int MODE, int BT, int GEN>
+template <int MODE, int BT, int GEN, int TN_>
 __device__ void conv_mainloop(const ConvProb& P, int m0, int n0, int kbeg, int kend, float* As, float* Bs,
                               v4f (&acc)[2][2]) {
   Ctx X;
   setup_ctx<MODE, GEN>(P, m0, X);
   float4 ra[2], rb[2];
-  load_slice<MODE, BT, GEN>(P, X, n0, kbeg, kend, ra, rb);
+  load_slice<MODE, BT, GEN, TN_>(P, X, n0, kbeg, kend, ra, rb);
   int it = 0;
   for (int k0 = kbeg; k0 < kend; k0 += TK, ++it) {
     float* as = As + (it & 1) * TILE_FLOATS;
     float* bs = Bs + (it & 1) * TILE_FLOATS;
-    store_slice<MODE, BT>(ra, rb, as, bs);
+    store_slice<MODE, BT, TN_>(ra, rb, as, bs);
     __syncthreads();
-    if (k0 + TK < kend) load_slice<MODE, BT, GEN>(P, X, n0, k0 + TK, kend, ra, rb);
-    mma_slice<MODE, BT>(as, bs, acc);
+    if (k0 + TK < kend) load_slice<MODE, BT, GEN, TN_>(P, X, n0, k0 + TK, kend, ra, rb);
+    mma_slice<MODE, BT, TN_>(as, bs, acc);
   }
 }
 
+template <int TN_>
 __device__ __forceinline__ void conv_epilogue(const ConvProb& P, const v4f (&acc)[2][2], int m0, int n0, int split,
                                               float slope) {
+  using W = TW<TN_>;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int wm = W::wm(wave), wn = W::wn(wave);
   const int li = lane & 15, lg = lane >> 4;
   LIPZ_GLOBAL float* gC = as_global(P.C);
   if (P.mode == CONV_WG) {
     gC += (int64_t)split * P.split_stride;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < W::TI; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + wm + 16 * i + 4 * lg + r;
@@ -382,7 +435,7 @@ __device__ __forceinline__ void conv_epilogue(const ConvProb& P, const v4f (&acc
         }
         if (crow < 0 || m >= P.M) continue;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < W::TJ; ++j) {
           const int n = n0 + wn + 16 * j + li;
           if (n < P.N) gC[(int64_t)crow * P.ldc + n] = acc[i][j][r];
         }
@@ -392,21 +445,21 @@ __device__ __forceinline__ void conv_epilogue(const ConvProb& P, const v4f (&acc
   float bias[2] = {0.f, 0.f};
   if (P.epi == EPI_BIAS_ACT && P.bias) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < W::TJ; ++j) {
       const int n = n0 + wn + 16 * j + li;
       bias[j] = n < P.N ? as_global(P.bias)[n] : 0.f;
     }
   }
   const LIPZ_GLOBAL float* gAux = as_global(P.aux);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < W::TI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int p = m0 + wm + 16 * i + 4 * lg + r;
       if (p >= P.M) continue;
       const int base = map_off(P.omap, grid_pos(p, P.gh_log, P.gw_log));
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < W::TJ; ++j) {
         const int n = n0 + wn + 16 * j + li;
         if (n >= P.N) continue;
         const int64_t o = (int64_t)base + n;
@@ -418,30 +471,9 @@ __device__ __forceinline__ void conv_epilogue(const ConvProb& P, const v4f (&acc
     }
 }
 
-__global__ __launch_bounds__(NT, 2) void conv_kernel(const ConvProb* __restrict__ probs, GemmGroups grp,
-                                                     float slope) {
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
-  int gi = 0;
-#pragma unroll
-  for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
-    if (q < grp.n && t >= grp.first_tile[q]) gi = q;
-  const int rel = t - grp.first_tile[gi];
-  const int pi = grp.first_prob[gi] + rel / grp.tiles_per_prob[gi];
-  const int lt = rel % grp.tiles_per_prob[gi];
-  const ConvProb P = probs[pi];
-  const int tiles_mn = P.tiles_m * P.tiles_n;
-  const int split = lt / tiles_mn;
-  const int rem = lt - split * tiles_mn;
-  const int m0 = (rem / P.tiles_n) * TM;
-  const int n0 = (rem % P.tiles_n) * TN;
-  int kbeg = 0, kend = P.K;
-  if (P.mode == CONV_WG) {
-    kbeg = split * P.ksplit;
-    kend = min(P.K, kbeg + P.ksplit);
-  }
-
-  __shared__ __align__(16) float As[2 * TILE_FLOATS];
-  __shared__ __align__(16) float Bs[2 * TILE_FLOATS];
+template <int TN_>
+__device__ __forceinline__ void conv_tile(const ConvProb& P, int m0, int n0, int split, int kbeg, int kend, float slope,
+                                          float* As, float* Bs) {
   v4f acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -450,17 +482,46 @@ __global__ __launch_bounds__(NT, 2) void conv_kernel(const ConvProb* __restrict_
   if (P.mode == CONV_FWD) {
     const bool bt = P.wsn != 1;
     if (P.gen) {
-      if (bt) conv_mainloop<CONV_FWD, 1, 1>(P, m0, n0, kbeg, kend, As, Bs, acc);
-      else conv_mainloop<CONV_FWD, 0, 1>(P, m0, n0, kbeg, kend, As, Bs, acc);
+      if (bt) conv_mainloop<CONV_FWD, 1, 1, TN_>(P, m0, n0, kbeg, kend, As, Bs, acc);
+      else conv_mainloop<CONV_FWD, 0, 1, TN_>(P, m0, n0, kbeg, kend, As, Bs, acc);
     } else {
-      if (bt) conv_mainloop<CONV_FWD, 1, 0>(P, m0, n0, kbeg, kend, As, Bs, acc);
-      else conv_mainloop<CONV_FWD, 0, 0>(P, m0, n0, kbeg, kend, As, Bs, acc);
+      if (bt) conv_mainloop<CONV_FWD, 1, 0, TN_>(P, m0, n0, kbeg, kend, As, Bs, acc);
+      else conv_mainloop<CONV_FWD, 0, 0, TN_>(P, m0, n0, kbeg, kend, As, Bs, acc);
     }
   } else {
-    if (P.gen) conv_mainloop<CONV_WG, 0, 1>(P, m0, n0, kbeg, kend, As, Bs, acc);
-    else conv_mainloop<CONV_WG, 0, 0>(P, m0, n0, kbeg, kend, As, Bs, acc);
+    if (P.gen) conv_mainloop<CONV_WG, 0, 1, TN_>(P, m0, n0, kbeg, kend, As, Bs, acc);
+    else conv_mainloop<CONV_WG, 0, 0, TN_>(P, m0, n0, kbeg, kend, As, Bs, acc);
   }
-  conv_epilogue(P, acc, m0, n0, split, slope);
+  conv_epilogue<TN_>(P, acc, m0, n0, split, slope);
+}
+
+__global__ __launch_bounds__(NT, 2) void conv_kernel(const ConvProb* __restrict__ probs, ConvGroups grp,
+                                                     float slope) {
+  const int b = blockIdx.x;
+  int gi = 0;
+#pragma unroll
+  for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
+    if (q < grp.n && b >= grp.first_block[q]) gi = q;
+  // first_block is a multiple of 8, so (b - first_block) % 8 is still the XCD
+  const int rel = xcd_remap(b - grp.first_block[gi], grp.blocks[gi]);
+  if (rel >= grp.real_tiles[gi]) return;
+  const int pi = grp.first_prob[gi] + rel / grp.tiles_per_prob[gi];
+  const int lt = rel % grp.tiles_per_prob[gi];
+  const ConvProb P = probs[pi];
+  const int tiles_mn = P.tiles_m * P.tiles_n;
+  const int split = lt / tiles_mn;
+  const int rem = lt - split * tiles_mn;
+  const int m0 = (rem / P.tiles_n) * TM;
+  const int n0 = (rem % P.tiles_n) * P.tn;
+  int kbeg = 0, kend = P.K;
+  if (P.mode == CONV_WG) {
+    kbeg = split * P.ksplit;
+    kend = min(P.K, kbeg + P.ksplit);
+  }
+  __shared__ __align__(16) float As[2 * TILE_FLOATS];
+  __shared__ __align__(16) float Bs[2 * TILE_FLOATS];
+  if (P.tn == 16) conv_tile<16>(P, m0, n0, split, kbeg, kend, slope, As, Bs);
+  else conv_tile<64>(P, m0, n0, split, kbeg, kend, slope, As, Bs);
 }
 
 // ---------------------------------------------------------------------------
@@ -732,10 +793,10 @@ int blocks_for(int64_t n, int cap = 16384) {
 
 }  // namespace
 
-hipError_t launch_conv_grouped(const ConvProb* d_probs, const GemmGroups& grp, int total_tiles, float slope,
+hipError_t launch_conv_grouped(const ConvProb* d_probs, const ConvGroups& grp, int total_blocks, float slope,
                                hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop) {
-  if (grp.n <= 0 || total_tiles <= 0) return hipSuccess;
-  hipExtLaunchKernelGGL(conv_kernel, dim3(total_tiles), dim3(NT), 0, s, ev_start, ev_stop, 0, d_probs, grp, slope);
+  if (grp.n <= 0 || total_blocks <= 0) return hipSuccess;
+  hipExtLaunchKernelGGL(conv_kernel, dim3(total_blocks), dim3(NT), 0, s, ev_start, ev_stop, 0, d_probs, grp, slope);
   return hipGetLastError();
 }
 

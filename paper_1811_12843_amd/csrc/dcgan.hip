@@ -46,8 +46,8 @@ struct DcNet {
 };
 
 struct ConvPhase {
-  int first = 0, count = 0, tiles = 0;
-  GemmGroups grp;
+  int first = 0, count = 0, tiles = 0;  // tiles: blocks of the launch
+  ConvGroups grp;
   double flops = 0.0;
   double bytes = 0.0;  // algorithmic: each tensor read or written once
 };
@@ -69,7 +69,10 @@ struct DcOp {
   int idx;
 };
 
-constexpr int KSPLIT = 1024;  // positions per split of a weight gradient
+#ifndef LIPZ_CONV_KSPLIT
+#define LIPZ_CONV_KSPLIT 1024
+#endif
+constexpr int KSPLIT = LIPZ_CONV_KSPLIT;  // positions per split of a weight gradient
 
 int ilog2(int v) {
   int l = 0;
@@ -520,28 +523,32 @@ int add_conv_phase(DcPlan& P, const std::vector<ConvProb>& ps) {
   ph.first = (int)P.conv_h.size();
   ph.count = (int)ps.size();
   memset(&ph.grp, 0, sizeof(ph.grp));
-  int tiles = 0, prev = -1;
+  auto round8 = [](int v) { return (v + 7) & ~7; };
+  int blocks = 0, prev = -1;
   for (size_t k = 0; k < ps.size(); ++k) {
     ConvProb p = ps[k];
+    p.tn = p.N <= 16 ? 16 : 64;
     p.tiles_m = (p.M + 63) / 64;
-    p.tiles_n = (p.N + 63) / 64;
+    p.tiles_n = (p.N + p.tn - 1) / p.tn;
     if (p.mode != CONV_WG) p.splits = 1;
-    p.tile_begin = tiles;
     const int tpp = p.tiles_m * p.tiles_n * p.splits;
     if (tpp != prev) {
       if (ph.grp.n == GEMM_MAX_GROUPS) abort();
-      ph.grp.first_tile[ph.grp.n] = tiles;
+      if (ph.grp.n > 0) blocks += round8(ph.grp.real_tiles[ph.grp.n - 1]);
+      ph.grp.first_block[ph.grp.n] = blocks;
       ph.grp.first_prob[ph.grp.n] = (int)k;
       ph.grp.tiles_per_prob[ph.grp.n] = tpp;
       ++ph.grp.n;
       prev = tpp;
     }
-    tiles += tpp;
+    p.tile_begin = ph.grp.real_tiles[ph.grp.n - 1];
+    ph.grp.real_tiles[ph.grp.n - 1] += tpp;
     ph.flops += conv_flops(p);
     ph.bytes += conv_bytes(p);
     P.conv_h.push_back(p);
   }
-  ph.tiles = tiles;
+  for (int gi = 0; gi < ph.grp.n; ++gi) ph.grp.blocks[gi] = round8(ph.grp.real_tiles[gi]);
+  ph.tiles = ph.grp.n ? ph.grp.first_block[ph.grp.n - 1] + ph.grp.blocks[ph.grp.n - 1] : 0;
   P.cph.push_back(ph);
   return (int)P.cph.size() - 1;
 }
@@ -783,7 +790,14 @@ void dc_build(lipz_grid* g) {
       const float* dout = k == n ? P.gdimg : P.gdz[k];
       const int64_t dout_cell = k == n ? (int64_t)B * xd : gsz(k);
       const int rows_total = 16 * L.cin + L.bias;
-      std::vector<ConvProb> ps;
+      // The input gradient (K = 16 c_out, the deepest tiles) and the weight
+      // gradient run as two launches: sharing one launch, the deep tiles of the
+      // first layer ran at less than half their separate speed (measured).
+      std::vector<ConvProb> pd, ps;
+      for (int c = 0; c < C; ++c)
+        pd.push_back(convT_dgrad(dout + c * dout_cell, B, L.in_log, L.cin, L.cout, Gw(c, k),
+                                 P.gdz[k - 1] + c * gsz(k - 1), P.gy[k - 1] + c * gsz(k - 1), G.L[k - 1].act));
+      conv(pd);
       for (int c = 0; c < C; ++c)
         for (int r = 0; r < 2; ++r)
           for (int q = 0; q < 2; ++q)
@@ -793,9 +807,6 @@ void dc_build(lipz_grid* g) {
         for (int c = 0; c < C; ++c)
           ps.push_back(convT_bias_grad(dout + c * dout_cell, B, L.out_log, L.cout, P.gpart[k] + c * P.gpart_cell[k],
                                        rows_total, 16 * L.cin));
-      for (int c = 0; c < C; ++c)
-        ps.push_back(convT_dgrad(dout + c * dout_cell, B, L.in_log, L.cin, L.cout, Gw(c, k),
-                                 P.gdz[k - 1] + c * gsz(k - 1), P.gy[k - 1] + c * gsz(k - 1), G.L[k - 1].act));
       conv(ps);
       // batch-norm backward of layer k - 1 (its dz is complete now)
       const DcLayer& Lb = G.L[k - 1];

@@ -242,12 +242,27 @@ struct ConvProb {
   int32_t epi, act;
   const float* bias;
   const float* aux;
+  int32_t tn;              // tile columns: 64, or 16 when N <= 16
   int32_t tiles_m, tiles_n, tile_begin;
 };
 
-// Launch every problem of one phase (problems in device memory, grouped as
-// for the GEMM); tile counts per problem = tiles_m * tiles_n * splits.
-hipError_t launch_conv_grouped(const ConvProb* d_probs, const GemmGroups& grp, int total_tiles, float slope,
+// A convolution phase's problems in up to 4 groups of consecutive problems
+// with equal tile counts (tiles_m * tiles_n * splits).  Each group starts at
+// a block index that is a multiple of 8 and spans a multiple of 8 blocks
+// (blocks past its real_tiles exit at once), so every XCD receives an equal,
+// contiguous share of every group: groups of long tiles (deep K) are not
+// piled onto a few XCDs.
+struct ConvGroups {
+  int32_t n;
+  int32_t first_block[GEMM_MAX_GROUPS];
+  int32_t blocks[GEMM_MAX_GROUPS];
+  int32_t real_tiles[GEMM_MAX_GROUPS];
+  int32_t first_prob[GEMM_MAX_GROUPS];
+  int32_t tiles_per_prob[GEMM_MAX_GROUPS];
+};
+
+// Launch every problem of one phase (problems in device memory).
+hipError_t launch_conv_grouped(const ConvProb* d_probs, const ConvGroups& grp, int total_blocks, float slope,
                                hipStream_t s, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // Sum of the split partial sums of a weight gradient, in split order, then
