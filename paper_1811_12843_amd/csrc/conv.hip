@@ -249,8 +249,11 @@ __device__ __forceinline__ void load_slice(const ConvProb& P, const Ctx& X, int 
         } else {
           float e4[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            e4[e] = ld1(X.rw, (kk < kend && n + e < P.N) ? (uint32_t)(base + (n + e) * P.wsn) * 4u : OOB);
+          for (int e = 0; e < 4; ++e) {
+            const int nn = n + e;
+            const int no = P.n_inner ? (nn / P.n_inner) * P.n_tap_stride + (nn % P.n_inner) * P.wsn : nn * P.wsn;
+            e4[e] = ld1(X.rw, (kk < kend && nn < P.N) ? (uint32_t)(base + no) * 4u : OOB);
+          }
           rb[h] = make_float4(e4[0], e4[1], e4[2], e4[3]);
         }
       } else {
@@ -420,6 +423,13 @@ __device__ __forceinline__ void conv_epilogue(const ConvProb& P, const v4f (&acc
   LIPZ_GLOBAL float* gC = as_global(P.C);
   if (P.mode == CONV_WG) {
     gC += (int64_t)split * P.split_stride;
+    // column part of the output offset, once per column
+    int coff[W::TJ];
+#pragma unroll
+    for (int j = 0; j < W::TJ; ++j) {
+      const int n = n0 + wn + 16 * j + li;
+      coff[j] = n >= P.N ? -1 : (P.n_inner ? (n / P.n_inner) * P.n_tap_stride + n % P.n_inner : n);
+    }
 #pragma unroll
     for (int i = 0; i < W::TI; ++i)
 #pragma unroll
@@ -435,10 +445,8 @@ __device__ __forceinline__ void conv_epilogue(const ConvProb& P, const v4f (&acc
         }
         if (crow < 0 || m >= P.M) continue;
 #pragma unroll
-        for (int j = 0; j < W::TJ; ++j) {
-          const int n = n0 + wn + 16 * j + li;
-          if (n < P.N) gC[(int64_t)crow * P.ldc + n] = acc[i][j][r];
-        }
+        for (int j = 0; j < W::TJ; ++j)
+          if (coff[j] >= 0) gC[(int64_t)crow * P.ldc + coff[j]] = acc[i][j][r];
       }
     return;
   }
@@ -786,6 +794,66 @@ __global__ void init_conv_params_kernel(float* p, int64_t stride, int64_t P, int
   }
 }
 
+// ---------------------------------------------------------------------------
+// Patches and their inverse gather (ColProb, lipz_internal.h): one thread per
+// column entry / output element, descriptor by binary search on `first`.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int find_col(const ColProb* probs, int n, int64_t i) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (probs[mid].first <= i) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__global__ void im2col_kernel(const ColProb* __restrict__ probs, int n_probs, int64_t total) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const ColProb& Q = probs[find_col(probs, n_probs, i)];
+    const int64_t e = i - Q.first;
+    const int cols = 16 * Q.ch;
+    const int64_t p = e / cols;
+    const int k = (int)(e - p * cols);
+    const int t = k / Q.ch, c = k - t * Q.ch;
+    const int g = Q.h_log - 1;  // grid side log2
+    const int img = (int)(p >> (2 * g)), y = (int)((p >> g) & ((1 << g) - 1)), x = (int)(p & ((1 << g) - 1));
+    const int sy = 2 * y - 1 + (t >> 2), sx = 2 * x - 1 + (t & 3);
+    const int S = 1 << Q.h_log;
+    float v = 0.f;
+    if (sy >= 0 && sy < S && sx >= 0 && sx < S) v = Q.src[(((int64_t)img * S + sy) * S + sx) * Q.ch + c];
+    Q.dst[e] = v;
+  }
+}
+
+__global__ void col2im_kernel(const ColProb* __restrict__ probs, int n_probs, int64_t total, float slope) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const ColProb& Q = probs[find_col(probs, n_probs, i)];
+    const int64_t e = i - Q.first;
+    const int S = 1 << Q.h_log, Gs = S >> 1;
+    const int c = (int)(e % Q.ch);
+    const int64_t pix = e / Q.ch;
+    const int X = (int)(pix % S), Y = (int)((pix / S) % S);
+    const int img = (int)(pix / ((int64_t)S * S));
+    float s = 0.f;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int kh = ((Y + 1) & 1) + 2 * a;
+      const int iy = (Y + 1 - kh) >> 1;
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int kw = ((X + 1) & 1) + 2 * b;
+        const int ix = (X + 1 - kw) >> 1;
+        if (iy >= 0 && iy < Gs && ix >= 0 && ix < Gs)
+          s += Q.src[(((int64_t)img * Gs + iy) * Gs + ix) * (16 * Q.ch) + (kh * 4 + kw) * Q.ch + c];
+      }
+    }
+    if (Q.epi == EPI_BIAS_ACT) s = act_fwd(Q.act, s + (Q.bias ? Q.bias[c] : 0.f), slope);
+    else if (Q.epi == EPI_DACT) s *= act_deriv_from_out(Q.act, Q.aux[e], slope);
+    Q.dst[e] = s;
+  }
+}
+
 int blocks_for(int64_t n, int cap = 16384) {
   const int64_t b = (n + NT - 1) / NT;
   return (int)(b < 1 ? 1 : (b > cap ? cap : b));
@@ -836,6 +904,18 @@ hipError_t launch_bn_backward(const BnProb* d_probs, int n_probs, int total_bloc
 hipError_t launch_dot_rows(const DotProb* d_probs, int n_probs, int total_rows, hipStream_t s) {
   if (n_probs <= 0 || total_rows <= 0) return hipSuccess;
   hipLaunchKernelGGL(dot_rows_kernel, dim3(total_rows), dim3(NT), 0, s, d_probs, n_probs);
+  return hipGetLastError();
+}
+
+hipError_t launch_im2col(const ColProb* d_probs, int n_probs, int64_t total, hipStream_t s) {
+  if (n_probs <= 0 || total <= 0) return hipSuccess;
+  hipLaunchKernelGGL(im2col_kernel, dim3(blocks_for(total, 65536)), dim3(NT), 0, s, d_probs, n_probs, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_col2im(const ColProb* d_probs, int n_probs, int64_t total, float slope, hipStream_t s) {
+  if (n_probs <= 0 || total <= 0) return hipSuccess;
+  hipLaunchKernelGGL(col2im_kernel, dim3(blocks_for(total, 65536)), dim3(NT), 0, s, d_probs, n_probs, total, slope);
   return hipGetLastError();
 }
 

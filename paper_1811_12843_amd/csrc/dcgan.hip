@@ -62,8 +62,14 @@ struct RedOp {
 struct DotOp {
   int first, count, rows;
 };
+struct ColOp {
+  int first, count;
+  int64_t total;
+};
 
-enum DcOpKind { DC_SAMPLE, DC_GEMM, DC_CONV, DC_BN_FWD, DC_BN_BWD, DC_REDUCE, DC_DOT, DC_HEAD_D, DC_HEAD_G };
+enum DcOpKind {
+  DC_SAMPLE, DC_GEMM, DC_CONV, DC_BN_FWD, DC_BN_BWD, DC_REDUCE, DC_DOT, DC_HEAD_D, DC_HEAD_G, DC_IM2COL, DC_COL2IM
+};
 struct DcOp {
   DcOpKind kind;
   int idx;
@@ -306,6 +312,70 @@ ConvProb convT_bias_grad(const float* dout, int NI, int h_out, int cout, float* 
   return p;
 }
 
+// Rows = the positions of a [NI][2^g]^2 grid of a position-major matrix
+// S[p][0..cs) (a 1-tap convolution): out[p][n] = sum_k S[p][k] W(k, n) with
+// W row-major [cs][N], or transposed [N][cs].
+ConvProb dense_rows(const float* S, int NI, int g, int cs, const float* W, int N, bool w_transposed, float* out,
+                    int epi, int act, const float* bias) {
+  ConvProb p = conv_base(CONV_FWD);
+  p.gh_log = p.gw_log = g;
+  p.M = NI << (2 * g);
+  p.N = N;
+  p.K = cs;
+  set_taps(p, 0, cs, 0, 0, 0, 0, 0, 0);
+  p.S = S;
+  p.smap = posmap(g, g, 1, 0, 1, 0, cs);
+  p.s_bytes = extent((int64_t)p.M * cs);
+  p.W = W;
+  p.wsc = w_transposed ? 1 : N;
+  p.wsn = w_transposed ? cs : 1;
+  p.w_bytes = extent((int64_t)cs * N);
+  p.omap = posmap(g, g, 1, 0, 1, 0, N);
+  p.C = out;
+  p.epi = epi;
+  p.act = act;
+  p.bias = bias;
+  p.gen = !(cs % 4 == 0 && N % 4 == 0 && aligned16(S) && aligned16(W));
+  return p;
+}
+
+// Weight gradient of dense_rows (row-major weights, + bias row when
+// with_bias): partial sums of S^T dY over the positions.
+ConvProb dense_rows_wgrad(const float* S, int NI, int g, int cs, const float* dY, int N, float* part, int rows_total,
+                          bool with_bias) {
+  ConvProb p = conv_base(CONV_WG);
+  p.gh_log = p.gw_log = g;
+  p.K = NI << (2 * g);
+  p.M = cs + (with_bias ? 1 : 0);
+  p.N = N;
+  set_taps(p, 0, cs, 0, 0, 0, 0, 0, 0);
+  p.S = S;
+  p.smap = posmap(g, g, 1, 0, 1, 0, cs);
+  p.s_bytes = extent((int64_t)p.K * cs);
+  p.P = dY;
+  p.pmap = posmap(g, g, 1, 0, 1, 0, N);
+  p.p_bytes = extent((int64_t)p.K * N);
+  p.ones_row = with_bias ? cs : -1;
+  p.brow = cs;
+  p.C = part;
+  set_split(p, KSPLIT, rows_total);
+  p.gen = !(cs % 4 == 0 && N % 4 == 0 && aligned16(S) && aligned16(dY));
+  return p;
+}
+
+// Columns of a stride-2 transposed convolution [c_in][16 taps x c_out]
+// (weights [tap][c_in][c_out] read with column taps): out = S W.
+ConvProb convT_cols(const float* S, int NI, int g, int cin, const float* W, int cout, float* cols) {
+  ConvProb p = dense_rows(S, NI, g, cin, W, 16 * cout, false, cols, EPI_STORE, 0, nullptr);
+  p.wsc = cout;
+  p.wsn = 1;
+  p.n_inner = cout;
+  p.n_tap_stride = cin * cout;
+  p.w_bytes = extent((int64_t)16 * cin * cout);
+  p.gen = 1;
+  return p;
+}
+
 double conv_flops(const ConvProb& p) {
   const double rows = p.mode == CONV_WG ? (double)p.taps * p.cs : (double)p.M;
   return 2.0 * rows * p.N * p.K;
@@ -344,7 +414,9 @@ struct DcPlan {
   float *gpart[LIPZ_MAX_HIDDEN + 1] = {}, *dpart[LIPZ_MAX_HIDDEN] = {};
   int64_t gpart_cell[LIPZ_MAX_HIDDEN + 1] = {}, dpart_cell[LIPZ_MAX_HIDDEN] = {};
   // evaluation (per (cell, slot))
+  float *patch = nullptr, *cols = nullptr;  // image patches [2B][..][16 ic]; 16-tap columns [B][..][16 ic]
   float *ze = nullptr, *Xe = nullptr, *part_e = nullptr;
+  float *epatch = nullptr, *ecols = nullptr;
   float *gex[LIPZ_MAX_HIDDEN] = {}, *dey[2] = {};
   float *bne_part[LIPZ_MAX_HIDDEN] = {}, *bne_stats[LIPZ_MAX_HIDDEN] = {};
   // tables
@@ -352,14 +424,17 @@ struct DcPlan {
   std::vector<BnProb> bn_h;
   std::vector<RedProb> red_h;
   std::vector<DotProb> dot_h;
+  std::vector<ColProb> col_h;
   ConvProb* conv_d = nullptr;
   BnProb* bn_d = nullptr;
   RedProb* red_d = nullptr;
   DotProb* dot_d = nullptr;
+  ColProb* col_d = nullptr;
   std::vector<ConvPhase> cph;
   std::vector<BnOp> bnops;
   std::vector<RedOp> redops;
   std::vector<DotOp> dotops;
+  std::vector<ColOp> colops;
   std::vector<DcOp> train_ops[2], eval_ops[2];
 };
 
@@ -484,6 +559,9 @@ void dc_carve(lipz_grid* g, Carver& cv) {
     P.gpart_cell[k] = (int64_t)splits_for(K) * (16 * L.cin + L.bias) * L.cout;
     P.gpart[k] = tf(C * P.gpart_cell[k]);
   }
+  const int64_t pcols = ((int64_t)1 << (2 * (P.img_log - 1))) * 16 * P.ic;  // patch / column floats per image
+  P.patch = tf((int64_t)C * 2 * B * pcols);
+  P.cols = tf((int64_t)C * B * pcols);
   P.part_tr = tf((int64_t)C * 2 * B);
   P.part_g = tf((int64_t)C * B);
   P.dlbuf = tf((int64_t)C * 2 * B * 4);
@@ -491,6 +569,8 @@ void dc_carve(lipz_grid* g, Carver& cv) {
   P.ze = tf((int64_t)C * B * zd);
   P.Xe = tf((int64_t)C * 6 * B * xd);
   P.part_e = tf((int64_t)C * 5 * 6 * B);
+  P.epatch = tf((int64_t)C * 6 * B * pcols);
+  P.ecols = tf((int64_t)C * 5 * B * pcols);
   for (int k = 0; k < n; ++k) {
     const DcLayer& L = P.G.L[k];
     const int64_t rows = (int64_t)B * side_sq(L.out_log);
@@ -514,6 +594,7 @@ void dc_carve_tables(lipz_grid* g, Carver& cv) {
   P.bn_d = cv.take<BnProb>(P.bn_h.size());
   P.red_d = cv.take<RedProb>(P.red_h.size());
   P.dot_d = cv.take<DotProb>(P.dot_h.size());
+  P.col_d = cv.take<ColProb>(P.col_h.size());
 }
 
 namespace {
@@ -583,6 +664,38 @@ int add_red_op(DcPlan& P, const std::vector<RedProb>& rs) {
   return (int)P.redops.size() - 1;
 }
 
+// im2col (to_cols) or col2im descriptors; elements = the columns' size or the map's.
+int add_col_op(DcPlan& P, const std::vector<ColProb>& cs, bool to_cols) {
+  ColOp op;
+  op.first = (int)P.col_h.size();
+  op.count = (int)cs.size();
+  op.total = 0;
+  for (ColProb c : cs) {
+    c.first = op.total;
+    const int64_t map = ((int64_t)c.n_img << (2 * c.h_log)) * c.ch;
+    op.total += to_cols ? 4 * map : map;  // 16 taps per position of the half-size grid
+    P.col_h.push_back(c);
+  }
+  P.colops.push_back(op);
+  return (int)P.colops.size() - 1;
+}
+
+ColProb col_prob(const float* src, float* dst, int n_img, int h_log, int ch, int epi, int act, const float* bias,
+                 const float* aux) {
+  ColProb c;
+  memset(&c, 0, sizeof(c));
+  c.src = src;
+  c.dst = dst;
+  c.n_img = n_img;
+  c.h_log = h_log;
+  c.ch = ch;
+  c.epi = epi;
+  c.act = act;
+  c.bias = bias;
+  c.aux = aux;
+  return c;
+}
+
 int add_dot_op(DcPlan& P, const std::vector<DotProb>& ds) {
   DotOp op;
   op.first = (int)P.dot_h.size();
@@ -624,10 +737,12 @@ void dc_build(lipz_grid* g) {
   P.bn_h.clear();
   P.red_h.clear();
   P.dot_h.clear();
+  P.col_h.clear();
   P.cph.clear();
   P.bnops.clear();
   P.redops.clear();
   P.dotops.clear();
+  P.colops.clear();
   const int C = g->C, B = g->B, zd = g->zd, xd = g->xd, n = P.n;
   const int64_t sG = g->G.stride, sD = g->D.stride;
   const DcNet &G = P.G, &D = P.D;
@@ -643,6 +758,16 @@ void dc_build(lipz_grid* g) {
     auto Dw = [&](int c, int l) { return S.Dp + c * sD + D.L[l].off_w; };
     auto gsz = [&](int k) { return (int64_t)B * side_sq(G.L[k].out_log) * G.L[k].nb; };
     auto dsz = [&](int k) { return side_sq(D.L[k].out_log) * D.L[k].cout; };  // per image
+    const int gimg = P.img_log - 1;                                    // grid side log2 of the image layers
+    const int64_t pcols = side_sq(gimg) * 16 * P.ic;                   // patch / column floats per image
+    const DcLayer& Lg = G.L[n];                                        // G's output layer
+    const DcLayer& L0 = D.L[0];                                        // D's input layer
+    auto im2col = [&](std::vector<DcOp>& o, const std::vector<ColProb>& cs) {
+      o.push_back({DC_IM2COL, add_col_op(P, cs, true)});
+    };
+    auto col2im = [&](std::vector<DcOp>& o, const std::vector<ColProb>& cs) {
+      o.push_back({DC_COL2IM, add_col_op(P, cs, false)});
+    };
     ops.push_back({DC_SAMPLE, -1});
     // ---- G forward ----
     {
@@ -664,33 +789,53 @@ void dc_build(lipz_grid* g) {
       ops.push_back({DC_BN_FWD, add_bn_op(P, bs)});
     };
     bn_fwd(0);
-    for (int k = 1; k <= n; ++k) {
+    for (int k = 1; k < n; ++k) {
       const DcLayer& L = G.L[k];
       std::vector<ConvProb> ps;
       for (int c = 0; c < C; ++c)
         for (int r = 0; r < 2; ++r)
-          for (int q = 0; q < 2; ++q) {
-            if (k < n)
-              ps.push_back(convT_phase(P.gy[k - 1] + c * gsz(k - 1), B, L.in_log, L.cin, Gw(c, k), L.cout,
-                                       P.gx[k] + c * gsz(k), r, q, EPI_STORE, 0, nullptr));
-            else
-              ps.push_back(convT_phase(P.gy[k - 1] + c * gsz(k - 1), B, L.in_log, L.cin, Gw(c, k), L.cout,
-                                       P.Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd, r, q, EPI_BIAS_ACT, L.act,
-                                       S.Gp + c * sG + L.off_b));
-          }
+          for (int q = 0; q < 2; ++q)
+            ps.push_back(convT_phase(P.gy[k - 1] + c * gsz(k - 1), B, L.in_log, L.cin, Gw(c, k), L.cout,
+                                     P.gx[k] + c * gsz(k), r, q, EPI_STORE, 0, nullptr));
       conv(ps);
-      if (k < n) bn_fwd(k);
+      bn_fwd(k);
+    }
+    {
+      // the image layer: 16-tap columns (one GEMM that reads the map once),
+      // then their gather into the fake images with bias and the output act
+      std::vector<ConvProb> ps;
+      std::vector<ColProb> cs;
+      for (int c = 0; c < C; ++c) {
+        ps.push_back(convT_cols(P.gy[n - 1] + c * gsz(n - 1), B, Lg.in_log, Lg.cin, Gw(c, n), Lg.cout,
+                                P.cols + c * B * pcols));
+        cs.push_back(col_prob(P.cols + c * B * pcols, P.Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd, B, P.img_log,
+                              P.ic, EPI_BIAS_ACT, Lg.act, S.Gp + c * sG + Lg.off_b, nullptr));
+      }
+      conv(ps);
+      col2im(ops, cs);
     }
     // ---- D forward on [real; fake] ----
     auto d_forward = [&](int rows_img, bool fake_only, float* const* acts, float* logits_base) {
+      if (!fake_only) {
+        // patches of the 2B real and fake images; the G step reuses the fake half
+        std::vector<ColProb> cs;
+        for (int c = 0; c < C; ++c)
+          cs.push_back(col_prob(P.Xtr + (size_t)c * 2 * B * xd, P.patch + c * 2 * B * pcols, 2 * B, P.img_log, P.ic,
+                                0, 0, nullptr, nullptr));
+        im2col(ops, cs);
+      }
       for (int k = 0; k < n; ++k) {
         const DcLayer& L = D.L[k];
         std::vector<ConvProb> ps;
         for (int c = 0; c < C; ++c) {
-          const float* in = k == 0 ? P.Xtr + (size_t)c * 2 * B * xd + (fake_only ? (size_t)B * xd : 0)
-                                   : acts[k - 1] + c * rows_img * dsz(k - 1);
-          ps.push_back(conv_fwd(in, rows_img, L.in_log, L.cin, Dw(c, k), L.cout, acts[k] + c * rows_img * dsz(k),
-                                EPI_BIAS_ACT, L.act, S.Dp + c * sD + L.off_b));
+          if (k == 0)
+            ps.push_back(dense_rows(P.patch + c * 2 * B * pcols + (fake_only ? B * pcols : 0), rows_img, gimg,
+                                    16 * P.ic, Dw(c, 0), L.cout, false, acts[0] + c * rows_img * dsz(0), EPI_BIAS_ACT,
+                                    L.act, S.Dp + c * sD + L.off_b));
+          else
+            ps.push_back(conv_fwd(acts[k - 1] + c * rows_img * dsz(k - 1), rows_img, L.in_log, L.cin, Dw(c, k),
+                                  L.cout, acts[k] + c * rows_img * dsz(k), EPI_BIAS_ACT, L.act,
+                                  S.Dp + c * sD + L.off_b));
         }
         conv(ps);
       }
@@ -739,9 +884,12 @@ void dc_build(lipz_grid* g) {
                                             P.ddel[k - 1] + c * 2 * B * dsz(k - 1),
                                             P.dy[k - 1] + c * 2 * B * dsz(k - 1), D.L[k - 1].act, r, q));
       for (int c = 0; c < C; ++c) {
-        const float* in = k == 0 ? P.Xtr + (size_t)c * 2 * B * xd : P.dy[k - 1] + c * 2 * B * dsz(k - 1);
-        ps.push_back(conv_wgrad(in, 2 * B, L.in_log, L.cin, P.ddel[k] + c * 2 * B * dsz(k), L.cout,
-                                P.dpart[k] + c * P.dpart_cell[k]));
+        if (k == 0)
+          ps.push_back(dense_rows_wgrad(P.patch + c * 2 * B * pcols, 2 * B, gimg, 16 * P.ic, P.ddel[0] + c * 2 * B * dsz(0),
+                                        L.cout, P.dpart[0] + c * P.dpart_cell[0], 16 * P.ic + 1, true));
+        else
+          ps.push_back(conv_wgrad(P.dy[k - 1] + c * 2 * B * dsz(k - 1), 2 * B, L.in_log, L.cin,
+                                  P.ddel[k] + c * 2 * B * dsz(k), L.cout, P.dpart[k] + c * P.dpart_cell[k]));
       }
       conv(ps);
     }
@@ -769,20 +917,30 @@ void dc_build(lipz_grid* g) {
     // ---- G step: D on the fakes with the updated D ----
     d_forward(B, true, P.dyg, P.part_g);
     ops.push_back({DC_HEAD_G, -1});
-    for (int k = n - 1; k >= 0; --k) {
+    for (int k = n - 1; k >= 1; --k) {
       const DcLayer& L = D.L[k];
       std::vector<ConvProb> ps;
       for (int c = 0; c < C; ++c)
         for (int r = 0; r < 2; ++r)
-          for (int q = 0; q < 2; ++q) {
-            float* din = k >= 1 ? P.ddelg[k - 1] + c * B * dsz(k - 1) : P.gdimg + (size_t)c * B * xd;
-            const float* aux = k >= 1 ? P.dyg[k - 1] + c * B * dsz(k - 1)
-                                      : P.Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd;
-            const int act = k >= 1 ? D.L[k - 1].act : G.L[n].act;
-            ps.push_back(conv_dgrad_phase(P.ddelg[k] + c * B * dsz(k), B, L.in_log, L.cin, L.cout, Dw(c, k), din, aux,
-                                          act, r, q));
-          }
+          for (int q = 0; q < 2; ++q)
+            ps.push_back(conv_dgrad_phase(P.ddelg[k] + c * B * dsz(k), B, L.in_log, L.cin, L.cout, Dw(c, k),
+                                          P.ddelg[k - 1] + c * B * dsz(k - 1), P.dyg[k - 1] + c * B * dsz(k - 1),
+                                          D.L[k - 1].act, r, q));
       conv(ps);
+    }
+    {
+      // into the image: 16-tap columns with D's input weights transposed, then
+      // their gather into dL/d(G's output pre-activation) (times act')
+      std::vector<ConvProb> ps;
+      std::vector<ColProb> cs;
+      for (int c = 0; c < C; ++c) {
+        ps.push_back(dense_rows(P.ddelg[0] + c * B * dsz(0), B, gimg, L0.cout, Dw(c, 0), 16 * P.ic, true,
+                                P.cols + c * B * pcols, EPI_STORE, 0, nullptr));
+        cs.push_back(col_prob(P.cols + c * B * pcols, P.gdimg + (size_t)c * B * xd, B, P.img_log, P.ic, EPI_DACT, Lg.act,
+                              nullptr, P.Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd));
+      }
+      conv(ps);
+      col2im(ops, cs);
     }
     // ---- G backward ----
     for (int k = n; k >= 1; --k) {
@@ -798,11 +956,30 @@ void dc_build(lipz_grid* g) {
         pd.push_back(convT_dgrad(dout + c * dout_cell, B, L.in_log, L.cin, L.cout, Gw(c, k),
                                  P.gdz[k - 1] + c * gsz(k - 1), P.gy[k - 1] + c * gsz(k - 1), G.L[k - 1].act));
       conv(pd);
-      for (int c = 0; c < C; ++c)
-        for (int r = 0; r < 2; ++r)
-          for (int q = 0; q < 2; ++q)
-            ps.push_back(convT_wgrad_phase(P.gy[k - 1] + c * gsz(k - 1), B, L.in_log, L.cin, dout + c * dout_cell,
-                                           L.cout, P.gpart[k] + c * P.gpart_cell[k], rows_total, r, q));
+      if (k == n) {
+        // patches of the image gradient: the 16 taps x c_out columns of every input position
+        std::vector<ColProb> cs;
+        for (int c = 0; c < C; ++c)
+          cs.push_back(col_prob(P.gdimg + (size_t)c * B * xd, P.cols + c * B * pcols, B, P.img_log, P.ic, 0, 0, nullptr,
+                                nullptr));
+        im2col(ops, cs);
+        for (int c = 0; c < C; ++c) {
+          ConvProb p = dense_rows_wgrad(P.gy[k - 1] + c * gsz(k - 1), B, L.in_log, L.cin, P.cols + c * B * pcols,
+                                        16 * L.cout, P.gpart[k] + c * P.gpart_cell[k], rows_total, false);
+          // column n = (tap, c_out) lands on weight row tap * c_in + c_in index
+          p.ldc = L.cout;
+          p.n_inner = L.cout;
+          p.n_tap_stride = L.cin * L.cout;
+          p.split_stride = (int64_t)rows_total * L.cout;
+          ps.push_back(p);
+        }
+      } else {
+        for (int c = 0; c < C; ++c)
+          for (int r = 0; r < 2; ++r)
+            for (int q = 0; q < 2; ++q)
+              ps.push_back(convT_wgrad_phase(P.gy[k - 1] + c * gsz(k - 1), B, L.in_log, L.cin, dout + c * dout_cell,
+                                             L.cout, P.gpart[k] + c * P.gpart_cell[k], rows_total, r, q));
+      }
       if (L.bias)
         for (int c = 0; c < C; ++c)
           ps.push_back(convT_bias_grad(dout + c * dout_cell, B, L.out_log, L.cout, P.gpart[k] + c * P.gpart_cell[k],
@@ -889,26 +1066,42 @@ void dc_build(lipz_grid* g) {
       ev.push_back({DC_BN_FWD, add_bn_op(P, bs)});
     };
     ebn(0);
-    for (int k = 1; k <= n; ++k) {
+    for (int k = 1; k < n; ++k) {
       const DcLayer& L = G.L[k];
       std::vector<ConvProb> ps;
       for (int c = 0; c < C; ++c)
         for (int i = 0; i < 5; ++i) {
           const int own = g->nbr_h[c * 5 + i];
           for (int r = 0; r < 2; ++r)
-            for (int q = 0; q < 2; ++q) {
-              const float* in = P.gex[k - 1] + (c * 5 + i) * egsz(k - 1);
-              if (k < n)
-                ps.push_back(convT_phase(in, B, L.in_log, L.cin, Gw(own, k), L.cout, P.gex[k] + (c * 5 + i) * egsz(k),
-                                         r, q, EPI_STORE, 0, nullptr));
-              else
-                ps.push_back(convT_phase(in, B, L.in_log, L.cin, Gw(own, k), L.cout,
-                                         P.Xe + (size_t)c * 6 * B * xd + (size_t)(1 + i) * B * xd, r, q, EPI_BIAS_ACT,
-                                         L.act, S.Gp + own * sG + L.off_b));
-            }
+            for (int q = 0; q < 2; ++q)
+              ps.push_back(convT_phase(P.gex[k - 1] + (c * 5 + i) * egsz(k - 1), B, L.in_log, L.cin, Gw(own, k), L.cout,
+                                       P.gex[k] + (c * 5 + i) * egsz(k), r, q, EPI_STORE, 0, nullptr));
         }
       ev.push_back({DC_CONV, add_conv_phase(P, ps)});
-      if (k < n) ebn(k);
+      ebn(k);
+    }
+    {
+      std::vector<ConvProb> ps;
+      std::vector<ColProb> cs;
+      for (int c = 0; c < C; ++c)
+        for (int i = 0; i < 5; ++i) {
+          const int own = g->nbr_h[c * 5 + i];
+          float* cols = P.ecols + (c * 5 + i) * B * pcols;
+          ps.push_back(convT_cols(P.gex[n - 1] + (c * 5 + i) * egsz(n - 1), B, Lg.in_log, Lg.cin, Gw(own, n), Lg.cout,
+                                  cols));
+          cs.push_back(col_prob(cols, P.Xe + (size_t)c * 6 * B * xd + (size_t)(1 + i) * B * xd, B, P.img_log, P.ic,
+                                EPI_BIAS_ACT, Lg.act, S.Gp + own * sG + Lg.off_b, nullptr));
+        }
+      ev.push_back({DC_CONV, add_conv_phase(P, ps)});
+      col2im(ev, cs);
+    }
+    {
+      // patches of each cell's 6B images, shared by its 5 discriminator slots
+      std::vector<ColProb> cs;
+      for (int c = 0; c < C; ++c)
+        cs.push_back(col_prob(P.Xe + (size_t)c * 6 * B * xd, P.epatch + c * NIe * pcols, NIe, P.img_log, P.ic, 0, 0,
+                              nullptr, nullptr));
+      im2col(ev, cs);
     }
     for (int k = 0; k < n; ++k) {
       const DcLayer& L = D.L[k];
@@ -916,9 +1109,13 @@ void dc_build(lipz_grid* g) {
       for (int c = 0; c < C; ++c)
         for (int j = 0; j < 5; ++j) {
           const int own = g->nbr_h[c * 5 + j];
-          const float* in = k == 0 ? P.Xe + (size_t)c * 6 * B * xd : P.dey[(k - 1) & 1] + (c * 5 + j) * NIe * dsz(k - 1);
-          ps.push_back(conv_fwd(in, NIe, L.in_log, L.cin, Dw(own, k), L.cout, P.dey[k & 1] + (c * 5 + j) * NIe * dsz(k),
-                                EPI_BIAS_ACT, L.act, S.Dp + own * sD + L.off_b));
+          float* out = P.dey[k & 1] + (c * 5 + j) * NIe * dsz(k);
+          if (k == 0)
+            ps.push_back(dense_rows(P.epatch + c * NIe * pcols, NIe, gimg, 16 * P.ic, Dw(own, 0), L.cout, false, out,
+                                    EPI_BIAS_ACT, L.act, S.Dp + own * sD + L.off_b));
+          else
+            ps.push_back(conv_fwd(P.dey[(k - 1) & 1] + (c * 5 + j) * NIe * dsz(k - 1), NIe, L.in_log, L.cin, Dw(own, k),
+                                  L.cout, out, EPI_BIAS_ACT, L.act, S.Dp + own * sD + L.off_b));
         }
       ev.push_back({DC_CONV, add_conv_phase(P, ps)});
     }
@@ -951,6 +1148,8 @@ hipError_t dc_upload_tables(lipz_grid* g, hipStream_t s) {
     e = hipMemcpyAsync(P.bn_d, P.bn_h.data(), P.bn_h.size() * sizeof(BnProb), hipMemcpyHostToDevice, s);
   if (e == hipSuccess && !P.red_h.empty())
     e = hipMemcpyAsync(P.red_d, P.red_h.data(), P.red_h.size() * sizeof(RedProb), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !P.col_h.empty())
+    e = hipMemcpyAsync(P.col_d, P.col_h.data(), P.col_h.size() * sizeof(ColProb), hipMemcpyHostToDevice, s);
   if (e == hipSuccess && !P.dot_h.empty())
     e = hipMemcpyAsync(P.dot_d, P.dot_h.data(), P.dot_h.size() * sizeof(DotProb), hipMemcpyHostToDevice, s);
   return e;
@@ -1009,6 +1208,14 @@ hipError_t run_op(lipz_grid* g, const DcOp& op, int step_local, hipStream_t s) {
     case DC_REDUCE: {
       const RedOp& r = P.redops[op.idx];
       return launch_reduce_adam(P.red_d + r.first, r.count, r.max_n, step_local, g->ac, s);
+    }
+    case DC_IM2COL: {
+      const ColOp& c = P.colops[op.idx];
+      return launch_im2col(P.col_d + c.first, c.count, c.total, s);
+    }
+    case DC_COL2IM: {
+      const ColOp& c = P.colops[op.idx];
+      return launch_col2im(P.col_d + c.first, c.count, c.total, g->slope, s);
     }
     case DC_DOT: {
       const DotOp& d = P.dotops[op.idx];
@@ -1138,6 +1345,18 @@ int64_t map_last(const PosMap& m, int NI, int gh, int gw, int N) {
 }
 int64_t map_first(const PosMap& m) { return (((int64_t)m.y0 << m.w_log) + m.x0) * m.ld; }
 
+// True when column descriptor i belongs to an im2col op.
+bool col_is_im2col(const DcPlan& P, int i) {
+  for (int par = 0; par < 2; ++par)
+    for (const auto* ops : {&P.train_ops[par], &P.eval_ops[par]})
+      for (const DcOp& op : *ops)
+        if (op.kind == DC_IM2COL || op.kind == DC_COL2IM) {
+          const ColOp& c = P.colops[op.idx];
+          if (i >= c.first && i < c.first + c.count) return op.kind == DC_IM2COL;
+        }
+  return false;
+}
+
 }  // namespace
 
 int dc_check_bounds(const lipz_grid* g, const char* const* lo, const char* const* hi, int nreg, std::string* msg) {
@@ -1159,7 +1378,10 @@ int dc_check_bounds(const lipz_grid* g, const char* const* lo, const char* const
         const int a = t >> p.tw_log, b = t & ((1 << p.tw_log) - 1);
         const int64_t wt = (int64_t)(a * p.khs + p.kh0) * p.kw_full + (b * p.khs + p.kw0);
         if (wt < 0) ck.fail_("conv", idx, "negative weight tap");
-        const int64_t o = wt * p.cs * p.N + (int64_t)(p.cs - 1) * p.wsc + (int64_t)(p.N - 1) * p.wsn;
+        const int64_t ncol = p.n_inner ? (int64_t)(p.N / p.n_inner - 1) * p.n_tap_stride + (int64_t)(p.n_inner - 1) * p.wsn
+                                       : (int64_t)(p.N - 1) * p.wsn;
+        if (p.n_inner && (p.N % p.n_inner || !p.gen)) ck.fail_("conv", idx, "column taps need element-wise loads");
+        const int64_t o = wt * p.cs * p.N + (int64_t)(p.cs - 1) * p.wsc + ncol;
         if (o > wmax) wmax = o;
       }
       if (wmax >= (int64_t)p.w_bytes / 4) ck.fail_("conv", idx, "weights beyond their extent");
@@ -1185,9 +1407,11 @@ int dc_check_bounds(const lipz_grid* g, const char* const* lo, const char* const
         if (wt < 0) ck.fail_("conv", idx, "negative weight tap");
         if (r > crow_max) crow_max = r;
       }
-      if ((crow_max + 1) * p.ldc > p.split_stride) ck.fail_("conv", idx, "partial rows overlap the next split");
+      const int64_t col_last = p.n_inner ? (int64_t)(p.N / p.n_inner - 1) * p.n_tap_stride + p.n_inner - 1 : p.N - 1;
+      if (p.n_inner && (p.N % p.n_inner || p.ldc < p.n_inner)) ck.fail_("conv", idx, "bad column taps");
+      if (crow_max * p.ldc + col_last >= p.split_stride) ck.fail_("conv", idx, "partial rows overlap the next split");
       if (p.splits < 1 || (int64_t)(p.splits - 1) * p.ksplit >= p.K) ck.fail_("conv", idx, "bad split count");
-      ck.range(p.C, 0, (int64_t)(p.splits - 1) * p.split_stride + crow_max * p.ldc + p.N - 1, "conv partial", idx);
+      ck.range(p.C, 0, (int64_t)(p.splits - 1) * p.split_stride + crow_max * p.ldc + col_last, "conv partial", idx);
     }
   }
   for (size_t i = 0; i < P.bn_h.size(); ++i) {
@@ -1213,6 +1437,16 @@ int dc_check_bounds(const lipz_grid* g, const char* const* lo, const char* const
     ck.range(r.v, 0, r.n - 1, "reduce v", idx);
     ck.range(r.lr, 0, 0, "reduce lr", idx);
     ck.range(r.t, 0, 0, "reduce t", idx);
+  }
+  for (size_t i = 0; i < P.col_h.size(); ++i) {
+    const ColProb& c = P.col_h[i];
+    const int idx = (int)i;
+    const int64_t map = ((int64_t)c.n_img << (2 * c.h_log)) * c.ch;
+    const bool to_cols = col_is_im2col(P, (int)i);
+    ck.range(c.src, 0, (to_cols ? map : 4 * map) - 1, "col src", idx);
+    ck.range(c.dst, 0, (to_cols ? 4 * map : map) - 1, "col dst", idx);
+    if (!to_cols && c.epi == EPI_BIAS_ACT && c.bias) ck.range(c.bias, 0, c.ch - 1, "col bias", idx);
+    if (!to_cols && c.epi == EPI_DACT) ck.range(c.aux, 0, map - 1, "col aux", idx);
   }
   for (size_t i = 0; i < P.dot_h.size(); ++i) {
     const DotProb& d = P.dot_h[i];

@@ -244,7 +244,37 @@ struct ConvProb {
   const float* aux;
   int32_t tn;              // tile columns: 64, or 16 when N <= 16
   int32_t tiles_m, tiles_n, tile_begin;
+  // Column taps (0 = off; element-wise loads only): column n is (tap n /
+  // n_inner, channel n % n_inner).  CONV_FWD: B(k, n) = W[k-part +
+  // (n / n_inner) * n_tap_stride + (n % n_inner) * wsn].  CONV_WG: output
+  // (m, n) goes to row-block n / n_inner: C + (n / n_inner) * n_tap_stride +
+  // row(m) * ldc + n % n_inner.
+  int32_t n_inner, n_tap_stride;
 };
+
+// Patches of a 4x4, stride-2, pad-1 window (im2col): for every position
+// (img, y, x) of a [NI][2^(h-1)]^2 grid,
+//   dst[p][(kh * 4 + kw) * ch + c] = src[img][2y - 1 + kh][2x - 1 + kw][c] (0 outside).
+// Its inverse gather (col2im) sums, for every element (img, Y, X, c) of a
+// [NI][2^h]^2[ch] map, the 4 column entries that land on it:
+//   out = sum over kh = (Y + 1) mod 2 + {0, 2}, kw likewise, with
+//         (iy, ix) = ((Y + 1 - kh) / 2, (X + 1 - kw) / 2) inside the grid, of
+//         cols[(img, iy, ix)][(kh * 4 + kw) * ch + c]
+// in the order kh, kw ascending, then the epilogue: act(out + bias[c])
+// (EPI_BIAS_ACT) or out * act'(aux at the output's index) (EPI_DACT).  The
+// first is a stride-2 transposed convolution's output from its 16-tap
+// columns; the second a stride-2 convolution's input gradient.
+struct ColProb {
+  const float* src;        // im2col: the map; col2im: the columns
+  float* dst;              // im2col: the columns; col2im: the map
+  const float* bias;
+  const float* aux;
+  int32_t n_img, h_log, ch;  // map [n_img][2^h][2^h][ch]
+  int32_t epi, act;
+  int64_t first;           // prefix of elements over preceding descriptors
+};
+hipError_t launch_im2col(const ColProb* d_probs, int n_probs, int64_t total, hipStream_t s);
+hipError_t launch_col2im(const ColProb* d_probs, int n_probs, int64_t total, float slope, hipStream_t s);
 
 // A convolution phase's problems in up to 4 groups of consecutive problems
 // with equal tile counts (tiles_m * tiles_n * splits).  Each group starts at

@@ -69,9 +69,9 @@ def test_workspace_sizing_and_validation():
     c.abi_version = 99
     assert L.lipz_workspace_bytes(c, 60000) == 0
     assert L.lipz_workspace_bytes(L.config_from_dict(w), 0) == 0
-    # the 64x64 DCGAN grid: ~21.7 GiB (evaluation activations of 80 (cell, slot) pairs dominate)
+    # the 64x64 DCGAN grid: ~24 GiB (evaluation activations of 80 (cell, slot) pairs dominate)
     nb = L.lipz_workspace_bytes(L.config_from_dict(synth.workload("celeba_dcgan_4x4")), 1000)
-    assert 20 * 2**30 < nb < 24 * 2**30 and nb % 256 == 0
+    assert 20 * 2**30 < nb < 28 * 2**30 and nb % 256 == 0
 
 
 def test_create_rejects_bad_arguments_without_touching_the_gpu():
