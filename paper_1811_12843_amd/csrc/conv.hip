@@ -795,46 +795,36 @@ __global__ void init_conv_params_kernel(float* p, int64_t stride, int64_t P, int
 }
 
 // ---------------------------------------------------------------------------
-// Patches and their inverse gather (ColProb, lipz_internal.h): one thread per
-// column entry / output element, descriptor by binary search on `first`.
+// Patches and their inverse gather (ColProb, lipz_internal.h).  Grid (x,
+// descriptor).  im2col: one thread per (position, tap) copies its ch
+// channels; col2im: one thread per output element.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int find_col(const ColProb* probs, int n, int64_t i) {
-  int lo = 0, hi = n - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (probs[mid].first <= i) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
-
-__global__ void im2col_kernel(const ColProb* __restrict__ probs, int n_probs, int64_t total) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    const ColProb& Q = probs[find_col(probs, n_probs, i)];
-    const int64_t e = i - Q.first;
-    const int cols = 16 * Q.ch;
-    const int64_t p = e / cols;
-    const int k = (int)(e - p * cols);
-    const int t = k / Q.ch, c = k - t * Q.ch;
-    const int g = Q.h_log - 1;  // grid side log2
+__global__ void im2col_kernel(const ColProb* __restrict__ probs) {
+  const ColProb& Q = probs[blockIdx.y];
+  const int g = Q.h_log - 1;  // grid side log2
+  const int S = 1 << Q.h_log;
+  const int64_t n = ((int64_t)Q.n_img << (2 * g)) * 16;  // (position, tap) pairs
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int t = (int)(i & 15);
+    const int64_t p = i >> 4;
     const int img = (int)(p >> (2 * g)), y = (int)((p >> g) & ((1 << g) - 1)), x = (int)(p & ((1 << g) - 1));
     const int sy = 2 * y - 1 + (t >> 2), sx = 2 * x - 1 + (t & 3);
-    const int S = 1 << Q.h_log;
-    float v = 0.f;
-    if (sy >= 0 && sy < S && sx >= 0 && sx < S) v = Q.src[(((int64_t)img * S + sy) * S + sx) * Q.ch + c];
-    Q.dst[e] = v;
+    const bool in = sy >= 0 && sy < S && sx >= 0 && sx < S;
+    const float* src = Q.src + (((int64_t)img * S + (in ? sy : 0)) * S + (in ? sx : 0)) * Q.ch;
+    float* dst = Q.dst + i * Q.ch;
+    for (int c = 0; c < Q.ch; ++c) dst[c] = in ? src[c] : 0.f;
   }
 }
 
-__global__ void col2im_kernel(const ColProb* __restrict__ probs, int n_probs, int64_t total, float slope) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    const ColProb& Q = probs[find_col(probs, n_probs, i)];
-    const int64_t e = i - Q.first;
-    const int S = 1 << Q.h_log, Gs = S >> 1;
+__global__ void col2im_kernel(const ColProb* __restrict__ probs, float slope) {
+  const ColProb& Q = probs[blockIdx.y];
+  const int S = 1 << Q.h_log, Gs = S >> 1;
+  const int64_t n = ((int64_t)Q.n_img << (2 * Q.h_log)) * Q.ch;
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
     const int c = (int)(e % Q.ch);
     const int64_t pix = e / Q.ch;
-    const int X = (int)(pix % S), Y = (int)((pix / S) % S);
-    const int img = (int)(pix / ((int64_t)S * S));
+    const int X = (int)(pix & (S - 1)), Y = (int)((pix >> Q.h_log) & (S - 1));
+    const int img = (int)(pix >> (2 * Q.h_log));
     float s = 0.f;
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
@@ -907,15 +897,15 @@ hipError_t launch_dot_rows(const DotProb* d_probs, int n_probs, int total_rows, 
   return hipGetLastError();
 }
 
-hipError_t launch_im2col(const ColProb* d_probs, int n_probs, int64_t total, hipStream_t s) {
-  if (n_probs <= 0 || total <= 0) return hipSuccess;
-  hipLaunchKernelGGL(im2col_kernel, dim3(blocks_for(total, 65536)), dim3(NT), 0, s, d_probs, n_probs, total);
+hipError_t launch_im2col(const ColProb* d_probs, int n_probs, int64_t max_pairs, hipStream_t s) {
+  if (n_probs <= 0 || max_pairs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(im2col_kernel, dim3(blocks_for(max_pairs, 8192), n_probs), dim3(NT), 0, s, d_probs);
   return hipGetLastError();
 }
 
-hipError_t launch_col2im(const ColProb* d_probs, int n_probs, int64_t total, float slope, hipStream_t s) {
-  if (n_probs <= 0 || total <= 0) return hipSuccess;
-  hipLaunchKernelGGL(col2im_kernel, dim3(blocks_for(total, 65536)), dim3(NT), 0, s, d_probs, n_probs, total, slope);
+hipError_t launch_col2im(const ColProb* d_probs, int n_probs, int64_t max_elems, float slope, hipStream_t s) {
+  if (n_probs <= 0 || max_elems <= 0) return hipSuccess;
+  hipLaunchKernelGGL(col2im_kernel, dim3(blocks_for(max_elems, 8192), n_probs), dim3(NT), 0, s, d_probs, slope);
   return hipGetLastError();
 }
 

@@ -64,7 +64,7 @@ struct DotOp {
 };
 struct ColOp {
   int first, count;
-  int64_t total;
+  int64_t max_work;  // im2col: (position, tap) pairs; col2im: map elements (per descriptor, the largest)
 };
 
 enum DcOpKind {
@@ -664,16 +664,15 @@ int add_red_op(DcPlan& P, const std::vector<RedProb>& rs) {
   return (int)P.redops.size() - 1;
 }
 
-// im2col (to_cols) or col2im descriptors; elements = the columns' size or the map's.
+// im2col (to_cols) or col2im descriptors.
 int add_col_op(DcPlan& P, const std::vector<ColProb>& cs, bool to_cols) {
   ColOp op;
   op.first = (int)P.col_h.size();
   op.count = (int)cs.size();
-  op.total = 0;
-  for (ColProb c : cs) {
-    c.first = op.total;
-    const int64_t map = ((int64_t)c.n_img << (2 * c.h_log)) * c.ch;
-    op.total += to_cols ? 4 * map : map;  // 16 taps per position of the half-size grid
+  op.max_work = 0;
+  for (const ColProb& c : cs) {
+    const int64_t w = to_cols ? ((int64_t)c.n_img << (2 * (c.h_log - 1))) * 16 : ((int64_t)c.n_img << (2 * c.h_log)) * c.ch;
+    if (w > op.max_work) op.max_work = w;
     P.col_h.push_back(c);
   }
   P.colops.push_back(op);
@@ -1211,11 +1210,11 @@ hipError_t run_op(lipz_grid* g, const DcOp& op, int step_local, hipStream_t s) {
     }
     case DC_IM2COL: {
       const ColOp& c = P.colops[op.idx];
-      return launch_im2col(P.col_d + c.first, c.count, c.total, s);
+      return launch_im2col(P.col_d + c.first, c.count, c.max_work, s);
     }
     case DC_COL2IM: {
       const ColOp& c = P.colops[op.idx];
-      return launch_col2im(P.col_d + c.first, c.count, c.total, g->slope, s);
+      return launch_col2im(P.col_d + c.first, c.count, c.max_work, g->slope, s);
     }
     case DC_DOT: {
       const DotOp& d = P.dotops[op.idx];

@@ -271,10 +271,11 @@ struct ColProb {
   const float* aux;
   int32_t n_img, h_log, ch;  // map [n_img][2^h][2^h][ch]
   int32_t epi, act;
-  int64_t first;           // prefix of elements over preceding descriptors
 };
-hipError_t launch_im2col(const ColProb* d_probs, int n_probs, int64_t total, hipStream_t s);
-hipError_t launch_col2im(const ColProb* d_probs, int n_probs, int64_t total, float slope, hipStream_t s);
+// max_pairs: the largest (position, tap) count of the descriptors (n_img *
+// 2^(2h-2) * 16); max_elems: the largest map (n_img * 2^(2h) * ch).
+hipError_t launch_im2col(const ColProb* d_probs, int n_probs, int64_t max_pairs, hipStream_t s);
+hipError_t launch_col2im(const ColProb* d_probs, int n_probs, int64_t max_elems, float slope, hipStream_t s);
 
 // A convolution phase's problems in up to 4 groups of consecutive problems
 // with equal tile counts (tiles_m * tiles_n * splits).  Each group starts at
