@@ -179,6 +179,7 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     g->fm = cv.take<float>((size_t)C * S * F);
     g->mu_k = cv.take<float>((size_t)C * F);
     g->s2_k = cv.take<float>((size_t)C * F);
+    g->mom_part = cv.take<float>((size_t)C * ((S + 63) / 64) * 2 * F);
     g->P = cv.take<float>((size_t)xd * F);
     g->mu_r = cv.take<float>(F);
     g->sd_r = cv.take<float>(F);
@@ -932,7 +933,7 @@ lipz_status lipz_mixture_update(lipz_grid* g, int32_t gen, float* d_w, float* d_
   if ((st = check_hip(g, e, "mixture latents"))) return st;
   for (int ph : g->mix_phases[par])
     if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "mixture forward"))) return st;
-  e = launch_moments(g->fm, g->C, g->S, g->F, g->mu_k, g->s2_k, s);
+  e = launch_moments(g->fm, g->C, g->S, g->F, g->mom_part, g->mu_k, g->s2_k, s);
   if ((st = check_hip(g, e, "mixture moments"))) return st;
   EsArgs ea;
   ea.mu = g->mu_k;

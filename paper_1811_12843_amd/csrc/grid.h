@@ -112,7 +112,7 @@ struct lipz_grid {
   float *ze = nullptr, *Xe = nullptr;
   float *he[LIPZ_MAX_HIDDEN] = {}, *ae[LIPZ_MAX_HIDDEN] = {};
   // mixture buffers
-  float *zeta = nullptr, *xm = nullptr, *fm = nullptr, *mu_k = nullptr, *s2_k = nullptr;
+  float *zeta = nullptr, *xm = nullptr, *fm = nullptr, *mu_k = nullptr, *s2_k = nullptr, *mom_part = nullptr;
   float *hm[LIPZ_MAX_HIDDEN] = {};
   float *P = nullptr, *mu_r = nullptr, *sd_r = nullptr, *realfeat = nullptr;
 

@@ -308,20 +308,51 @@ __global__ void copy_winners_kernel(CopyArgs A) {
     A.w_dst[c * 5 + threadIdx.x] = A.w_src[c * 5 + threadIdx.x];
 }
 
-// Per-cell feature moments over S samples: mu = mean f, s2 = mean f^2.
-__global__ void moments_kernel(const float* feats, int S, int F, float* mu, float* s2) {
-  const int c = blockIdx.x;
-  for (int f = threadIdx.x; f < F; f += blockDim.x) {
+// Per-cell feature moments over S samples: mu = mean f, s2 = mean f^2, in a
+// fixed order.  Stage 1, block (chunk, cell): 4 row lanes x 64 features sum
+// MOM_ROWS rows of a chunk, combined in lane order; stage 2, thread (cell, f):
+// the chunk sums in chunk order.
+constexpr int MOM_ROWS = 64;
+
+__global__ __launch_bounds__(NT) void moments_chunk_kernel(const float* feats, int S, int F, float* part) {
+  __shared__ float red[2][4][64];
+  const int chunk = blockIdx.x, c = blockIdx.y, n_chunks = gridDim.x;
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  for (int f0 = 0; f0 < F; f0 += 64) {
+    const int f = f0 + l;
     float s = 0.f, q = 0.f;
-    const float* x = feats + (int64_t)c * S * F + f;
-    for (int r = 0; r < S; ++r) {
-      const float v = x[(int64_t)r * F];
-      s += v;
-      q += v * v;
+    if (f < F) {
+      const int r1 = min(S, (chunk + 1) * MOM_ROWS);
+      for (int r = chunk * MOM_ROWS + w; r < r1; r += 4) {
+        const float v = feats[((int64_t)c * S + r) * F + f];
+        s += v;
+        q += v * v;
+      }
     }
-    mu[c * F + f] = s / (float)S;
-    s2[c * F + f] = q / (float)S;
+    __syncthreads();
+    red[0][w][l] = s;
+    red[1][w][l] = q;
+    __syncthreads();
+    if (w == 0 && f < F) {
+      float* o = part + (((int64_t)c * n_chunks + chunk) * 2) * F;
+      o[f] = (red[0][0][l] + red[0][1][l]) + (red[0][2][l] + red[0][3][l]);
+      o[F + f] = (red[1][0][l] + red[1][1][l]) + (red[1][2][l] + red[1][3][l]);
+    }
   }
+}
+
+__global__ void moments_final_kernel(const float* part, int n_chunks, int C, int S, int F, float* mu, float* s2) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= C * F) return;
+  const int c = i / F, f = i - c * F;
+  float s = 0.f, q = 0.f;
+  for (int k = 0; k < n_chunks; ++k) {
+    const float* o = part + (((int64_t)c * n_chunks + k) * 2) * F;
+    s += o[f];
+    q += o[F + f];
+  }
+  mu[i] = s / (float)S;
+  s2[i] = q / (float)S;
 }
 
 // Column mean and (biased, two-pass) standard deviation over N rows.
@@ -470,9 +501,12 @@ hipError_t launch_copy_winners(const CopyArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(copy_winners_kernel, dim3(grid_for(n4, NT, 64), a.C, 2), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
-hipError_t launch_moments(const float* feats, int C, int S, int F, float* mu, float* s2,
+hipError_t launch_moments(const float* feats, int C, int S, int F, float* part, float* mu, float* s2,
                           hipStream_t s) {
-  hipLaunchKernelGGL(moments_kernel, dim3(C), dim3(64), 0, s, feats, S, F, mu, s2);
+  const int n_chunks = (S + MOM_ROWS - 1) / MOM_ROWS;
+  hipLaunchKernelGGL(moments_chunk_kernel, dim3(n_chunks, C), dim3(NT), 0, s, feats, S, F, part);
+  hipLaunchKernelGGL(moments_final_kernel, dim3(grid_for((int64_t)C * F)), dim3(NT), 0, s, part, n_chunks, C, S, F,
+                     mu, s2);
   return hipGetLastError();
 }
 hipError_t launch_col_stats(const float* feats, int64_t N, int F, float* mu, float* sd,

@@ -447,7 +447,8 @@ struct CopyArgs {
 hipError_t launch_copy_winners(const CopyArgs& a, hipStream_t s);
 hipError_t launch_add_i32(int32_t* p, int n, int32_t v, hipStream_t s);
 
-hipError_t launch_moments(const float* feats, int C, int S, int F, float* mu, float* s2, hipStream_t s);
+// part: scratch of C * ceil(S / 64) * 2 * F floats.
+hipError_t launch_moments(const float* feats, int C, int S, int F, float* part, float* mu, float* s2, hipStream_t s);
 hipError_t launch_col_stats(const float* feats, int64_t N, int F, float* mu, float* sd, hipStream_t s);
 
 struct EsArgs {
