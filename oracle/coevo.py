@@ -28,6 +28,15 @@ Readings where the paper is silent (each is a workload field):
  * training: per step one discriminator step (real vs detached fake), then
    one non-saturating generator step against the updated discriminator on
    the same latent batch; Adam with beta1, beta2, eps, bias-corrected.
+
+The Wasserstein trainer (workload loss "wasserstein"; the paper names WGAN as
+the next trainer to add, Section 5, and its trainers differ only in the weight
+update and the fitness evaluation, Section 3): D is a critic with a linear
+output a; L(u_i, v_j) = mean a_fake - mean a_real (the critic's loss, lower is
+better for it), the generator's own loss is -mean a_fake; training minimises
+those two losses with the same Adam steps, and after every discriminator
+update each of its parameters is clipped to [-c, c] (weight clipping of the
+original WGAN, c = wgan_clip).
 """
 import numpy as np
 from scipy.special import expit
@@ -104,6 +113,12 @@ class Setup:
                 raise ValueError("the mixture step is defined for the MLP workloads only")
             self.Gnet, self.Dnet = ConvNet("G", wl), ConvNet("D", wl)
         self.PG, self.PD = self.Gnet.P, self.Dnet.P
+        self.loss = wl.get("loss", "bce")
+        if self.loss not in ("bce", "wasserstein"):
+            raise ValueError(f"unknown loss {self.loss!r}")
+        if self.loss == "wasserstein" and wl["net"] != "mlp":
+            raise ValueError("the Wasserstein trainer is defined for the MLP workloads")
+        self.clip = float(wl.get("wgan_clip", 0.01))
 
 
 class State:
@@ -148,6 +163,30 @@ def d_logits(S, p, x):
     return S.Dnet.forward(p, x)
 
 
+def pair_losses(S, a_r, a_f):
+    """(L, Lg) of one (generator, discriminator) pair from the critic outputs
+    on the real and the fake rows: the discriminator's loss and the
+    generator's own loss."""
+    if S.loss == "wasserstein":
+        return a_f.mean() - a_r.mean(), -a_f.mean()
+    return softplus(-a_r).mean() + softplus(a_f).mean(), softplus(-a_f).mean()
+
+
+def d_loss_grads(S, a_r, a_f):
+    """dL_D/da for the real and the fake rows of a discriminator step."""
+    B = len(a_r)
+    if S.loss == "wasserstein":
+        return np.full(B, -1.0 / B), np.full(len(a_f), 1.0 / len(a_f))
+    return (expit(a_r) - 1.0) / B, expit(a_f) / len(a_f)
+
+
+def g_loss_grad(S, a_f):
+    """dL_G/da for the fake rows of a generator step."""
+    if S.loss == "wasserstein":
+        return np.full(len(a_f), -1.0 / len(a_f))
+    return (expit(a_f) - 1.0) / len(a_f)
+
+
 def evaluate(S, st, data, gen):
     """Step 2: all 5x5 pairs of each neighbourhood, then fitness.
 
@@ -162,11 +201,9 @@ def evaluate(S, st, data, gen):
         fakes = [g_forward(S, st.Gp[S.nbr[c, i]], z)[1] for i in range(5)]
         for j in range(5):
             dp = st.Dp[S.nbr[c, j]]
-            real_term = softplus(-d_logits(S, dp, x)[1]).mean()
+            a_r = d_logits(S, dp, x)[1]
             for i in range(5):
-                a_f = d_logits(S, dp, fakes[i])[1]
-                L[c, i, j] = real_term + softplus(a_f).mean()
-                Lg[c, i, j] = softplus(-a_f).mean()
+                L[c, i, j], Lg[c, i, j] = pair_losses(S, a_r, d_logits(S, dp, fakes[i])[1])
     fit_d = L.mean(axis=1)
     if S.wl["fitness_mode"] == 0:
         fit_g = -L.mean(axis=2)
@@ -256,14 +293,17 @@ def train_step(S, st, data, gen, step):
         # discriminator step on real and detached fake
         cache_r, a_r = d_logits(S, st.Dp[c], x)
         cache_f, a_f = d_logits(S, st.Dp[c], xf)
-        losses[c, 0] = softplus(-a_r).mean() + softplus(a_f).mean()
-        g_r, _ = S.Dnet.backward(st.Dp[c], cache_r, (expit(a_r) - 1.0) / B)
-        g_f, _ = S.Dnet.backward(st.Dp[c], cache_f, expit(a_f) / B)
+        losses[c, 0] = pair_losses(S, a_r, a_f)[0]
+        d_r, d_f = d_loss_grads(S, a_r, a_f)
+        g_r, _ = S.Dnet.backward(st.Dp[c], cache_r, d_r)
+        g_f, _ = S.Dnet.backward(st.Dp[c], cache_f, d_f)
         st.Dt[c] = adam(S, st.Dp[c], st.Dm[c], st.Dv[c], st.Dt[c], st.Dlr[c], g_r + g_f)
+        if S.loss == "wasserstein":
+            np.clip(st.Dp[c], -S.clip, S.clip, out=st.Dp[c])
         # generator step (non-saturating) against the updated discriminator, same z
         cache2, a2 = d_logits(S, st.Dp[c], xf)
-        losses[c, 1] = softplus(-a2).mean()
-        _, dxf = S.Dnet.backward(st.Dp[c], cache2, (expit(a2) - 1.0) / B, want_input_grad=True)
+        losses[c, 1] = pair_losses(S, a2, a2)[1]
+        _, dxf = S.Dnet.backward(st.Dp[c], cache2, g_loss_grad(S, a2), want_input_grad=True)
         gG, _ = S.Gnet.backward(st.Gp[c], gcache, dxf)
         st.Gt[c] = adam(S, st.Gp[c], st.Gm[c], st.Gv[c], st.Gt[c], st.Glr[c], gG)
     return losses

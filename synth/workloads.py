@@ -19,6 +19,9 @@ Every field is plain data.  Fields:
   lr0_g, lr0_d, beta1, beta2, eps
   lr_mutation, lr_mut_std, lr_mut_prob
   tournament_size, fitness_mode (0: paper's single-objective fitness)
+  loss                 "bce" (the paper's GAN objective) or "wasserstein" (the
+                       WGAN trainer the paper names as the next one to add)
+  wgan_clip            weight-clipping bound of the Wasserstein critic
   mix_enable, mix_sigma, mix_samples, mix_feat_dim
   seed
   data                 dataset recipe name + size (see datasets.py)
@@ -31,6 +34,7 @@ _BASE = dict(
     lr0_g=2e-4, lr0_d=2e-4, beta1=0.9, beta2=0.999, eps=1e-8,
     lr_mutation=1, lr_mut_std=1e-4, lr_mut_prob=0.5,
     tournament_size=2, fitness_mode=0,
+    loss="bce", wgan_clip=0.01,
     mix_enable=0, mix_sigma=0.01, mix_samples=1024, mix_feat_dim=64,
     seed=0,
 )
@@ -60,6 +64,12 @@ WORKLOADS = {
                             batch=100, steps=100, gens=10,
                             mix_enable=1, mix_sigma=0.01,
                             data=dict(kind="mnist_like", n=60000, seed=0)),
+    # 4x4 torus, MNIST-shaped MLPs, Wasserstein critic with weight clipping
+    "mnist_mlp_4x4_wgan": _w(rows=4, cols=4, z_dim=64, x_dim=784,
+                             g_hidden=[256, 256], d_hidden=[256, 256],
+                             batch=100, steps=100, gens=10,
+                             loss="wasserstein", wgan_clip=0.01,
+                             data=dict(kind="mnist_like", n=60000, seed=0)),
     # 8x8 torus, MNIST-shaped MLPs
     "mnist_mlp_8x8": _w(rows=8, cols=8, z_dim=64, x_dim=784,
                         g_hidden=[256, 256], d_hidden=[256, 256],

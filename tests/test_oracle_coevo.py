@@ -226,6 +226,7 @@ def _textbook_gan_generation(S, st, data, gen):
     og = torch.optim.Adam([Gp], lr=float(st.Glr[0]), betas=b, eps=S.wl["eps"])
     od = torch.optim.Adam([Dp], lr=float(st.Dlr[0]), betas=b, eps=S.wl["eps"])
     bce = torch.nn.functional.binary_cross_entropy_with_logits
+    wgan = S.wl.get("loss", "bce") == "wasserstein"
     for s in range(S.wl["steps"]):
         idx = rng.indices(S.seed, S.B, S.N, 0, gen, s + 1)
         z = torch.tensor(rng.normals(S.seed, S.B * S.zd, 0, gen, s + 1, "Z").reshape(S.B, S.zd))
@@ -233,23 +234,32 @@ def _textbook_gan_generation(S, st, data, gen):
         xf = net(Gp, S.g_sizes, S.g_acts, z)
         ar = net(Dp, S.d_sizes, S.d_acts, x)
         af = net(Dp, S.d_sizes, S.d_acts, xf.detach())
-        ld = bce(ar, torch.ones_like(ar)) + bce(af, torch.zeros_like(af))
+        if wgan:  # critic loss, then weight clipping
+            ld = af.mean() - ar.mean()
+        else:
+            ld = bce(ar, torch.ones_like(ar)) + bce(af, torch.zeros_like(af))
         od.zero_grad()
         ld.backward()
         od.step()
+        if wgan:
+            with torch.no_grad():
+                Dp.clamp_(-S.wl["wgan_clip"], S.wl["wgan_clip"])
         af2 = net(Dp, S.d_sizes, S.d_acts, xf)
-        lg = bce(af2, torch.ones_like(af2))
+        lg = -af2.mean() if wgan else bce(af2, torch.ones_like(af2))
         og.zero_grad()
         lg.backward()
         og.step()
     return Gp.detach().numpy(), Dp.detach().numpy()
 
 
-@pytest.mark.parametrize("name", ["ring8_mlp_2x2", "mnist_mlp_3x3"])
-def test_one_by_one_grid_is_plain_gan_training(name):
+@pytest.mark.parametrize("name,loss", [("ring8_mlp_2x2", "bce"), ("mnist_mlp_3x3", "bce"),
+                                       ("mnist_mlp_3x3", "wasserstein")])
+def test_one_by_one_grid_is_plain_gan_training(name, loss):
     """On a 1x1 torus all five slots are the cell itself: selection is the
-    identity and a generation reduces to textbook alternating GAN training."""
-    over = dict(rows=1, cols=1, steps=4, lr_mutation=0)
+    identity and a generation reduces to textbook alternating GAN training
+    (for the Wasserstein trainer: critic loss mean D(fake) - mean D(real),
+    clamp of the critic's weights after its step, generator loss -mean D(fake))."""
+    over = dict(rows=1, cols=1, steps=4, lr_mutation=0, loss=loss, wgan_clip=0.05)
     if name == "mnist_mlp_3x3":
         over.update(g_hidden=[32, 32], d_hidden=[32, 32], batch=16)
     S, st, data = _setup(name, n=1000, **over)
@@ -296,3 +306,72 @@ def test_train_step_gradients_match_finite_differences():
         e[k] = h
         fd = (loss_g(st.Gp[0] + e, st.Dp[0]) - loss_g(st.Gp[0] - e, st.Dp[0])) / (2 * h)
         assert abs(fd - gG[k]) < 1e-7 + 1e-6 * abs(fd)
+
+
+def test_wasserstein_closed_form_constant_critic():
+    """A critic whose output layer is zero but for its bias b outputs b on every
+    row: each pair's critic loss mean a_fake - mean a_real is 0 and the
+    generator's own loss is -b."""
+    S, st, data = _setup(rows=2, cols=3, g_hidden=[16], d_hidden=[16, 8], z_dim=8, batch=10,
+                         loss="wasserstein")
+    off, fi, fo = mlp.layout(S.d_sizes)[0][-1]
+    st.Dp[:, off:off + fi * fo] = 0.0
+    st.Dp[:, off + fi * fo] = 0.3
+    L, Lg, fg, fd = coevo.evaluate(S, st, data, 0)
+    assert np.all(np.abs(L) < 1e-15) and np.allclose(Lg, -0.3, rtol=0, atol=1e-15)
+    assert np.all(np.abs(fd) < 1e-15) and np.all(np.abs(fg) < 1e-15)
+
+
+def test_wasserstein_gradients_match_finite_differences():
+    """The critic and generator gradients of the Wasserstein step equal central
+    differences of mean D(fake) - mean D(real) and of -mean D(G(z)); the clip
+    bound is set out of reach so that the step itself is a plain Adam step."""
+    S, st, data = _setup(rows=1, cols=1, g_hidden=[3], d_hidden=[4], z_dim=2, x_dim=784, batch=3,
+                         loss="wasserstein", wgan_clip=100.0)
+    _, x, z = coevo.sample(S, data, 0, 0, 1)
+
+    def loss_d(dp):
+        ar = coevo.d_logits(S, dp, x)[1]
+        af = coevo.d_logits(S, dp, coevo.g_forward(S, st.Gp[0], z)[1])[1]
+        return af.mean() - ar.mean()
+
+    def loss_g(gp, dp):
+        return -coevo.d_logits(S, dp, coevo.g_forward(S, gp, z)[1])[1].mean()
+
+    st2 = st.copy()
+    st2.Dlr[:] = 0.0
+    st2.Glr[:] = 0.0
+    losses = coevo.train_step(S, st2, data, 0, 0)
+    assert abs(losses[0, 0] - loss_d(st.Dp[0])) < 1e-14 and abs(losses[0, 1] - loss_g(st.Gp[0], st.Dp[0])) < 1e-14
+    gD = st2.Dm[0] / (1 - S.wl["beta1"])
+    gG = st2.Gm[0] / (1 - S.wl["beta1"])
+    h = 1e-6
+    for k in range(len(gD)):
+        e = np.zeros_like(gD)
+        e[k] = h
+        fd = (loss_d(st.Dp[0] + e) - loss_d(st.Dp[0] - e)) / (2 * h)
+        assert abs(fd - gD[k]) < 1e-7 + 1e-6 * abs(fd)
+    for k in range(len(gG)):
+        e = np.zeros_like(gG)
+        e[k] = h
+        fd = (loss_g(st.Gp[0] + e, st.Dp[0]) - loss_g(st.Gp[0] - e, st.Dp[0])) / (2 * h)
+        assert abs(fd - gG[k]) < 1e-7 + 1e-6 * abs(fd)
+
+
+def test_wasserstein_critic_weights_are_clipped():
+    """After a Wasserstein step every critic parameter lies in [-c, c]; the
+    ones the Adam step left inside are exactly the Adam results, the others
+    sit on the bound with the sign of the Adam result."""
+    c = 0.02
+    S, st, data = _setup(rows=1, cols=2, g_hidden=[16], d_hidden=[16], z_dim=8, batch=6,
+                         loss="wasserstein", wgan_clip=c, lr0_d=0.05)
+    free = coevo.Setup(dict(S.wl, wgan_clip=1e9), S.N)
+    st_free = st.copy()
+    coevo.train_step(S, st, data, 0, 0)
+    coevo.train_step(free, st_free, data, 0, 0)
+    assert np.all(np.abs(st.Dp) <= c)
+    inside = np.abs(st_free.Dp) <= c
+    assert np.array_equal(st.Dp[inside], st_free.Dp[inside])
+    assert np.array_equal(st.Dp[~inside], np.sign(st_free.Dp[~inside]) * c)
+    assert inside.mean() < 1.0  # the bound was hit somewhere
+    assert np.array_equal(st.Dm, st_free.Dm) and np.array_equal(st.Dv, st_free.Dv)
