@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define LIPZ_ABI_VERSION 1
+#define LIPZ_ABI_VERSION 2
 #define LIPZ_SLOTS 5          /* centre, north, south, west, east */
 #define LIPZ_MAX_HIDDEN 4
 
@@ -81,6 +81,12 @@ enum {
 enum { LIPZ_NET_MLP = 0, LIPZ_NET_DCGAN = 1 };
 enum { LIPZ_ACT_LINEAR = 0, LIPZ_ACT_RELU = 1, LIPZ_ACT_LRELU = 2, LIPZ_ACT_TANH = 3 };
 enum { LIPZ_ROLE_G = 0, LIPZ_ROLE_D = 1 };
+/* The trainer's GAN objective.  BCE: the paper's minimax objective with a
+ * sigmoid discriminator (Section 3).  WASSERSTEIN: the WGAN trainer the
+ * paper names as the next one to add (Section 5): a linear critic, critic
+ * loss mean D(fake) - mean D(real), generator loss -mean D(fake), and every
+ * critic parameter clipped to [-wgan_clip, wgan_clip] after its update. */
+enum { LIPZ_LOSS_BCE = 0, LIPZ_LOSS_WASSERSTEIN = 1 };
 enum {
   LIPZ_TAG_IDX = 1, LIPZ_TAG_Z = 2, LIPZ_TAG_TOURN_G = 3, LIPZ_TAG_TOURN_D = 4,
   LIPZ_TAG_LRMUT_G = 5, LIPZ_TAG_LRMUT_D = 6, LIPZ_TAG_MIXN = 7, LIPZ_TAG_MIXZ = 8,
@@ -127,6 +133,8 @@ typedef struct {
   int32_t mix_feat_dim;             /* random feature width F */
   float mix_sigma;                  /* (1+1)-ES mutation scale */
   uint64_t seed;
+  int32_t loss_kind;                /* LIPZ_LOSS_BCE (paper) or LIPZ_LOSS_WASSERSTEIN (MLP only) */
+  float wgan_clip;                  /* critic clipping bound (> 0) for LIPZ_LOSS_WASSERSTEIN */
 } lipz_config;
 
 typedef struct lipz_grid lipz_grid;  /* opaque host handle */
@@ -154,6 +162,8 @@ lipz_status lipz_grid_destroy(lipz_grid* g);
  * discriminator slot j of its neighbourhood:
  *   L [c][i][j] = mean_b softplus(-D_j(x_b)) + mean_b softplus(D_j(G_i(z_b)))
  *   Lg[c][i][j] = mean_b softplus(-D_j(G_i(z_b)))
+ *   (LIPZ_LOSS_WASSERSTEIN: L = mean_b D_j(G_i(z_b)) - mean_b D_j(x_b),
+ *    Lg = -mean_b D_j(G_i(z_b)))
  *   fit_d[c][j] = mean_i L[c][i][j];  fit_g[c][i] = -mean_j L[c][i][j]
  *   (fitness_mode 1: fit_g[c][i] = mean_j Lg[c][i][j]).  Lower is better.
  * Outputs fp32 [C][5][5] / [C][5]; any may be NULL.  A non-finite value sets
@@ -183,8 +193,10 @@ lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forc
  * mean softplus(-D(x)) + mean softplus(D(G(z))) with G(z) detached; then
  * generator Adam step on mean softplus(-D'(G(z))) against the updated
  * discriminator D' and the same z.  Adam: bias-corrected, per-cell learning
- * rate and step count.  d_losses [n_steps][C][2] fp32 (L_D, L_G before each
- * update) may be NULL. */
+ * rate and step count.  LIPZ_LOSS_WASSERSTEIN: the critic minimises
+ * mean D(G(z)) - mean D(x), then every critic parameter is clipped to
+ * [-wgan_clip, wgan_clip]; the generator minimises -mean D'(G(z)).
+ * d_losses [n_steps][C][2] fp32 (L_D, L_G before each update) may be NULL. */
 lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_steps,
                             float* d_losses);
 

@@ -54,6 +54,11 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
   if (!(c->lrelu_slope > 0.f) || c->lrelu_slope >= 1.f) return "lrelu_slope must be in (0, 1)";
   if (c->tournament_size < 1 || c->tournament_size > 5) return "tournament_size must be in [1, 5]";
   if (c->fitness_mode != 0 && c->fitness_mode != 1) return "fitness_mode must be 0 or 1";
+  if (c->loss_kind != LIPZ_LOSS_BCE && c->loss_kind != LIPZ_LOSS_WASSERSTEIN) return "unknown loss_kind";
+  if (c->loss_kind == LIPZ_LOSS_WASSERSTEIN) {
+    if (c->net != LIPZ_NET_MLP) return "the Wasserstein trainer is implemented for the MLP networks";
+    if (!(c->wgan_clip > 0.f && c->wgan_clip < 1e30f)) return "wgan_clip must be a positive finite bound";
+  }
   if (!(c->beta1 >= 0.f && c->beta1 < 1.f && c->beta2 >= 0.f && c->beta2 < 1.f && c->eps > 0.f))
     return "bad Adam constants";
   if (!(c->lr0_g >= 0.f && c->lr0_d >= 0.f)) return "learning rates must be >= 0";
@@ -353,6 +358,8 @@ void build_tables(lipz_grid* g) {
   const Net &G = g->G, &D = g->D;
   const int LG = G.nl, LD = D.nl;
   const size_t sG = G.stride, sD = D.stride;
+  // the Wasserstein critic's parameters are clipped after every update
+  const float d_clip = g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN ? g->cfg.wgan_clip : 0.f;
   for (int par = 0; par < 2; ++par) {
     const StateBuf& S = g->st[par];
     for (int grp = 0; grp < g->n_groups; ++grp) {
@@ -398,6 +405,8 @@ void build_tables(lipz_grid* g) {
       p.lr = S.Dlr + c;
       p.t = S.Dt + c;
       p.epi = EPI_ADAM;
+      p.clip = d_clip;
+      if (g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN) p.gscale = 1.f / (float)B;  // dL/da stored as exact +-1
       head_grad.push_back(p);
     }
     backward_phases(
@@ -414,9 +423,10 @@ void build_tables(lipz_grid* g) {
             const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
                                     : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
             const size_t o = c * sD + D.off[l];
-            ph->push_back(wgrad_adam_prob(x, 2 * B, D.fi[l], g->dD[l] + (size_t)c * 2 * B * D.fo[l],
-                                          D.fo[l], S.Dp + o, S.Dm + o, S.Dv + o, S.Dlr + c,
-                                          S.Dt + c));
+            GemmProb p = wgrad_adam_prob(x, 2 * B, D.fi[l], g->dD[l] + (size_t)c * 2 * B * D.fo[l],
+                                         D.fo[l], S.Dp + o, S.Dm + o, S.Dv + o, S.Dlr + c, S.Dt + c);
+            p.clip = d_clip;
+            ph->push_back(p);
           }
         },
         &ops, head_grad);
@@ -759,12 +769,14 @@ lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float
     for (int ph : g->eval_phases[par])
       if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "eval forward"))) return st;
     EvalHeadArgs ha;
+    memset(&ha, 0, sizeof(ha));
     ha.part = g->part_e;
     ha.tn = g->tn;
     ha.L = g->L;
     ha.Lg = g->Lg;
     ha.B = B;
     ha.C = C;
+    ha.loss_kind = g->cfg.loss_kind;
     if ((st = check_hip(g, launch_head_eval(ha, s), "eval head"))) return st;
   }
   e = launch_fitness(g->L, g->Lg, C, g->cfg.fitness_mode, g->fit_g, g->fit_d, g->flags, d_L, d_Lg,
@@ -856,6 +868,7 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   const StateBuf& S = g->st[par];
   const int C = g->C, B = g->B, LD = g->D.nl;
   HeadArgs hd;
+  memset(&hd, 0, sizeof(hd));
   hd.part = g->part_tr;
   hd.tn = g->tn;
   hd.act = g->a[LD - 2];
@@ -870,6 +883,7 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   hd.C = C;
   hd.hidden_act = g->D.act[LD - 2];
   hd.slope = g->slope;
+  hd.loss_kind = g->cfg.loss_kind;
   HeadArgs hg = hd;
   hg.part = g->part_g;
   hg.act = g->ag[LD - 2];

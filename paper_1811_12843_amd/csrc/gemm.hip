@@ -255,10 +255,11 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = (i * 2 + j) * 4 + r;
-          const float g = acc[i][j][r];
+          const float g = P.gscale != 0.f ? acc[i][j][r] * P.gscale : acc[i][j][r];
           const float m = ac.beta1 * mm[e] + ac.one_minus_beta1 * g;
           const float v = ac.beta2 * vv[e] + ac.one_minus_beta2 * g * g;
-          const float p = pp[e] - lr * (m / bc1) / (sqrtf(v / bc2) + ac.eps);
+          float p = pp[e] - lr * (m / bc1) / (sqrtf(v / bc2) + ac.eps);
+          if (P.clip > 0.f) p = p > P.clip ? P.clip : (p < -P.clip ? -P.clip : p);  // keeps NaN
           if (ok[e]) {
             gM[off[e]] = m;
             gV[off[e]] = v;

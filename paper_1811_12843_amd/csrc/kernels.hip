@@ -110,7 +110,10 @@ __global__ void sample_kernel(const float* __restrict__ data, int64_t N, int xd,
 // ---------------------------------------------------------------------------
 constexpr int HEAD_ROWS = 32;
 
-__device__ __forceinline__ float head_dl(float a, bool real_target, float invB) {
+// dL/da of one row (the mean over B rows included): BCE (sigmoid(a) - target) / B;
+// Wasserstein -1 / B for a real target, +1 / B for a fake one.
+__device__ __forceinline__ float head_dl(int loss_kind, float a, bool real_target, float invB) {
+  if (loss_kind == LIPZ_LOSS_WASSERSTEIN) return real_target ? -invB : invB;
   return (sigmoid_f(a) - (real_target ? 1.f : 0.f)) * invB;
 }
 
@@ -129,11 +132,13 @@ __global__ __launch_bounds__(NT) void head_kernel(HeadArgs A) {
     const int r = r0 + threadIdx.x;
     float a = 0.f;
     for (int t = 0; t < tn; ++t) a += part[(int64_t)r * tn + t];
-    const float d = head_dl(a, !D_STEP || r < A.B, invB);
+    const float d = head_dl(A.loss_kind, a, !D_STEP || r < A.B, invB);
     dl[threadIdx.x] = d;
     if (D_STEP && cb == 0) {
       float* o = A.dlbuf + ((int64_t)c * rows + r) * 4;
-      o[0] = d;
+      // the Wasserstein critic's output bias has a zero gradient: store the
+      // exact +-1 (the weight-gradient GEMM scales by 1 / B afterwards)
+      o[0] = A.loss_kind == LIPZ_LOSS_WASSERSTEIN ? (r < A.B ? -1.f : 1.f) : d;
       o[1] = 0.f;
       o[2] = 0.f;
       o[3] = 0.f;
@@ -144,8 +149,8 @@ __global__ __launch_bounds__(NT) void head_kernel(HeadArgs A) {
     for (int r = threadIdx.x; r < rows; r += NT) {
       float a = 0.f;
       for (int t = 0; t < tn; ++t) a += part[(int64_t)r * tn + t];
-      if (D_STEP && r >= A.B) lf += softplus_f(a);
-      else lr_ += softplus_f(-a);
+      if (D_STEP && r >= A.B) lf += fake_term(A.loss_kind, a);
+      else lr_ += real_term(A.loss_kind, a);
     }
     lr_ = block_sum(lr_, red);
     lf = block_sum(lf, red);
@@ -198,7 +203,10 @@ __global__ __launch_bounds__(NT) void head_eval_kernel(EvalHeadArgs A) {
     const int blk = q == 0 ? 0 : (q <= 5 ? q : q - 5);
     const float sgn = (q == 0 || q > 5) ? -1.f : 1.f;
     float s = 0.f;
-    for (int b = lane; b < A.B; b += 64) s += softplus_f(sgn * logit[blk * A.B + b]);
+    for (int b = lane; b < A.B; b += 64) {
+      const float a = logit[blk * A.B + b];
+      s += sgn > 0.f ? fake_term(A.loss_kind, a) : real_term(A.loss_kind, a);
+    }
     s = wave_sum(s);
     if (lane == 0) logit[rows + q] = s / (float)A.B;
   }

@@ -89,6 +89,15 @@ __device__ __forceinline__ float softplus_f(float x) {
   return fmaxf(x, 0.f) + log1pf(expf(-fabsf(x)));
 }
 __device__ __forceinline__ float sigmoid_f(float x) { return 1.f / (1.f + expf(-x)); }
+// Per-row loss terms of a logit / critic output a, for a row whose target is
+// "real" (data rows in the D step; every row of the G step) or "fake".
+// BCE: softplus(-a) and softplus(a); Wasserstein: -a and a.
+__device__ __forceinline__ float real_term(int loss_kind, float a) {
+  return loss_kind == LIPZ_LOSS_WASSERSTEIN ? -a : softplus_f(-a);
+}
+__device__ __forceinline__ float fake_term(int loss_kind, float a) {
+  return loss_kind == LIPZ_LOSS_WASSERSTEIN ? a : softplus_f(a);
+}
 
 // ---------------------------------------------------------------------------
 // Grouped GEMM: one launch computes many independent problems
@@ -133,6 +142,8 @@ struct GemmProb {
   int32_t dot_ld;
   uint32_t a_bytes;    // extent of A from its base: a_rows * lda (a_trans 0) or K * lda floats
   uint32_t b_bytes;    // extent of B: K * ldb (b_trans 0) or N * ldb floats
+  float clip;          // EPI_ADAM: when > 0 the updated parameter is clipped to [-clip, clip]
+  float gscale;        // EPI_ADAM: the gradient is acc * gscale (0 stands for 1: descriptors start zeroed)
 };
 
 struct AdamConsts {
@@ -390,12 +401,14 @@ struct HeadArgs {
   float* delta;          // out: gradient w.r.t. the last hidden pre-activation, same layout
   const float* w;        // output-layer weights of cell 0; cell c at w + c * p_stride
   int64_t p_stride;
-  float* dlbuf;          // D step: out dL/da as [C][2B][4] (column 0), else null
+  float* dlbuf;          // D step: out dL/da as [C][2B][4] (column 0), else null;
+                         // Wasserstein: B dL/da = -1 / +1, exact, so its sum over rows is exactly 0
   float* losses;         // [cells][2] slice for this step, or null
   int H, B;
   int c0, C;             // the launch covers cells c0 .. c0 + C - 1
   int hidden_act;
   float slope;
+  int loss_kind;         // LIPZ_LOSS_BCE or LIPZ_LOSS_WASSERSTEIN
 };
 // Discriminator step head: logits of 2B rows (B real then B fake), BCE, its
 // gradient dL/da into dlbuf and delta.
@@ -409,6 +422,7 @@ struct EvalHeadArgs {
   float* L;              // [C][5][5]
   float* Lg;
   int B, C;
+  int loss_kind;         // LIPZ_LOSS_BCE or LIPZ_LOSS_WASSERSTEIN
 };
 hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s);
 hipError_t launch_fitness(const float* L, const float* Lg, int C, int mode, float* fit_g, float* fit_d,

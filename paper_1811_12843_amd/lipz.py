@@ -11,13 +11,15 @@ import os
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("LIPZ_LIBRARY") or os.path.join(_PKG, "liblipz.so")
 
-LIPZ_ABI_VERSION = 1
+LIPZ_ABI_VERSION = 2
 LIPZ_MAX_HIDDEN = 4
 LIPZ_OK, LIPZ_E_INVAL, LIPZ_E_WORKSPACE, LIPZ_E_HIP, LIPZ_E_ORDER, LIPZ_E_NONFINITE, \
     LIPZ_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 LIPZ_NET_MLP, LIPZ_NET_DCGAN = 0, 1
 LIPZ_ACT_LINEAR, LIPZ_ACT_RELU, LIPZ_ACT_LRELU, LIPZ_ACT_TANH = 0, 1, 2, 3
 LIPZ_ROLE_G, LIPZ_ROLE_D = 0, 1
+LIPZ_LOSS_BCE, LIPZ_LOSS_WASSERSTEIN = 0, 1
+LOSSES = {"bce": LIPZ_LOSS_BCE, "wasserstein": LIPZ_LOSS_WASSERSTEIN}
 ACTS = {"linear": LIPZ_ACT_LINEAR, "relu": LIPZ_ACT_RELU, "lrelu": LIPZ_ACT_LRELU, "tanh": LIPZ_ACT_TANH}
 
 _i32, _i64, _f32, _u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_uint64
@@ -37,6 +39,7 @@ class lipz_config(ctypes.Structure):
         ("lr_mut_std", _f32), ("lr_mut_prob", _f32),
         ("mix_enable", _i32), ("mix_samples", _i32), ("mix_feat_dim", _i32), ("mix_sigma", _f32),
         ("seed", _u64),
+        ("loss_kind", _i32), ("wgan_clip", _f32),
     ]
 
 
@@ -72,6 +75,8 @@ def config_from_dict(d):
     c.mix_enable = d["mix_enable"]
     c.mix_samples, c.mix_feat_dim, c.mix_sigma = d["mix_samples"], d["mix_feat_dim"], d["mix_sigma"]
     c.seed = d["seed"]
+    c.loss_kind = LOSSES[d.get("loss", "bce")]
+    c.wgan_clip = d.get("wgan_clip", 0.01)
     return c
 
 

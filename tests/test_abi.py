@@ -62,9 +62,18 @@ def test_workspace_sizing_and_validation():
     w2 = dict(w, mix_enable=1)
     assert L.lipz_workspace_bytes(L.config_from_dict(w2), 60000) > base
     bad = [dict(w, batch=0), dict(w, tournament_size=6), dict(w, rows=0), dict(w, g_hidden=[]),
-           dict(w, lrelu_slope=0.0), dict(w, beta1=1.0), dict(w, fitness_mode=2)]
+           dict(w, lrelu_slope=0.0), dict(w, beta1=1.0), dict(w, fitness_mode=2),
+           dict(w, loss="wasserstein", wgan_clip=0.0), dict(w, loss="wasserstein", wgan_clip=float("inf"))]
     for b in bad:
         assert L.lipz_workspace_bytes(L.config_from_dict(b), 60000) == 0
+    c = L.config_from_dict(w)
+    c.loss_kind = 2
+    assert L.lipz_workspace_bytes(c, 60000) == 0
+    # the Wasserstein trainer: same buffers as the BCE one; MLP networks only
+    assert L.lipz_workspace_bytes(L.config_from_dict(dict(w, loss="wasserstein")), 60000) == base
+    assert L.lipz_workspace_bytes(L.config_from_dict(synth.workload("mnist_mlp_4x4_wgan")), 60000) > 0
+    d = dict(synth.workload("celeba_dcgan_4x4"), loss="wasserstein")
+    assert L.lipz_workspace_bytes(L.config_from_dict(d), 1000) == 0
     c = L.config_from_dict(w)
     c.abi_version = 99
     assert L.lipz_workspace_bytes(c, 60000) == 0
