@@ -17,10 +17,12 @@ Modules
   coevo    state, evaluation, fitness, tournament, replacement, mutation,
            training step (Adam), one generation
   mixture  the (1+1)-ES over the generator-mixture weights and its score
+  nes      the gradient-free NES trainer (antithetic estimate + Adam)
 
 Pinned by tests/test_oracle_*.py against: published Philox known-answer
 vectors and rocRAND's host Philox, hand-enumerated neighbourhoods, BCE closed
 forms, finite differences, torch CPU fp64 convolutions, batch norm and autograd, Adam closed forms and
 torch.optim.Adam, brute-force tournament enumeration, the 1x1-grid reduction
-to plain alternating GAN training, and Frechet-distance closed forms.
+to plain alternating GAN training, Frechet-distance closed forms, and, for
+NES, exactness on quadratics and convergence to the backpropagated gradient.
 """

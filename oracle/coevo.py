@@ -119,6 +119,11 @@ class Setup:
         if self.loss == "wasserstein" and wl["net"] != "mlp":
             raise ValueError("the Wasserstein trainer is defined for the MLP workloads")
         self.clip = float(wl.get("wgan_clip", 0.01))
+        self.trainer = wl.get("trainer", "gradient")
+        if self.trainer not in ("gradient", "nes"):
+            raise ValueError(f"unknown trainer {self.trainer!r}")
+        if self.trainer == "nes" and wl["net"] != "mlp":
+            raise ValueError("the NES trainer is defined for the MLP workloads")
 
 
 class State:
@@ -311,10 +316,11 @@ def train_step(S, st, data, gen, step):
 
 def generation(S, st, data, gen, mix_stats=None):
     """Steps 2-4 for one generation; returns (new state, record dict)."""
-    from . import mixture
+    from . import mixture, nes
     L, Lg, fg, fd = evaluate(S, st, data, gen)
     st2, sel = select_replace(S, st, fg, fd, gen)
-    losses = [train_step(S, st2, data, gen, s) for s in range(S.wl["steps"])]
+    step_fn = nes.train_step if S.trainer == "nes" else train_step
+    losses = [step_fn(S, st2, data, gen, s) for s in range(S.wl["steps"])]
     rec = dict(L=L, Lg=Lg, fit_g=fg, fit_d=fd, sel=sel, losses=np.array(losses))
     if S.wl["mix_enable"]:
         w, score, acc = mixture.update(S, st2, mix_stats, gen)

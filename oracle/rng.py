@@ -22,7 +22,7 @@ PHILOX_W0 = np.uint64(0x9E3779B9)
 PHILOX_W1 = np.uint64(0xBB67AE85)
 
 TAG = dict(IDX=1, Z=2, TOURN_G=3, TOURN_D=4, LRMUT_G=5, LRMUT_D=6,
-           MIXN=7, MIXZ=8, PROJ=9, INIT_G=10, INIT_D=11)
+           MIXN=7, MIXZ=8, PROJ=9, INIT_G=10, INIT_D=11, NES_G=12, NES_D=13)
 
 
 def philox4x32_10(ctr, key):

@@ -22,6 +22,9 @@ Every field is plain data.  Fields:
   loss                 "bce" (the paper's GAN objective) or "wasserstein" (the
                        WGAN trainer the paper names as the next one to add)
   wgan_clip            weight-clipping bound of the Wasserstein critic
+  trainer              "gradient" (backpropagation + Adam, the paper's experiments)
+                       or "nes" (the gradient-free NES trainer, oracle/nes.py)
+  nes_pairs, nes_sigma antithetic direction pairs and perturbation scale of NES
   mix_enable, mix_sigma, mix_samples, mix_feat_dim
   seed
   data                 dataset recipe name + size (see datasets.py)
@@ -35,6 +38,7 @@ _BASE = dict(
     lr_mutation=1, lr_mut_std=1e-4, lr_mut_prob=0.5,
     tournament_size=2, fitness_mode=0,
     loss="bce", wgan_clip=0.01,
+    trainer="gradient", nes_pairs=8, nes_sigma=0.01,
     mix_enable=0, mix_sigma=0.01, mix_samples=1024, mix_feat_dim=64,
     seed=0,
 )
@@ -70,6 +74,12 @@ WORKLOADS = {
                              batch=100, steps=100, gens=10,
                              loss="wasserstein", wgan_clip=0.01,
                              data=dict(kind="mnist_like", n=60000, seed=0)),
+    # 3x3 torus, MNIST-shaped MLPs trained by NES (8 antithetic pairs) instead of backpropagation
+    "mnist_mlp_3x3_nes": _w(rows=3, cols=3, z_dim=64, x_dim=784,
+                            g_hidden=[256, 256], d_hidden=[256, 256],
+                            batch=100, steps=100, gens=1,
+                            trainer="nes", nes_pairs=8, nes_sigma=0.01,
+                            data=dict(kind="mnist_like", n=60000, seed=0)),
     # 8x8 torus, MNIST-shaped MLPs
     "mnist_mlp_8x8": _w(rows=8, cols=8, z_dim=64, x_dim=784,
                         g_hidden=[256, 256], d_hidden=[256, 256],
