@@ -87,10 +87,19 @@ enum { LIPZ_ROLE_G = 0, LIPZ_ROLE_D = 1 };
  * loss mean D(fake) - mean D(real), generator loss -mean D(fake), and every
  * critic parameter clipped to [-wgan_clip, wgan_clip] after its update. */
 enum { LIPZ_LOSS_BCE = 0, LIPZ_LOSS_WASSERSTEIN = 1 };
+/* How lipz_train_step updates a cell's pair.  GRADIENT: backpropagation and
+ * Adam (the paper's experiments, Section 4).  NES: the gradient-free Natural
+ * Evolution Strategies trainer the system also offers (Section 3,
+ * "Implementation and Distribution"): per step and role, nes_pairs antithetic
+ * Gaussian directions eps_k (normal k P + e of stream (cell, gen, s + 1,
+ * NES_G / NES_D)), the role's loss F at theta +- nes_sigma eps_k on the
+ * step's minibatch, g = sum_k (F_k+ - F_k-) eps_k / (2 nes_pairs nes_sigma),
+ * one Adam step of theta on g.  MLP networks only. */
+enum { LIPZ_TRAINER_GRADIENT = 0, LIPZ_TRAINER_NES = 1 };
 enum {
   LIPZ_TAG_IDX = 1, LIPZ_TAG_Z = 2, LIPZ_TAG_TOURN_G = 3, LIPZ_TAG_TOURN_D = 4,
   LIPZ_TAG_LRMUT_G = 5, LIPZ_TAG_LRMUT_D = 6, LIPZ_TAG_MIXN = 7, LIPZ_TAG_MIXZ = 8,
-  LIPZ_TAG_PROJ = 9, LIPZ_TAG_INIT_G = 10, LIPZ_TAG_INIT_D = 11
+  LIPZ_TAG_PROJ = 9, LIPZ_TAG_INIT_G = 10, LIPZ_TAG_INIT_D = 11, LIPZ_TAG_NES_G = 12, LIPZ_TAG_NES_D = 13
 };
 
 /* Experiment configuration (the paper's single configuration file, Section 3,
@@ -135,6 +144,9 @@ typedef struct {
   uint64_t seed;
   int32_t loss_kind;                /* LIPZ_LOSS_BCE (paper) or LIPZ_LOSS_WASSERSTEIN (MLP only) */
   float wgan_clip;                  /* critic clipping bound (> 0) for LIPZ_LOSS_WASSERSTEIN */
+  int32_t trainer;                  /* LIPZ_TRAINER_GRADIENT (paper's experiments) or LIPZ_TRAINER_NES */
+  int32_t nes_pairs;                /* NES: antithetic direction pairs, 1..64 */
+  float nes_sigma;                  /* NES: perturbation scale (> 0) */
 } lipz_config;
 
 typedef struct lipz_grid lipz_grid;  /* opaque host handle */
@@ -196,6 +208,9 @@ lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forc
  * rate and step count.  LIPZ_LOSS_WASSERSTEIN: the critic minimises
  * mean D(G(z)) - mean D(x), then every critic parameter is clipped to
  * [-wgan_clip, wgan_clip]; the generator minimises -mean D'(G(z)).
+ * LIPZ_TRAINER_NES: the same two losses, each minimised by one Adam step on
+ * the NES estimate of its gradient (see LIPZ_TRAINER_NES); the losses
+ * reported are those at the unperturbed parameters.
  * d_losses [n_steps][C][2] fp32 (L_D, L_G before each update) may be NULL. */
 lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_steps,
                             float* d_losses);

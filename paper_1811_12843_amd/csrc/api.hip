@@ -55,6 +55,12 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
   if (c->tournament_size < 1 || c->tournament_size > 5) return "tournament_size must be in [1, 5]";
   if (c->fitness_mode != 0 && c->fitness_mode != 1) return "fitness_mode must be 0 or 1";
   if (c->loss_kind != LIPZ_LOSS_BCE && c->loss_kind != LIPZ_LOSS_WASSERSTEIN) return "unknown loss_kind";
+  if (c->trainer != LIPZ_TRAINER_GRADIENT && c->trainer != LIPZ_TRAINER_NES) return "unknown trainer";
+  if (c->trainer == LIPZ_TRAINER_NES) {
+    if (c->net != LIPZ_NET_MLP) return "the NES trainer is implemented for the MLP networks";
+    if (c->nes_pairs < 1 || c->nes_pairs > 64) return "nes_pairs must be in [1, 64]";
+    if (!(c->nes_sigma > 0.f && c->nes_sigma < 1e30f)) return "nes_sigma must be a positive finite scale";
+  }
   if (c->loss_kind == LIPZ_LOSS_WASSERSTEIN) {
     if (c->net != LIPZ_NET_MLP) return "the Wasserstein trainer is implemented for the MLP networks";
     if (!(c->wgan_clip > 0.f && c->wgan_clip < 1e30f)) return "wgan_clip must be a positive finite bound";
@@ -189,6 +195,21 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     g->mu_r = cv.take<float>(F);
     g->sd_r = cv.take<float>(F);
     g->realfeat = cv.take<float>((size_t)g->N * F);
+  }
+  if (g->cfg.trainer == LIPZ_TRAINER_NES) {
+    const int Q = g->nes_q = 2 * g->cfg.nes_pairs + 1;
+    g->nes_pd = cv.take<float>((size_t)C * Q * D.stride);
+    g->nes_pg = cv.take<float>((size_t)C * Q * G.stride);
+    for (int l = 0; l + 1 < D.nl; ++l) {
+      g->nes_aq[l] = cv.take<float>((size_t)C * Q * 2 * B * D.fo[l]);
+      g->nes_agq[l] = cv.take<float>((size_t)C * Q * B * D.fo[l]);
+    }
+    for (int l = 0; l + 1 < G.nl; ++l) g->nes_hq[l] = cv.take<float>((size_t)C * Q * B * G.fo[l]);
+    g->nes_xq = cv.take<float>((size_t)C * Q * B * xd);
+    g->nes_part_d = cv.take<float>((size_t)C * Q * 2 * B * g->tn);
+    g->nes_part_g = cv.take<float>((size_t)C * Q * B * g->tn);
+    g->nes_fd = cv.take<float>((size_t)C * Q);
+    g->nes_fg = cv.take<float>((size_t)C * Q);
   }
   g->probs_d = cv.take<GemmProb>(g->probs_h.size());
   *total = align_up(cv.off, kAlign);
@@ -349,6 +370,77 @@ void setup_groups(lipz_grid* g) {
   if (n > g->C) n = g->C;
   g->n_groups = n;
   for (int i = 0; i <= n; ++i) g->group_c0[i] = (int)((int64_t)g->C * i / n);
+}
+
+// The NES trainer's step (reading of Section 3's gradient-free trainers):
+// sample; G forward (its samples score the critic's perturbations); the
+// discriminator's Q parameter sets, each D forward over the 2B rows, their
+// losses, the estimate + Adam; then the generator's Q sets, each G forward,
+// the updated D over all Q B generated rows, their losses, estimate + Adam.
+void build_nes_ops(lipz_grid* g) {
+  const int C = g->C, B = g->B, zd = g->zd, xd = g->xd, Q = g->nes_q;
+  const Net &G = g->G, &D = g->D;
+  const int LG = G.nl, LD = D.nl;
+  const size_t sG = G.stride, sD = D.stride;
+  for (int par = 0; par < 2; ++par) {
+    const StateBuf& S = g->st[par];
+    std::vector<Op>& ops = g->nes_ops[par];
+    ops.clear();
+    ops.push_back({OP_SAMPLE, -1});
+    for (int l = 0; l < LG; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c) {
+        const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
+        float* y = l + 1 < LG ? g->h[l] + (size_t)c * B * G.fo[l]
+                              : g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd;
+        ps.push_back(fwd_prob(x, B, S.Gp + c * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
+      }
+      ops.push_back({OP_GEMM, add_phase(g, ps)});
+    }
+    ops.push_back({OP_NES_PERTURB, LIPZ_ROLE_D});
+    for (int l = 0; l + 1 < LD; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c)
+        for (int q = 0; q < Q; ++q) {
+          const size_t cq = (size_t)c * Q + q;
+          const float* W = g->nes_pd + cq * sD;
+          const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd : g->nes_aq[l - 1] + cq * 2 * B * D.fi[l];
+          GemmProb p = fwd_prob(x, 2 * B, W + D.off[l], D.fi[l], D.fo[l], g->nes_aq[l] + cq * 2 * B * D.fo[l],
+                                D.act[l]);
+          if (l == LD - 2) p = with_head(p, W + D.off[LD - 1], g->nes_part_d + cq * 2 * B * g->tn, g->tn);
+          ps.push_back(p);
+        }
+      ops.push_back({OP_GEMM, add_phase(g, ps)});
+    }
+    ops.push_back({OP_NES_HEAD, LIPZ_ROLE_D});
+    ops.push_back({OP_NES_UPDATE, LIPZ_ROLE_D});
+    ops.push_back({OP_NES_PERTURB, LIPZ_ROLE_G});
+    for (int l = 0; l < LG; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c)
+        for (int q = 0; q < Q; ++q) {
+          const size_t cq = (size_t)c * Q + q;
+          const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->nes_hq[l - 1] + cq * B * G.fi[l];
+          float* y = l + 1 < LG ? g->nes_hq[l] + cq * B * G.fo[l] : g->nes_xq + cq * B * xd;
+          ps.push_back(fwd_prob(x, B, g->nes_pg + cq * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
+        }
+      ops.push_back({OP_GEMM, add_phase(g, ps)});
+    }
+    for (int l = 0; l + 1 < LD; ++l) {
+      std::vector<GemmProb> ps;
+      for (int c = 0; c < C; ++c) {
+        const float* x = l == 0 ? g->nes_xq + (size_t)c * Q * B * xd : g->nes_agq[l - 1] + (size_t)c * Q * B * D.fi[l];
+        GemmProb p = fwd_prob(x, Q * B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
+                              g->nes_agq[l] + (size_t)c * Q * B * D.fo[l], D.act[l]);
+        if (l == LD - 2)
+          p = with_head(p, S.Dp + c * sD + D.off[LD - 1], g->nes_part_g + (size_t)c * Q * B * g->tn, g->tn);
+        ps.push_back(p);
+      }
+      ops.push_back({OP_GEMM, add_phase(g, ps)});
+    }
+    ops.push_back({OP_NES_HEAD, LIPZ_ROLE_G});
+    ops.push_back({OP_NES_UPDATE, LIPZ_ROLE_G});
+  }
 }
 
 void build_tables(lipz_grid* g) {
@@ -537,6 +629,7 @@ void build_tables(lipz_grid* g) {
     ps.push_back(base_prob(g->data, g->xd, 0, g->P, g->F, 0, g->realfeat, g->F, (int)g->N, g->F, g->xd));
     g->real_phase = add_phase(g, ps);
   }
+  if (g->cfg.trainer == LIPZ_TRAINER_NES) build_nes_ops(g);
 }
 
 // With timing on: a start / stop event pair for the next matrix-core launch.
@@ -890,6 +983,63 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   hg.act_cell_stride = (int64_t)B * g->D.fi[LD - 1];
   hg.delta = g->dDg[LD - 2];
   hg.dlbuf = nullptr;
+  if (g->cfg.trainer == LIPZ_TRAINER_NES) {
+    NesArgs na[2];
+    for (int role = 0; role < 2; ++role) {
+      NesArgs& a = na[role];
+      memset(&a, 0, sizeof(a));
+      const bool d = role == LIPZ_ROLE_D;
+      a.p = d ? S.Dp : S.Gp;
+      a.m = d ? S.Dm : S.Gm;
+      a.v = d ? S.Dv : S.Gv;
+      a.lr = d ? S.Dlr : S.Glr;
+      a.t = d ? S.Dt : S.Gt;
+      a.sets = d ? g->nes_pd : g->nes_pg;
+      a.part = d ? g->nes_part_d : g->nes_part_g;
+      a.fit = d ? g->nes_fd : g->nes_fg;
+      a.stride = d ? g->D.stride : g->G.stride;
+      a.P = d ? g->D.P : g->G.P;
+      a.n = g->cfg.nes_pairs;
+      a.tn = g->tn;
+      a.B = B;
+      a.C = C;
+      a.role = role;
+      a.loss_kind = g->cfg.loss_kind;
+      a.sigma = g->cfg.nes_sigma;
+      a.clip = (d && g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN) ? g->cfg.wgan_clip : 0.f;
+      a.key = g->key;
+      a.gen = (uint32_t)gen;
+      a.tag = d ? LIPZ_TAG_NES_D : LIPZ_TAG_NES_G;
+      a.ac = g->ac;
+    }
+    for (int k = 0; k < n_steps; ++k) {
+      const int step = step0 + k;
+      for (const Op& op : g->nes_ops[par]) {
+        hipError_t e = hipSuccess;
+        NesArgs a = op.kind >= OP_NES_PERTURB ? na[op.phase] : na[0];
+        a.sf = (uint32_t)(step + 1);
+        a.step_local = k;
+        a.losses = d_losses ? d_losses + (size_t)k * C * 2 : nullptr;
+        switch (op.kind) {
+          case OP_SAMPLE:
+            e = launch_sample(g->data, g->N, g->xd, g->zd, B, 0, C, g->key, (uint32_t)gen, (uint32_t)(step + 1),
+                              g->Xtr, (int64_t)2 * B * g->xd, g->z, (int64_t)B * g->zd, s);
+            break;
+          case OP_GEMM: e = run_gemm_phase(g, op.phase, k, s); break;
+          case OP_NES_PERTURB: e = launch_nes_perturb(a, s); break;
+          case OP_NES_HEAD: e = launch_nes_head(a, s); break;
+          case OP_NES_UPDATE: e = launch_nes_update(a, s); break;
+          default: e = hipErrorInvalidValue; break;
+        }
+        if ((st = check_hip(g, e, "NES step"))) return st;
+      }
+    }
+    hipError_t e = launch_add_i32(S.Gt, C, n_steps, s);
+    if (e == hipSuccess) e = launch_add_i32(S.Dt, C, n_steps, s);
+    if ((st = check_hip(g, e, "step count"))) return st;
+    g->fitness_valid = false;
+    return LIPZ_OK;
+  }
   // fork: every group stream waits for the work already on the caller's stream
   if (g->n_groups > 1) {
     if ((st = check_hip(g, hipEventRecord(g->fork_ev, s), "fork"))) return st;
@@ -1129,6 +1279,17 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
     if (p.dot_out && (!inside(p.dot_out, 0, (int64_t)(p.M - 1) * p.dot_ld + (p.N + GEMM_BN - 1) / GEMM_BN - 1) ||
                       !inside(p.dotw, 0, p.N - 1)))
       note("gemm dot", i);
+  }
+  if (g->cfg.trainer == LIPZ_TRAINER_NES) {
+    // the NES kernels' extents: sets [C][Q][stride] (elements e < P), partial
+    // logits [C][Q][rows][tn], losses [C][Q]
+    const int64_t Q = g->nes_q, C = g->C, B = g->B, tn = g->tn;
+    if (g->D.P > g->D.stride || g->G.P > g->G.stride) note("nes parameter row", 0);
+    if (!inside(g->nes_pd, 0, C * Q * g->D.stride - 1)) note("nes sets D", 0);
+    if (!inside(g->nes_pg, 0, C * Q * g->G.stride - 1)) note("nes sets G", 0);
+    if (!inside(g->nes_part_d, 0, C * Q * 2 * B * tn - 1)) note("nes logits D", 0);
+    if (!inside(g->nes_part_g, 0, C * Q * B * tn - 1)) note("nes logits G", 0);
+    if (!inside(g->nes_fd, 0, C * Q - 1) || !inside(g->nes_fg, 0, C * Q - 1)) note("nes losses", 0);
   }
   if (g->dc) bad += dc_check_bounds(g, lo, hi, 2, &text);
   *n_bad = bad;

@@ -65,7 +65,9 @@ struct Phase {
   double bytes = 0.0;  // algorithmic: each operand read once, each output written once
 };
 
-enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G };
+// A training-step op: a GEMM phase, or a kernel of the step; for the NES ops
+// `phase` holds the role (LIPZ_ROLE_G / LIPZ_ROLE_D).
+enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G, OP_NES_PERTURB, OP_NES_HEAD, OP_NES_UPDATE };
 struct Op {
   OpKind kind;
   int phase;
@@ -142,6 +144,16 @@ struct lipz_grid {
   int64_t gemm_launches = 0;
 
   lipz::DcPlan* dc = nullptr;  // set for LIPZ_NET_DCGAN
+
+  // NES trainer: Q = 2 nes_pairs + 1 parameter sets per role and cell (the
+  // + and - perturbations, then the unperturbed parameters)
+  int nes_q = 0;
+  float *nes_pd = nullptr, *nes_pg = nullptr;                         // [C][Q][stride]
+  float *nes_aq[LIPZ_MAX_HIDDEN] = {}, *nes_part_d = nullptr;         // D per set on the 2B rows
+  float *nes_hq[LIPZ_MAX_HIDDEN] = {}, *nes_xq = nullptr;             // G per set
+  float *nes_agq[LIPZ_MAX_HIDDEN] = {}, *nes_part_g = nullptr;        // D on the Q B generated rows
+  float *nes_fd = nullptr, *nes_fg = nullptr;                         // losses per set [C][Q]
+  std::vector<Op> nes_ops[2];
 };
 
 namespace lipz {

@@ -218,6 +218,78 @@ __global__ __launch_bounds__(NT) void head_eval_kernel(EvalHeadArgs A) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// NES trainer (Section 3 lists NES among the trainers; reading: antithetic
+// estimate + Adam).  eps_k[e] = normal k P + e of stream (cell, gen, sf, tag).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float nes_eps(const NesArgs& A, int c, int k, int64_t e) {
+  const int64_t i = (int64_t)k * A.P + e;
+  const uint4 w = stream_block(A.key, (uint32_t)(i >> 2), (uint32_t)c, A.gen, A.sf, A.tag);
+  return (float)normal_of(w, (int)(i & 3));
+}
+
+// block (x, q, c): elements of set q of cell c
+__global__ __launch_bounds__(NT) void nes_perturb_kernel(NesArgs A) {
+  const int q = blockIdx.y, c = blockIdx.z;
+  const int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (e >= A.P) return;
+  const float th = A.p[c * A.stride + e];
+  float y = th;
+  if (q < 2 * A.n) {
+    const int k = q < A.n ? q : q - A.n;
+    const float se = A.sigma * nes_eps(A, c, k, e);
+    y = q < A.n ? th + se : th - se;
+  }
+  A.sets[((int64_t)c * (2 * A.n + 1) + q) * A.stride + e] = y;
+}
+
+// block (q, c): the loss of set q from the partial logits, in a fixed order.
+// D role: rows [x; G(z)] (2B); G role: the B rows generated by set q.
+__global__ __launch_bounds__(NT) void nes_head_kernel(NesArgs A) {
+  __shared__ float red[4];
+  const int q = blockIdx.x, c = blockIdx.y, Q = 2 * A.n + 1;
+  const bool d_role = A.role == LIPZ_ROLE_D;
+  const int rows = d_role ? 2 * A.B : A.B;
+  const float* part = A.part + ((int64_t)c * Q + q) * rows * A.tn;
+  float s = 0.f;
+  for (int r = threadIdx.x; r < rows; r += NT) {
+    float a = 0.f;
+    for (int t = 0; t < A.tn; ++t) a += part[(int64_t)r * A.tn + t];
+    s += (d_role && r >= A.B) ? fake_term(A.loss_kind, a) : real_term(A.loss_kind, a);
+  }
+  s = block_sum(s, red);
+  if (threadIdx.x == 0) {
+    const float f = s / (float)A.B;
+    A.fit[c * Q + q] = f;
+    if (q == 2 * A.n && A.losses) A.losses[c * 2 + (d_role ? 0 : 1)] = f;
+  }
+}
+
+// block (x, c): g[e] = sum_k (F_k+ - F_k-) eps_k[e] / (2 n sigma), then one
+// bias-corrected Adam step of parameter e (and the clip, when set)
+__global__ __launch_bounds__(NT) void nes_update_kernel(NesArgs A) {
+  const int c = blockIdx.y, Q = 2 * A.n + 1;
+  const int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (e >= A.P) return;
+  const float* f = A.fit + c * Q;
+  float g = 0.f;
+  for (int k = 0; k < A.n; ++k) g += (f[k] - f[A.n + k]) * nes_eps(A, c, k, e);
+  g /= 2.f * (float)A.n * A.sigma;
+  const int64_t o = c * A.stride + e;
+  const float lr = A.lr[c];
+  const int tt = A.t[c] + A.step_local + 1;
+  const AdamConsts& ac = A.ac;
+  const float bc1 = (float)(1.0 - pow((double)ac.beta1, (double)tt));
+  const float bc2 = (float)(1.0 - pow((double)ac.beta2, (double)tt));
+  const float m = ac.beta1 * A.m[o] + ac.one_minus_beta1 * g;
+  const float v = ac.beta2 * A.v[o] + ac.one_minus_beta2 * g * g;
+  float p = A.p[o] - lr * (m / bc1) / (sqrtf(v / bc2) + ac.eps);
+  if (A.clip > 0.f) p = p > A.clip ? A.clip : (p < -A.clip ? -A.clip : p);
+  A.m[o] = m;
+  A.v[o] = v;
+  A.p[o] = p;
+}
+
 // fit_d[c][j] = mean_i L[c][i][j]; fit_g[c][i] = -mean_j L[c][i][j] (mode 0)
 // or mean_j Lg[c][i][j] (mode 1).  Flags bit 0 on any non-finite value.
 __global__ void fitness_kernel(const float* L, const float* Lg, int C, int mode, float* fit_g,
@@ -487,6 +559,18 @@ hipError_t launch_head_d(const HeadArgs& a, hipStream_t s) {
 hipError_t launch_head_g(const HeadArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(head_kernel<false>, dim3(a.C, (a.H + 63) / 64, (a.B + HEAD_ROWS - 1) / HEAD_ROWS),
                      dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_nes_perturb(const NesArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(nes_perturb_kernel, dim3((unsigned)((a.P + NT - 1) / NT), 2 * a.n + 1, a.C), dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_nes_head(const NesArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(nes_head_kernel, dim3(2 * a.n + 1, a.C), dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_nes_update(const NesArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(nes_update_kernel, dim3((unsigned)((a.P + NT - 1) / NT), a.C), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s) {

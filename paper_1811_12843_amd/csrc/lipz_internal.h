@@ -425,6 +425,34 @@ struct EvalHeadArgs {
   int loss_kind;         // LIPZ_LOSS_BCE or LIPZ_LOSS_WASSERSTEIN
 };
 hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s);
+
+// NES trainer (one role): perturbed parameter sets, their losses, and the
+// estimate + Adam step.  Set q < n holds theta + sigma eps_q, set n + k holds
+// theta - sigma eps_k, set 2n holds theta; eps_k[e] is normal k P + e of
+// stream (cell, gen, sf, tag).
+struct NesArgs {
+  float* p;              // the role's parameters, cell c at p + c * stride (updated in place)
+  float* m;
+  float* v;
+  const float* lr;       // [C]
+  const int32_t* t;      // [C] Adam step count before this call
+  float* sets;           // [C][Q][stride]
+  const float* part;     // partial logits: D role [C][Q][2B][tn], G role [C][Q B][tn]
+  float* fit;            // [C][Q] loss of each set
+  float* losses;         // [C][2] slice of this step, or null
+  int64_t stride, P;
+  int n, tn, B, C;
+  int role;              // LIPZ_ROLE_G / LIPZ_ROLE_D
+  int loss_kind;
+  float sigma, clip;     // clip > 0: clip the updated parameters (Wasserstein critic)
+  uint2 key;
+  uint32_t gen, sf, tag;
+  int step_local;
+  AdamConsts ac;
+};
+hipError_t launch_nes_perturb(const NesArgs& a, hipStream_t s);
+hipError_t launch_nes_head(const NesArgs& a, hipStream_t s);
+hipError_t launch_nes_update(const NesArgs& a, hipStream_t s);
 hipError_t launch_fitness(const float* L, const float* Lg, int C, int mode, float* fit_g, float* fit_d,
                           int32_t* flags, float* out_L, float* out_Lg, float* out_fg, float* out_fd,
                           hipStream_t s);

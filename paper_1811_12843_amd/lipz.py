@@ -20,6 +20,8 @@ LIPZ_ACT_LINEAR, LIPZ_ACT_RELU, LIPZ_ACT_LRELU, LIPZ_ACT_TANH = 0, 1, 2, 3
 LIPZ_ROLE_G, LIPZ_ROLE_D = 0, 1
 LIPZ_LOSS_BCE, LIPZ_LOSS_WASSERSTEIN = 0, 1
 LOSSES = {"bce": LIPZ_LOSS_BCE, "wasserstein": LIPZ_LOSS_WASSERSTEIN}
+LIPZ_TRAINER_GRADIENT, LIPZ_TRAINER_NES = 0, 1
+TRAINERS = {"gradient": LIPZ_TRAINER_GRADIENT, "nes": LIPZ_TRAINER_NES}
 ACTS = {"linear": LIPZ_ACT_LINEAR, "relu": LIPZ_ACT_RELU, "lrelu": LIPZ_ACT_LRELU, "tanh": LIPZ_ACT_TANH}
 
 _i32, _i64, _f32, _u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_uint64
@@ -40,6 +42,7 @@ class lipz_config(ctypes.Structure):
         ("mix_enable", _i32), ("mix_samples", _i32), ("mix_feat_dim", _i32), ("mix_sigma", _f32),
         ("seed", _u64),
         ("loss_kind", _i32), ("wgan_clip", _f32),
+        ("trainer", _i32), ("nes_pairs", _i32), ("nes_sigma", _f32),
     ]
 
 
@@ -77,6 +80,9 @@ def config_from_dict(d):
     c.seed = d["seed"]
     c.loss_kind = LOSSES[d.get("loss", "bce")]
     c.wgan_clip = d.get("wgan_clip", 0.01)
+    c.trainer = TRAINERS[d.get("trainer", "gradient")]
+    c.nes_pairs = d.get("nes_pairs", 8)
+    c.nes_sigma = d.get("nes_sigma", 0.01)
     return c
 
 

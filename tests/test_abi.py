@@ -74,6 +74,16 @@ def test_workspace_sizing_and_validation():
     assert L.lipz_workspace_bytes(L.config_from_dict(synth.workload("mnist_mlp_4x4_wgan")), 60000) > 0
     d = dict(synth.workload("celeba_dcgan_4x4"), loss="wasserstein")
     assert L.lipz_workspace_bytes(L.config_from_dict(d), 1000) == 0
+    # the NES trainer: its Q = 2 nes_pairs + 1 parameter sets per role and cell add to the workspace
+    nes = synth.workload("mnist_mlp_3x3_nes")
+    assert L.lipz_workspace_bytes(L.config_from_dict(nes), 60000) > base
+    for b in (dict(nes, nes_pairs=0), dict(nes, nes_pairs=65), dict(nes, nes_sigma=0.0)):
+        assert L.lipz_workspace_bytes(L.config_from_dict(b), 60000) == 0
+    c = L.config_from_dict(nes)
+    c.trainer = 2
+    assert L.lipz_workspace_bytes(c, 60000) == 0
+    d = dict(synth.workload("celeba_dcgan_4x4"), trainer="nes")
+    assert L.lipz_workspace_bytes(L.config_from_dict(d), 1000) == 0
     c = L.config_from_dict(w)
     c.abi_version = 99
     assert L.lipz_workspace_bytes(c, 60000) == 0
