@@ -92,6 +92,9 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
   };
   build(Gn, c->z_dim, c->n_g_hidden, c->g_hidden, c->x_dim, c->g_hidden_act, c->g_out_act);
   build(Dn, c->x_dim, c->n_d_hidden, c->d_hidden, 1, c->d_hidden_act, LIPZ_ACT_LINEAR);
+  if (c->trainer == LIPZ_TRAINER_NES &&
+      (int64_t)c->nes_pairs * (Gn->P > Dn->P ? Gn->P : Dn->P) >= ((int64_t)1 << 31))
+    return "nes_pairs x parameters of a network must stay below 2^31";
   return "";
 }
 
@@ -198,8 +201,13 @@ void carve(lipz_grid* g, char* base, size_t* total) {
   }
   if (g->cfg.trainer == LIPZ_TRAINER_NES) {
     const int Q = g->nes_q = 2 * g->cfg.nes_pairs + 1;
-    g->nes_pd = cv.take<float>((size_t)C * Q * D.stride);
-    g->nes_pg = cv.take<float>((size_t)C * Q * G.stride);
+    // the perturbed sets (the unperturbed one is the parameters themselves),
+    // and one direction buffer shared by the two roles, which run one after
+    // the other on the stream
+    g->nes_pd = cv.take<float>((size_t)C * (Q - 1) * D.stride);
+    g->nes_pg = cv.take<float>((size_t)C * (Q - 1) * G.stride);
+    g->nes_eps_stride = D.stride > G.stride ? D.stride : G.stride;
+    g->nes_eps = cv.take<float>((size_t)C * g->cfg.nes_pairs * g->nes_eps_stride);
     for (int l = 0; l + 1 < D.nl; ++l) {
       g->nes_aq[l] = cv.take<float>((size_t)C * Q * 2 * B * D.fo[l]);
       g->nes_agq[l] = cv.take<float>((size_t)C * Q * B * D.fo[l]);
@@ -403,7 +411,7 @@ void build_nes_ops(lipz_grid* g) {
       for (int c = 0; c < C; ++c)
         for (int q = 0; q < Q; ++q) {
           const size_t cq = (size_t)c * Q + q;
-          const float* W = g->nes_pd + cq * sD;
+          const float* W = q + 1 < Q ? g->nes_pd + ((size_t)c * (Q - 1) + q) * sD : S.Dp + c * sD;
           const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd : g->nes_aq[l - 1] + cq * 2 * B * D.fi[l];
           GemmProb p = fwd_prob(x, 2 * B, W + D.off[l], D.fi[l], D.fo[l], g->nes_aq[l] + cq * 2 * B * D.fo[l],
                                 D.act[l]);
@@ -422,7 +430,8 @@ void build_nes_ops(lipz_grid* g) {
           const size_t cq = (size_t)c * Q + q;
           const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->nes_hq[l - 1] + cq * B * G.fi[l];
           float* y = l + 1 < LG ? g->nes_hq[l] + cq * B * G.fo[l] : g->nes_xq + cq * B * xd;
-          ps.push_back(fwd_prob(x, B, g->nes_pg + cq * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
+          const float* W = q + 1 < Q ? g->nes_pg + ((size_t)c * (Q - 1) + q) * sG : S.Gp + c * sG;
+          ps.push_back(fwd_prob(x, B, W + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
         }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
     }
@@ -995,6 +1004,8 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
       a.lr = d ? S.Dlr : S.Glr;
       a.t = d ? S.Dt : S.Gt;
       a.sets = d ? g->nes_pd : g->nes_pg;
+      a.eps = g->nes_eps;
+      a.eps_stride = g->nes_eps_stride;
       a.part = d ? g->nes_part_d : g->nes_part_g;
       a.fit = d ? g->nes_fd : g->nes_fg;
       a.stride = d ? g->D.stride : g->G.stride;
@@ -1281,12 +1292,15 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
       note("gemm dot", i);
   }
   if (g->cfg.trainer == LIPZ_TRAINER_NES) {
-    // the NES kernels' extents: sets [C][Q][stride] (elements e < P), partial
-    // logits [C][Q][rows][tn], losses [C][Q]
-    const int64_t Q = g->nes_q, C = g->C, B = g->B, tn = g->tn;
+    // the NES kernels' extents: sets [C][2n][stride] and directions
+    // [C][n][eps_stride] (elements e < P), partial logits [C][Q][rows][tn],
+    // losses [C][Q]
+    const int64_t Q = g->nes_q, C = g->C, B = g->B, tn = g->tn, n = g->cfg.nes_pairs;
     if (g->D.P > g->D.stride || g->G.P > g->G.stride) note("nes parameter row", 0);
-    if (!inside(g->nes_pd, 0, C * Q * g->D.stride - 1)) note("nes sets D", 0);
-    if (!inside(g->nes_pg, 0, C * Q * g->G.stride - 1)) note("nes sets G", 0);
+    if (g->D.P > g->nes_eps_stride || g->G.P > g->nes_eps_stride) note("nes direction row", 0);
+    if (!inside(g->nes_pd, 0, C * 2 * n * g->D.stride - 1)) note("nes sets D", 0);
+    if (!inside(g->nes_pg, 0, C * 2 * n * g->G.stride - 1)) note("nes sets G", 0);
+    if (!inside(g->nes_eps, 0, C * n * g->nes_eps_stride - 1)) note("nes directions", 0);
     if (!inside(g->nes_part_d, 0, C * Q * 2 * B * tn - 1)) note("nes logits D", 0);
     if (!inside(g->nes_part_g, 0, C * Q * B * tn - 1)) note("nes logits G", 0);
     if (!inside(g->nes_fd, 0, C * Q - 1) || !inside(g->nes_fg, 0, C * Q - 1)) note("nes losses", 0);

@@ -148,7 +148,9 @@ struct lipz_grid {
   // NES trainer: Q = 2 nes_pairs + 1 parameter sets per role and cell (the
   // + and - perturbations, then the unperturbed parameters)
   int nes_q = 0;
-  float *nes_pd = nullptr, *nes_pg = nullptr;                         // [C][Q][stride]
+  float *nes_pd = nullptr, *nes_pg = nullptr;                         // [C][2n][stride]
+  float* nes_eps = nullptr;                                           // [C][n][nes_eps_stride]
+  int64_t nes_eps_stride = 0;
   float *nes_aq[LIPZ_MAX_HIDDEN] = {}, *nes_part_d = nullptr;         // D per set on the 2B rows
   float *nes_hq[LIPZ_MAX_HIDDEN] = {}, *nes_xq = nullptr;             // G per set
   float *nes_agq[LIPZ_MAX_HIDDEN] = {}, *nes_part_g = nullptr;        // D on the Q B generated rows

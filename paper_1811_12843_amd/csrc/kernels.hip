@@ -222,25 +222,43 @@ __global__ __launch_bounds__(NT) void head_eval_kernel(EvalHeadArgs A) {
 // NES trainer (Section 3 lists NES among the trainers; reading: antithetic
 // estimate + Adam).  eps_k[e] = normal k P + e of stream (cell, gen, sf, tag).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float nes_eps(const NesArgs& A, int c, int k, int64_t e) {
-  const int64_t i = (int64_t)k * A.P + e;
-  const uint4 w = stream_block(A.key, (uint32_t)(i >> 2), (uint32_t)c, A.gen, A.sf, A.tag);
-  return (float)normal_of(w, (int)(i & 3));
-}
-
-// block (x, q, c): elements of set q of cell c
+// Thread b of cell c draws Philox block b of the cell's direction stream:
+// normals i = 4b .. 4b+3 of the n P (direction k = i / P, element e = i % P).
+// The workgroup's 4 NT normals pass through LDS so that each store writes NT
+// consecutive elements.  Every normal is drawn once; it goes to eps and to
+// the sets theta + sigma eps_k and theta - sigma eps_k.  n P < 2^31.
 __global__ __launch_bounds__(NT) void nes_perturb_kernel(NesArgs A) {
-  const int q = blockIdx.y, c = blockIdx.z;
-  const int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x;
-  if (e >= A.P) return;
-  const float th = A.p[c * A.stride + e];
-  float y = th;
-  if (q < 2 * A.n) {
-    const int k = q < A.n ? q : q - A.n;
-    const float se = A.sigma * nes_eps(A, c, k, e);
-    y = q < A.n ? th + se : th - se;
+  __shared__ float4 zs4[NT];
+  const int c = blockIdx.y;
+  const uint32_t P = (uint32_t)A.P, total = (uint32_t)A.n * P;
+  const uint32_t b0 = blockIdx.x * NT, b = b0 + threadIdx.x;
+  if (4u * b < total) {
+    const uint4 w = stream_block(A.key, b, (uint32_t)c, A.gen, A.sf, A.tag);
+    const double r01 = sqrt(-2.0 * log(uniform_of(w.x)));
+    const double r23 = sqrt(-2.0 * log(uniform_of(w.z)));
+    double s01, c01, s23, c23;
+    // the angle 2 pi u as sincospi(2 u): no argument reduction by 2 pi
+    sincospi(2.0 * uniform_of(w.y), &s01, &c01);
+    sincospi(2.0 * uniform_of(w.w), &s23, &c23);
+    zs4[threadIdx.x] = make_float4((float)(r01 * c01), (float)(r01 * s01), (float)(r23 * c23), (float)(r23 * s23));
   }
-  A.sets[((int64_t)c * (2 * A.n + 1) + q) * A.stride + e] = y;
+  __syncthreads();
+  const float* zs = reinterpret_cast<const float*>(zs4);
+  const float* th = A.p + c * A.stride;
+  float* sets = A.sets + (int64_t)c * 2 * A.n * A.stride;
+  float* dir = A.eps + (int64_t)c * A.n * A.eps_stride;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t i = 4u * b0 + threadIdx.x + j * NT;
+    if (i >= total) break;
+    const float z = zs[threadIdx.x + j * NT];
+    const uint32_t k = i / P, e = i - k * P;
+    const float se = A.sigma * z;
+    const float t = th[e];
+    sets[(int64_t)k * A.stride + e] = t + se;
+    sets[(int64_t)(A.n + k) * A.stride + e] = t - se;
+    dir[(int64_t)k * A.eps_stride + e] = z;
+  }
 }
 
 // block (q, c): the loss of set q from the partial logits, in a fixed order.
@@ -268,22 +286,36 @@ __global__ __launch_bounds__(NT) void nes_head_kernel(NesArgs A) {
 // block (x, c): g[e] = sum_k (F_k+ - F_k-) eps_k[e] / (2 n sigma), then one
 // bias-corrected Adam step of parameter e (and the clip, when set)
 __global__ __launch_bounds__(NT) void nes_update_kernel(NesArgs A) {
+  __shared__ float bc[2];
   const int c = blockIdx.y, Q = 2 * A.n + 1;
+  const AdamConsts& ac = A.ac;
+  if (threadIdx.x == 0) {
+    const int tt = A.t[c] + A.step_local + 1;
+    bc[0] = (float)(1.0 - pow((double)ac.beta1, (double)tt));
+    bc[1] = (float)(1.0 - pow((double)ac.beta2, (double)tt));
+  }
+  __syncthreads();
   const int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x;
   if (e >= A.P) return;
   const float* f = A.fit + c * Q;
+  const float* dir = A.eps + (int64_t)c * A.n * A.eps_stride + e;
+  // eight directions' loads in flight at once; the sum keeps the order k = 0, 1, ...
   float g = 0.f;
-  for (int k = 0; k < A.n; ++k) g += (f[k] - f[A.n + k]) * nes_eps(A, c, k, e);
+  int k = 0;
+  for (; k + 8 <= A.n; k += 8) {
+    float d[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) d[j] = dir[(int64_t)(k + j) * A.eps_stride];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) g += (f[k + j] - f[A.n + k + j]) * d[j];
+  }
+  for (; k < A.n; ++k) g += (f[k] - f[A.n + k]) * dir[(int64_t)k * A.eps_stride];
   g /= 2.f * (float)A.n * A.sigma;
   const int64_t o = c * A.stride + e;
   const float lr = A.lr[c];
-  const int tt = A.t[c] + A.step_local + 1;
-  const AdamConsts& ac = A.ac;
-  const float bc1 = (float)(1.0 - pow((double)ac.beta1, (double)tt));
-  const float bc2 = (float)(1.0 - pow((double)ac.beta2, (double)tt));
   const float m = ac.beta1 * A.m[o] + ac.one_minus_beta1 * g;
   const float v = ac.beta2 * A.v[o] + ac.one_minus_beta2 * g * g;
-  float p = A.p[o] - lr * (m / bc1) / (sqrtf(v / bc2) + ac.eps);
+  float p = A.p[o] - lr * (m / bc[0]) / (sqrtf(v / bc[1]) + ac.eps);
   if (A.clip > 0.f) p = p > A.clip ? A.clip : (p < -A.clip ? -A.clip : p);
   A.m[o] = m;
   A.v[o] = v;
@@ -562,7 +594,8 @@ hipError_t launch_head_g(const HeadArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 hipError_t launch_nes_perturb(const NesArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(nes_perturb_kernel, dim3((unsigned)((a.P + NT - 1) / NT), 2 * a.n + 1, a.C), dim3(NT), 0, s, a);
+  const int64_t blocks = ((int64_t)a.n * a.P + 3) / 4;
+  hipLaunchKernelGGL(nes_perturb_kernel, dim3((unsigned)((blocks + NT - 1) / NT), a.C), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_nes_head(const NesArgs& a, hipStream_t s) {

@@ -436,11 +436,12 @@ struct NesArgs {
   float* v;
   const float* lr;       // [C]
   const int32_t* t;      // [C] Adam step count before this call
-  float* sets;           // [C][Q][stride]
+  float* sets;           // [C][2n][stride]: theta + sigma eps_k (k < n), theta - sigma eps_(k-n)
+  float* eps;            // [C][n][eps_stride]: the directions eps_k in fp32
   const float* part;     // partial logits: D role [C][Q][2B][tn], G role [C][Q B][tn]
   float* fit;            // [C][Q] loss of each set
   float* losses;         // [C][2] slice of this step, or null
-  int64_t stride, P;
+  int64_t stride, P, eps_stride;
   int n, tn, B, C;
   int role;              // LIPZ_ROLE_G / LIPZ_ROLE_D
   int loss_kind;

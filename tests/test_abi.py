@@ -77,7 +77,8 @@ def test_workspace_sizing_and_validation():
     # the NES trainer: its Q = 2 nes_pairs + 1 parameter sets per role and cell add to the workspace
     nes = synth.workload("mnist_mlp_3x3_nes")
     assert L.lipz_workspace_bytes(L.config_from_dict(nes), 60000) > base
-    for b in (dict(nes, nes_pairs=0), dict(nes, nes_pairs=65), dict(nes, nes_sigma=0.0)):
+    for b in (dict(nes, nes_pairs=0), dict(nes, nes_pairs=65), dict(nes, nes_sigma=0.0),
+              dict(nes, g_hidden=[65536, 8192])):  # nes_pairs x parameters >= 2^31
         assert L.lipz_workspace_bytes(L.config_from_dict(b), 60000) == 0
     c = L.config_from_dict(nes)
     c.trainer = 2

@@ -30,7 +30,7 @@ RAGGED = dict(rows=2, cols=3, z_dim=7, x_dim=37, g_hidden=[33, 70], d_hidden=[45
 
 CASES = {
     "mnist_3x3_nes": dict(name="mnist_mlp_3x3_nes", over=dict(nes_pairs=4)),
-    "ragged_2x3_nes": dict(name="mnist_mlp_3x3_nes", over=dict(RAGGED, nes_pairs=3, nes_sigma=0.02)),
+    "ragged_2x3_nes": dict(name="mnist_mlp_3x3_nes", over=dict(RAGGED, nes_pairs=9, nes_sigma=0.02)),
     "ragged_2x3_nes_wgan": dict(name="mnist_mlp_3x3_nes", over=dict(RAGGED, nes_pairs=3, loss="wasserstein",
                                                                      wgan_clip=0.05)),
 }

@@ -39,6 +39,25 @@ def test_small_dcgan_plans_stay_in_bounds(i):
     assert n_bad == 0, msg
 
 
+SMALL_NES = [
+    dict(rows=2, cols=3, z_dim=7, x_dim=37, g_hidden=[33, 70], d_hidden=[45, 19], batch=19, nes_pairs=3,
+         data=dict(kind="mnist_like", n=300)),
+    dict(rows=1, cols=1, z_dim=3, x_dim=5, g_hidden=[6], d_hidden=[7], batch=2, nes_pairs=1,
+         data=dict(kind="mnist_like", n=50)),
+    dict(rows=2, cols=2, z_dim=9, x_dim=11, g_hidden=[13], d_hidden=[17, 3], batch=4, nes_pairs=64,
+         loss="wasserstein", data=dict(kind="mnist_like", n=50)),
+]
+
+
+@pytest.mark.parametrize("i", range(len(SMALL_NES)))
+def test_small_nes_plans_stay_in_bounds(i):
+    """Parameter counts that are not multiples of 4, so a thread's four
+    directions straddle two directions and the end of the stream."""
+    wl = synth.small_workload("mnist_mlp_3x3_nes", **SMALL_NES[i])
+    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
+    assert n_bad == 0, msg
+
+
 def test_invalid_dcgan_shapes_are_rejected():
     wl = synth.small_workload("celeba_dcgan_4x4", img=(48, 48, 3), x_dim=48 * 48 * 3)
     assert L.lipz_workspace_bytes(L.config_from_dict(wl), 100) == 0
