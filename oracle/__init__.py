@@ -18,11 +18,15 @@ Modules
            training step (Adam), one generation
   mixture  the (1+1)-ES over the generator-mixture weights and its score
   nes      the gradient-free NES trainer (antithetic estimate + Adam)
+  es       the gradient-free (1+lambda)-ES trainer (plus-selection over
+           antithetic Gaussian mutants)
 
 Pinned by tests/test_oracle_*.py against: published Philox known-answer
 vectors and rocRAND's host Philox, hand-enumerated neighbourhoods, BCE closed
 forms, finite differences, torch CPU fp64 convolutions, batch norm and autograd, Adam closed forms and
 torch.optim.Adam, brute-force tournament enumeration, the 1x1-grid reduction
 to plain alternating GAN training, Frechet-distance closed forms, and, for
-NES, exactness on quadratics and convergence to the backpropagated gradient.
+NES, exactness on quadratics and convergence to the backpropagated gradient;
+for ES, the selection rule on hand-made losses, brute-force scoring of every
+candidate with torch networks and the elitist invariant.
 """

@@ -120,10 +120,10 @@ class Setup:
             raise ValueError("the Wasserstein trainer is defined for the MLP workloads")
         self.clip = float(wl.get("wgan_clip", 0.01))
         self.trainer = wl.get("trainer", "gradient")
-        if self.trainer not in ("gradient", "nes"):
+        if self.trainer not in ("gradient", "nes", "es"):
             raise ValueError(f"unknown trainer {self.trainer!r}")
-        if self.trainer == "nes" and wl["net"] != "mlp":
-            raise ValueError("the NES trainer is defined for the MLP workloads")
+        if self.trainer in ("nes", "es") and wl["net"] != "mlp":
+            raise ValueError("the gradient-free trainers are defined for the MLP workloads")
 
 
 class State:
@@ -316,10 +316,10 @@ def train_step(S, st, data, gen, step):
 
 def generation(S, st, data, gen, mix_stats=None):
     """Steps 2-4 for one generation; returns (new state, record dict)."""
-    from . import mixture, nes
+    from . import es, mixture, nes
     L, Lg, fg, fd = evaluate(S, st, data, gen)
     st2, sel = select_replace(S, st, fg, fd, gen)
-    step_fn = nes.train_step if S.trainer == "nes" else train_step
+    step_fn = {"nes": nes.train_step, "es": es.train_step}.get(S.trainer, train_step)
     losses = [step_fn(S, st2, data, gen, s) for s in range(S.wl["steps"])]
     rec = dict(L=L, Lg=Lg, fit_g=fg, fit_d=fd, sel=sel, losses=np.array(losses))
     if S.wl["mix_enable"]:
