@@ -18,8 +18,9 @@ Prints one JSON line:
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
 Other workloads (--workload): ring8_mlp_2x2, mnist_mlp_3x3, mnist_mlp_8x8,
-mnist_mlp_4x4_wgan (the Wasserstein trainer), mnist_mlp_3x3_nes (the
-gradient-free NES trainer) and celeba_dcgan_4x4 (the 64x64 DCGAN grid; its
+mnist_mlp_4x4_wgan (the Wasserstein trainer), mnist_mlp_3x3_nes and
+mnist_mlp_3x3_es (the gradient-free NES and (1+lambda)-ES trainers) and
+celeba_dcgan_4x4 (the 64x64 DCGAN grid; its
 roofline kernel is the implicit-GEMM convolution together with the grouped
 GEMM).
 """
@@ -64,8 +65,8 @@ def gemm_flops_per_generation(wl):
     macs_g, g_first, macs_d, d_first = macs_per_sample(wl)
     # evaluation: 5 G forwards per cell, D forwards on B real + 5B fake rows per D slot
     ev = C * (5 * B * macs_g + 5 * 6 * B * macs_d)
-    if wl.get("trainer", "gradient") == "nes":
-        # NES: G fwd; Q = 2 pairs + 1 critic parameter sets, each D fwd over 2B rows;
+    if wl.get("trainer", "gradient") in ("nes", "es"):
+        # NES / ES: G fwd; Q = 2 pairs + 1 critic parameter sets, each D fwd over 2B rows;
         # Q generator sets, each G fwd, and the updated D over their Q B rows
         Q = 2 * wl["nes_pairs"] + 1
         train = C * wl["steps"] * (B * macs_g + Q * 2 * B * macs_d + Q * B * macs_g + Q * B * macs_d)
@@ -120,9 +121,9 @@ def cpu_baseline(wl, data, budget_s=20.0):
     forwards) and one cell's training step (a 1x1 grid draws cell 0's samples),
     each scaled by the number of cells."""
     import numpy as np
-    from oracle import coevo, mixture, nes
+    from oracle import coevo, es, mixture, nes
     cores = _oracle_cores()
-    step_fn = nes.train_step if wl.get("trainer", "gradient") == "nes" else coevo.train_step
+    step_fn = {"nes": nes.train_step, "es": es.train_step}.get(wl.get("trainer", "gradient"), coevo.train_step)
     S = coevo.Setup(wl, len(data))
     st = coevo.create(S)
     if wl["net"] != "mlp":

@@ -94,8 +94,16 @@ enum { LIPZ_LOSS_BCE = 0, LIPZ_LOSS_WASSERSTEIN = 1 };
  * Gaussian directions eps_k (normal k P + e of stream (cell, gen, s + 1,
  * NES_G / NES_D)), the role's loss F at theta +- nes_sigma eps_k on the
  * step's minibatch, g = sum_k (F_k+ - F_k-) eps_k / (2 nes_pairs nes_sigma),
- * one Adam step of theta on g.  MLP networks only. */
-enum { LIPZ_TRAINER_GRADIENT = 0, LIPZ_TRAINER_NES = 1 };
+ * one Adam step of theta on g.  ES: the gradient-free evolution-strategies
+ * trainer of the same passage, read as a (1+lambda)-ES like the mixture
+ * step's (1+1)-ES: per step and role the same 2 nes_pairs mutants
+ * theta +- nes_sigma eps_k and the parent theta are scored on the step's
+ * minibatch; the mutant of lowest loss replaces theta only if its loss is
+ * strictly lower (among equal mutants the first in the order +eps_0 ..
+ * +eps_(n-1), -eps_0 .. -eps_(n-1)); Adam's moments are not used.  Both
+ * gradient-free trainers: MLP networks only, nes_pairs x (parameters of a
+ * network) < 2^31. */
+enum { LIPZ_TRAINER_GRADIENT = 0, LIPZ_TRAINER_NES = 1, LIPZ_TRAINER_ES = 2 };
 enum {
   LIPZ_TAG_IDX = 1, LIPZ_TAG_Z = 2, LIPZ_TAG_TOURN_G = 3, LIPZ_TAG_TOURN_D = 4,
   LIPZ_TAG_LRMUT_G = 5, LIPZ_TAG_LRMUT_D = 6, LIPZ_TAG_MIXN = 7, LIPZ_TAG_MIXZ = 8,
@@ -144,9 +152,9 @@ typedef struct {
   uint64_t seed;
   int32_t loss_kind;                /* LIPZ_LOSS_BCE (paper) or LIPZ_LOSS_WASSERSTEIN (MLP only) */
   float wgan_clip;                  /* critic clipping bound (> 0) for LIPZ_LOSS_WASSERSTEIN */
-  int32_t trainer;                  /* LIPZ_TRAINER_GRADIENT (paper's experiments) or LIPZ_TRAINER_NES */
-  int32_t nes_pairs;                /* NES: antithetic direction pairs, 1..64 */
-  float nes_sigma;                  /* NES: perturbation scale (> 0) */
+  int32_t trainer;                  /* LIPZ_TRAINER_GRADIENT (paper's experiments), _NES or _ES */
+  int32_t nes_pairs;                /* NES / ES: antithetic direction (mutant) pairs, 1..64 */
+  float nes_sigma;                  /* NES / ES: perturbation (mutation) scale (> 0) */
 } lipz_config;
 
 typedef struct lipz_grid lipz_grid;  /* opaque host handle */
@@ -210,7 +218,9 @@ lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forc
  * [-wgan_clip, wgan_clip]; the generator minimises -mean D'(G(z)).
  * LIPZ_TRAINER_NES: the same two losses, each minimised by one Adam step on
  * the NES estimate of its gradient (see LIPZ_TRAINER_NES); the losses
- * reported are those at the unperturbed parameters.
+ * reported are those at the unperturbed parameters.  LIPZ_TRAINER_ES: the
+ * same two losses, each by one plus-selection (see LIPZ_TRAINER_ES), then
+ * the critic clip; losses at the parents; step counts advance by n_steps.
  * d_losses [n_steps][C][2] fp32 (L_D, L_G before each update) may be NULL. */
 lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_steps,
                             float* d_losses);

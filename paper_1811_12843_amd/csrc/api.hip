@@ -55,9 +55,10 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
   if (c->tournament_size < 1 || c->tournament_size > 5) return "tournament_size must be in [1, 5]";
   if (c->fitness_mode != 0 && c->fitness_mode != 1) return "fitness_mode must be 0 or 1";
   if (c->loss_kind != LIPZ_LOSS_BCE && c->loss_kind != LIPZ_LOSS_WASSERSTEIN) return "unknown loss_kind";
-  if (c->trainer != LIPZ_TRAINER_GRADIENT && c->trainer != LIPZ_TRAINER_NES) return "unknown trainer";
-  if (c->trainer == LIPZ_TRAINER_NES) {
-    if (c->net != LIPZ_NET_MLP) return "the NES trainer is implemented for the MLP networks";
+  if (c->trainer != LIPZ_TRAINER_GRADIENT && c->trainer != LIPZ_TRAINER_NES && c->trainer != LIPZ_TRAINER_ES)
+    return "unknown trainer";
+  if (c->trainer != LIPZ_TRAINER_GRADIENT) {
+    if (c->net != LIPZ_NET_MLP) return "the gradient-free trainers are implemented for the MLP networks";
     if (c->nes_pairs < 1 || c->nes_pairs > 64) return "nes_pairs must be in [1, 64]";
     if (!(c->nes_sigma > 0.f && c->nes_sigma < 1e30f)) return "nes_sigma must be a positive finite scale";
   }
@@ -92,7 +93,7 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
   };
   build(Gn, c->z_dim, c->n_g_hidden, c->g_hidden, c->x_dim, c->g_hidden_act, c->g_out_act);
   build(Dn, c->x_dim, c->n_d_hidden, c->d_hidden, 1, c->d_hidden_act, LIPZ_ACT_LINEAR);
-  if (c->trainer == LIPZ_TRAINER_NES &&
+  if (c->trainer != LIPZ_TRAINER_GRADIENT &&
       (int64_t)c->nes_pairs * (Gn->P > Dn->P ? Gn->P : Dn->P) >= ((int64_t)1 << 31))
     return "nes_pairs x parameters of a network must stay below 2^31";
   return "";
@@ -199,15 +200,17 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     g->sd_r = cv.take<float>(F);
     g->realfeat = cv.take<float>((size_t)g->N * F);
   }
-  if (g->cfg.trainer == LIPZ_TRAINER_NES) {
+  if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
     const int Q = g->nes_q = 2 * g->cfg.nes_pairs + 1;
     // the perturbed sets (the unperturbed one is the parameters themselves),
     // and one direction buffer shared by the two roles, which run one after
     // the other on the stream
     g->nes_pd = cv.take<float>((size_t)C * (Q - 1) * D.stride);
     g->nes_pg = cv.take<float>((size_t)C * (Q - 1) * G.stride);
-    g->nes_eps_stride = D.stride > G.stride ? D.stride : G.stride;
-    g->nes_eps = cv.take<float>((size_t)C * g->cfg.nes_pairs * g->nes_eps_stride);
+    if (g->cfg.trainer == LIPZ_TRAINER_NES) {  // the ES trainer keeps no directions
+      g->nes_eps_stride = D.stride > G.stride ? D.stride : G.stride;
+      g->nes_eps = cv.take<float>((size_t)C * g->cfg.nes_pairs * g->nes_eps_stride);
+    }
     for (int l = 0; l + 1 < D.nl; ++l) {
       g->nes_aq[l] = cv.take<float>((size_t)C * Q * 2 * B * D.fo[l]);
       g->nes_agq[l] = cv.take<float>((size_t)C * Q * B * D.fo[l]);
@@ -380,7 +383,8 @@ void setup_groups(lipz_grid* g) {
   for (int i = 0; i <= n; ++i) g->group_c0[i] = (int)((int64_t)g->C * i / n);
 }
 
-// The NES trainer's step (reading of Section 3's gradient-free trainers):
+// The gradient-free trainers' step (reading of Section 3's NES and ES
+// trainers; the ES trainer's last op of each role is the plus-selection):
 // sample; G forward (its samples score the critic's perturbations); the
 // discriminator's Q parameter sets, each D forward over the 2B rows, their
 // losses, the estimate + Adam; then the generator's Q sets, each G forward,
@@ -638,7 +642,7 @@ void build_tables(lipz_grid* g) {
     ps.push_back(base_prob(g->data, g->xd, 0, g->P, g->F, 0, g->realfeat, g->F, (int)g->N, g->F, g->xd));
     g->real_phase = add_phase(g, ps);
   }
-  if (g->cfg.trainer == LIPZ_TRAINER_NES) build_nes_ops(g);
+  if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) build_nes_ops(g);
 }
 
 // With timing on: a start / stop event pair for the next matrix-core launch.
@@ -992,7 +996,8 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   hg.act_cell_stride = (int64_t)B * g->D.fi[LD - 1];
   hg.delta = g->dDg[LD - 2];
   hg.dlbuf = nullptr;
-  if (g->cfg.trainer == LIPZ_TRAINER_NES) {
+  if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
+    const bool es = g->cfg.trainer == LIPZ_TRAINER_ES;
     NesArgs na[2];
     for (int role = 0; role < 2; ++role) {
       NesArgs& a = na[role];
@@ -1039,10 +1044,10 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
           case OP_GEMM: e = run_gemm_phase(g, op.phase, k, s); break;
           case OP_NES_PERTURB: e = launch_nes_perturb(a, s); break;
           case OP_NES_HEAD: e = launch_nes_head(a, s); break;
-          case OP_NES_UPDATE: e = launch_nes_update(a, s); break;
+          case OP_NES_UPDATE: e = es ? launch_es_select(a, s) : launch_nes_update(a, s); break;
           default: e = hipErrorInvalidValue; break;
         }
-        if ((st = check_hip(g, e, "NES step"))) return st;
+        if ((st = check_hip(g, e, es ? "ES step" : "NES step"))) return st;
       }
     }
     hipError_t e = launch_add_i32(S.Gt, C, n_steps, s);
@@ -1291,16 +1296,18 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
                       !inside(p.dotw, 0, p.N - 1)))
       note("gemm dot", i);
   }
-  if (g->cfg.trainer == LIPZ_TRAINER_NES) {
-    // the NES kernels' extents: sets [C][2n][stride] and directions
+  if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
+    // the NES / ES kernels' extents: sets [C][2n][stride] and directions
     // [C][n][eps_stride] (elements e < P), partial logits [C][Q][rows][tn],
     // losses [C][Q]
     const int64_t Q = g->nes_q, C = g->C, B = g->B, tn = g->tn, n = g->cfg.nes_pairs;
     if (g->D.P > g->D.stride || g->G.P > g->G.stride) note("nes parameter row", 0);
-    if (g->D.P > g->nes_eps_stride || g->G.P > g->nes_eps_stride) note("nes direction row", 0);
+    if (g->cfg.trainer == LIPZ_TRAINER_NES && (g->D.P > g->nes_eps_stride || g->G.P > g->nes_eps_stride))
+      note("nes direction row", 0);
     if (!inside(g->nes_pd, 0, C * 2 * n * g->D.stride - 1)) note("nes sets D", 0);
     if (!inside(g->nes_pg, 0, C * 2 * n * g->G.stride - 1)) note("nes sets G", 0);
-    if (!inside(g->nes_eps, 0, C * n * g->nes_eps_stride - 1)) note("nes directions", 0);
+    if (g->cfg.trainer == LIPZ_TRAINER_NES && !inside(g->nes_eps, 0, C * n * g->nes_eps_stride - 1))
+      note("nes directions", 0);
     if (!inside(g->nes_part_d, 0, C * Q * 2 * B * tn - 1)) note("nes logits D", 0);
     if (!inside(g->nes_part_g, 0, C * Q * B * tn - 1)) note("nes logits G", 0);
     if (!inside(g->nes_fd, 0, C * Q - 1) || !inside(g->nes_fg, 0, C * Q - 1)) note("nes losses", 0);

@@ -246,7 +246,7 @@ __global__ __launch_bounds__(NT) void nes_perturb_kernel(NesArgs A) {
   const float* zs = reinterpret_cast<const float*>(zs4);
   const float* th = A.p + c * A.stride;
   float* sets = A.sets + (int64_t)c * 2 * A.n * A.stride;
-  float* dir = A.eps + (int64_t)c * A.n * A.eps_stride;
+  float* dir = A.eps ? A.eps + (int64_t)c * A.n * A.eps_stride : nullptr;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const uint32_t i = 4u * b0 + threadIdx.x + j * NT;
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(NT) void nes_perturb_kernel(NesArgs A) {
     const float t = th[e];
     sets[(int64_t)k * A.stride + e] = t + se;
     sets[(int64_t)(A.n + k) * A.stride + e] = t - se;
-    dir[(int64_t)k * A.eps_stride + e] = z;
+    if (A.eps) dir[(int64_t)k * A.eps_stride + e] = z;
   }
 }
 
@@ -319,6 +319,29 @@ __global__ __launch_bounds__(NT) void nes_update_kernel(NesArgs A) {
   if (A.clip > 0.f) p = p > A.clip ? A.clip : (p < -A.clip ? -A.clip : p);
   A.m[o] = m;
   A.v[o] = v;
+  A.p[o] = p;
+}
+
+// block (x, c): the ES trainer's plus-selection.  Set q of cell c (q < 2n the
+// mutants, q = 2n the parent) has loss fit[c][q]; the first mutant of lowest
+// loss replaces the parent only if that loss is strictly lower.  Then the
+// critic clip, on whichever set was kept.
+__global__ __launch_bounds__(NT) void es_select_kernel(NesArgs A) {
+  __shared__ int win;
+  const int c = blockIdx.y, parent = 2 * A.n;
+  if (threadIdx.x == 0) {
+    const float* f = A.fit + c * (parent + 1);
+    int q = 0;
+    for (int j = 1; j < parent; ++j)
+      if (f[j] < f[q]) q = j;
+    win = f[q] < f[parent] ? q : parent;
+  }
+  __syncthreads();
+  const int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (e >= A.P) return;
+  const int64_t o = c * A.stride + e;
+  float p = win == parent ? A.p[o] : A.sets[((int64_t)c * parent + win) * A.stride + e];
+  if (A.clip > 0.f) p = p > A.clip ? A.clip : (p < -A.clip ? -A.clip : p);
   A.p[o] = p;
 }
 
@@ -604,6 +627,10 @@ hipError_t launch_nes_head(const NesArgs& a, hipStream_t s) {
 }
 hipError_t launch_nes_update(const NesArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(nes_update_kernel, dim3((unsigned)((a.P + NT - 1) / NT), a.C), dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_es_select(const NesArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(es_select_kernel, dim3((unsigned)((a.P + NT - 1) / NT), a.C), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s) {

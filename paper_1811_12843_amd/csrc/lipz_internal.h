@@ -437,7 +437,7 @@ struct NesArgs {
   const float* lr;       // [C]
   const int32_t* t;      // [C] Adam step count before this call
   float* sets;           // [C][2n][stride]: theta + sigma eps_k (k < n), theta - sigma eps_(k-n)
-  float* eps;            // [C][n][eps_stride]: the directions eps_k in fp32
+  float* eps;            // [C][n][eps_stride]: the directions eps_k in fp32 (null: not kept)
   const float* part;     // partial logits: D role [C][Q][2B][tn], G role [C][Q B][tn]
   float* fit;            // [C][Q] loss of each set
   float* losses;         // [C][2] slice of this step, or null
@@ -454,6 +454,7 @@ struct NesArgs {
 hipError_t launch_nes_perturb(const NesArgs& a, hipStream_t s);
 hipError_t launch_nes_head(const NesArgs& a, hipStream_t s);
 hipError_t launch_nes_update(const NesArgs& a, hipStream_t s);
+hipError_t launch_es_select(const NesArgs& a, hipStream_t s);
 hipError_t launch_fitness(const float* L, const float* Lg, int C, int mode, float* fit_g, float* fit_d,
                           int32_t* flags, float* out_L, float* out_Lg, float* out_fg, float* out_fd,
                           hipStream_t s);

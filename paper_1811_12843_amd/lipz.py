@@ -20,8 +20,8 @@ LIPZ_ACT_LINEAR, LIPZ_ACT_RELU, LIPZ_ACT_LRELU, LIPZ_ACT_TANH = 0, 1, 2, 3
 LIPZ_ROLE_G, LIPZ_ROLE_D = 0, 1
 LIPZ_LOSS_BCE, LIPZ_LOSS_WASSERSTEIN = 0, 1
 LOSSES = {"bce": LIPZ_LOSS_BCE, "wasserstein": LIPZ_LOSS_WASSERSTEIN}
-LIPZ_TRAINER_GRADIENT, LIPZ_TRAINER_NES = 0, 1
-TRAINERS = {"gradient": LIPZ_TRAINER_GRADIENT, "nes": LIPZ_TRAINER_NES}
+LIPZ_TRAINER_GRADIENT, LIPZ_TRAINER_NES, LIPZ_TRAINER_ES = 0, 1, 2
+TRAINERS = {"gradient": LIPZ_TRAINER_GRADIENT, "nes": LIPZ_TRAINER_NES, "es": LIPZ_TRAINER_ES}
 ACTS = {"linear": LIPZ_ACT_LINEAR, "relu": LIPZ_ACT_RELU, "lrelu": LIPZ_ACT_LRELU, "tanh": LIPZ_ACT_TANH}
 
 _i32, _i64, _f32, _u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_uint64

@@ -24,7 +24,9 @@ Every field is plain data.  Fields:
   wgan_clip            weight-clipping bound of the Wasserstein critic
   trainer              "gradient" (backpropagation + Adam, the paper's experiments)
                        or "nes" (the gradient-free NES trainer, oracle/nes.py)
+                       or "es" (the gradient-free (1+lambda)-ES trainer, oracle/es.py)
   nes_pairs, nes_sigma antithetic direction pairs and perturbation scale of NES
+                       and of the ES trainer's mutants
   mix_enable, mix_sigma, mix_samples, mix_feat_dim
   seed
   data                 dataset recipe name + size (see datasets.py)
@@ -80,6 +82,12 @@ WORKLOADS = {
                             batch=100, steps=100, gens=1,
                             trainer="nes", nes_pairs=8, nes_sigma=0.01,
                             data=dict(kind="mnist_like", n=60000, seed=0)),
+    # 3x3 torus, MNIST-shaped MLPs trained by a (1+16)-ES (8 antithetic mutant pairs)
+    "mnist_mlp_3x3_es": _w(rows=3, cols=3, z_dim=64, x_dim=784,
+                           g_hidden=[256, 256], d_hidden=[256, 256],
+                           batch=100, steps=100, gens=1,
+                           trainer="es", nes_pairs=8, nes_sigma=0.01,
+                           data=dict(kind="mnist_like", n=60000, seed=0)),
     # 8x8 torus, MNIST-shaped MLPs
     "mnist_mlp_8x8": _w(rows=8, cols=8, z_dim=64, x_dim=784,
                         g_hidden=[256, 256], d_hidden=[256, 256],

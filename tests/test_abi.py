@@ -81,10 +81,17 @@ def test_workspace_sizing_and_validation():
               dict(nes, g_hidden=[65536, 8192])):  # nes_pairs x parameters >= 2^31
         assert L.lipz_workspace_bytes(L.config_from_dict(b), 60000) == 0
     c = L.config_from_dict(nes)
-    c.trainer = 2
+    c.trainer = 3
     assert L.lipz_workspace_bytes(c, 60000) == 0
-    d = dict(synth.workload("celeba_dcgan_4x4"), trainer="nes")
-    assert L.lipz_workspace_bytes(L.config_from_dict(d), 1000) == 0
+    for t in ("nes", "es"):
+        d = dict(synth.workload("celeba_dcgan_4x4"), trainer=t)
+        assert L.lipz_workspace_bytes(L.config_from_dict(d), 1000) == 0
+    # the ES trainer: the same sets, no direction buffer
+    es = synth.workload("mnist_mlp_3x3_es")
+    assert base < L.lipz_workspace_bytes(L.config_from_dict(es), 60000) < L.lipz_workspace_bytes(
+        L.config_from_dict(nes), 60000)
+    for b in (dict(es, nes_pairs=0), dict(es, nes_sigma=-1.0), dict(es, g_hidden=[65536, 8192])):
+        assert L.lipz_workspace_bytes(L.config_from_dict(b), 60000) == 0
     c = L.config_from_dict(w)
     c.abi_version = 99
     assert L.lipz_workspace_bytes(c, 60000) == 0

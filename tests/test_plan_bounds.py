@@ -53,9 +53,10 @@ SMALL_NES = [
 def test_small_nes_plans_stay_in_bounds(i):
     """Parameter counts that are not multiples of 4, so a thread's four
     directions straddle two directions and the end of the stream."""
-    wl = synth.small_workload("mnist_mlp_3x3_nes", **SMALL_NES[i])
-    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
-    assert n_bad == 0, msg
+    for trainer in ("nes", "es"):
+        wl = synth.small_workload("mnist_mlp_3x3_nes", trainer=trainer, **SMALL_NES[i])
+        n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
+        assert n_bad == 0, msg
 
 
 def test_invalid_dcgan_shapes_are_rejected():
