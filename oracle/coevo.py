@@ -29,6 +29,29 @@ Readings where the paper is silent (each is a workload field):
    one non-saturating generator step against the updated discriminator on
    the same latent batch; Adam with beta1, beta2, eps, bias-corrected.
 
+Sub-populations (workload pop_size s; Table 1 fixes 1 per cell) and elitist
+replacement (workload elitism), a reading of step 3 for more than one
+individual per cell:
+ * cell c holds s generators and s discriminators, individuals c s + i
+   (i < s); its neighbourhood population is the 5 s individuals of its 5
+   slots, neighbourhood index k s + i for member i of slot k; evaluation
+   scores all 5s x 5s pairs on the cell's minibatch;
+ * s tournaments per role and cell: tournament i draws from words
+   8 i .. 8 i + 7 of the cell's tournament stream and fills member i of the
+   new sub-population, whose learning rate mutates with words 4 i .. 4 i + 3
+   of the cell's mutation stream;
+ * member i of cell c trains on the minibatches and latents of stream
+   c s + i (a training unit); with s = 1 every draw is the one above;
+ * elitism 1: after training, the cell's s trained generators are scored
+   against the 5 s discriminators of the previous state (and its trained
+   discriminators against the 5 s previous generators) on step 2's
+   minibatch, the same opponents and rows that gave the cell's own s
+   previous individuals their fitness; of those 2 s per role the s of lowest
+   fitness are kept (NaN last; ties to the trained one, then the lower
+   member): a kept trained individual stays in its slot, and the kept
+   previous ones, best first, take the slots of the dropped trained ones in
+   slot order, with their Adam state and learning rate (elitist_replace).
+
 The Wasserstein trainer (workload loss "wasserstein"; the paper names WGAN as
 the next trainer to add, Section 5, and its trainers differ only in the weight
 update and the fitness evaluation, Section 3): D is a critic with a linear
@@ -124,6 +147,18 @@ class Setup:
             raise ValueError(f"unknown trainer {self.trainer!r}")
         if self.trainer in ("nes", "es") and wl["net"] != "mlp":
             raise ValueError("the gradient-free trainers are defined for the MLP workloads")
+        self.s = int(wl.get("pop_size", 1))
+        self.elitism = int(wl.get("elitism", 0))
+        if not 1 <= self.s <= 4 or self.elitism not in (0, 1):
+            raise ValueError("pop_size must be in [1, 4] and elitism 0 or 1")
+        if (self.s > 1 or self.elitism) and wl["net"] != "mlp":
+            raise ValueError("sub-populations and elitism are defined for the MLP workloads")
+        if self.s > 1 and wl["mix_enable"]:
+            raise ValueError("the mixture step is defined for one generator per cell")
+        self.U = self.C * self.s            # individuals (training units) per role
+        self.n = grid.N_SLOTS * self.s      # neighbourhood population per role
+        # pool[c, k s + i] = individual of member i of slot k
+        self.pool = (self.nbr[:, :, None] * self.s + np.arange(self.s)[None, None, :]).reshape(self.C, self.n)
 
 
 class State:
@@ -140,14 +175,15 @@ class State:
 
 
 def create(S):
-    """Step 1: random initial individuals, zero Adam state, initial learning rates, w = 1/5."""
+    """Step 1: random initial individuals (individual u from stream u), zero Adam
+    state, initial learning rates, w = 1/5."""
     wl = S.wl
-    Gp = np.stack([S.Gnet.init(S.seed, c, "INIT_G") for c in range(S.C)])
-    Dp = np.stack([S.Dnet.init(S.seed, c, "INIT_D") for c in range(S.C)])
+    Gp = np.stack([S.Gnet.init(S.seed, u, "INIT_G") for u in range(S.U)])
+    Dp = np.stack([S.Dnet.init(S.seed, u, "INIT_D") for u in range(S.U)])
     return State(Gp=Gp, Gm=np.zeros_like(Gp), Gv=np.zeros_like(Gp),
-                 Gt=np.zeros(S.C, dtype=np.int64), Glr=np.full(S.C, float(wl["lr0_g"])),
+                 Gt=np.zeros(S.U, dtype=np.int64), Glr=np.full(S.U, float(wl["lr0_g"])),
                  Dp=Dp, Dm=np.zeros_like(Dp), Dv=np.zeros_like(Dp),
-                 Dt=np.zeros(S.C, dtype=np.int64), Dlr=np.full(S.C, float(wl["lr0_d"])),
+                 Dt=np.zeros(S.U, dtype=np.int64), Dlr=np.full(S.U, float(wl["lr0_d"])),
                  w=np.full((S.C, grid.N_SLOTS), 1.0 / grid.N_SLOTS))
 
 
@@ -193,21 +229,21 @@ def g_loss_grad(S, a_f):
 
 
 def evaluate(S, st, data, gen):
-    """Step 2: all 5x5 pairs of each neighbourhood, then fitness.
+    """Step 2: all n x n pairs of each neighbourhood (n = 5 s), then fitness.
 
-    Returns L[C,5,5] (discriminator BCE), Lg[C,5,5] (non-saturating generator
-    loss), fit_g[C,5], fit_d[C,5].
+    Returns L[C,n,n] (discriminator BCE), Lg[C,n,n] (non-saturating generator
+    loss), fit_g[C,n], fit_d[C,n], indexed by neighbourhood index k s + i.
     """
-    C = S.C
-    L = np.zeros((C, 5, 5))
-    Lg = np.zeros((C, 5, 5))
+    C, n = S.C, S.n
+    L = np.zeros((C, n, n))
+    Lg = np.zeros((C, n, n))
     for c in range(C):
         _, x, z = sample(S, data, c, gen, 0)
-        fakes = [g_forward(S, st.Gp[S.nbr[c, i]], z)[1] for i in range(5)]
-        for j in range(5):
-            dp = st.Dp[S.nbr[c, j]]
+        fakes = [g_forward(S, st.Gp[S.pool[c, i]], z)[1] for i in range(n)]
+        for j in range(n):
+            dp = st.Dp[S.pool[c, j]]
             a_r = d_logits(S, dp, x)[1]
-            for i in range(5):
+            for i in range(n):
                 L[c, i, j], Lg[c, i, j] = pair_losses(S, a_r, d_logits(S, dp, fakes[i])[1])
     fit_d = L.mean(axis=1)
     if S.wl["fitness_mode"] == 0:
@@ -217,17 +253,19 @@ def evaluate(S, st, data, gen):
     return L, Lg, fit_g, fit_d
 
 
-def tournament_draw(S, cell, gen, tag):
-    """Distinct slots in draw order: draw j picks position floor(w_j * (5 - j) / 2^32)
-    among the slots not yet drawn (kept in slot order)."""
-    size = S.wl["tournament_size"]
-    w = rng.raw_words(S.seed, 4, cell, gen, 0, tag)
-    remaining = list(range(5))
+def tournament_draw(S, cell, gen, tag, member=0):
+    """Distinct neighbourhood indices in draw order for tournament `member`:
+    draw j picks position floor(w_(8 member + j) * (n - j) / 2^32) among the
+    indices not yet drawn (kept in order); a tournament of all n takes the
+    last one without a draw."""
+    size, n = S.wl["tournament_size"], S.n
+    w = rng.raw_words(S.seed, 8 * (member + 1), cell, gen, 0, tag)[8 * member:]
+    remaining = list(range(n))
     drawn = []
-    for j in range(min(size, 4)):
-        pos = int((int(w[j]) * (5 - j)) >> 32)
+    for j in range(min(size, n - 1)):
+        pos = int((int(w[j]) * (n - j)) >> 32)
         drawn.append(remaining.pop(pos))
-    if size == 5:
+    if size == n:
         drawn.append(remaining.pop(0))
     return drawn
 
@@ -243,12 +281,13 @@ def tournament_winner(fit_row, drawn):
     return best
 
 
-def mutate_lr(S, lr, cell, gen, tag):
-    """Gaussian hyper-parameter update: with probability p, lr += std * n; clamp at 0."""
+def mutate_lr(S, lr, cell, gen, tag, member=0):
+    """Gaussian hyper-parameter update of member `member`'s copy: with
+    probability p, lr += std * n; clamp at 0 (words 4 member .. 4 member + 3)."""
     wl = S.wl
     if not wl["lr_mutation"]:
         return lr
-    u = rng.to_uniform(rng.raw_words(S.seed, 4, cell, gen, 0, tag))
+    u = rng.to_uniform(rng.raw_words(S.seed, 4 * (member + 1), cell, gen, 0, tag)[4 * member:])
     if u[0] < wl["lr_mut_prob"]:
         n = rng.box_muller(u)[2]
         lr = max(lr + wl["lr_mut_std"] * n, 0.0)
@@ -256,20 +295,22 @@ def mutate_lr(S, lr, cell, gen, tag):
 
 
 def select_replace(S, st, fit_g, fit_d, gen, forced=None):
-    """Step 3 (selection part): returns (state g+1, sel[C,2] source cells (G, D))."""
+    """Step 3 (selection part): returns (state g+1, sel[U,2] source individuals (G, D))."""
     new = st.copy()
-    sel = np.zeros((S.C, 2), dtype=np.int64)
+    sel = np.zeros((S.U, 2), dtype=np.int64)
     for c in range(S.C):
-        for r, (fit, ttag, mtag, pre) in enumerate(((fit_g, "TOURN_G", "LRMUT_G", "G"),
-                                                     (fit_d, "TOURN_D", "LRMUT_D", "D"))):
-            if forced is not None:
-                src = int(forced[c, r])
-            else:
-                src = int(S.nbr[c, tournament_winner(fit[c], tournament_draw(S, c, gen, ttag))])
-            sel[c, r] = src
-            for f in ("p", "m", "v", "t"):
-                getattr(new, pre + f)[c] = getattr(st, pre + f)[src]
-            getattr(new, pre + "lr")[c] = mutate_lr(S, getattr(st, pre + "lr")[src], c, gen, mtag)
+        for i in range(S.s):
+            u = c * S.s + i
+            for r, (fit, ttag, mtag, pre) in enumerate(((fit_g, "TOURN_G", "LRMUT_G", "G"),
+                                                         (fit_d, "TOURN_D", "LRMUT_D", "D"))):
+                if forced is not None:
+                    src = int(forced[u, r])
+                else:
+                    src = int(S.pool[c, tournament_winner(fit[c], tournament_draw(S, c, gen, ttag, i))])
+                sel[u, r] = src
+                for f in ("p", "m", "v", "t"):
+                    getattr(new, pre + f)[u] = getattr(st, pre + f)[src]
+                getattr(new, pre + "lr")[u] = mutate_lr(S, getattr(st, pre + "lr")[src], c, gen, mtag, i)
     return new, sel
 
 
@@ -289,10 +330,11 @@ def adam(S, p, m, v, t, lr, g):
 
 def train_step(S, st, data, gen, step):
     """Step 3 (training part): one discriminator and one generator Adam step for
-    every cell, in place.  Returns losses[C, 2] = (L_D, L_G) before the updates."""
+    every training unit (individual pair) c, in place.  Returns losses[U, 2] =
+    (L_D, L_G) before the updates."""
     B = S.B
-    losses = np.zeros((S.C, 2))
-    for c in range(S.C):
+    losses = np.zeros((S.U, 2))
+    for c in range(S.U):
         _, x, z = sample(S, data, c, gen, step + 1)
         gcache, xf = g_forward(S, st.Gp[c], z)
         # discriminator step on real and detached fake
@@ -314,6 +356,58 @@ def train_step(S, st, data, gen, step):
     return losses
 
 
+def merge_elite(f_old, f_new):
+    """Elitist truncation of one role of one cell: f_old[s] the previous
+    members' fitness, f_new[s] the trained ones'.  Returns src[s]: -1 where the
+    trained member stays, else the previous member that takes the slot."""
+    s = len(f_old)
+
+    def key(f):
+        return np.inf if np.isnan(f) else float(f)
+    ranked = sorted([(key(f_new[i]), 0, i) for i in range(s)] + [(key(f_old[i]), 1, i) for i in range(s)])[:s]
+    kept_new = {i for _, kind, i in ranked if kind == 0}
+    kept_old = [i for _, kind, i in ranked if kind == 1]  # best first
+    free = [i for i in range(s) if i not in kept_new]
+    src = np.full(s, -1, dtype=np.int64)
+    for slot, i in zip(free, kept_old):
+        src[slot] = i
+    return src
+
+
+def elitist_replace(S, old, new, data, gen, fit_g, fit_d):
+    """Post-training re-evaluation and elitist replacement (elitism 1): returns
+    (state, info) with info = dict(fit_g2[C,s], fit_d2[C,s], src[U,2]);
+    src[c s + i, r] = -1 (trained member stays) or the previous member j whose
+    individual c s + j of `old` took the slot."""
+    s, n = S.s, S.n
+    out = new.copy()
+    fg2, fd2 = np.zeros((S.C, s)), np.zeros((S.C, s))
+    src = np.full((S.U, 2), -1, dtype=np.int64)
+    for c in range(S.C):
+        _, x, z = sample(S, data, c, gen, 0)
+        pool = S.pool[c]
+        for i in range(s):
+            xf = g_forward(S, new.Gp[c * s + i], z)[1]
+            L2, Lg2 = np.zeros(n), np.zeros(n)
+            for j in range(n):
+                dp = old.Dp[pool[j]]
+                L2[j], Lg2[j] = pair_losses(S, d_logits(S, dp, x)[1], d_logits(S, dp, xf)[1])
+            fg2[c, i] = -L2.mean() if S.wl["fitness_mode"] == 0 else Lg2.mean()
+        fakes = [g_forward(S, old.Gp[pool[k]], z)[1] for k in range(n)]
+        for j in range(s):
+            dp = new.Dp[c * s + j]
+            a_r = d_logits(S, dp, x)[1]
+            fd2[c, j] = np.mean([pair_losses(S, a_r, d_logits(S, dp, fakes[k])[1])[0] for k in range(n)])
+        for r, (f_old, f_new, pre) in enumerate(((fit_g[c, :s], fg2[c], "G"), (fit_d[c, :s], fd2[c], "D"))):
+            src[c * s:(c + 1) * s, r] = merge_elite(f_old, f_new)
+            for i in range(s):
+                j = src[c * s + i, r]
+                if j >= 0:
+                    for f in ("p", "m", "v", "t", "lr"):
+                        getattr(out, pre + f)[c * s + i] = getattr(old, pre + f)[c * s + j]
+    return out, dict(fit_g2=fg2, fit_d2=fd2, src=src)
+
+
 def generation(S, st, data, gen, mix_stats=None):
     """Steps 2-4 for one generation; returns (new state, record dict)."""
     from . import es, mixture, nes
@@ -322,6 +416,9 @@ def generation(S, st, data, gen, mix_stats=None):
     step_fn = {"nes": nes.train_step, "es": es.train_step}.get(S.trainer, train_step)
     losses = [step_fn(S, st2, data, gen, s) for s in range(S.wl["steps"])]
     rec = dict(L=L, Lg=Lg, fit_g=fg, fit_d=fd, sel=sel, losses=np.array(losses))
+    if S.elitism:
+        st2, info = elitist_replace(S, st, st2, data, gen, fg, fd)
+        rec.update(info)
     if S.wl["mix_enable"]:
         w, score, acc = mixture.update(S, st2, mix_stats, gen)
         st2.w[...] = w

@@ -47,16 +47,16 @@ def candidates(theta, eps, sigma):
 
 
 def train_step(S, st, data, gen, step, forced=None, info=None):
-    """One ES step of every cell's pair, in place; returns losses [C, 2].
+    """One ES step of every training unit's pair, in place; returns losses [U, 2].
 
-    forced[c] = (q_D, q_G) overrides the choice (a caller replaying another
+    forced[u] = (q_D, q_G) overrides the choice (a caller replaying another
     implementation's decisions on near-ties); info, a dict, receives the
-    choices "q" [C, 2] and their margins "margin" [C, 2]."""
+    choices "q" [U, 2] and their margins "margin" [U, 2]."""
     sigma = S.wl["nes_sigma"]
-    losses = np.zeros((S.C, 2))
-    qs = np.zeros((S.C, 2), dtype=np.int64)
-    margins = np.zeros((S.C, 2))
-    for c in range(S.C):
+    losses = np.zeros((S.U, 2))
+    qs = np.zeros((S.U, 2), dtype=np.int64)
+    margins = np.zeros((S.U, 2))
+    for c in range(S.U):
         _, x, z = coevo.sample(S, data, c, gen, step + 1)
         xf = coevo.g_forward(S, st.Gp[c], z)[1]
 

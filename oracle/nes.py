@@ -43,10 +43,10 @@ def directions(S, role, cell, gen, step):
 
 
 def train_step(S, st, data, gen, step):
-    """One NES step of every cell's pair, in place; returns losses [C, 2]."""
+    """One NES step of every training unit's pair, in place; returns losses [U, 2]."""
     sigma = S.wl["nes_sigma"]
-    losses = np.zeros((S.C, 2))
-    for c in range(S.C):
+    losses = np.zeros((S.U, 2))
+    for c in range(S.U):
         _, x, z = coevo.sample(S, data, c, gen, step + 1)
         xf = coevo.g_forward(S, st.Gp[c], z)[1]
 

@@ -27,6 +27,8 @@ Every field is plain data.  Fields:
                        or "es" (the gradient-free (1+lambda)-ES trainer, oracle/es.py)
   nes_pairs, nes_sigma antithetic direction pairs and perturbation scale of NES
                        and of the ES trainer's mutants
+  pop_size             individuals per role and cell (Table 1: 1)
+  elitism              1: post-training re-evaluation and elitist replacement
   mix_enable, mix_sigma, mix_samples, mix_feat_dim
   seed
   data                 dataset recipe name + size (see datasets.py)
@@ -41,6 +43,7 @@ _BASE = dict(
     tournament_size=2, fitness_mode=0,
     loss="bce", wgan_clip=0.01,
     trainer="gradient", nes_pairs=8, nes_sigma=0.01,
+    pop_size=1, elitism=0,
     mix_enable=0, mix_sigma=0.01, mix_samples=1024, mix_feat_dim=64,
     seed=0,
 )
