@@ -19,7 +19,8 @@ Prints one JSON line:
 
 Other workloads (--workload): ring8_mlp_2x2, mnist_mlp_3x3, mnist_mlp_8x8,
 mnist_mlp_4x4_wgan (the Wasserstein trainer), mnist_mlp_3x3_nes and
-mnist_mlp_3x3_es (the gradient-free NES and (1+lambda)-ES trainers) and
+mnist_mlp_3x3_es (the gradient-free NES and (1+lambda)-ES trainers),
+mnist_mlp_4x4_pop2 (two individuals per role and cell, elitist replacement) and
 celeba_dcgan_4x4 (the 64x64 DCGAN grid; its
 roofline kernel is the implicit-GEMM convolution together with the grouped
 GEMM).
@@ -60,36 +61,49 @@ def macs_per_sample(wl):
 
 def gemm_flops_per_generation(wl):
     """Algorithmic matrix-core FLOPs (2 per multiply-add, bias terms excluded)
-    of one generation: evaluation, S training steps, and the mixture step."""
+    of one generation: evaluation, S training steps, and the rest (the
+    mixture step, the re-evaluation of elitist replacement)."""
     C, B = wl["rows"] * wl["cols"], wl["batch"]
+    s = wl.get("pop_size", 1)
+    n = 5 * s  # neighbourhood population
     macs_g, g_first, macs_d, d_first = macs_per_sample(wl)
-    # evaluation: 5 G forwards per cell, D forwards on B real + 5B fake rows per D slot
-    ev = C * (5 * B * macs_g + 5 * 6 * B * macs_d)
+    # evaluation: n G forwards per cell, D forwards on B real + n B fake rows per D
+    ev = C * (n * B * macs_g + n * (1 + n) * B * macs_d)
+    rest = 0
+    if wl.get("elitism", 0):
+        # re-evaluation: s trained G forwards, n previous D on their s B rows,
+        # s trained D on the (1 + n) B evaluation rows
+        rest += C * (s * B * macs_g + n * s * B * macs_d + s * (1 + n) * B * macs_d)
+    if wl["mix_enable"]:
+        rest += C * wl["mix_samples"] * (macs_g + wl["x_dim"] * wl["mix_feat_dim"])
+    C = C * s  # training units
     if wl.get("trainer", "gradient") in ("nes", "es"):
         # NES / ES: G fwd; Q = 2 pairs + 1 critic parameter sets, each D fwd over 2B rows;
         # Q generator sets, each G fwd, and the updated D over their Q B rows
         Q = 2 * wl["nes_pairs"] + 1
         train = C * wl["steps"] * (B * macs_g + Q * 2 * B * macs_d + Q * B * macs_g + Q * B * macs_d)
-        mix = C * wl["mix_samples"] * (macs_g + wl["x_dim"] * wl["mix_feat_dim"]) if wl["mix_enable"] else 0
-        return 2.0 * ev, 2.0 * train, 2.0 * mix
+        return 2.0 * ev, 2.0 * train, 2.0 * rest
     # D step: G fwd, D fwd (2B), D weight grads (2B), D input grads below layer 1 (2B)
     d_step = B * macs_g + 2 * B * macs_d + 2 * B * macs_d + 2 * B * (macs_d - d_first)
     # G step: D fwd (B), D input grads down to x (B), G weight grads, G input grads above z
     g_step = B * macs_d + B * macs_d + B * macs_g + B * (macs_g - g_first)
     train = C * wl["steps"] * (d_step + g_step)
-    mix = 0
-    if wl["mix_enable"]:
-        mix = C * wl["mix_samples"] * (macs_g + wl["x_dim"] * wl["mix_feat_dim"])
-    return 2.0 * ev, 2.0 * train, 2.0 * mix
+    return 2.0 * ev, 2.0 * train, 2.0 * rest
 
 
 def gemm_source_digest():
+    """SHA-256 of the GEMM kernels' source: gemm.hip and the part of
+    lipz_internal.h up to the declaration of launch_gemm_grouped (the device
+    helpers and the GEMM's descriptor types; the rest of the header declares
+    other kernels)."""
     import hashlib
-    h = hashlib.sha256()
-    for name in ("gemm.hip", "lipz_internal.h"):
-        with open(os.path.join(ROOT, "paper_1811_12843_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()
+    csrc = os.path.join(ROOT, "paper_1811_12843_amd", "csrc")
+    with open(os.path.join(csrc, "gemm.hip"), "rb") as f:
+        gemm = f.read()
+    with open(os.path.join(csrc, "lipz_internal.h"), "rb") as f:
+        head = f.read()
+    cut = head.index(b";", head.index(b"hipError_t launch_gemm_grouped(")) + 1
+    return hashlib.sha256(gemm + head[:cut]).hexdigest()
 
 
 def stored_gemm_traffic(workload):
@@ -166,13 +180,20 @@ def cpu_baseline(wl, data, budget_s=20.0):
         t0 = time.perf_counter()
         mixture.update(S, st, stats, 0)
         t_mix = time.perf_counter() - t0
-    t_gen = t_eval + wl["steps"] * t_step + t_mix
+    t_elite = 0.0
+    if wl.get("elitism", 0):
+        _, _, fg, fd = coevo.evaluate(S, st, data, 0)
+        t0 = time.perf_counter()
+        coevo.elitist_replace(S, st, st, data, 0, fg, fd)
+        t_elite = time.perf_counter() - t0
+    t_gen = t_eval + wl["steps"] * t_step + t_mix + t_elite
     return {"value": 1.0 / t_gen, "unit": "generations/s", "cores": int(cores), "kind": "oracle",
             "sample": (f"1 evaluation ({t_eval:.2f} s), {k} training steps ({t_step:.3f} s each)"
                        + (f", 1 mixture step ({t_mix:.2f} s)" if wl["mix_enable"] else "")
+                       + (f", 1 elitist replacement ({t_elite:.2f} s)" if wl.get("elitism", 0) else "")
                        + f" of {wl['rows']}x{wl['cols']} grid; generation = eval + "
                        f"{wl['steps']} x step + mixture"),
-            "pair_evals_per_s": S.C * 25 / t_eval}
+            "pair_evals_per_s": S.C * S.n * S.n / t_eval}
 
 
 def main():
@@ -232,6 +253,8 @@ def main():
         L.lipz_eval_neighborhoods(g, gen)
         L.lipz_select_replace(g, gen)
         L.lipz_train_step(g, gen, 0, S)
+        if wl.get("elitism", 0):
+            L.lipz_elitist_replace(g, gen)
         if wl["mix_enable"]:
             L.lipz_mixture_update(g, gen)
 
@@ -256,7 +279,8 @@ def main():
         L.lipz_eval_neighborhoods(g, gen + r)
     torch.cuda.synchronize()
     t_eval = (time.perf_counter() - t0) / args.eval_reps
-    pair_evals = C * 25 / t_eval
+    nbh = 5 * wl.get("pop_size", 1)
+    pair_evals = C * nbh * nbh / t_eval
 
     # grouped-GEMM kernel timing with HIP events on the grid's stream
     # one instrumented generation first, so the timed ones reuse its event pairs
@@ -276,7 +300,7 @@ def main():
 
     traffic = stored_gemm_traffic(args.workload)
     cfg_desc = {"workload": args.workload, "grid": f"{wl['rows']}x{wl['cols']}", "cells": C,
-                "pairings_per_eval": 25 * C, "batch": wl["batch"], "steps_per_generation": S,
+                "pairings_per_eval": nbh * nbh * C, "batch": wl["batch"], "steps_per_generation": S,
                 "mixture_es": bool(wl["mix_enable"])}
     if wl["net"] == "mlp":
         cfg_desc.update(g=[wl["z_dim"]] + wl["g_hidden"] + [wl["x_dim"]], d=[wl["x_dim"]] + wl["d_hidden"] + [1])

@@ -32,6 +32,17 @@
  * latent batch; the mixture score is a diagonal Frechet distance in a fixed
  * random feature space (the paper's FID needs a pretrained network).
  *
+ * Sub-populations (pop_size s > 1; the paper's experiments use 1 per cell)
+ * and elitist replacement, a reading of step 3 for more than one individual
+ * per cell: cell c holds the individuals u = c s + i, i < s, of each role; its
+ * neighbourhood population is the n = 5 s individuals nbr[c][k] s + i at
+ * neighbourhood index k s + i; evaluation scores all n x n pairs;
+ * selection runs s tournaments per role (member i from words 8 i .. 8 i + 7 of
+ * the cell's tournament stream, learning-rate mutation from words
+ * 4 i .. 4 i + 3); member i of cell c trains as unit u on the streams of cell
+ * field u.  With s = 1 every draw is the one described below.  Elitism: see
+ * lipz_elitist_replace.
+ *
  * Random numbers: Philox4x32-10 (Salmon et al., SC 2011) with key = seed and
  * counter = (element / 4, cell, (gen << 16) | step_field, tag), word
  * element % 4; step_field = 0 for evaluation, s + 1 for training step s.
@@ -63,7 +74,7 @@
 extern "C" {
 #endif
 
-#define LIPZ_ABI_VERSION 2
+#define LIPZ_ABI_VERSION 3
 #define LIPZ_SLOTS 5          /* centre, north, south, west, east */
 #define LIPZ_MAX_HIDDEN 4
 
@@ -155,6 +166,8 @@ typedef struct {
   int32_t trainer;                  /* LIPZ_TRAINER_GRADIENT (paper's experiments), _NES or _ES */
   int32_t nes_pairs;                /* NES / ES: antithetic direction (mutant) pairs, 1..64 */
   float nes_sigma;                  /* NES / ES: perturbation (mutation) scale (> 0) */
+  int32_t pop_size;                 /* s: individuals per role and cell, 1..4 (1 in the paper) */
+  int32_t elitism;                  /* 1: allow lipz_elitist_replace (MLP only) */
 } lipz_config;
 
 typedef struct lipz_grid lipz_grid;  /* opaque host handle */
@@ -186,22 +199,25 @@ lipz_status lipz_grid_destroy(lipz_grid* g);
  *    Lg = -mean_b D_j(G_i(z_b)))
  *   fit_d[c][j] = mean_i L[c][i][j];  fit_g[c][i] = -mean_j L[c][i][j]
  *   (fitness_mode 1: fit_g[c][i] = mean_j Lg[c][i][j]).  Lower is better.
- * Outputs fp32 [C][5][5] / [C][5]; any may be NULL.  A non-finite value sets
- * the sticky LIPZ_E_NONFINITE flag reported by lipz_sync. */
+ * Outputs fp32 [C][n][n] / [C][n] (n = 5 pop_size, neighbourhood index
+ * k s + i); any may be NULL.  A non-finite value sets the sticky
+ * LIPZ_E_NONFINITE flag reported by lipz_sync. */
 lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float* d_Lg,
                                     float* d_fit_g, float* d_fit_d);
 
-/* Step 3, selection (Section 3): per cell and role, a tournament of
- * tournament_size distinct slots on the fitness of the last evaluation
- * (draw j picks position floor(w_j (5 - j) / 2^32) among the undrawn slots;
- * lowest fitness wins, NaN loses, ties go to the first drawn).  The winner's
- * parameters, Adam m, v, t and learning rate are copied into the cell (the
+/* Step 3, selection (Section 3): per cell, member i < s and role, a
+ * tournament of tournament_size distinct neighbourhood indices on the
+ * fitness of the last evaluation (draw j picks position
+ * floor(w_(8i+j) (n - j) / 2^32) among the undrawn indices; lowest fitness
+ * wins, NaN loses, ties go to the first drawn).  The winner's parameters,
+ * Adam m, v, t and learning rate are copied into individual c s + i (the
  * next state buffer becomes current), then with probability lr_mut_prob the
- * learning rate gets + N(0, lr_mut_std^2), clamped at 0 (words 0 / 2,3 of tag
- * LRMUT_G / LRMUT_D).  d_forced [C][2] int32 (source cells for G, D) replaces
- * the tournament when not NULL (an id outside [0, C) keeps the cell's own
- * individual and is reported by lipz_sync).  d_sel [C][2] int32 receives the source cell
- * ids, d_lr [C][2] fp32 the new learning rates; either may be NULL.
+ * learning rate gets + N(0, lr_mut_std^2), clamped at 0 (words 4i / 4i+2,
+ * 4i+3 of tag LRMUT_G / LRMUT_D).  d_forced [U][2] int32 (source
+ * individuals for G, D; U = C pop_size) replaces the tournaments when not
+ * NULL (an id outside [0, U) keeps the individual and is reported by
+ * lipz_sync).  d_sel [U][2] int32 receives the source individuals, d_lr
+ * [U][2] fp32 the new learning rates; either may be NULL.
  * Without d_forced, requires a preceding lipz_eval_neighborhoods since the
  * last state change (else LIPZ_E_ORDER). */
 lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forced,
@@ -221,9 +237,34 @@ lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forc
  * reported are those at the unperturbed parameters.  LIPZ_TRAINER_ES: the
  * same two losses, each by one plus-selection (see LIPZ_TRAINER_ES), then
  * the critic clip; losses at the parents; step counts advance by n_steps.
- * d_losses [n_steps][C][2] fp32 (L_D, L_G before each update) may be NULL. */
+ * Every individual pair u < U = C pop_size trains (its minibatches and
+ * latents from cell field u).
+ * d_losses [n_steps][U][2] fp32 (L_D, L_G before each update) may be NULL. */
 lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_steps,
                             float* d_losses);
+
+/* Post-training re-evaluation and elitist replacement (a reading of step 3
+ * for elitism = 1; the paper's experiments replace unconditionally).  Scores
+ * each cell's s trained generators against the n discriminators of the
+ * previous state's neighbourhood, and its s trained discriminators against
+ * the n previous generators, on the minibatch of generation gen's
+ * evaluation (step_field 0), the opponents and rows that gave the cell's own
+ * s previous individuals their fitness:
+ *   fit2_g[c][i] = -mean_j L(G'_i, D_j)  (fitness_mode 1: mean_j Lg),
+ *   fit2_d[c][j] = mean_k L(G_k, D'_j).
+ * Of the 2 s per role the s of lowest fitness are kept (NaN last; ties to
+ * the trained individual, then the lower member): a kept trained individual
+ * stays in its slot; the kept previous ones, best first, take the slots of
+ * the dropped trained ones in slot order, with their parameters, Adam state,
+ * step count and learning rate.  Requires lipz_eval_neighborhoods(gen), then
+ * lipz_select_replace (the previous state is the buffer it read), then any
+ * number of lipz_train_step calls; another evaluation, selection, state load
+ * or elitist replacement in between gives LIPZ_E_ORDER.  Outputs (any
+ * may be NULL): d_src [U][2] int32 (-1: the trained individual stays, else
+ * the previous member j < s whose individual c s + j took the slot),
+ * d_fit2_g / d_fit2_d [C][s] fp32.  LIPZ_E_ORDER if elitism = 0. */
+lipz_status lipz_elitist_replace(lipz_grid* g, int32_t gen, int32_t* d_src, float* d_fit2_g,
+                                 float* d_fit2_d);
 
 /* Step 4 (Section 3): one (1+1)-ES step on every cell's mixture weights over
  * the generators of its neighbourhood (current state).  Features f = x P,
@@ -234,7 +275,8 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
  * proposal w' = max(w + mix_sigma n, 0) / sum (n: tag MIXN), accepted iff
  * score(w') < score(w).  Outputs (any may be NULL): d_w [C][5] fp32,
  * d_score [C] fp32 (score of the kept w), d_accepted [C] int32.
- * LIPZ_E_ORDER if the grid was created with mix_enable = 0. */
+ * LIPZ_E_ORDER if the grid was created with mix_enable = 0 (which
+ * pop_size > 1 requires). */
 lipz_status lipz_mixture_update(lipz_grid* g, int32_t gen, float* d_w, float* d_score,
                                 int32_t* d_accepted);
 
@@ -254,9 +296,9 @@ lipz_status lipz_param_layout(const lipz_grid* g, int32_t role, int64_t* h_offse
 
 /* State blob: the current population, in this layout (byte offsets written
  * to h_offsets[0..11] by lipz_state_layout; h_offsets[11] = total bytes):
- *   [0] Gp float [C][stride_G]  [1] Gm  [2] Gv
- *   [3] Dp float [C][stride_D]  [4] Dm  [5] Dv
- *   [6] Gt int32 [C]  [7] Dt int32 [C]  [8] Glr float [C]  [9] Dlr float [C]
+ *   [0] Gp float [U][stride_G]  [1] Gm  [2] Gv     (U = C pop_size)
+ *   [3] Dp float [U][stride_D]  [4] Dm  [5] Dv
+ *   [6] Gt int32 [U]  [7] Dt int32 [U]  [8] Glr float [U]  [9] Dlr float [U]
  *   [10] w float [C][5]
  * h_strides[0] = stride_G, h_strides[1] = stride_D (floats per cell row,
  * >= the role's parameter count; the padding is ignored). */
@@ -268,8 +310,8 @@ lipz_status lipz_save_state(lipz_grid* g, void* d_dst);
 lipz_status lipz_load_state(lipz_grid* g, const void* d_src);
 
 /* Synchronise the grid's stream; returns a sticky HIP error, then
- * LIPZ_E_INVAL if a forced source cell of lipz_select_replace was outside
- * [0, C) (that cell kept its own individual), then LIPZ_E_NONFINITE if any
+ * LIPZ_E_INVAL if a forced source individual of lipz_select_replace was
+ * outside [0, U) (that individual kept itself), then LIPZ_E_NONFINITE if any
  * evaluation produced a non-finite value.  Both flags are sticky. */
 lipz_status lipz_sync(lipz_grid* g);
 const char* lipz_error_string(lipz_status s);

@@ -374,11 +374,13 @@ def merge_elite(f_old, f_new):
     return src
 
 
-def elitist_replace(S, old, new, data, gen, fit_g, fit_d):
+def elitist_replace(S, old, new, data, gen, fit_g, fit_d, forced=None):
     """Post-training re-evaluation and elitist replacement (elitism 1): returns
     (state, info) with info = dict(fit_g2[C,s], fit_d2[C,s], src[U,2]);
     src[c s + i, r] = -1 (trained member stays) or the previous member j whose
-    individual c s + j of `old` took the slot."""
+    individual c s + j of `old` took the slot.  forced [U,2], in the same
+    form, replaces the truncation's choice (a caller replaying another
+    implementation's decisions on near-ties)."""
     s, n = S.s, S.n
     out = new.copy()
     fg2, fd2 = np.zeros((S.C, s)), np.zeros((S.C, s))
@@ -399,7 +401,7 @@ def elitist_replace(S, old, new, data, gen, fit_g, fit_d):
             a_r = d_logits(S, dp, x)[1]
             fd2[c, j] = np.mean([pair_losses(S, a_r, d_logits(S, dp, fakes[k])[1])[0] for k in range(n)])
         for r, (f_old, f_new, pre) in enumerate(((fit_g[c, :s], fg2[c], "G"), (fit_d[c, :s], fd2[c], "D"))):
-            src[c * s:(c + 1) * s, r] = merge_elite(f_old, f_new)
+            src[c * s:(c + 1) * s, r] = merge_elite(f_old, f_new) if forced is None else forced[c * s:(c + 1) * s, r]
             for i in range(s):
                 j = src[c * s + i, r]
                 if j >= 0:

@@ -76,6 +76,12 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
     if (c->mix_feat_dim < 1 || c->mix_feat_dim > 4096) return "bad mix_feat_dim";
     if (!(c->mix_sigma >= 0.f)) return "bad mix_sigma";
   }
+  if (c->pop_size < 1 || c->pop_size > 4) return "pop_size must be in [1, 4]";
+  if (c->elitism != 0 && c->elitism != 1) return "elitism must be 0 or 1";
+  if ((c->pop_size > 1 || c->elitism) && c->net != LIPZ_NET_MLP)
+    return "sub-populations and elitism are implemented for the MLP networks";
+  if (c->pop_size > 1 && c->mix_enable) return "the mixture step needs pop_size 1";
+  if ((int64_t)c->rows * c->cols * c->pop_size > 4096) return "grid size x pop_size out of range";
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31) - 1) return "n_samples must be in [1, 2^31)";
   if (c->net == LIPZ_NET_DCGAN) return dc_validate(c, Gn, Dn);
   auto build = [](Net* n, int in, int nh, const int32_t* hid, int out, int hact, int oact) {
@@ -101,7 +107,7 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
 
 // The two state buffers in the documented blob layout.
 void carve_state(lipz_grid* g, Carver& cv, char* base) {
-  const int C = g->C;
+  const int C = g->C, U = g->U;
   const Net &G = g->G, &D = g->D;
   for (int b = 0; b < 2; ++b) {
     StateBuf sb;
@@ -119,16 +125,16 @@ void carve_state(lipz_grid* g, Carver& cv, char* base) {
       return cv.take<int32_t>(n);
     };
     sb.base = base + start;
-    sb.Gp = take_f(0, (size_t)C * G.stride);
-    sb.Gm = take_f(1, (size_t)C * G.stride);
-    sb.Gv = take_f(2, (size_t)C * G.stride);
-    sb.Dp = take_f(3, (size_t)C * D.stride);
-    sb.Dm = take_f(4, (size_t)C * D.stride);
-    sb.Dv = take_f(5, (size_t)C * D.stride);
-    sb.Gt = take_i(6, C);
-    sb.Dt = take_i(7, C);
-    sb.Glr = take_f(8, C);
-    sb.Dlr = take_f(9, C);
+    sb.Gp = take_f(0, (size_t)U * G.stride);
+    sb.Gm = take_f(1, (size_t)U * G.stride);
+    sb.Gv = take_f(2, (size_t)U * G.stride);
+    sb.Dp = take_f(3, (size_t)U * D.stride);
+    sb.Dm = take_f(4, (size_t)U * D.stride);
+    sb.Dv = take_f(5, (size_t)U * D.stride);
+    sb.Gt = take_i(6, U);
+    sb.Dt = take_i(7, U);
+    sb.Glr = take_f(8, U);
+    sb.Dlr = take_f(9, U);
     sb.w = take_f(10, (size_t)C * LIPZ_SLOTS);
     cv.off = align_up(cv.off, kAlign);
     so[11] = (int64_t)(cv.off - start);
@@ -158,33 +164,51 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     *total = align_up(cv.off, kAlign);
     return;
   }
+  const int U = g->U, s = g->s, nn = g->nn, er = 1 + nn;  // er: evaluation row blocks per cell
   g->nbr = cv.take<int32_t>((size_t)C * 5);
-  g->sel = cv.take<int32_t>((size_t)C * 2);
+  g->sel = cv.take<int32_t>((size_t)U * 2);
   g->flags = cv.take<int32_t>(4);
-  g->L = cv.take<float>((size_t)C * 25);
-  g->Lg = cv.take<float>((size_t)C * 25);
-  g->fit_g = cv.take<float>((size_t)C * 5);
-  g->fit_d = cv.take<float>((size_t)C * 5);
-  // training
-  g->z = cv.take<float>((size_t)C * B * zd);
-  g->Xtr = cv.take<float>((size_t)C * 2 * B * xd);
-  for (int l = 0; l + 1 < G.nl; ++l) g->h[l] = cv.take<float>((size_t)C * B * G.fo[l]);
-  for (int l = 0; l < G.nl; ++l) g->dG[l] = cv.take<float>((size_t)C * B * G.fo[l]);
-  g->part_tr = cv.take<float>((size_t)C * 2 * B * g->tn);
-  g->dlbuf = cv.take<float>((size_t)C * 2 * B * 4);
-  g->part_g = cv.take<float>((size_t)C * B * g->tn);
-  g->part_e = cv.take<float>((size_t)C * 5 * 6 * B * g->tn);
+  g->L = cv.take<float>((size_t)C * nn * nn);
+  g->Lg = cv.take<float>((size_t)C * nn * nn);
+  g->fit_g = cv.take<float>((size_t)C * nn);
+  g->fit_d = cv.take<float>((size_t)C * nn);
+  // training (one unit per individual pair)
+  g->z = cv.take<float>((size_t)U * B * zd);
+  g->Xtr = cv.take<float>((size_t)U * 2 * B * xd);
+  for (int l = 0; l + 1 < G.nl; ++l) g->h[l] = cv.take<float>((size_t)U * B * G.fo[l]);
+  for (int l = 0; l < G.nl; ++l) g->dG[l] = cv.take<float>((size_t)U * B * G.fo[l]);
+  g->part_tr = cv.take<float>((size_t)U * 2 * B * g->tn);
+  g->dlbuf = cv.take<float>((size_t)U * 2 * B * 4);
+  g->part_g = cv.take<float>((size_t)U * B * g->tn);
+  g->part_e = cv.take<float>((size_t)C * nn * er * B * g->tn);
   for (int l = 0; l + 1 < D.nl; ++l) {
-    g->a[l] = cv.take<float>((size_t)C * 2 * B * D.fo[l]);
-    g->dD[l] = cv.take<float>((size_t)C * 2 * B * D.fo[l]);
-    g->ag[l] = cv.take<float>((size_t)C * B * D.fo[l]);
-    g->dDg[l] = cv.take<float>((size_t)C * B * D.fo[l]);
+    g->a[l] = cv.take<float>((size_t)U * 2 * B * D.fo[l]);
+    g->dD[l] = cv.take<float>((size_t)U * 2 * B * D.fo[l]);
+    g->ag[l] = cv.take<float>((size_t)U * B * D.fo[l]);
+    g->dDg[l] = cv.take<float>((size_t)U * B * D.fo[l]);
   }
-  // evaluation
+  // evaluation: rows [x_c; G_0(z_c); ...; G_(nn-1)(z_c)] per cell
   g->ze = cv.take<float>((size_t)C * B * zd);
-  g->Xe = cv.take<float>((size_t)C * 6 * B * xd);
-  for (int l = 0; l + 1 < G.nl; ++l) g->he[l] = cv.take<float>((size_t)C * 5 * B * G.fo[l]);
-  for (int l = 0; l + 1 < D.nl; ++l) g->ae[l] = cv.take<float>((size_t)C * 5 * 6 * B * D.fo[l]);
+  g->Xe = cv.take<float>((size_t)C * er * B * xd);
+  for (int l = 0; l + 1 < G.nl; ++l) g->he[l] = cv.take<float>((size_t)C * nn * B * G.fo[l]);
+  for (int l = 0; l + 1 < D.nl; ++l) g->ae[l] = cv.take<float>((size_t)C * nn * er * B * D.fo[l]);
+  if (g->cfg.elitism) {
+    g->rmean = cv.take<float>((size_t)C * nn);
+    for (int l = 0; l + 1 < G.nl; ++l) g->he2[l] = cv.take<float>((size_t)C * s * B * G.fo[l]);
+    g->xe2 = cv.take<float>((size_t)C * s * B * xd);
+    for (int l = 0; l + 1 < D.nl; ++l) {
+      g->ae2[l] = cv.take<float>((size_t)C * nn * s * B * D.fo[l]);
+      g->ae3[l] = cv.take<float>((size_t)C * s * er * B * D.fo[l]);
+    }
+    g->part_e2 = cv.take<float>((size_t)C * nn * s * B * g->tn);
+    g->part_e3 = cv.take<float>((size_t)C * s * er * B * g->tn);
+    g->fit2_g = cv.take<float>((size_t)C * s);
+    g->fit2_d = cv.take<float>((size_t)C * s);
+    g->el_L2 = cv.take<float>((size_t)C * s * nn);
+    g->el_Lg2 = cv.take<float>((size_t)C * s * nn);
+    g->el_M3 = cv.take<float>((size_t)C * (1 + nn) * s);
+    g->esrc = cv.take<int32_t>((size_t)U * 2);
+  }
   // mixture
   if (g->cfg.mix_enable) {
     const int S = g->S, F = g->F;
@@ -205,22 +229,22 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     // the perturbed sets (the unperturbed one is the parameters themselves),
     // and one direction buffer shared by the two roles, which run one after
     // the other on the stream
-    g->nes_pd = cv.take<float>((size_t)C * (Q - 1) * D.stride);
-    g->nes_pg = cv.take<float>((size_t)C * (Q - 1) * G.stride);
+    g->nes_pd = cv.take<float>((size_t)U * (Q - 1) * D.stride);
+    g->nes_pg = cv.take<float>((size_t)U * (Q - 1) * G.stride);
     if (g->cfg.trainer == LIPZ_TRAINER_NES) {  // the ES trainer keeps no directions
       g->nes_eps_stride = D.stride > G.stride ? D.stride : G.stride;
-      g->nes_eps = cv.take<float>((size_t)C * g->cfg.nes_pairs * g->nes_eps_stride);
+      g->nes_eps = cv.take<float>((size_t)U * g->cfg.nes_pairs * g->nes_eps_stride);
     }
     for (int l = 0; l + 1 < D.nl; ++l) {
-      g->nes_aq[l] = cv.take<float>((size_t)C * Q * 2 * B * D.fo[l]);
-      g->nes_agq[l] = cv.take<float>((size_t)C * Q * B * D.fo[l]);
+      g->nes_aq[l] = cv.take<float>((size_t)U * Q * 2 * B * D.fo[l]);
+      g->nes_agq[l] = cv.take<float>((size_t)U * Q * B * D.fo[l]);
     }
-    for (int l = 0; l + 1 < G.nl; ++l) g->nes_hq[l] = cv.take<float>((size_t)C * Q * B * G.fo[l]);
-    g->nes_xq = cv.take<float>((size_t)C * Q * B * xd);
-    g->nes_part_d = cv.take<float>((size_t)C * Q * 2 * B * g->tn);
-    g->nes_part_g = cv.take<float>((size_t)C * Q * B * g->tn);
-    g->nes_fd = cv.take<float>((size_t)C * Q);
-    g->nes_fg = cv.take<float>((size_t)C * Q);
+    for (int l = 0; l + 1 < G.nl; ++l) g->nes_hq[l] = cv.take<float>((size_t)U * Q * B * G.fo[l]);
+    g->nes_xq = cv.take<float>((size_t)U * Q * B * xd);
+    g->nes_part_d = cv.take<float>((size_t)U * Q * 2 * B * g->tn);
+    g->nes_part_g = cv.take<float>((size_t)U * Q * B * g->tn);
+    g->nes_fd = cv.take<float>((size_t)U * Q);
+    g->nes_fg = cv.take<float>((size_t)U * Q);
   }
   g->probs_d = cv.take<GemmProb>(g->probs_h.size());
   *total = align_up(cv.off, kAlign);
@@ -378,9 +402,9 @@ void setup_groups(lipz_grid* g) {
   int n = LIPZ_CELL_GROUPS;
   if (n <= 0) n = 1;
   if (n > LIPZ_MAX_GROUPS) n = LIPZ_MAX_GROUPS;
-  if (n > g->C) n = g->C;
+  if (n > g->U) n = g->U;
   g->n_groups = n;
-  for (int i = 0; i <= n; ++i) g->group_c0[i] = (int)((int64_t)g->C * i / n);
+  for (int i = 0; i <= n; ++i) g->group_c0[i] = (int)((int64_t)g->U * i / n);
 }
 
 // The gradient-free trainers' step (reading of Section 3's NES and ES
@@ -390,7 +414,7 @@ void setup_groups(lipz_grid* g) {
 // losses, the estimate + Adam; then the generator's Q sets, each G forward,
 // the updated D over all Q B generated rows, their losses, estimate + Adam.
 void build_nes_ops(lipz_grid* g) {
-  const int C = g->C, B = g->B, zd = g->zd, xd = g->xd, Q = g->nes_q;
+  const int C = g->U, B = g->B, zd = g->zd, xd = g->xd, Q = g->nes_q;  // C: training units
   const Net &G = g->G, &D = g->D;
   const int LG = G.nl, LD = D.nl;
   const size_t sG = G.stride, sD = D.stride;
@@ -584,18 +608,20 @@ void build_tables(lipz_grid* g) {
         &ops);
     }  // groups
 
-    // ---- evaluation ----
+    // ---- evaluation: rows [x_c; G_0(z_c); ...; G_(nn-1)(z_c)] per cell ----
+    const int s = g->s, nn = g->nn, er = 1 + nn;
+    auto owner_of = [&](int c, int i) { return g->nbr_h[c * 5 + i / s] * s + i % s; };
     std::vector<int>& ev = g->eval_phases[par];
     ev.clear();
     for (int l = 0; l < LG; ++l) {
       std::vector<GemmProb> ps;
       for (int c = 0; c < C; ++c)
-        for (int i = 0; i < 5; ++i) {
-          const int owner = g->nbr_h[c * 5 + i];
+        for (int i = 0; i < nn; ++i) {
+          const int owner = owner_of(c, i);
           const float* x = l == 0 ? g->ze + (size_t)c * B * zd
-                                  : g->he[l - 1] + (size_t)(c * 5 + i) * B * G.fi[l];
-          float* y = l + 1 < LG ? g->he[l] + (size_t)(c * 5 + i) * B * G.fo[l]
-                                : g->Xe + (size_t)c * 6 * B * xd + (size_t)(1 + i) * B * xd;
+                                  : g->he[l - 1] + (size_t)(c * nn + i) * B * G.fi[l];
+          float* y = l + 1 < LG ? g->he[l] + (size_t)(c * nn + i) * B * G.fo[l]
+                                : g->Xe + (size_t)c * er * B * xd + (size_t)(1 + i) * B * xd;
           ps.push_back(fwd_prob(x, B, S.Gp + owner * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
         }
       ev.push_back(add_phase(g, ps));
@@ -603,18 +629,62 @@ void build_tables(lipz_grid* g) {
     for (int l = 0; l + 1 < LD; ++l) {
       std::vector<GemmProb> ps;
       for (int c = 0; c < C; ++c)
-        for (int j = 0; j < 5; ++j) {
-          const int owner = g->nbr_h[c * 5 + j];
-          const float* x = l == 0 ? g->Xe + (size_t)c * 6 * B * xd
-                                  : g->ae[l - 1] + (size_t)(c * 5 + j) * 6 * B * D.fi[l];
-          GemmProb p = fwd_prob(x, 6 * B, S.Dp + owner * sD + D.off[l], D.fi[l], D.fo[l],
-                                g->ae[l] + (size_t)(c * 5 + j) * 6 * B * D.fo[l], D.act[l]);
+        for (int j = 0; j < nn; ++j) {
+          const int owner = owner_of(c, j);
+          const float* x = l == 0 ? g->Xe + (size_t)c * er * B * xd
+                                  : g->ae[l - 1] + (size_t)(c * nn + j) * er * B * D.fi[l];
+          GemmProb p = fwd_prob(x, er * B, S.Dp + owner * sD + D.off[l], D.fi[l], D.fo[l],
+                                g->ae[l] + (size_t)(c * nn + j) * er * B * D.fo[l], D.act[l]);
           if (l == LD - 2)
             p = with_head(p, S.Dp + owner * sD + D.off[LD - 1],
-                          g->part_e + (size_t)(c * 5 + j) * 6 * B * g->tn, g->tn);
+                          g->part_e + (size_t)(c * nn + j) * er * B * g->tn, g->tn);
           ps.push_back(p);
         }
       ev.push_back(add_phase(g, ps));
+    }
+    // ---- post-training re-evaluation (elitism): this buffer holds the trained
+    // individuals, the other one the previous state ----
+    std::vector<int>& el = g->elite_phases[par];
+    el.clear();
+    if (g->cfg.elitism) {
+      const StateBuf& O = g->st[1 - par];
+      for (int l = 0; l < LG; ++l) {  // trained G'_i on the cell's evaluation latents
+        std::vector<GemmProb> ps;
+        for (int c = 0; c < C; ++c)
+          for (int i = 0; i < s; ++i) {
+            const size_t ci = (size_t)c * s + i;
+            const float* x = l == 0 ? g->ze + (size_t)c * B * zd : g->he2[l - 1] + ci * B * G.fi[l];
+            float* y = l + 1 < LG ? g->he2[l] + ci * B * G.fo[l] : g->xe2 + ci * B * xd;
+            ps.push_back(fwd_prob(x, B, S.Gp + ci * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
+          }
+        el.push_back(add_phase(g, ps));
+      }
+      for (int l = 0; l + 1 < LD; ++l) {
+        // one phase, two problem shapes (all cells' first kind, then the second)
+        std::vector<GemmProb> ps;
+        for (int c = 0; c < C; ++c)
+          for (int j = 0; j < nn; ++j) {  // previous D_j on the s B rows of the trained generators
+            const int owner = owner_of(c, j);
+            const size_t cj = (size_t)c * nn + j;
+            const float* x = l == 0 ? g->xe2 + (size_t)c * s * B * xd : g->ae2[l - 1] + cj * s * B * D.fi[l];
+            GemmProb p = fwd_prob(x, s * B, O.Dp + owner * sD + D.off[l], D.fi[l], D.fo[l],
+                                  g->ae2[l] + cj * s * B * D.fo[l], D.act[l]);
+            if (l == LD - 2)
+              p = with_head(p, O.Dp + owner * sD + D.off[LD - 1], g->part_e2 + cj * s * B * g->tn, g->tn);
+            ps.push_back(p);
+          }
+        for (int c = 0; c < C; ++c)
+          for (int j = 0; j < s; ++j) {  // trained D'_j on the evaluation rows
+            const size_t cj = (size_t)c * s + j;
+            const float* x = l == 0 ? g->Xe + (size_t)c * er * B * xd : g->ae3[l - 1] + cj * er * B * D.fi[l];
+            GemmProb p = fwd_prob(x, er * B, S.Dp + cj * sD + D.off[l], D.fi[l], D.fo[l],
+                                  g->ae3[l] + cj * er * B * D.fo[l], D.act[l]);
+            if (l == LD - 2)
+              p = with_head(p, S.Dp + cj * sD + D.off[LD - 1], g->part_e3 + cj * er * B * g->tn, g->tn);
+            ps.push_back(p);
+          }
+        el.push_back(add_phase(g, ps));
+      }
     }
     // ---- mixture ----
     std::vector<int>& mx = g->mix_phases[par];
@@ -699,6 +769,9 @@ lipz_grid* plan_grid(const lipz_config* cfg, int64_t n_samples, char* base, cons
   if (!g) return nullptr;
   g->cfg = *cfg;
   g->C = cfg->rows * cfg->cols;
+  g->s = cfg->pop_size;
+  g->U = g->C * g->s;
+  g->nn = LIPZ_SLOTS * g->s;
   g->B = cfg->batch;
   g->zd = cfg->z_dim;
   g->xd = cfg->x_dim;
@@ -800,7 +873,7 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
      "upload GEMM tables");
   if (g->dc) ck(dc_upload_tables(g, s), "upload convolution tables");
   const StateBuf& S0 = g->st[0];
-  const int C = g->C;
+  const int C = g->C, U = g->U;
   // both state buffers, padding included, start at zero so saved blobs are deterministic
   for (int b = 0; b < 2; ++b)
     ck(launch_fill_i32(reinterpret_cast<int32_t*>(g->st[b].base), (int64_t)(g->state_bytes / 4), 0, s),
@@ -808,17 +881,18 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
   if (g->dc) {
     ck(dc_init_params(g, S0, s), "init");
   } else {
-    ck(launch_init_params(S0.Gp, g->G.stride, g->G.P, C, g->G.layers(), g->key, LIPZ_TAG_INIT_G, s), "init G");
-    ck(launch_init_params(S0.Dp, g->D.stride, g->D.P, C, g->D.layers(), g->key, LIPZ_TAG_INIT_D, s), "init D");
+    // individual u from stream (cell field) u
+    ck(launch_init_params(S0.Gp, g->G.stride, g->G.P, U, g->G.layers(), g->key, LIPZ_TAG_INIT_G, s), "init G");
+    ck(launch_init_params(S0.Dp, g->D.stride, g->D.P, U, g->D.layers(), g->key, LIPZ_TAG_INIT_D, s), "init D");
   }
-  ck(launch_fill_f32(S0.Gm, (int64_t)C * g->G.stride, 0.f, s), "zero");
-  ck(launch_fill_f32(S0.Gv, (int64_t)C * g->G.stride, 0.f, s), "zero");
-  ck(launch_fill_f32(S0.Dm, (int64_t)C * g->D.stride, 0.f, s), "zero");
-  ck(launch_fill_f32(S0.Dv, (int64_t)C * g->D.stride, 0.f, s), "zero");
-  ck(launch_fill_i32(S0.Gt, C, 0, s), "zero");
-  ck(launch_fill_i32(S0.Dt, C, 0, s), "zero");
-  ck(launch_fill_f32(S0.Glr, C, cfg->lr0_g, s), "fill");
-  ck(launch_fill_f32(S0.Dlr, C, cfg->lr0_d, s), "fill");
+  ck(launch_fill_f32(S0.Gm, (int64_t)U * g->G.stride, 0.f, s), "zero");
+  ck(launch_fill_f32(S0.Gv, (int64_t)U * g->G.stride, 0.f, s), "zero");
+  ck(launch_fill_f32(S0.Dm, (int64_t)U * g->D.stride, 0.f, s), "zero");
+  ck(launch_fill_f32(S0.Dv, (int64_t)U * g->D.stride, 0.f, s), "zero");
+  ck(launch_fill_i32(S0.Gt, U, 0, s), "zero");
+  ck(launch_fill_i32(S0.Dt, U, 0, s), "zero");
+  ck(launch_fill_f32(S0.Glr, U, cfg->lr0_g, s), "fill");
+  ck(launch_fill_f32(S0.Dlr, U, cfg->lr0_d, s), "fill");
   ck(launch_fill_f32(S0.w, (int64_t)C * 5, 1.f / 5.f, s), "fill");
   ck(launch_fill_i32(g->flags, 4, 0, s), "zero");
   if (cfg->mix_enable) {
@@ -870,7 +944,7 @@ lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float
     if ((st = dc_eval(g, gen))) return st;
   } else {
     e = launch_sample(g->data, g->N, g->xd, g->zd, B, 0, C, g->key, (uint32_t)gen, 0, g->Xe,
-                      (int64_t)6 * B * g->xd, g->ze, (int64_t)B * g->zd, s);
+                      (int64_t)(1 + g->nn) * B * g->xd, g->ze, (int64_t)B * g->zd, s);
     if ((st = check_hip(g, e, "eval sample"))) return st;
     for (int ph : g->eval_phases[par])
       if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "eval forward"))) return st;
@@ -880,15 +954,19 @@ lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float
     ha.tn = g->tn;
     ha.L = g->L;
     ha.Lg = g->Lg;
+    ha.rmean = g->rmean;
     ha.B = B;
     ha.C = C;
+    ha.nn = g->nn;
     ha.loss_kind = g->cfg.loss_kind;
     if ((st = check_hip(g, launch_head_eval(ha, s), "eval head"))) return st;
   }
-  e = launch_fitness(g->L, g->Lg, C, g->cfg.fitness_mode, g->fit_g, g->fit_d, g->flags, d_L, d_Lg,
+  e = launch_fitness(g->L, g->Lg, C, g->nn, g->cfg.fitness_mode, g->fit_g, g->fit_d, g->flags, d_L, d_Lg,
                      d_fit_g, d_fit_d, s);
   if ((st = check_hip(g, e, "fitness"))) return st;
   g->fitness_valid = true;
+  g->elite_state = 1;
+  g->elite_gen = gen;
   return LIPZ_OK;
 }
 
@@ -920,6 +998,7 @@ lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forc
   sa.lr_dst[0] = Bn.Glr;
   sa.lr_dst[1] = Bn.Dlr;
   sa.C = g->C;
+  sa.s = g->s;
   sa.tsize = g->cfg.tournament_size;
   sa.mutate = g->cfg.lr_mutation;
   sa.mut_std = g->cfg.lr_mut_std;
@@ -945,9 +1024,81 @@ lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forc
   ca.stride[1] = g->D.stride;
   ca.w_src = A.w;
   ca.w_dst = Bn.w;
+  ca.U = g->U;
   ca.C = g->C;
   if ((st = check_hip(g, launch_copy_winners(ca, s), "replace"))) return st;
   g->cur = 1 - g->cur;
+  g->fitness_valid = false;
+  g->elite_state = g->elite_state == 1 ? 2 : 0;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_elitist_replace(lipz_grid* g, int32_t gen, int32_t* d_src, float* d_fit2_g, float* d_fit2_d) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (!g->cfg.elitism) return fail(g, LIPZ_E_ORDER, "grid created with elitism = 0");
+  if (g->elite_state != 2 || gen != g->elite_gen)
+    return fail(g, LIPZ_E_ORDER, "elitist_replace needs eval_neighborhoods(gen), select_replace, training");
+  hipStream_t s = g->stream;
+  const int par = g->cur;  // trained individuals; 1 - par: the state selection read
+  for (int ph : g->elite_phases[par])
+    if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "re-evaluation"))) return st;
+  const StateBuf& O = g->st[1 - par];
+  const StateBuf& N = g->st[par];
+  EliteArgs ea;
+  memset(&ea, 0, sizeof(ea));
+  ea.part2 = g->part_e2;
+  ea.part3 = g->part_e3;
+  ea.rmean = g->rmean;
+  ea.L2 = g->el_L2;
+  ea.Lg2 = g->el_Lg2;
+  ea.M3 = g->el_M3;
+  ea.fit_g = g->fit_g;
+  ea.fit_d = g->fit_d;
+  ea.fit2_g = g->fit2_g;
+  ea.fit2_d = g->fit2_d;
+  ea.src = g->esrc;
+  ea.src_out = d_src;
+  ea.fit2_g_out = d_fit2_g;
+  ea.fit2_d_out = d_fit2_d;
+  ea.flags = g->flags;
+  ea.t_old[0] = O.Gt;
+  ea.t_old[1] = O.Dt;
+  ea.lr_old[0] = O.Glr;
+  ea.lr_old[1] = O.Dlr;
+  ea.t_new[0] = N.Gt;
+  ea.t_new[1] = N.Dt;
+  ea.lr_new[0] = N.Glr;
+  ea.lr_new[1] = N.Dlr;
+  ea.tn = g->tn;
+  ea.B = g->B;
+  ea.C = g->C;
+  ea.s = g->s;
+  ea.nn = g->nn;
+  ea.mode = g->cfg.fitness_mode;
+  ea.loss_kind = g->cfg.loss_kind;
+  if ((st = check_hip(g, launch_elite(ea, s), "elitist truncation"))) return st;
+  CopyArgs ca;
+  memset(&ca, 0, sizeof(ca));
+  ca.sel = g->esrc;
+  ca.src[0][0] = O.Gp;
+  ca.src[0][1] = O.Gm;
+  ca.src[0][2] = O.Gv;
+  ca.src[1][0] = O.Dp;
+  ca.src[1][1] = O.Dm;
+  ca.src[1][2] = O.Dv;
+  ca.dst[0][0] = N.Gp;
+  ca.dst[0][1] = N.Gm;
+  ca.dst[0][2] = N.Gv;
+  ca.dst[1][0] = N.Dp;
+  ca.dst[1][1] = N.Dm;
+  ca.dst[1][2] = N.Dv;
+  ca.stride[0] = g->G.stride;
+  ca.stride[1] = g->D.stride;
+  ca.U = g->U;
+  ca.C = g->C;
+  if ((st = check_hip(g, launch_copy_winners(ca, s), "elitist copy"))) return st;
+  g->elite_state = 0;
   g->fitness_valid = false;
   return LIPZ_OK;
 }
@@ -972,7 +1123,7 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   }
   const int par = g->cur;
   const StateBuf& S = g->st[par];
-  const int C = g->C, B = g->B, LD = g->D.nl;
+  const int C = g->U, B = g->B, LD = g->D.nl;  // C: training units
   HeadArgs hd;
   memset(&hd, 0, sizeof(hd));
   hd.part = g->part_tr;
@@ -1179,6 +1330,7 @@ lipz_status lipz_load_state(lipz_grid* g, const void* d_src) {
   if (st) return st;
   if (!d_src) return fail(g, LIPZ_E_INVAL, "null source");
   g->fitness_valid = false;
+  g->elite_state = 0;
   return check_hip(g, hipMemcpyAsync(g->st[g->cur].base, d_src, g->state_bytes, hipMemcpyDeviceToDevice,
                                      g->stream),
                    "load state");
@@ -1193,7 +1345,7 @@ lipz_status lipz_sync(lipz_grid* g) {
   e = hipMemcpy(&flags, g->flags, sizeof(flags), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return check_hip(g, e, "read flags");
   if (flags & 2) {
-    g->last_err = "a forced source cell was out of range (the cell kept itself)";
+    g->last_err = "a forced source individual was out of range (the individual kept itself)";
     return LIPZ_E_INVAL;
   }
   if (flags & 1) {
@@ -1296,11 +1448,34 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
                       !inside(p.dotw, 0, p.N - 1)))
       note("gemm dot", i);
   }
+  if (!g->dc) {
+    // the sample, evaluation-head, fitness, selection and re-evaluation
+    // kernels' extents (cells C, individuals U, neighbourhood nn)
+    const int64_t C = g->C, U = g->U, B = g->B, tn = g->tn, nn = g->nn, s = g->s, er = 1 + nn;
+    if (!inside(g->Xe, 0, C * er * B * g->xd - 1) || !inside(g->ze, 0, C * B * g->zd - 1)) note("eval sample", 0);
+    if (!inside(g->Xtr, 0, U * 2 * B * g->xd - 1) || !inside(g->z, 0, U * B * g->zd - 1)) note("train sample", 0);
+    if (!inside(g->part_e, 0, C * nn * er * B * tn - 1)) note("eval logits", 0);
+    if (!inside(g->L, 0, C * nn * nn - 1) || !inside(g->Lg, 0, C * nn * nn - 1)) note("eval losses", 0);
+    if (!inside(g->fit_g, 0, C * nn - 1) || !inside(g->fit_d, 0, C * nn - 1)) note("fitness", 0);
+    if (!inside(g->sel, 0, U * 2 - 1) || !inside(g->nbr, 0, C * 5 - 1)) note("selection", 0);
+    if (!inside(g->dlbuf, 0, U * 2 * B * 4 - 1) || !inside(g->part_tr, 0, U * 2 * B * tn - 1) ||
+        !inside(g->part_g, 0, U * B * tn - 1))
+      note("train heads", 0);
+    if (g->cfg.elitism) {
+      if (!inside(g->part_e2, 0, C * nn * s * B * tn - 1) || !inside(g->part_e3, 0, C * s * er * B * tn - 1))
+        note("re-evaluation logits", 0);
+      if (!inside(g->rmean, 0, C * nn - 1) || !inside(g->el_L2, 0, C * s * nn - 1) ||
+          !inside(g->el_Lg2, 0, C * s * nn - 1) || !inside(g->el_M3, 0, C * (1 + nn) * s - 1))
+        note("re-evaluation means", 0);
+      if (!inside(g->fit2_g, 0, C * s - 1) || !inside(g->fit2_d, 0, C * s - 1) || !inside(g->esrc, 0, U * 2 - 1))
+        note("elitist truncation", 0);
+    }
+  }
   if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
     // the NES / ES kernels' extents: sets [C][2n][stride] and directions
     // [C][n][eps_stride] (elements e < P), partial logits [C][Q][rows][tn],
     // losses [C][Q]
-    const int64_t Q = g->nes_q, C = g->C, B = g->B, tn = g->tn, n = g->cfg.nes_pairs;
+    const int64_t Q = g->nes_q, C = g->U, B = g->B, tn = g->tn, n = g->cfg.nes_pairs;
     if (g->D.P > g->D.stride || g->G.P > g->G.stride) note("nes parameter row", 0);
     if (g->cfg.trainer == LIPZ_TRAINER_NES && (g->D.P > g->nes_eps_stride || g->G.P > g->nes_eps_stride))
       note("nes direction row", 0);

@@ -1243,6 +1243,8 @@ lipz_status dc_eval(lipz_grid* g, int gen) {
   ha.Lg = g->Lg;
   ha.B = B;
   ha.C = C;
+  ha.nn = LIPZ_SLOTS;
+  ha.rmean = nullptr;
   ha.loss_kind = LIPZ_LOSS_BCE;
   return check_hip(g, launch_head_eval(ha, s), "eval head");
 }

@@ -87,6 +87,9 @@ struct lipz_grid {
   typedef lipz::GemmProb GemmProb;
   lipz_config cfg;
   int C = 0, B = 0, zd = 0, xd = 0, S = 0, F = 0;
+  // sub-populations: s individuals per role and cell, U = C s individuals
+  // (training units), nn = 5 s individuals per neighbourhood
+  int s = 1, U = 0, nn = LIPZ_SLOTS;
   Net G, D;
   hipStream_t stream = nullptr;
   const float* data = nullptr;
@@ -131,6 +134,18 @@ struct lipz_grid {
   std::vector<Op> train_ops[2][LIPZ_MAX_GROUPS];
   std::vector<int> eval_phases[2], mix_phases[2];
   int real_phase = -1;
+
+  // post-training re-evaluation and elitist replacement
+  float *rmean = nullptr;                                   // [C][nn] real-row term means of the evaluation
+  float *he2[LIPZ_MAX_HIDDEN] = {}, *xe2 = nullptr;          // trained G' on the evaluation latents [C][s][B]
+  float *ae2[LIPZ_MAX_HIDDEN] = {}, *part_e2 = nullptr;      // previous D_j on those rows [C][nn][sB]
+  float *ae3[LIPZ_MAX_HIDDEN] = {}, *part_e3 = nullptr;      // trained D'_j on the evaluation rows [C][s][(1+nn)B]
+  float *fit2_g = nullptr, *fit2_d = nullptr;                // [C][s]
+  float *el_L2 = nullptr, *el_Lg2 = nullptr, *el_M3 = nullptr; // [C][s][nn] x2, [C][1 + nn][s]
+  int32_t* esrc = nullptr;                                   // [U][2]
+  std::vector<int> elite_phases[2];
+  int elite_state = 0;  // 1: evaluated; 2: selected after that evaluation (training allowed)
+  int32_t elite_gen = -1;
 
   bool fitness_valid = false;
   lipz_status sticky = LIPZ_OK;

@@ -179,43 +179,41 @@ __global__ __launch_bounds__(NT) void head_kernel(HeadArgs A) {
 }
 
 // ---------------------------------------------------------------------------
-// Evaluation head for block (j, c): logits of the 6B rows [x_c; G_0(z_c);
-// ...; G_4(z_c)] under discriminator slot j (from the partial sums), then
+// Evaluation head for block (j, c): logits of the (1 + nn) B rows
+// [x_c; G_0(z_c); ...; G_(nn-1)(z_c)] under discriminator j (from the partial
+// sums), then
 //   L[c][i][j] = mean softplus(-a_real) + mean softplus(a_fake_i)
 //   Lg[c][i][j] = mean softplus(-a_fake_i)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NT) void head_eval_kernel(EvalHeadArgs A) {
-  extern __shared__ float logit[];
-  const int j = blockIdx.x, c = blockIdx.y;
-  const int rows = 6 * A.B;
-  const float* part = A.part + (int64_t)(c * 5 + j) * rows * A.tn;
-  for (int r = threadIdx.x; r < rows; r += NT) {
-    float a = 0.f;
-    for (int t = 0; t < A.tn; ++t) a += part[(int64_t)r * A.tn + t];
-    logit[r] = a;
-  }
-  __syncthreads();
-  // one wave per mean: wave w < 11 sums its B terms (lane-strided, then a
-  // fixed shuffle tree).  Mean 0: real rows; 1..5: fake slot i = w - 1;
-  // 6..10: generator terms of slot w - 6.
+  extern __shared__ float mean[];  // [1 + 2 nn]
+  const int j = blockIdx.x, c = blockIdx.y, nn = A.nn;
+  const int rows = (1 + nn) * A.B;
+  const float* part = A.part + (int64_t)(c * nn + j) * rows * A.tn;
+  // one wave per mean: mean 0 is the real rows' term, 1 .. nn the fake
+  // block i = q - 1, nn + 1 .. 2 nn the generator term of block q - nn; each
+  // sums its B terms lane-strided (a row's logit is its partial sums in
+  // order), then a fixed shuffle tree
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int q = wave; q < 11; q += NT / 64) {
-    const int blk = q == 0 ? 0 : (q <= 5 ? q : q - 5);
-    const float sgn = (q == 0 || q > 5) ? -1.f : 1.f;
+  for (int q = wave; q <= 2 * nn; q += NT / 64) {
+    const int blk = q <= nn ? q : q - nn;
+    const bool fake = q >= 1 && q <= nn;
     float s = 0.f;
     for (int b = lane; b < A.B; b += 64) {
-      const float a = logit[blk * A.B + b];
-      s += sgn > 0.f ? fake_term(A.loss_kind, a) : real_term(A.loss_kind, a);
+      const float* pr = part + (int64_t)(blk * A.B + b) * A.tn;
+      float a = 0.f;
+      for (int t = 0; t < A.tn; ++t) a += pr[t];
+      s += fake ? fake_term(A.loss_kind, a) : real_term(A.loss_kind, a);
     }
     s = wave_sum(s);
-    if (lane == 0) logit[rows + q] = s / (float)A.B;
+    if (lane == 0) mean[q] = s / (float)A.B;
   }
   __syncthreads();
-  if (threadIdx.x < 5) {
-    const int t = threadIdx.x;
-    A.L[(c * 5 + t) * 5 + j] = logit[rows] + logit[rows + 1 + t];
-    A.Lg[(c * 5 + t) * 5 + j] = logit[rows + 6 + t];
+  for (int i = threadIdx.x; i < nn; i += NT) {
+    A.L[(c * nn + i) * nn + j] = mean[0] + mean[1 + i];
+    A.Lg[(c * nn + i) * nn + j] = mean[1 + nn + i];
   }
+  if (A.rmean && threadIdx.x == 0) A.rmean[c * nn + j] = mean[0];
 }
 
 // ---------------------------------------------------------------------------
@@ -347,29 +345,30 @@ __global__ __launch_bounds__(NT) void es_select_kernel(NesArgs A) {
 
 // fit_d[c][j] = mean_i L[c][i][j]; fit_g[c][i] = -mean_j L[c][i][j] (mode 0)
 // or mean_j Lg[c][i][j] (mode 1).  Flags bit 0 on any non-finite value.
-__global__ void fitness_kernel(const float* L, const float* Lg, int C, int mode, float* fit_g,
+__global__ void fitness_kernel(const float* L, const float* Lg, int C, int nn, int mode, float* fit_g,
                                float* fit_d, int32_t* flags, float* oL, float* oLg, float* ofg,
                                float* ofd) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < C * 25) {
+  const int nn2 = nn * nn;
+  if (i < C * nn2) {
     if (oL) oL[i] = L[i];
     if (oLg) oLg[i] = Lg[i];
     if (!isfinite(L[i]) || !isfinite(Lg[i])) atomicOr(flags, 1);
   }
-  if (i >= C * 5) return;
-  const int c = i / 5, k = i % 5;
-  const float* Lc = L + c * 25;
+  if (i >= C * nn) return;
+  const int c = i / nn, k = i % nn;
+  const float* Lc = L + (int64_t)c * nn2;
   float sd = 0.f;
-  for (int a = 0; a < 5; ++a) sd += Lc[a * 5 + k];
+  for (int a = 0; a < nn; ++a) sd += Lc[a * nn + k];
   float sg = 0.f;
   if (mode == 0) {
-    for (int b = 0; b < 5; ++b) sg += Lc[k * 5 + b];
-    sg = -(sg / 5.f);
+    for (int b = 0; b < nn; ++b) sg += Lc[k * nn + b];
+    sg = -(sg / (float)nn);
   } else {
-    for (int b = 0; b < 5; ++b) sg += Lg[c * 25 + k * 5 + b];
-    sg = sg / 5.f;
+    for (int b = 0; b < nn; ++b) sg += Lg[(int64_t)c * nn2 + k * nn + b];
+    sg = sg / (float)nn;
   }
-  sd = sd / 5.f;
+  sd = sd / (float)nn;
   fit_d[i] = sd;
   fit_g[i] = sg;
   if (ofd) ofd[i] = sd;
@@ -381,66 +380,172 @@ __global__ void fitness_kernel(const float* L, const float* Lg, int C, int mode,
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float fit_key(float f) { return f != f ? INFINITY : f; }
 
+// Thread (cell c, member i, role): tournament i of the cell over its nn
+// neighbourhood individuals, words 8 i .. 8 i + 7 of the cell's stream
+// (Philox blocks 2 i, 2 i + 1); the copy's learning-rate mutation from words
+// 4 i .. 4 i + 3 (block i) of the mutation stream.
 __global__ void select_kernel(SelectArgs A) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= 2 * A.C) return;
-  const int c = i >> 1, role = i & 1;
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  const int U = A.C * A.s, nn = LIPZ_SLOTS * A.s;
+  if (t >= 2 * U) return;
+  const int u = t >> 1, role = t & 1, c = u / A.s, i = u % A.s;
   int src;
   if (A.forced) {
-    src = A.forced[c * 2 + role];
-    if (src < 0 || src >= A.C) {
+    src = A.forced[u * 2 + role];
+    if (src < 0 || src >= U) {
       atomicOr(A.flags, 2);
-      src = c;
+      src = u;
     }
   } else {
-    const float* fit = (role == 0 ? A.fit_g : A.fit_d) + c * 5;
-    const uint4 w = stream_block(A.key, 0, (uint32_t)c, A.gen, 0,
-                                 role == 0 ? LIPZ_TAG_TOURN_G : LIPZ_TAG_TOURN_D);
-    int remaining[5] = {0, 1, 2, 3, 4};
-    int n_rem = 5;
+    const float* fit = (role == 0 ? A.fit_g : A.fit_d) + c * nn;
+    const uint32_t tag = role == 0 ? LIPZ_TAG_TOURN_G : LIPZ_TAG_TOURN_D;
+    const uint4 w0 = stream_block(A.key, 2 * i, (uint32_t)c, A.gen, 0, tag);
+    const uint4 w1 = stream_block(A.key, 2 * i + 1, (uint32_t)c, A.gen, 0, tag);
+    int remaining[LIPZ_SLOTS * 4];
+    for (int q = 0; q < nn; ++q) remaining[q] = q;
+    int n_rem = nn;
     int best = -1;
-    const int draws = A.tsize < 4 ? A.tsize : 4;
+    const int draws = A.tsize < nn - 1 ? A.tsize : nn - 1;
     for (int j = 0; j < A.tsize; ++j) {
       int pos = 0;
-      if (j < draws) pos = (int)(((uint64_t)word_of(w, j) * (uint64_t)(5 - j)) >> 32);
+      if (j < draws) pos = (int)(((uint64_t)word_of(j < 4 ? w0 : w1, j & 3) * (uint64_t)(nn - j)) >> 32);
       const int k = remaining[pos];
       for (int q = pos; q + 1 < n_rem; ++q) remaining[q] = remaining[q + 1];
       --n_rem;
       if (best < 0 || fit_key(fit[k]) < fit_key(fit[best])) best = k;
     }
-    src = A.nbr[c * 5 + best];
+    src = A.nbr[c * LIPZ_SLOTS + best / A.s] * A.s + best % A.s;
   }
-  A.sel[c * 2 + role] = src;
-  if (A.sel_out) A.sel_out[c * 2 + role] = src;
-  A.t_dst[role][c] = A.t_src[role][src];
+  A.sel[u * 2 + role] = src;
+  if (A.sel_out) A.sel_out[u * 2 + role] = src;
+  A.t_dst[role][u] = A.t_src[role][src];
   float lr = A.lr_src[role][src];
   if (A.mutate) {
-    const uint4 w = stream_block(A.key, 0, (uint32_t)c, A.gen, 0,
+    const uint4 w = stream_block(A.key, i, (uint32_t)c, A.gen, 0,
                                  role == 0 ? LIPZ_TAG_LRMUT_G : LIPZ_TAG_LRMUT_D);
     if (uniform_of(w.x) < (double)A.mut_prob) {
       const double nv = (double)lr + (double)A.mut_std * normal_of(w, 2);
       lr = (float)(nv > 0.0 ? nv : 0.0);
     }
   }
-  A.lr_dst[role][c] = lr;
-  if (A.lr_out) A.lr_out[c * 2 + role] = lr;
+  A.lr_dst[role][u] = lr;
+  if (A.lr_out) A.lr_out[u * 2 + role] = lr;
+}
+// means of one block of B rows of partial logits, one wave per mean (see
+// head_eval_kernel): q < nq means, mean q over rows [row0(q), row0(q) + B)
+__global__ __launch_bounds__(NT) void elite_means_kernel(EliteArgs A) {
+  const int c = blockIdx.y, nn = A.nn, s = A.s;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const bool prev = (int)blockIdx.x < nn;
+  const int j = prev ? blockIdx.x : blockIdx.x - nn;
+  // previous D_j: s fake means then s generator terms; trained D'_j: real
+  // mean then nn fake means
+  const int nq = prev ? 2 * s : 1 + nn;
+  const float* part = prev ? A.part2 + (int64_t)(c * nn + j) * s * A.B * A.tn
+                           : A.part3 + (int64_t)(c * s + j) * (1 + nn) * A.B * A.tn;
+  for (int q = wave; q < nq; q += NT / 64) {
+    const int blk = prev ? (q < s ? q : q - s) : q;
+    const bool fake = prev ? q < s : q > 0;
+    float acc = 0.f;
+    for (int b = lane; b < A.B; b += 64) {
+      const float* pr = part + (int64_t)(blk * A.B + b) * A.tn;
+      float a = 0.f;
+      for (int t = 0; t < A.tn; ++t) a += pr[t];
+      acc += fake ? fake_term(A.loss_kind, a) : real_term(A.loss_kind, a);
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) {
+      const float m = acc / (float)A.B;
+      if (prev) {
+        if (q < s) A.L2[(c * s + q) * nn + j] = A.rmean[c * nn + j] + m;
+        else A.Lg2[(c * s + q - s) * nn + j] = m;
+      } else {
+        A.M3[(c * (1 + nn) + q) * s + j] = m;  // q = 0: real rows; 1 + k: G_k's rows
+      }
+    }
+  }
 }
 
-// Copy every winner's parameters and Adam moments into its cell of the next
-// buffer: grid (chunks, C, 2 roles), float4 copies.
+// thread (cell c, role): the elitist truncation of the cell's s previous and
+// s trained individuals of the role
+__global__ void elite_merge_kernel(EliteArgs A) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= 2 * A.C) return;
+  const int c = t >> 1, role = t & 1, s = A.s, nn = A.nn;
+  float fo[4], fn[4];
+  bool bad = false;
+  for (int i = 0; i < s; ++i) {
+    float acc = 0.f;
+    if (role == 0) {
+      const float* row = (A.mode == 0 ? A.L2 : A.Lg2) + (c * s + i) * nn;
+      for (int j = 0; j < nn; ++j) acc += row[j];
+      acc = A.mode == 0 ? -(acc / (float)nn) : acc / (float)nn;
+      fo[i] = A.fit_g[c * nn + i];
+    } else {
+      const float* m = A.M3 + (int64_t)c * (1 + nn) * s;
+      for (int k = 0; k < nn; ++k) acc += m[i] + m[(1 + k) * s + i];
+      acc = acc / (float)nn;
+      fo[i] = A.fit_d[c * nn + i];
+    }
+    fn[i] = acc;
+    bad |= !isfinite(acc);
+    float* out = role == 0 ? A.fit2_g : A.fit2_d;
+    out[c * s + i] = acc;
+    float* ext = role == 0 ? A.fit2_g_out : A.fit2_d_out;
+    if (ext) ext[c * s + i] = acc;
+  }
+  if (bad) atomicOr(A.flags, 1);
+  // rank of each of the 2 s candidates in the order (fitness, NaN last;
+  // trained before previous; lower member first); the first s are kept
+  int rank_new[4], rank_old[4];
+  for (int r = 0; r < 2 * s; ++r) {
+    const bool rn = r < s;
+    const int ri = rn ? r : r - s;
+    const float f = fit_key(rn ? fn[ri] : fo[ri]);
+    int rank = 0;
+    for (int q = 0; q < 2 * s; ++q) {
+      const bool qn = q < s;
+      const int qi = qn ? q : q - s;
+      const float g = fit_key(qn ? fn[qi] : fo[qi]);
+      rank += g < f || (g == f && (qn != rn ? qn : qi < ri));
+    }
+    if (rn) rank_new[ri] = rank;
+    else rank_old[ri] = rank;
+  }
+  int kept_old[4], n_old = 0;
+  for (int r = 0; r < s; ++r)
+    for (int i = 0; i < s; ++i)
+      if (rank_old[i] == r) kept_old[n_old++] = i;
+  // the dropped trained slots, in slot order, take the kept previous members
+  // in rank order
+  int k = 0;
+  for (int i = 0; i < s; ++i) {
+    const int u = c * s + i;
+    const int src = rank_new[i] < s ? -1 : c * s + kept_old[k++];
+    A.src[u * 2 + role] = src;
+    if (A.src_out) A.src_out[u * 2 + role] = src < 0 ? -1 : src - c * s;
+    if (src >= 0) {
+      A.t_new[role][u] = A.t_old[role][src];
+      A.lr_new[role][u] = A.lr_old[role][src];
+    }
+  }
+}
+
+// block (x, u, role): p, m, v of individual sel[u][role] into individual u
 __global__ void copy_winners_kernel(CopyArgs A) {
-  const int c = blockIdx.y, role = blockIdx.z;
-  const int src = A.sel[c * 2 + role];
+  const int u = blockIdx.y, role = blockIdx.z;
+  const int src = A.sel[u * 2 + role];
+  if (A.w_dst && role == 0 && u < A.C && blockIdx.x == 0 && threadIdx.x < 5)
+    A.w_dst[u * 5 + threadIdx.x] = A.w_src[u * 5 + threadIdx.x];
+  if (src < 0) return;
   const int64_t n4 = A.stride[role] >> 2;
   for (int a = 0; a < 3; ++a) {
     const float4* s = reinterpret_cast<const float4*>(A.src[role][a] + src * A.stride[role]);
-    float4* d = reinterpret_cast<float4*>(A.dst[role][a] + c * A.stride[role]);
+    float4* d = reinterpret_cast<float4*>(A.dst[role][a] + u * A.stride[role]);
     for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n4;
          q += (int64_t)gridDim.x * blockDim.x)
       d[q] = s[q];
   }
-  if (role == 0 && blockIdx.x == 0 && threadIdx.x < 5)
-    A.w_dst[c * 5 + threadIdx.x] = A.w_src[c * 5 + threadIdx.x];
 }
 
 // Per-cell feature moments over S samples: mu = mean f, s2 = mean f^2, in a
@@ -633,24 +738,29 @@ hipError_t launch_es_select(const NesArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(es_select_kernel, dim3((unsigned)((a.P + NT - 1) / NT), a.C), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
-hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(head_eval_kernel, dim3(5, a.C), dim3(NT), (6 * a.B + 11) * sizeof(float), s, a);
+hipError_t launch_elite(const EliteArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(elite_means_kernel, dim3(a.nn + a.s, a.C), dim3(NT), 0, s, a);
+  hipLaunchKernelGGL(elite_merge_kernel, dim3(grid_for(2 * a.C)), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
-hipError_t launch_fitness(const float* L, const float* Lg, int C, int mode, float* fit_g,
+hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(head_eval_kernel, dim3(a.nn, a.C), dim3(NT), (1 + 2 * a.nn) * sizeof(float), s, a);
+  return hipGetLastError();
+}
+hipError_t launch_fitness(const float* L, const float* Lg, int C, int nn, int mode, float* fit_g,
                           float* fit_d, int32_t* flags, float* oL, float* oLg, float* ofg,
                           float* ofd, hipStream_t s) {
-  hipLaunchKernelGGL(fitness_kernel, dim3(grid_for((int64_t)C * 25)), dim3(NT), 0, s, L, Lg, C,
+  hipLaunchKernelGGL(fitness_kernel, dim3(grid_for((int64_t)C * nn * nn)), dim3(NT), 0, s, L, Lg, C, nn,
                      mode, fit_g, fit_d, flags, oL, oLg, ofg, ofd);
   return hipGetLastError();
 }
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(select_kernel, dim3(grid_for(2 * a.C)), dim3(NT), 0, s, a);
+  hipLaunchKernelGGL(select_kernel, dim3(grid_for(2 * a.C * a.s)), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_copy_winners(const CopyArgs& a, hipStream_t s) {
   const int64_t n4 = (a.stride[0] > a.stride[1] ? a.stride[0] : a.stride[1]) >> 2;
-  hipLaunchKernelGGL(copy_winners_kernel, dim3(grid_for(n4, NT, 64), a.C, 2), dim3(NT), 0, s, a);
+  hipLaunchKernelGGL(copy_winners_kernel, dim3(grid_for(n4, NT, 64), a.U, 2), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_moments(const float* feats, int C, int S, int F, float* part, float* mu, float* s2,

@@ -417,11 +417,12 @@ hipError_t launch_head_d(const HeadArgs& a, hipStream_t s);
 hipError_t launch_head_g(const HeadArgs& a, hipStream_t s);
 
 struct EvalHeadArgs {
-  const float* part;     // partial logits [C][5][6B][tn] (bias included)
+  const float* part;     // partial logits [C][nn][(1 + nn) B][tn] (bias included)
   int tn;
-  float* L;              // [C][5][5]
+  float* L;              // [C][nn][nn]
   float* Lg;
-  int B, C;
+  float* rmean;          // [C][nn] real-row term means, or null
+  int B, C, nn;
   int loss_kind;         // LIPZ_LOSS_BCE or LIPZ_LOSS_WASSERSTEIN
 };
 hipError_t launch_head_eval(const EvalHeadArgs& a, hipStream_t s);
@@ -455,7 +456,7 @@ hipError_t launch_nes_perturb(const NesArgs& a, hipStream_t s);
 hipError_t launch_nes_head(const NesArgs& a, hipStream_t s);
 hipError_t launch_nes_update(const NesArgs& a, hipStream_t s);
 hipError_t launch_es_select(const NesArgs& a, hipStream_t s);
-hipError_t launch_fitness(const float* L, const float* Lg, int C, int mode, float* fit_g, float* fit_d,
+hipError_t launch_fitness(const float* L, const float* Lg, int C, int nn, int mode, float* fit_g, float* fit_d,
                           int32_t* flags, float* out_L, float* out_Lg, float* out_fg, float* out_fd,
                           hipStream_t s);
 
@@ -463,30 +464,65 @@ struct SelectArgs {
   const float* fit_g;
   const float* fit_d;
   const int32_t* nbr;
-  const int32_t* forced;   // or null
-  int32_t* sel;            // internal [C][2]
-  int32_t* flags;          // bit 1 set when a forced source cell is out of range
+  const int32_t* forced;   // [U][2] source individuals, or null
+  int32_t* sel;            // internal [U][2]
+  int32_t* flags;          // bit 1 set when a forced source individual is out of range
   int32_t* sel_out;        // or null
   float* lr_out;           // or null
   const int32_t* t_src[2]; // current buffer Gt, Dt
   const float* lr_src[2];
   int32_t* t_dst[2];       // next buffer
   float* lr_dst[2];
-  int C, tsize, mutate;
+  int C, s, tsize, mutate;  // cells, individuals per role and cell
   float mut_std, mut_prob;
   uint2 key;
   uint32_t gen;
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 
+// Post-training re-evaluation (elitism).  Block (j, c), j < nn: previous
+// discriminator j of the cell's neighbourhood on the s B rows of the trained
+// generators (part2 [C][nn][s B][tn]); block (nn + j, c), j < s: trained
+// discriminator j on the (1 + nn) B evaluation rows (part3 [C][s][(1+nn)B][tn]).
+//   L2[c][i][j] = rmean[c][j] + mean fake term of G'_i under D_j, Lg2 its
+//   generator term; M3[c][0][j] the real-row mean of D'_j, M3[c][1 + k][j]
+//   its fake mean on G_k's rows (L(G_k, D'_j) = M3[c][0][j] + M3[c][1+k][j]).
+// The merge (one thread per cell and role) forms fit2 = -mean_j L2 (or
+// mean_j Lg2) and mean_k L3 in a fixed order, keeps the s best of the 2 s,
+// writes src (previous individual or -1) and the step counts and learning
+// rates of the slots given back.
+struct EliteArgs {
+  const float* part2;
+  const float* part3;
+  const float* rmean;    // [C][nn]
+  float* L2;             // [C][s][nn]
+  float* Lg2;            // [C][s][nn]
+  float* M3;             // [C][1 + nn][s]
+  const float* fit_g;    // [C][nn] fitness of the previous neighbourhood (evaluation)
+  const float* fit_d;
+  float* fit2_g;         // [C][s]
+  float* fit2_d;
+  int32_t* src;          // [U][2] internal: previous individual or -1
+  int32_t* src_out;      // [U][2] previous member or -1, or null
+  float* fit2_g_out;     // or null
+  float* fit2_d_out;
+  int32_t* flags;        // bit 0 on a non-finite value
+  const int32_t* t_old[2];
+  const float* lr_old[2];
+  int32_t* t_new[2];
+  float* lr_new[2];
+  int tn, B, C, s, nn, mode, loss_kind;
+};
+hipError_t launch_elite(const EliteArgs& a, hipStream_t s);
+
 struct CopyArgs {
-  const int32_t* sel;      // [C][2]
+  const int32_t* sel;      // [U][2] source individual of each destination, < 0: no copy
   const float* src[2][3];  // role, (p, m, v)
   float* dst[2][3];
   int64_t stride[2];       // floats per row, multiple of 4
-  const float* w_src;
+  const float* w_src;      // mixture weights [C][5] copied along, or null
   float* w_dst;
-  int C;
+  int U, C;
 };
 hipError_t launch_copy_winners(const CopyArgs& a, hipStream_t s);
 hipError_t launch_add_i32(int32_t* p, int n, int32_t v, hipStream_t s);

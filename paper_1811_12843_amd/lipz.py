@@ -11,7 +11,7 @@ import os
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("LIPZ_LIBRARY") or os.path.join(_PKG, "liblipz.so")
 
-LIPZ_ABI_VERSION = 2
+LIPZ_ABI_VERSION = 3
 LIPZ_MAX_HIDDEN = 4
 LIPZ_OK, LIPZ_E_INVAL, LIPZ_E_WORKSPACE, LIPZ_E_HIP, LIPZ_E_ORDER, LIPZ_E_NONFINITE, \
     LIPZ_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
@@ -43,6 +43,7 @@ class lipz_config(ctypes.Structure):
         ("seed", _u64),
         ("loss_kind", _i32), ("wgan_clip", _f32),
         ("trainer", _i32), ("nes_pairs", _i32), ("nes_sigma", _f32),
+        ("pop_size", _i32), ("elitism", _i32),
     ]
 
 
@@ -83,6 +84,8 @@ def config_from_dict(d):
     c.trainer = TRAINERS[d.get("trainer", "gradient")]
     c.nes_pairs = d.get("nes_pairs", 8)
     c.nes_sigma = d.get("nes_sigma", 0.01)
+    c.pop_size = d.get("pop_size", 1)
+    c.elitism = d.get("elitism", 0)
     return c
 
 
@@ -94,6 +97,7 @@ _SIGS = {
     "lipz_eval_neighborhoods": (_i32, [_vp, _i32, _vp, _vp, _vp, _vp]),
     "lipz_select_replace": (_i32, [_vp, _i32, _vp, _vp, _vp]),
     "lipz_train_step": (_i32, [_vp, _i32, _i32, _i32, _vp]),
+    "lipz_elitist_replace": (_i32, [_vp, _i32, _vp, _vp, _vp]),
     "lipz_mixture_update": (_i32, [_vp, _i32, _vp, _vp, _vp]),
     "lipz_get_neighbors": (_i32, [_vp, ctypes.POINTER(_i32)]),
     "lipz_param_layout": (_i32, [_vp, _i32, ctypes.POINTER(_i64), ctypes.POINTER(_i32)]),
@@ -185,6 +189,11 @@ def lipz_select_replace(g, gen, d_forced=None, d_sel=None, d_lr=None):
 def lipz_train_step(g, gen, step0, n_steps, d_losses=None):
     return _check(load_library().lipz_train_step(_p(g), gen, step0, n_steps, _p(d_losses)),
                   "lipz_train_step", g)
+
+
+def lipz_elitist_replace(g, gen, d_src=None, d_fit2_g=None, d_fit2_d=None):
+    return _check(load_library().lipz_elitist_replace(_p(g), gen, _p(d_src), _p(d_fit2_g), _p(d_fit2_d)),
+                  "lipz_elitist_replace", g)
 
 
 def lipz_mixture_update(g, gen, d_w=None, d_score=None, d_accepted=None):

@@ -91,6 +91,11 @@ WORKLOADS = {
                            batch=100, steps=100, gens=1,
                            trainer="es", nes_pairs=8, nes_sigma=0.01,
                            data=dict(kind="mnist_like", n=60000, seed=0)),
+    # 4x4 torus, MNIST-shaped MLPs, two individuals per role and cell, elitist replacement
+    "mnist_mlp_4x4_pop2": _w(rows=4, cols=4, z_dim=64, x_dim=784,
+                             g_hidden=[256, 256], d_hidden=[256, 256],
+                             batch=100, steps=100, gens=10, pop_size=2, elitism=1,
+                             data=dict(kind="mnist_like", n=60000, seed=0)),
     # 8x8 torus, MNIST-shaped MLPs
     "mnist_mlp_8x8": _w(rows=8, cols=8, z_dim=64, x_dim=784,
                         g_hidden=[256, 256], d_hidden=[256, 256],

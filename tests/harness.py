@@ -22,6 +22,8 @@ class GpuGrid:
         self.cfg = L.config_from_dict(wl)
         self.N = int(len(data_np))
         self.C = wl["rows"] * wl["cols"]
+        self.s = int(wl.get("pop_size", 1))
+        self.U, self.nn = self.C * self.s, 5 * self.s  # individuals, neighbourhood population
         self.device = device
         self.data = torch.from_numpy(np.ascontiguousarray(data_np, dtype=np.float32)).to(device)
         nb = L.lipz_workspace_bytes(self.cfg, self.N)
@@ -74,13 +76,14 @@ class GpuGrid:
         return torch.zeros(*shape, dtype=torch.int32, device=self.device)
 
     def eval(self, gen):
-        Lm, Lg, fg, fd = self._f(self.C, 5, 5), self._f(self.C, 5, 5), self._f(self.C, 5), self._f(self.C, 5)
+        C, n = self.C, self.nn
+        Lm, Lg, fg, fd = self._f(C, n, n), self._f(C, n, n), self._f(C, n), self._f(C, n)
         L.lipz_eval_neighborhoods(self.g, gen, Lm.data_ptr(), Lg.data_ptr(), fg.data_ptr(), fd.data_ptr())
         self.sync()
         return [t.cpu().numpy().astype(np.float64) for t in (Lm, Lg, fg, fd)]
 
     def select(self, gen, forced=None):
-        sel, lr = self._i(self.C, 2), self._f(self.C, 2)
+        sel, lr = self._i(self.U, 2), self._f(self.U, 2)
         fp = None
         if forced is not None:
             ft = torch.from_numpy(np.ascontiguousarray(forced, dtype=np.int32)).to(self.device)
@@ -90,10 +93,17 @@ class GpuGrid:
         return sel.cpu().numpy().astype(np.int64), lr.cpu().numpy().astype(np.float64)
 
     def train(self, gen, step0, n):
-        losses = self._f(max(n, 1), self.C, 2)
+        losses = self._f(max(n, 1), self.U, 2)
         L.lipz_train_step(self.g, gen, step0, n, losses.data_ptr())
         self.sync()
         return losses.cpu().numpy().astype(np.float64)[:n]
+
+    def elite(self, gen):
+        src, f2g, f2d = self._i(self.U, 2), self._f(self.C, self.s), self._f(self.C, self.s)
+        L.lipz_elitist_replace(self.g, gen, src.data_ptr(), f2g.data_ptr(), f2d.data_ptr())
+        self.sync()
+        return (src.cpu().numpy().astype(np.int64), f2g.cpu().numpy().astype(np.float64),
+                f2d.cpu().numpy().astype(np.float64))
 
     def mixture(self, gen):
         w, sc, acc = self._f(self.C, 5), self._f(self.C), self._i(self.C)
@@ -105,7 +115,7 @@ class GpuGrid:
 
 def state_to_blob(st, S, offs, strides, nbytes):
     blob = np.zeros(nbytes, dtype=np.uint8)
-    C = S.C
+    C = S.U  # parameter rows: one per individual
 
     def put(k, arr, dtype):
         a = np.ascontiguousarray(arr, dtype=dtype).view(np.uint8).ravel()
@@ -125,7 +135,7 @@ def state_to_blob(st, S, offs, strides, nbytes):
 
 
 def blob_to_state(blob, S, offs, strides):
-    C = S.C
+    C = S.U  # parameter rows: one per individual
 
     def get(k, n, dtype):
         return np.frombuffer(blob[offs[k]:offs[k] + n * np.dtype(dtype).itemsize].tobytes(), dtype=dtype)
@@ -138,7 +148,7 @@ def blob_to_state(blob, S, offs, strides):
     kw["Dt"] = get(7, C, np.int32).astype(np.int64)
     kw["Glr"] = get(8, C, np.float32).astype(np.float64)
     kw["Dlr"] = get(9, C, np.float32).astype(np.float64)
-    kw["w"] = get(10, C * 5, np.float32).reshape(C, 5).astype(np.float64)
+    kw["w"] = get(10, S.C * 5, np.float32).reshape(S.C, 5).astype(np.float64)
     return coevo.State(**kw)
 
 
@@ -166,3 +176,22 @@ def decisive(f, k1, k2, tol=1e-4):
     if np.isnan(a) or np.isnan(b):
         return not (np.isnan(a) and np.isnan(b))
     return abs(a - b) > tol * max(abs(a), abs(b))
+
+
+def check_selection(S, gsel, ofg, ofd, gen):
+    """GPU tournament decisions gsel [U][2] against the oracle's tournaments on
+    the oracle's fitness: equal wherever the first drawn individual's margin to
+    every other drawn one is decisive, else one of the drawn.  Returns the
+    number of decisive tournaments."""
+    n_decisive = 0
+    for c in range(S.C):
+        for i in range(S.s):
+            u = c * S.s + i
+            for r, (fit, tag) in enumerate(((ofg, "TOURN_G"), (ofd, "TOURN_D"))):
+                drawn = coevo.tournament_draw(S, c, gen, tag, i)
+                if all(decisive(fit[c], drawn[0], k) for k in drawn[1:]):
+                    n_decisive += 1
+                    assert gsel[u, r] == S.pool[c, coevo.tournament_winner(fit[c], drawn)], (u, r)
+                else:
+                    assert gsel[u, r] in [S.pool[c, k] for k in drawn]
+    return n_decisive

@@ -86,6 +86,17 @@ def test_workspace_sizing_and_validation():
     for t in ("nes", "es"):
         d = dict(synth.workload("celeba_dcgan_4x4"), trainer=t)
         assert L.lipz_workspace_bytes(L.config_from_dict(d), 1000) == 0
+    # sub-populations: per-individual state and training buffers grow with s; elitism adds the re-evaluation
+    w1 = synth.workload("mnist_mlp_3x3")
+    b1 = L.lipz_workspace_bytes(L.config_from_dict(w1), 60000)
+    b2 = L.lipz_workspace_bytes(L.config_from_dict(dict(w1, pop_size=2)), 60000)
+    b2e = L.lipz_workspace_bytes(L.config_from_dict(dict(w1, pop_size=2, elitism=1)), 60000)
+    assert 0 < b1 < b2 < b2e
+    for b in (dict(w1, pop_size=0), dict(w1, pop_size=5), dict(w1, elitism=2),
+              dict(w2, pop_size=2),  # the mixture step needs one generator per cell
+              dict(synth.workload("celeba_dcgan_4x4"), pop_size=2),
+              dict(synth.workload("celeba_dcgan_4x4"), elitism=1)):
+        assert L.lipz_workspace_bytes(L.config_from_dict(b), 60000) == 0
     # the ES trainer: the same sets, no direction buffer
     es = synth.workload("mnist_mlp_3x3_es")
     assert base < L.lipz_workspace_bytes(L.config_from_dict(es), 60000) < L.lipz_workspace_bytes(

@@ -24,7 +24,7 @@ if not torch.cuda.is_available():  # pragma: no cover - collected on CPU, skippe
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_1811_12843_amd as L  # noqa: E402
-from harness import GpuGrid, decisive, fp32_state, per_tensor_rel, rel_err  # noqa: E402
+from harness import GpuGrid, check_selection, fp32_state, per_tensor_rel, rel_err  # noqa: E402
 
 RTOL = 1e-4
 
@@ -218,21 +218,6 @@ def test_eval_matches_oracle(key):
                 assert np.array_equal(Lm[:, 1], Lm[:, 2]) and np.array_equal(Lm[:, :, 3], Lm[:, :, 4])
 
 
-def _check_selection(S, st, gsel, ofg, ofd, gen):
-    """Decisions must match the oracle's tournaments wherever the margin is decisive."""
-    n_decisive = 0
-    for c in range(S.C):
-        for r, (fit, tag) in enumerate(((ofg, "TOURN_G"), (ofd, "TOURN_D"))):
-            drawn = coevo.tournament_draw(S, c, gen, tag)
-            ok = all(decisive(fit[c], drawn[0], k) for k in drawn[1:])
-            if ok:
-                n_decisive += 1
-                assert gsel[c, r] == S.nbr[c, coevo.tournament_winner(fit[c], drawn)], (c, r)
-            else:
-                assert gsel[c, r] in [S.nbr[c, k] for k in drawn]
-    return n_decisive
-
-
 @pytest.mark.parametrize("key", ["ring8_2x2", "ragged_2x3", "mnist_4x4_mix", "mnist_3x3_fm1", "mnist_3x3_wgan"])
 def test_select_replace_matches_oracle(key):
     wl, data, S = _setup(key)
@@ -244,7 +229,7 @@ def test_select_replace_matches_oracle(key):
         gg.eval(gen)
         gsel, glr = gg.select(gen)
         _, _, ofg, ofd = coevo.evaluate(S, st, data, gen)
-        assert _check_selection(S, st, gsel, ofg, ofd, gen) > 0
+        assert check_selection(S, gsel, ofg, ofd, gen) > 0
         new, osel = coevo.select_replace(S, st, ofg, ofd, gen, forced=gsel)
         got = gg.get_state()
         for f in ("Gp", "Gm", "Gv", "Dp", "Dm", "Dv", "Gt", "Dt", "w"):
@@ -338,7 +323,7 @@ def _generation_parity(key, **over):
         oL, _, ofg, ofd = coevo.evaluate(S, st, data, gen)
         assert _close(Lm, oL, wl)
         gsel, _ = gg.select(gen)
-        _check_selection(S, st, gsel, ofg, ofd, gen)
+        check_selection(S, gsel, ofg, ofd, gen)
         ref, _ = coevo.select_replace(S, st, ofg, ofd, gen, forced=gsel)
         glosses = gg.train(gen, 0, wl["steps"])
         olosses = np.array([coevo.train_step(S, ref, data, gen, s) for s in range(wl["steps"])])
@@ -463,7 +448,7 @@ def test_nonfinite_individual_loses_and_is_flagged():
         assert np.array_equal(np.isnan(Lm), np.isnan(oL))
         assert np.array_equal(np.isnan(fd), np.isnan(ofd))
         gsel, _ = gg.select(0)
-        _check_selection(S, st, gsel, ofg, ofd, 0)
+        check_selection(S, gsel, ofg, ofd, 0)
         for c in range(S.C):
             drawn = coevo.tournament_draw(S, c, 0, "TOURN_D")
             if any(not np.isnan(ofd[c, k]) for k in drawn):

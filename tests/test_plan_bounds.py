@@ -59,6 +59,26 @@ def test_small_nes_plans_stay_in_bounds(i):
         assert n_bad == 0, msg
 
 
+SMALL_SUBPOP = [
+    dict(rows=2, cols=3, z_dim=7, x_dim=37, g_hidden=[33, 70], d_hidden=[45, 19], batch=19, pop_size=2,
+         elitism=1, data=dict(kind="mnist_like", n=300)),
+    dict(rows=1, cols=1, z_dim=3, x_dim=5, g_hidden=[6], d_hidden=[7], batch=2, pop_size=4, elitism=1,
+         tournament_size=5, data=dict(kind="mnist_like", n=50)),
+    dict(rows=3, cols=2, z_dim=9, x_dim=70, g_hidden=[13, 8], d_hidden=[130], batch=5, pop_size=3,
+         elitism=0, data=dict(kind="mnist_like", n=50)),
+]
+
+
+@pytest.mark.parametrize("i", range(len(SMALL_SUBPOP)))
+@pytest.mark.parametrize("trainer", ["gradient", "nes", "es"])
+def test_subpopulation_plans_stay_in_bounds(i, trainer):
+    """Sub-populations (training per individual, evaluation over 5 s
+    neighbourhood individuals, the re-evaluation of elitism)."""
+    wl = synth.small_workload("mnist_mlp_3x3", trainer=trainer, nes_pairs=2, **SMALL_SUBPOP[i])
+    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
+    assert n_bad == 0, msg
+
+
 def test_invalid_dcgan_shapes_are_rejected():
     wl = synth.small_workload("celeba_dcgan_4x4", img=(48, 48, 3), x_dim=48 * 48 * 3)
     assert L.lipz_workspace_bytes(L.config_from_dict(wl), 100) == 0
