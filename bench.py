@@ -209,6 +209,9 @@ def main():
     ap.add_argument("--eval-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--bands", type=int, default=0,
+                    help="run the timed generations with lipz_run_generations on this many row bands "
+                         "(asynchronous cells; MLP workloads without the mixture step)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -236,6 +239,8 @@ def main():
         from paper_1811_12843_amd import build as _b
         _b.build()
     wl = synth.workload(args.workload)
+    if args.bands:
+        wl["bands"] = args.bands
     n_data = args.data_n or (8192 if wl["net"] == "dcgan" else wl["data"]["n"])
     wl["data"] = dict(wl["data"], n=n_data)
     data_np = synth.make_dataset(wl["data"])
@@ -264,9 +269,13 @@ def main():
         gen += 1
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        generation(gen)
-        gen += 1
+    if args.bands:  # one call: the bands run ahead of each other across generations
+        L.lipz_run_generations(g, gen, args.steps, S)
+        gen += args.steps
+    else:
+        for _ in range(args.steps):
+            generation(gen)
+            gen += 1
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     assert L.lipz_sync(g) in (L.LIPZ_OK, L.LIPZ_E_NONFINITE)
@@ -301,7 +310,7 @@ def main():
     traffic = stored_gemm_traffic(args.workload)
     cfg_desc = {"workload": args.workload, "grid": f"{wl['rows']}x{wl['cols']}", "cells": C,
                 "pairings_per_eval": nbh * nbh * C, "batch": wl["batch"], "steps_per_generation": S,
-                "mixture_es": bool(wl["mix_enable"])}
+                "mixture_es": bool(wl["mix_enable"]), "bands": args.bands}
     if wl["net"] == "mlp":
         cfg_desc.update(g=[wl["z_dim"]] + wl["g_hidden"] + [wl["x_dim"]], d=[wl["x_dim"]] + wl["d_hidden"] + [1])
         data_desc = (f"synthetic (seeded MNIST-shaped blobs, {len(data_np)} x {wl['x_dim']}); "

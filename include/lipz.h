@@ -77,6 +77,7 @@ extern "C" {
 #define LIPZ_ABI_VERSION 3
 #define LIPZ_SLOTS 5          /* centre, north, south, west, east */
 #define LIPZ_MAX_HIDDEN 4
+#define LIPZ_MAX_BANDS 8      /* row bands of lipz_run_generations */
 
 typedef int32_t lipz_status;
 enum {
@@ -168,6 +169,7 @@ typedef struct {
   float nes_sigma;                  /* NES / ES: perturbation (mutation) scale (> 0) */
   int32_t pop_size;                 /* s: individuals per role and cell, 1..4 (1 in the paper) */
   int32_t elitism;                  /* 1: allow lipz_elitist_replace (MLP only) */
+  int32_t bands;                    /* lipz_run_generations: 0 or 1 one batch; b >= 2 row bands */
 } lipz_config;
 
 typedef struct lipz_grid lipz_grid;  /* opaque host handle */
@@ -265,6 +267,24 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
  * d_fit2_g / d_fit2_d [C][s] fp32.  LIPZ_E_ORDER if elitism = 0. */
 lipz_status lipz_elitist_replace(lipz_grid* g, int32_t gen, int32_t* d_src, float* d_fit2_g,
                                  float* d_fit2_d);
+
+/* Steps 2-3 for n_gens generations gen0 .. gen0 + n_gens - 1, each of them
+ * lipz_eval_neighborhoods, lipz_select_replace, lipz_train_step(gen, 0,
+ * n_steps) and (elitism = 1) lipz_elitist_replace, and, with mix_enable,
+ * lipz_mixture_update, with the same results bit for bit.
+ *
+ * bands >= 2 (MLP networks, gradient trainer, no mixture step): the paper's
+ * cells run asynchronously (Section 3, step 1 and its Figure 1), and this is
+ * that scheduling on one device.  The grid's rows are split into `bands` row
+ * bands, each on its own stream, and nothing waits for the whole grid: a
+ * band starts generation g + 1 as soon as the bands holding its cells'
+ * neighbour rows have finished generation g (a readiness event per band),
+ * so bands that are not neighbours drift apart by up to the grid's band
+ * distance in generations, and neighbours by at most one.  That rule keeps
+ * every read of a neighbour's individuals and every overwrite of a state
+ * buffer ordered as in the synchronous schedule.  Returns after enqueuing;
+ * the caller's stream waits for every band at the end. */
+lipz_status lipz_run_generations(lipz_grid* g, int32_t gen0, int32_t n_gens, int32_t n_steps);
 
 /* Step 4 (Section 3): one (1+1)-ES step on every cell's mixture weights over
  * the generators of its neighbourhood (current state).  Features f = x P,

@@ -81,6 +81,10 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
   if ((c->pop_size > 1 || c->elitism) && c->net != LIPZ_NET_MLP)
     return "sub-populations and elitism are implemented for the MLP networks";
   if (c->pop_size > 1 && c->mix_enable) return "the mixture step needs pop_size 1";
+  if (c->bands < 0 || c->bands > LIPZ_MAX_BANDS || (c->bands > 1 && c->bands > c->rows))
+    return "bands must be in [0, 8] and at most rows";
+  if (c->bands > 1 && (c->net != LIPZ_NET_MLP || c->trainer != LIPZ_TRAINER_GRADIENT))
+    return "row bands are implemented for the MLP networks and the gradient trainer";
   if ((int64_t)c->rows * c->cols * c->pop_size > 4096) return "grid size x pop_size out of range";
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31) - 1) return "n_samples must be in [1, 2^31)";
   if (c->net == LIPZ_NET_DCGAN) return dc_validate(c, Gn, Dn);
@@ -212,7 +216,7 @@ void carve(lipz_grid* g, char* base, size_t* total) {
   // mixture
   if (g->cfg.mix_enable) {
     const int S = g->S, F = g->F;
-    g->zeta = cv.take<float>((size_t)S * zd);
+    g->zeta = cv.take<float>((size_t)(g->n_bands > 1 ? g->n_bands : 1) * S * zd);  // one copy per row band
     for (int l = 0; l + 1 < G.nl; ++l) g->hm[l] = cv.take<float>((size_t)C * S * G.fo[l]);
     g->xm = cv.take<float>((size_t)C * S * xd);
     g->fm = cv.take<float>((size_t)C * S * F);
@@ -396,12 +400,32 @@ void backward_phases(lipz_grid* g, int top, Dgrad dgrad, Wgrad wgrad, std::vecto
 
 
 void setup_groups(lipz_grid* g) {
+  if (g->cfg.bands >= 2) {
+    // row bands: rows split as evenly as possible; the training groups are
+    // the bands' individuals
+    const int R = g->cfg.rows, Q = g->cfg.cols, nb = g->cfg.bands;
+    g->n_bands = nb;
+    for (int b = 0; b <= nb; ++b) g->band_c0[b] = (int)((int64_t)R * b / nb) * Q;
+    for (int b = 0; b < nb; ++b) {
+      uint32_t m = 0;
+      for (int c = g->band_c0[b]; c < g->band_c0[b + 1]; ++c)
+        for (int k = 0; k < LIPZ_SLOTS; ++k) {
+          const int cn = g->nbr_h[c * LIPZ_SLOTS + k];
+          for (int b2 = 0; b2 < nb; ++b2)
+            if (cn >= g->band_c0[b2] && cn < g->band_c0[b2 + 1]) m |= 1u << b2;
+        }
+      g->band_wait[b] = m;
+    }
+    g->n_groups = nb;
+    for (int b = 0; b <= nb; ++b) g->group_c0[b] = g->band_c0[b] * g->s;
+    return;
+  }
   // Measured on the 4x4 MNIST-shaped grid: 1, 2 and 4 groups are within a
   // few percent of each other, so by default one stream keeps the phases
   // in a single dependency chain.
   int n = LIPZ_CELL_GROUPS;
   if (n <= 0) n = 1;
-  if (n > LIPZ_MAX_GROUPS) n = LIPZ_MAX_GROUPS;
+  if (n > 4) n = 4;
   if (n > g->U) n = g->U;
   g->n_groups = n;
   for (int i = 0; i <= n; ++i) g->group_c0[i] = (int)((int64_t)g->U * i / n);
@@ -611,46 +635,46 @@ void build_tables(lipz_grid* g) {
     // ---- evaluation: rows [x_c; G_0(z_c); ...; G_(nn-1)(z_c)] per cell ----
     const int s = g->s, nn = g->nn, er = 1 + nn;
     auto owner_of = [&](int c, int i) { return g->nbr_h[c * 5 + i / s] * s + i % s; };
-    std::vector<int>& ev = g->eval_phases[par];
-    ev.clear();
-    for (int l = 0; l < LG; ++l) {
-      std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c)
-        for (int i = 0; i < nn; ++i) {
-          const int owner = owner_of(c, i);
-          const float* x = l == 0 ? g->ze + (size_t)c * B * zd
-                                  : g->he[l - 1] + (size_t)(c * nn + i) * B * G.fi[l];
-          float* y = l + 1 < LG ? g->he[l] + (size_t)(c * nn + i) * B * G.fo[l]
-                                : g->Xe + (size_t)c * er * B * xd + (size_t)(1 + i) * B * xd;
-          ps.push_back(fwd_prob(x, B, S.Gp + owner * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
-        }
-      ev.push_back(add_phase(g, ps));
-    }
-    for (int l = 0; l + 1 < LD; ++l) {
-      std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c)
-        for (int j = 0; j < nn; ++j) {
-          const int owner = owner_of(c, j);
-          const float* x = l == 0 ? g->Xe + (size_t)c * er * B * xd
-                                  : g->ae[l - 1] + (size_t)(c * nn + j) * er * B * D.fi[l];
-          GemmProb p = fwd_prob(x, er * B, S.Dp + owner * sD + D.off[l], D.fi[l], D.fo[l],
-                                g->ae[l] + (size_t)(c * nn + j) * er * B * D.fo[l], D.act[l]);
-          if (l == LD - 2)
-            p = with_head(p, S.Dp + owner * sD + D.off[LD - 1],
-                          g->part_e + (size_t)(c * nn + j) * er * B * g->tn, g->tn);
-          ps.push_back(p);
-        }
-      ev.push_back(add_phase(g, ps));
-    }
+    auto eval_phases = [&](int cb, int ce, std::vector<int>& ev) {
+      ev.clear();
+      for (int l = 0; l < LG; ++l) {
+        std::vector<GemmProb> ps;
+        for (int c = cb; c < ce; ++c)
+          for (int i = 0; i < nn; ++i) {
+            const int owner = owner_of(c, i);
+            const float* x = l == 0 ? g->ze + (size_t)c * B * zd
+                                    : g->he[l - 1] + (size_t)(c * nn + i) * B * G.fi[l];
+            float* y = l + 1 < LG ? g->he[l] + (size_t)(c * nn + i) * B * G.fo[l]
+                                  : g->Xe + (size_t)c * er * B * xd + (size_t)(1 + i) * B * xd;
+            ps.push_back(fwd_prob(x, B, S.Gp + owner * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
+          }
+        ev.push_back(add_phase(g, ps));
+      }
+      for (int l = 0; l + 1 < LD; ++l) {
+        std::vector<GemmProb> ps;
+        for (int c = cb; c < ce; ++c)
+          for (int j = 0; j < nn; ++j) {
+            const int owner = owner_of(c, j);
+            const float* x = l == 0 ? g->Xe + (size_t)c * er * B * xd
+                                    : g->ae[l - 1] + (size_t)(c * nn + j) * er * B * D.fi[l];
+            GemmProb p = fwd_prob(x, er * B, S.Dp + owner * sD + D.off[l], D.fi[l], D.fo[l],
+                                  g->ae[l] + (size_t)(c * nn + j) * er * B * D.fo[l], D.act[l]);
+            if (l == LD - 2)
+              p = with_head(p, S.Dp + owner * sD + D.off[LD - 1],
+                            g->part_e + (size_t)(c * nn + j) * er * B * g->tn, g->tn);
+            ps.push_back(p);
+          }
+        ev.push_back(add_phase(g, ps));
+      }
+    };
     // ---- post-training re-evaluation (elitism): this buffer holds the trained
     // individuals, the other one the previous state ----
-    std::vector<int>& el = g->elite_phases[par];
-    el.clear();
-    if (g->cfg.elitism) {
+    auto elite_phases = [&](int cb, int ce, std::vector<int>& el) {
+      el.clear();
       const StateBuf& O = g->st[1 - par];
       for (int l = 0; l < LG; ++l) {  // trained G'_i on the cell's evaluation latents
         std::vector<GemmProb> ps;
-        for (int c = 0; c < C; ++c)
+        for (int c = cb; c < ce; ++c)
           for (int i = 0; i < s; ++i) {
             const size_t ci = (size_t)c * s + i;
             const float* x = l == 0 ? g->ze + (size_t)c * B * zd : g->he2[l - 1] + ci * B * G.fi[l];
@@ -662,7 +686,7 @@ void build_tables(lipz_grid* g) {
       for (int l = 0; l + 1 < LD; ++l) {
         // one phase, two problem shapes (all cells' first kind, then the second)
         std::vector<GemmProb> ps;
-        for (int c = 0; c < C; ++c)
+        for (int c = cb; c < ce; ++c)
           for (int j = 0; j < nn; ++j) {  // previous D_j on the s B rows of the trained generators
             const int owner = owner_of(c, j);
             const size_t cj = (size_t)c * nn + j;
@@ -673,7 +697,7 @@ void build_tables(lipz_grid* g) {
               p = with_head(p, O.Dp + owner * sD + D.off[LD - 1], g->part_e2 + cj * s * B * g->tn, g->tn);
             ps.push_back(p);
           }
-        for (int c = 0; c < C; ++c)
+        for (int c = cb; c < ce; ++c)
           for (int j = 0; j < s; ++j) {  // trained D'_j on the evaluation rows
             const size_t cj = (size_t)c * s + j;
             const float* x = l == 0 ? g->Xe + (size_t)c * er * B * xd : g->ae3[l - 1] + cj * er * B * D.fi[l];
@@ -685,26 +709,39 @@ void build_tables(lipz_grid* g) {
           }
         el.push_back(add_phase(g, ps));
       }
+    };
+    eval_phases(0, C, g->eval_phases[par]);
+    g->elite_phases[par].clear();
+    if (g->cfg.elitism) elite_phases(0, C, g->elite_phases[par]);
+    for (int b = 0; b < g->n_bands; ++b) {  // the same plans per row band
+      eval_phases(g->band_c0[b], g->band_c0[b + 1], g->band_eval_phases[par][b]);
+      g->band_elite_phases[par][b].clear();
+      if (g->cfg.elitism) elite_phases(g->band_c0[b], g->band_c0[b + 1], g->band_elite_phases[par][b]);
     }
     // ---- mixture ----
-    std::vector<int>& mx = g->mix_phases[par];
-    mx.clear();
-    if (g->cfg.mix_enable) {
+    auto mix_phases = [&](int cb, int ce, const float* zeta, std::vector<int>& mx) {
+      mx.clear();
       const int Sm = g->S, F = g->F;
       for (int l = 0; l < LG; ++l) {
         std::vector<GemmProb> ps;
-        for (int c = 0; c < C; ++c) {
-          const float* x = l == 0 ? g->zeta : g->hm[l - 1] + (size_t)c * Sm * G.fi[l];
+        for (int c = cb; c < ce; ++c) {
+          const float* x = l == 0 ? zeta : g->hm[l - 1] + (size_t)c * Sm * G.fi[l];
           float* y = l + 1 < LG ? g->hm[l] + (size_t)c * Sm * G.fo[l] : g->xm + (size_t)c * Sm * xd;
           ps.push_back(fwd_prob(x, Sm, S.Gp + c * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
         }
         mx.push_back(add_phase(g, ps));
       }
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c)
+      for (int c = cb; c < ce; ++c)
         ps.push_back(base_prob(g->xm + (size_t)c * Sm * xd, xd, 0, g->P, F, 0,
                                g->fm + (size_t)c * Sm * F, F, Sm, F, xd));
       mx.push_back(add_phase(g, ps));
+    };
+    g->mix_phases[par].clear();
+    if (g->cfg.mix_enable) {
+      mix_phases(0, C, g->zeta, g->mix_phases[par]);
+      for (int b = 0; b < g->n_bands; ++b)
+        mix_phases(g->band_c0[b], g->band_c0[b + 1], g->zeta + (size_t)b * g->S * zd, g->band_mix_phases[par][b]);
     }
   }
   if (g->cfg.mix_enable) {
@@ -821,6 +858,219 @@ lipz_grid* plan_grid(const lipz_config* cfg, int64_t n_samples, char* base, cons
   return g;
 }
 
+// ---- enqueue helpers shared by the entry points and the row-band executor ----
+
+// Evaluation of cells c0 .. c0 + nc - 1 of the current plan `phases`.
+lipz_status enq_eval(lipz_grid* g, int gen, int c0, int nc, const std::vector<int>& phases, hipStream_t s,
+                     float* d_L, float* d_Lg, float* d_fit_g, float* d_fit_d) {
+  const int B = g->B, nn = g->nn, er = 1 + nn;
+  const size_t n2 = (size_t)nn * nn;
+  lipz_status st;
+  hipError_t e = launch_sample(g->data, g->N, g->xd, g->zd, B, c0, nc, g->key, (uint32_t)gen, 0, g->Xe,
+                               (int64_t)er * B * g->xd, g->ze, (int64_t)B * g->zd, s);
+  if ((st = check_hip(g, e, "eval sample"))) return st;
+  for (int ph : phases)
+    if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "eval forward"))) return st;
+  EvalHeadArgs ha;
+  memset(&ha, 0, sizeof(ha));
+  ha.part = g->part_e + (size_t)c0 * nn * er * B * g->tn;
+  ha.tn = g->tn;
+  ha.L = g->L + c0 * n2;
+  ha.Lg = g->Lg + c0 * n2;
+  ha.rmean = g->rmean ? g->rmean + (size_t)c0 * nn : nullptr;
+  ha.B = B;
+  ha.C = nc;
+  ha.nn = nn;
+  ha.loss_kind = g->cfg.loss_kind;
+  if ((st = check_hip(g, launch_head_eval(ha, s), "eval head"))) return st;
+  e = launch_fitness(g->L + c0 * n2, g->Lg + c0 * n2, nc, nn, g->cfg.fitness_mode, g->fit_g + (size_t)c0 * nn,
+                     g->fit_d + (size_t)c0 * nn, g->flags, d_L, d_Lg, d_fit_g, d_fit_d, s);
+  return check_hip(g, e, "fitness");
+}
+
+// Tournaments and copies of cells c0 .. c0 + nc - 1 from buffer par into 1 - par.
+lipz_status enq_select(lipz_grid* g, int gen, int par, int c0, int nc, const int32_t* d_forced, int32_t* d_sel,
+                       float* d_lr, hipStream_t s) {
+  const StateBuf& A = g->st[par];
+  const StateBuf& Bn = g->st[1 - par];
+  const int sp = g->s;
+  lipz_status st;
+  SelectArgs sa;
+  memset(&sa, 0, sizeof(sa));
+  sa.fit_g = g->fit_g;
+  sa.fit_d = g->fit_d;
+  sa.nbr = g->nbr;
+  sa.forced = d_forced;
+  sa.sel = g->sel;
+  sa.flags = g->flags;
+  sa.sel_out = d_sel;
+  sa.lr_out = d_lr;
+  sa.t_src[0] = A.Gt;
+  sa.t_src[1] = A.Dt;
+  sa.lr_src[0] = A.Glr;
+  sa.lr_src[1] = A.Dlr;
+  sa.t_dst[0] = Bn.Gt;
+  sa.t_dst[1] = Bn.Dt;
+  sa.lr_dst[0] = Bn.Glr;
+  sa.lr_dst[1] = Bn.Dlr;
+  sa.c0 = c0;
+  sa.C = nc;
+  sa.s = sp;
+  sa.U = g->U;
+  sa.tsize = g->cfg.tournament_size;
+  sa.mutate = g->cfg.lr_mutation;
+  sa.mut_std = g->cfg.lr_mut_std;
+  sa.mut_prob = g->cfg.lr_mut_prob;
+  sa.key = g->key;
+  sa.gen = (uint32_t)gen;
+  if ((st = check_hip(g, launch_select(sa, s), "tournament"))) return st;
+  CopyArgs ca;
+  memset(&ca, 0, sizeof(ca));
+  const size_t u0 = (size_t)c0 * sp;
+  ca.sel = g->sel + u0 * 2;
+  ca.src[0][0] = A.Gp;
+  ca.src[0][1] = A.Gm;
+  ca.src[0][2] = A.Gv;
+  ca.src[1][0] = A.Dp;
+  ca.src[1][1] = A.Dm;
+  ca.src[1][2] = A.Dv;
+  ca.dst[0][0] = Bn.Gp + u0 * g->G.stride;
+  ca.dst[0][1] = Bn.Gm + u0 * g->G.stride;
+  ca.dst[0][2] = Bn.Gv + u0 * g->G.stride;
+  ca.dst[1][0] = Bn.Dp + u0 * g->D.stride;
+  ca.dst[1][1] = Bn.Dm + u0 * g->D.stride;
+  ca.dst[1][2] = Bn.Dv + u0 * g->D.stride;
+  ca.stride[0] = g->G.stride;
+  ca.stride[1] = g->D.stride;
+  ca.w_src = A.w + (size_t)c0 * LIPZ_SLOTS;
+  ca.w_dst = Bn.w + (size_t)c0 * LIPZ_SLOTS;
+  ca.U = nc * sp;
+  ca.C = nc;
+  return check_hip(g, launch_copy_winners(ca, s), "replace");
+}
+
+// Post-training re-evaluation and elitist truncation of cells c0 .. c0 + nc - 1:
+// trained individuals in buffer par, the previous state in 1 - par.
+lipz_status enq_elite(lipz_grid* g, int par, int c0, int nc, const std::vector<int>& phases, hipStream_t s,
+                      int32_t* d_src, float* d_fit2_g, float* d_fit2_d) {
+  lipz_status st;
+  for (int ph : phases)
+    if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "re-evaluation"))) return st;
+  const StateBuf& O = g->st[1 - par];
+  const StateBuf& N = g->st[par];
+  const int sp = g->s;
+  EliteArgs ea;
+  memset(&ea, 0, sizeof(ea));
+  ea.part2 = g->part_e2;
+  ea.part3 = g->part_e3;
+  ea.rmean = g->rmean;
+  ea.L2 = g->el_L2;
+  ea.Lg2 = g->el_Lg2;
+  ea.M3 = g->el_M3;
+  ea.fit_g = g->fit_g;
+  ea.fit_d = g->fit_d;
+  ea.fit2_g = g->fit2_g;
+  ea.fit2_d = g->fit2_d;
+  ea.src = g->esrc;
+  ea.src_out = d_src;
+  ea.fit2_g_out = d_fit2_g;
+  ea.fit2_d_out = d_fit2_d;
+  ea.flags = g->flags;
+  ea.t_old[0] = O.Gt;
+  ea.t_old[1] = O.Dt;
+  ea.lr_old[0] = O.Glr;
+  ea.lr_old[1] = O.Dlr;
+  ea.t_new[0] = N.Gt;
+  ea.t_new[1] = N.Dt;
+  ea.lr_new[0] = N.Glr;
+  ea.lr_new[1] = N.Dlr;
+  ea.tn = g->tn;
+  ea.B = g->B;
+  ea.c0 = c0;
+  ea.C = nc;
+  ea.s = sp;
+  ea.nn = g->nn;
+  ea.mode = g->cfg.fitness_mode;
+  ea.loss_kind = g->cfg.loss_kind;
+  if ((st = check_hip(g, launch_elite(ea, s), "elitist truncation"))) return st;
+  CopyArgs ca;
+  memset(&ca, 0, sizeof(ca));
+  const size_t u0 = (size_t)c0 * sp;
+  ca.sel = g->esrc + u0 * 2;
+  ca.src[0][0] = O.Gp;
+  ca.src[0][1] = O.Gm;
+  ca.src[0][2] = O.Gv;
+  ca.src[1][0] = O.Dp;
+  ca.src[1][1] = O.Dm;
+  ca.src[1][2] = O.Dv;
+  ca.dst[0][0] = N.Gp + u0 * g->G.stride;
+  ca.dst[0][1] = N.Gm + u0 * g->G.stride;
+  ca.dst[0][2] = N.Gv + u0 * g->G.stride;
+  ca.dst[1][0] = N.Dp + u0 * g->D.stride;
+  ca.dst[1][1] = N.Dm + u0 * g->D.stride;
+  ca.dst[1][2] = N.Dv + u0 * g->D.stride;
+  ca.stride[0] = g->G.stride;
+  ca.stride[1] = g->D.stride;
+  ca.U = nc * sp;
+  ca.C = nc;
+  return check_hip(g, launch_copy_winners(ca, s), "elitist copy");
+}
+
+// The training heads of buffer par (all units; a group narrows c0, C).
+void train_heads(lipz_grid* g, int par, HeadArgs* hd, HeadArgs* hg) {
+  const StateBuf& S = g->st[par];
+  const int B = g->B, LD = g->D.nl;
+  memset(hd, 0, sizeof(*hd));
+  hd->part = g->part_tr;
+  hd->tn = g->tn;
+  hd->act = g->a[LD - 2];
+  hd->act_cell_stride = (int64_t)2 * B * g->D.fi[LD - 1];
+  hd->delta = g->dD[LD - 2];
+  hd->w = S.Dp + g->D.off[LD - 1];
+  hd->p_stride = g->D.stride;
+  hd->dlbuf = g->dlbuf;
+  hd->H = g->D.fi[LD - 1];
+  hd->B = B;
+  hd->c0 = 0;
+  hd->C = g->U;
+  hd->hidden_act = g->D.act[LD - 2];
+  hd->slope = g->slope;
+  hd->loss_kind = g->cfg.loss_kind;
+  *hg = *hd;
+  hg->part = g->part_g;
+  hg->act = g->ag[LD - 2];
+  hg->act_cell_stride = (int64_t)B * g->D.fi[LD - 1];
+  hg->delta = g->dDg[LD - 2];
+  hg->dlbuf = nullptr;
+}
+
+// Gradient-trainer step k (training step `step`) of group grp of buffer par.
+lipz_status enq_train_group_step(lipz_grid* g, int gen, int par, int grp, int k, int step, float* d_losses,
+                                 const HeadArgs& hd, const HeadArgs& hg, hipStream_t gs) {
+  const int B = g->B;
+  const int c0 = g->group_c0[grp], nc = g->group_c0[grp + 1] - c0;
+  HeadArgs gd = hd, gg = hg;
+  gd.c0 = gg.c0 = c0;
+  gd.C = gg.C = nc;
+  gd.losses = gg.losses = d_losses ? d_losses + (size_t)k * g->U * 2 : nullptr;
+  lipz_status st;
+  for (const Op& op : g->train_ops[par][grp]) {
+    hipError_t e = hipSuccess;
+    switch (op.kind) {
+      case OP_SAMPLE:
+        e = launch_sample(g->data, g->N, g->xd, g->zd, B, c0, nc, g->key, (uint32_t)gen, (uint32_t)(step + 1),
+                          g->Xtr, (int64_t)2 * B * g->xd, g->z, (int64_t)B * g->zd, gs);
+        break;
+      case OP_GEMM: e = run_gemm_phase(g, op.phase, k, gs); break;
+      case OP_HEAD_D: e = launch_head_d(gd, gs); break;
+      case OP_HEAD_G: e = launch_head_g(gg, gs); break;
+      default: e = hipErrorInvalidValue; break;
+    }
+    if ((st = check_hip(g, e, "train step"))) return st;
+  }
+  return LIPZ_OK;
+}
+
 }  // namespace lipz
 
 extern "C" {
@@ -865,6 +1115,10 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
   for (int i = 1; i < g->n_groups; ++i) {
     ck(hipStreamCreateWithFlags(&g->gstream[i], hipStreamNonBlocking), "create stream");
     ck(hipEventCreateWithFlags(&g->join_ev[i], hipEventDisableTiming), "create event");
+  }
+  for (int b = 0; b < g->n_bands; ++b) {
+    ck(hipEventCreateWithFlags(&g->band_ev[b], hipEventDisableTiming), "create event");
+    ck(hipEventCreateWithFlags(&g->mom_ev[b], hipEventDisableTiming), "create event");
   }
   ck(hipMemcpyAsync(g->nbr, g->nbr_h.data(), g->nbr_h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s),
      "upload neighbours");
@@ -921,6 +1175,10 @@ lipz_status lipz_grid_destroy(lipz_grid* g) {
     if (g->join_ev[i]) hipEventDestroy(g->join_ev[i]);
   }
   if (g->fork_ev) hipEventDestroy(g->fork_ev);
+  for (int b = 0; b < g->n_bands; ++b) {
+    if (g->band_ev[b]) hipEventDestroy(g->band_ev[b]);
+    if (g->mom_ev[b]) hipEventDestroy(g->mom_ev[b]);
+  }
   for (auto& e : g->ev_pool) hipEventDestroy(e);
   for (auto& p : g->ev_live) {
     hipEventDestroy(p.first);
@@ -937,33 +1195,14 @@ lipz_status lipz_eval_neighborhoods(lipz_grid* g, int32_t gen, float* d_L, float
   if (st) return st;
   if (gen < 0 || gen > 65535) return fail(g, LIPZ_E_INVAL, "gen must be in [0, 65535]");
   hipStream_t s = g->stream;
-  const int par = g->cur;
-  const int C = g->C, B = g->B;
-  hipError_t e;
   if (g->dc) {
     if ((st = dc_eval(g, gen))) return st;
-  } else {
-    e = launch_sample(g->data, g->N, g->xd, g->zd, B, 0, C, g->key, (uint32_t)gen, 0, g->Xe,
-                      (int64_t)(1 + g->nn) * B * g->xd, g->ze, (int64_t)B * g->zd, s);
-    if ((st = check_hip(g, e, "eval sample"))) return st;
-    for (int ph : g->eval_phases[par])
-      if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "eval forward"))) return st;
-    EvalHeadArgs ha;
-    memset(&ha, 0, sizeof(ha));
-    ha.part = g->part_e;
-    ha.tn = g->tn;
-    ha.L = g->L;
-    ha.Lg = g->Lg;
-    ha.rmean = g->rmean;
-    ha.B = B;
-    ha.C = C;
-    ha.nn = g->nn;
-    ha.loss_kind = g->cfg.loss_kind;
-    if ((st = check_hip(g, launch_head_eval(ha, s), "eval head"))) return st;
+    hipError_t e = launch_fitness(g->L, g->Lg, g->C, g->nn, g->cfg.fitness_mode, g->fit_g, g->fit_d, g->flags,
+                                  d_L, d_Lg, d_fit_g, d_fit_d, s);
+    if ((st = check_hip(g, e, "fitness"))) return st;
+  } else if ((st = enq_eval(g, gen, 0, g->C, g->eval_phases[g->cur], s, d_L, d_Lg, d_fit_g, d_fit_d))) {
+    return st;
   }
-  e = launch_fitness(g->L, g->Lg, C, g->nn, g->cfg.fitness_mode, g->fit_g, g->fit_d, g->flags, d_L, d_Lg,
-                     d_fit_g, d_fit_d, s);
-  if ((st = check_hip(g, e, "fitness"))) return st;
   g->fitness_valid = true;
   g->elite_state = 1;
   g->elite_gen = gen;
@@ -977,56 +1216,7 @@ lipz_status lipz_select_replace(lipz_grid* g, int32_t gen, const int32_t* d_forc
   if (gen < 0 || gen > 65535) return fail(g, LIPZ_E_INVAL, "gen must be in [0, 65535]");
   if (!d_forced && !g->fitness_valid)
     return fail(g, LIPZ_E_ORDER, "select_replace needs an evaluation of the current state");
-  hipStream_t s = g->stream;
-  const StateBuf& A = g->st[g->cur];
-  const StateBuf& Bn = g->st[1 - g->cur];
-  SelectArgs sa;
-  sa.fit_g = g->fit_g;
-  sa.fit_d = g->fit_d;
-  sa.nbr = g->nbr;
-  sa.forced = d_forced;
-  sa.sel = g->sel;
-  sa.flags = g->flags;
-  sa.sel_out = d_sel;
-  sa.lr_out = d_lr;
-  sa.t_src[0] = A.Gt;
-  sa.t_src[1] = A.Dt;
-  sa.lr_src[0] = A.Glr;
-  sa.lr_src[1] = A.Dlr;
-  sa.t_dst[0] = Bn.Gt;
-  sa.t_dst[1] = Bn.Dt;
-  sa.lr_dst[0] = Bn.Glr;
-  sa.lr_dst[1] = Bn.Dlr;
-  sa.C = g->C;
-  sa.s = g->s;
-  sa.tsize = g->cfg.tournament_size;
-  sa.mutate = g->cfg.lr_mutation;
-  sa.mut_std = g->cfg.lr_mut_std;
-  sa.mut_prob = g->cfg.lr_mut_prob;
-  sa.key = g->key;
-  sa.gen = (uint32_t)gen;
-  if ((st = check_hip(g, launch_select(sa, s), "tournament"))) return st;
-  CopyArgs ca;
-  ca.sel = g->sel;
-  ca.src[0][0] = A.Gp;
-  ca.src[0][1] = A.Gm;
-  ca.src[0][2] = A.Gv;
-  ca.src[1][0] = A.Dp;
-  ca.src[1][1] = A.Dm;
-  ca.src[1][2] = A.Dv;
-  ca.dst[0][0] = Bn.Gp;
-  ca.dst[0][1] = Bn.Gm;
-  ca.dst[0][2] = Bn.Gv;
-  ca.dst[1][0] = Bn.Dp;
-  ca.dst[1][1] = Bn.Dm;
-  ca.dst[1][2] = Bn.Dv;
-  ca.stride[0] = g->G.stride;
-  ca.stride[1] = g->D.stride;
-  ca.w_src = A.w;
-  ca.w_dst = Bn.w;
-  ca.U = g->U;
-  ca.C = g->C;
-  if ((st = check_hip(g, launch_copy_winners(ca, s), "replace"))) return st;
+  if ((st = enq_select(g, gen, g->cur, 0, g->C, d_forced, d_sel, d_lr, g->stream))) return st;
   g->cur = 1 - g->cur;
   g->fitness_valid = false;
   g->elite_state = g->elite_state == 1 ? 2 : 0;
@@ -1039,65 +1229,9 @@ lipz_status lipz_elitist_replace(lipz_grid* g, int32_t gen, int32_t* d_src, floa
   if (!g->cfg.elitism) return fail(g, LIPZ_E_ORDER, "grid created with elitism = 0");
   if (g->elite_state != 2 || gen != g->elite_gen)
     return fail(g, LIPZ_E_ORDER, "elitist_replace needs eval_neighborhoods(gen), select_replace, training");
-  hipStream_t s = g->stream;
-  const int par = g->cur;  // trained individuals; 1 - par: the state selection read
-  for (int ph : g->elite_phases[par])
-    if ((st = check_hip(g, run_gemm_phase(g, ph, 0, s), "re-evaluation"))) return st;
-  const StateBuf& O = g->st[1 - par];
-  const StateBuf& N = g->st[par];
-  EliteArgs ea;
-  memset(&ea, 0, sizeof(ea));
-  ea.part2 = g->part_e2;
-  ea.part3 = g->part_e3;
-  ea.rmean = g->rmean;
-  ea.L2 = g->el_L2;
-  ea.Lg2 = g->el_Lg2;
-  ea.M3 = g->el_M3;
-  ea.fit_g = g->fit_g;
-  ea.fit_d = g->fit_d;
-  ea.fit2_g = g->fit2_g;
-  ea.fit2_d = g->fit2_d;
-  ea.src = g->esrc;
-  ea.src_out = d_src;
-  ea.fit2_g_out = d_fit2_g;
-  ea.fit2_d_out = d_fit2_d;
-  ea.flags = g->flags;
-  ea.t_old[0] = O.Gt;
-  ea.t_old[1] = O.Dt;
-  ea.lr_old[0] = O.Glr;
-  ea.lr_old[1] = O.Dlr;
-  ea.t_new[0] = N.Gt;
-  ea.t_new[1] = N.Dt;
-  ea.lr_new[0] = N.Glr;
-  ea.lr_new[1] = N.Dlr;
-  ea.tn = g->tn;
-  ea.B = g->B;
-  ea.C = g->C;
-  ea.s = g->s;
-  ea.nn = g->nn;
-  ea.mode = g->cfg.fitness_mode;
-  ea.loss_kind = g->cfg.loss_kind;
-  if ((st = check_hip(g, launch_elite(ea, s), "elitist truncation"))) return st;
-  CopyArgs ca;
-  memset(&ca, 0, sizeof(ca));
-  ca.sel = g->esrc;
-  ca.src[0][0] = O.Gp;
-  ca.src[0][1] = O.Gm;
-  ca.src[0][2] = O.Gv;
-  ca.src[1][0] = O.Dp;
-  ca.src[1][1] = O.Dm;
-  ca.src[1][2] = O.Dv;
-  ca.dst[0][0] = N.Gp;
-  ca.dst[0][1] = N.Gm;
-  ca.dst[0][2] = N.Gv;
-  ca.dst[1][0] = N.Dp;
-  ca.dst[1][1] = N.Dm;
-  ca.dst[1][2] = N.Dv;
-  ca.stride[0] = g->G.stride;
-  ca.stride[1] = g->D.stride;
-  ca.U = g->U;
-  ca.C = g->C;
-  if ((st = check_hip(g, launch_copy_winners(ca, s), "elitist copy"))) return st;
+  // the current buffer holds the trained individuals; the other one the state selection read
+  if ((st = enq_elite(g, g->cur, 0, g->C, g->elite_phases[g->cur], g->stream, d_src, d_fit2_g, d_fit2_d)))
+    return st;
   g->elite_state = 0;
   g->fitness_valid = false;
   return LIPZ_OK;
@@ -1123,30 +1257,9 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   }
   const int par = g->cur;
   const StateBuf& S = g->st[par];
-  const int C = g->U, B = g->B, LD = g->D.nl;  // C: training units
-  HeadArgs hd;
-  memset(&hd, 0, sizeof(hd));
-  hd.part = g->part_tr;
-  hd.tn = g->tn;
-  hd.act = g->a[LD - 2];
-  hd.act_cell_stride = (int64_t)2 * B * g->D.fi[LD - 1];
-  hd.delta = g->dD[LD - 2];
-  hd.w = S.Dp + g->D.off[LD - 1];
-  hd.p_stride = g->D.stride;
-  hd.dlbuf = g->dlbuf;
-  hd.H = g->D.fi[LD - 1];
-  hd.B = B;
-  hd.c0 = 0;
-  hd.C = C;
-  hd.hidden_act = g->D.act[LD - 2];
-  hd.slope = g->slope;
-  hd.loss_kind = g->cfg.loss_kind;
-  HeadArgs hg = hd;
-  hg.part = g->part_g;
-  hg.act = g->ag[LD - 2];
-  hg.act_cell_stride = (int64_t)B * g->D.fi[LD - 1];
-  hg.delta = g->dDg[LD - 2];
-  hg.dlbuf = nullptr;
+  const int C = g->U, B = g->B;  // C: training units
+  HeadArgs hd, hg;
+  train_heads(g, par, &hd, &hg);
   if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
     const bool es = g->cfg.trainer == LIPZ_TRAINER_ES;
     NesArgs na[2];
@@ -1214,31 +1327,9 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
       if ((st = check_hip(g, hipStreamWaitEvent(g->gstream[i], g->fork_ev, 0), "fork"))) return st;
   }
   // enqueue step by step across the groups so every stream has work early
-  for (int k = 0; k < n_steps; ++k) {
-    const int step = step0 + k;
-    for (int grp = 0; grp < g->n_groups; ++grp) {
-      const int c0 = g->group_c0[grp], nc = g->group_c0[grp + 1] - c0;
-      hipStream_t gs = g->gstream[grp];
-      HeadArgs gd = hd, gg = hg;
-      gd.c0 = gg.c0 = c0;
-      gd.C = gg.C = nc;
-      gd.losses = gg.losses = d_losses ? d_losses + (size_t)k * C * 2 : nullptr;
-      for (const Op& op : g->train_ops[par][grp]) {
-        hipError_t e = hipSuccess;
-        switch (op.kind) {
-          case OP_SAMPLE:
-            e = launch_sample(g->data, g->N, g->xd, g->zd, B, c0, nc, g->key, (uint32_t)gen,
-                              (uint32_t)(step + 1), g->Xtr, (int64_t)2 * B * g->xd, g->z,
-                              (int64_t)B * g->zd, gs);
-            break;
-          case OP_GEMM: e = run_gemm_phase(g, op.phase, k, gs); break;
-          case OP_HEAD_D: e = launch_head_d(gd, gs); break;
-          case OP_HEAD_G: e = launch_head_g(gg, gs); break;
-        }
-        if ((st = check_hip(g, e, "train step"))) return st;
-      }
-    }
-  }
+  for (int k = 0; k < n_steps; ++k)
+    for (int grp = 0; grp < g->n_groups; ++grp)
+      if ((st = enq_train_group_step(g, gen, par, grp, k, step0 + k, d_losses, hd, hg, g->gstream[grp]))) return st;
   // join: the caller's stream waits for every group
   for (int i = 1; i < g->n_groups; ++i) {
     if ((st = check_hip(g, hipEventRecord(g->join_ev[i], g->gstream[i]), "join"))) return st;
@@ -1248,6 +1339,113 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   if (e == hipSuccess) e = launch_add_i32(S.Dt, C, n_steps, s);
   if ((st = check_hip(g, e, "step count"))) return st;
   g->fitness_valid = false;
+  return LIPZ_OK;
+}
+
+lipz_status lipz_run_generations(lipz_grid* g, int32_t gen0, int32_t n_gens, int32_t n_steps) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (gen0 < 0 || n_gens < 0 || (int64_t)gen0 + n_gens > 65536)
+    return fail(g, LIPZ_E_INVAL, "generations must lie in [0, 65535]");
+  if (n_steps < 0 || n_steps > 65535) return fail(g, LIPZ_E_INVAL, "n_steps must be in [0, 65535]");
+  if (g->n_bands < 2) {  // one batch: the entry points in order
+    for (int i = 0; i < n_gens; ++i) {
+      const int gen = gen0 + i;
+      if ((st = lipz_eval_neighborhoods(g, gen, nullptr, nullptr, nullptr, nullptr))) return st;
+      if ((st = lipz_select_replace(g, gen, nullptr, nullptr, nullptr))) return st;
+      if ((st = lipz_train_step(g, gen, 0, n_steps, nullptr))) return st;
+      if (g->cfg.elitism && (st = lipz_elitist_replace(g, gen, nullptr, nullptr, nullptr))) return st;
+      if (g->cfg.mix_enable && (st = lipz_mixture_update(g, gen, nullptr, nullptr, nullptr))) return st;
+    }
+    return LIPZ_OK;
+  }
+  const int nb = g->n_bands, sp = g->s;
+  hipStream_t s = g->stream;
+  // fork: every band waits for the work already on the caller's stream
+  if ((st = check_hip(g, hipEventRecord(g->fork_ev, s), "fork"))) return st;
+  for (int b = 1; b < nb; ++b)
+    if ((st = check_hip(g, hipStreamWaitEvent(g->gstream[b], g->fork_ev, 0), "fork"))) return st;
+  for (int i = 0; i < n_gens; ++i) {
+    const int gen = gen0 + i, par = g->cur;
+    HeadArgs hd, hg;
+    train_heads(g, 1 - par, &hd, &hg);
+    // each band: wait for its neighbour bands' previous generation, then
+    // evaluate and select its cells
+    for (int b = 0; b < nb; ++b) {
+      hipStream_t bs = g->gstream[b];
+      if (i > 0)
+        for (int b2 = 0; b2 < nb; ++b2)
+          if (b2 != b && (g->band_wait[b] >> b2 & 1u))
+            if ((st = check_hip(g, hipStreamWaitEvent(bs, g->band_ev[b2], 0), "band wait"))) return st;
+      const int c0 = g->band_c0[b], nc = g->band_c0[b + 1] - c0;
+      if ((st = enq_eval(g, gen, c0, nc, g->band_eval_phases[par][b], bs, nullptr, nullptr, nullptr, nullptr)))
+        return st;
+      if ((st = enq_select(g, gen, par, c0, nc, nullptr, nullptr, nullptr, bs))) return st;
+    }
+    // training, step by step across the bands so every stream has work early
+    for (int k = 0; k < n_steps; ++k)
+      for (int b = 0; b < nb; ++b)
+        if ((st = enq_train_group_step(g, gen, 1 - par, b, k, k, nullptr, hd, hg, g->gstream[b]))) return st;
+    for (int b = 0; b < nb; ++b) {
+      hipStream_t bs = g->gstream[b];
+      const int c0 = g->band_c0[b], nc = g->band_c0[b + 1] - c0;
+      const StateBuf& N = g->st[1 - par];
+      if (n_steps > 0) {
+        hipError_t e = launch_add_i32(N.Gt + (size_t)c0 * sp, nc * sp, n_steps, bs);
+        if (e == hipSuccess) e = launch_add_i32(N.Dt + (size_t)c0 * sp, nc * sp, n_steps, bs);
+        if ((st = check_hip(g, e, "step count"))) return st;
+      }
+      if (g->cfg.elitism &&
+          (st = enq_elite(g, 1 - par, c0, nc, g->band_elite_phases[1 - par][b], bs, nullptr, nullptr, nullptr)))
+        return st;
+      if (g->cfg.mix_enable) {  // the band's generators' feature moments
+        float* zeta = g->zeta + (size_t)b * g->S * g->zd;
+        hipError_t e = launch_normals(zeta, (int64_t)g->S * g->zd, 1.0, g->key, 0, (uint32_t)gen, 0, LIPZ_TAG_MIXZ, bs);
+        if ((st = check_hip(g, e, "mixture latents"))) return st;
+        for (int ph : g->band_mix_phases[1 - par][b])
+          if ((st = check_hip(g, run_gemm_phase(g, ph, 0, bs), "mixture forward"))) return st;
+        const int nch = (g->S + 63) / 64;
+        e = launch_moments(g->fm + (size_t)c0 * g->S * g->F, nc, g->S, g->F,
+                           g->mom_part + (size_t)c0 * nch * 2 * g->F, g->mu_k + (size_t)c0 * g->F,
+                           g->s2_k + (size_t)c0 * g->F, bs);
+        if ((st = check_hip(g, e, "mixture moments"))) return st;
+        if ((st = check_hip(g, hipEventRecord(g->mom_ev[b], bs), "moments ready"))) return st;
+      } else if ((st = check_hip(g, hipEventRecord(g->band_ev[b], bs), "band ready"))) {
+        return st;
+      }
+    }
+    if (g->cfg.mix_enable) {
+      // the ES step of a cell scores the moments of its neighbours' generators
+      for (int b = 0; b < nb; ++b) {
+        hipStream_t bs = g->gstream[b];
+        for (int b2 = 0; b2 < nb; ++b2)
+          if (b2 != b && (g->band_wait[b] >> b2 & 1u))
+            if ((st = check_hip(g, hipStreamWaitEvent(bs, g->mom_ev[b2], 0), "moments wait"))) return st;
+        EsArgs ea;
+        memset(&ea, 0, sizeof(ea));
+        ea.mu = g->mu_k;
+        ea.s2 = g->s2_k;
+        ea.mu_r = g->mu_r;
+        ea.sd_r = g->sd_r;
+        ea.nbr = g->nbr;
+        ea.w = g->st[1 - par].w;
+        ea.c0 = g->band_c0[b];
+        ea.C = g->band_c0[b + 1] - g->band_c0[b];
+        ea.F = g->F;
+        ea.sigma = g->cfg.mix_sigma;
+        ea.key = g->key;
+        ea.gen = (uint32_t)gen;
+        if ((st = check_hip(g, launch_es(ea, bs), "mixture ES"))) return st;
+        if ((st = check_hip(g, hipEventRecord(g->band_ev[b], bs), "band ready"))) return st;
+      }
+    }
+    g->cur = 1 - par;
+  }
+  // join: the caller's stream waits for every band
+  for (int b = 1; b < nb; ++b)
+    if ((st = check_hip(g, hipStreamWaitEvent(s, g->band_ev[b], 0), "join"))) return st;
+  g->fitness_valid = false;
+  g->elite_state = 0;
   return LIPZ_OK;
 }
 
@@ -1276,6 +1474,7 @@ lipz_status lipz_mixture_update(lipz_grid* g, int32_t gen, float* d_w, float* d_
   ea.w_out = d_w;
   ea.score_out = d_score;
   ea.acc_out = d_accepted;
+  ea.c0 = 0;
   ea.C = g->C;
   ea.F = g->F;
   ea.sigma = g->cfg.mix_sigma;

@@ -11,7 +11,7 @@
 namespace lipz {
 
 constexpr size_t kAlign = 256;
-#define LIPZ_MAX_GROUPS 4
+#define LIPZ_MAX_GROUPS 8
 #ifndef LIPZ_CELL_GROUPS
 #define LIPZ_CELL_GROUPS 0  // 0: choose from the grid size
 #endif
@@ -132,6 +132,17 @@ struct lipz_grid {
   hipStream_t gstream[LIPZ_MAX_GROUPS] = {};
   hipEvent_t fork_ev = nullptr, join_ev[LIPZ_MAX_GROUPS] = {};
   std::vector<Op> train_ops[2][LIPZ_MAX_GROUPS];
+  // Row bands of lipz_run_generations (config bands >= 2): band b holds cells
+  // band_c0[b] .. band_c0[b + 1] - 1 (whole rows); the training groups are
+  // the bands' individuals, and each band has its own evaluation and
+  // re-evaluation plans and a readiness event
+  int n_bands = 0;
+  int band_c0[LIPZ_MAX_GROUPS + 1] = {};
+  uint32_t band_wait[LIPZ_MAX_GROUPS] = {};  // bit b': band b' holds a neighbour row of the band
+  std::vector<int> band_eval_phases[2][LIPZ_MAX_GROUPS], band_elite_phases[2][LIPZ_MAX_GROUPS];
+  std::vector<int> band_mix_phases[2][LIPZ_MAX_GROUPS];  // on the band's own copy of the mixture latents
+  hipEvent_t band_ev[LIPZ_MAX_GROUPS] = {};   // the band finished its generation
+  hipEvent_t mom_ev[LIPZ_MAX_GROUPS] = {};    // the band's generator moments of the generation are ready
   std::vector<int> eval_phases[2], mix_phases[2];
   int real_phase = -1;
 

@@ -386,13 +386,13 @@ __device__ __forceinline__ float fit_key(float f) { return f != f ? INFINITY : f
 // 4 i .. 4 i + 3 (block i) of the mutation stream.
 __global__ void select_kernel(SelectArgs A) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  const int U = A.C * A.s, nn = LIPZ_SLOTS * A.s;
-  if (t >= 2 * U) return;
-  const int u = t >> 1, role = t & 1, c = u / A.s, i = u % A.s;
+  const int nn = LIPZ_SLOTS * A.s;
+  if (t >= 2 * A.C * A.s) return;
+  const int u = A.c0 * A.s + (t >> 1), role = t & 1, c = u / A.s, i = u % A.s;
   int src;
   if (A.forced) {
     src = A.forced[u * 2 + role];
-    if (src < 0 || src >= U) {
+    if (src < 0 || src >= A.U) {
       atomicOr(A.flags, 2);
       src = u;
     }
@@ -434,7 +434,7 @@ __global__ void select_kernel(SelectArgs A) {
 // means of one block of B rows of partial logits, one wave per mean (see
 // head_eval_kernel): q < nq means, mean q over rows [row0(q), row0(q) + B)
 __global__ __launch_bounds__(NT) void elite_means_kernel(EliteArgs A) {
-  const int c = blockIdx.y, nn = A.nn, s = A.s;
+  const int c = A.c0 + blockIdx.y, nn = A.nn, s = A.s;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const bool prev = (int)blockIdx.x < nn;
   const int j = prev ? blockIdx.x : blockIdx.x - nn;
@@ -471,7 +471,7 @@ __global__ __launch_bounds__(NT) void elite_means_kernel(EliteArgs A) {
 __global__ void elite_merge_kernel(EliteArgs A) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= 2 * A.C) return;
-  const int c = t >> 1, role = t & 1, s = A.s, nn = A.nn;
+  const int c = A.c0 + (t >> 1), role = t & 1, s = A.s, nn = A.nn;
   float fo[4], fn[4];
   bool bad = false;
   for (int i = 0; i < s; ++i) {
@@ -633,8 +633,8 @@ __device__ float mixture_score(const float* w, const int32_t* ks, const float* m
 
 // (1+1)-ES on the mixture weights of cell i.
 __global__ void es_kernel(EsArgs A) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= A.C) return;
+  const int c = A.c0 + blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= A.c0 + A.C) return;
   const int32_t* ks = A.nbr + c * 5;
   float w[5], wp[5];
   for (int k = 0; k < 5; ++k) w[k] = A.w[c * 5 + k];

@@ -473,7 +473,7 @@ struct SelectArgs {
   const float* lr_src[2];
   int32_t* t_dst[2];       // next buffer
   float* lr_dst[2];
-  int C, s, tsize, mutate;  // cells, individuals per role and cell
+  int c0, C, s, U, tsize, mutate;  // cells c0 .. c0 + C - 1; individuals per role and cell; all individuals
   float mut_std, mut_prob;
   uint2 key;
   uint32_t gen;
@@ -511,7 +511,7 @@ struct EliteArgs {
   const float* lr_old[2];
   int32_t* t_new[2];
   float* lr_new[2];
-  int tn, B, C, s, nn, mode, loss_kind;
+  int tn, B, c0, C, s, nn, mode, loss_kind;  // cells c0 .. c0 + C - 1
 };
 hipError_t launch_elite(const EliteArgs& a, hipStream_t s);
 
@@ -541,7 +541,7 @@ struct EsArgs {
   float* w_out;
   float* score_out;
   int32_t* acc_out;
-  int C, F;
+  int c0, C, F;            // cells c0 .. c0 + C - 1
   float sigma;
   uint2 key;
   uint32_t gen;

@@ -43,7 +43,7 @@ class lipz_config(ctypes.Structure):
         ("seed", _u64),
         ("loss_kind", _i32), ("wgan_clip", _f32),
         ("trainer", _i32), ("nes_pairs", _i32), ("nes_sigma", _f32),
-        ("pop_size", _i32), ("elitism", _i32),
+        ("pop_size", _i32), ("elitism", _i32), ("bands", _i32),
     ]
 
 
@@ -86,6 +86,7 @@ def config_from_dict(d):
     c.nes_sigma = d.get("nes_sigma", 0.01)
     c.pop_size = d.get("pop_size", 1)
     c.elitism = d.get("elitism", 0)
+    c.bands = d.get("bands", 0)
     return c
 
 
@@ -98,6 +99,7 @@ _SIGS = {
     "lipz_select_replace": (_i32, [_vp, _i32, _vp, _vp, _vp]),
     "lipz_train_step": (_i32, [_vp, _i32, _i32, _i32, _vp]),
     "lipz_elitist_replace": (_i32, [_vp, _i32, _vp, _vp, _vp]),
+    "lipz_run_generations": (_i32, [_vp, _i32, _i32, _i32]),
     "lipz_mixture_update": (_i32, [_vp, _i32, _vp, _vp, _vp]),
     "lipz_get_neighbors": (_i32, [_vp, ctypes.POINTER(_i32)]),
     "lipz_param_layout": (_i32, [_vp, _i32, ctypes.POINTER(_i64), ctypes.POINTER(_i32)]),
@@ -194,6 +196,10 @@ def lipz_train_step(g, gen, step0, n_steps, d_losses=None):
 def lipz_elitist_replace(g, gen, d_src=None, d_fit2_g=None, d_fit2_d=None):
     return _check(load_library().lipz_elitist_replace(_p(g), gen, _p(d_src), _p(d_fit2_g), _p(d_fit2_d)),
                   "lipz_elitist_replace", g)
+
+
+def lipz_run_generations(g, gen0, n_gens, n_steps):
+    return _check(load_library().lipz_run_generations(_p(g), gen0, n_gens, n_steps), "lipz_run_generations", g)
 
 
 def lipz_mixture_update(g, gen, d_w=None, d_score=None, d_accepted=None):

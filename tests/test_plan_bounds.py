@@ -79,6 +79,18 @@ def test_subpopulation_plans_stay_in_bounds(i, trainer):
     assert n_bad == 0, msg
 
 
+@pytest.mark.parametrize("over", [dict(rows=8, cols=3, bands=4), dict(rows=7, cols=2, bands=3, pop_size=2, elitism=1),
+                                  dict(rows=5, cols=3, bands=5), dict(rows=8, cols=8, bands=8),
+                                  dict(rows=4, cols=4, bands=2, mix_enable=1, mix_samples=200)])
+def test_band_plans_stay_in_bounds(over):
+    wl = synth.small_workload("mnist_mlp_3x3", z_dim=7, x_dim=37, g_hidden=[33, 70], d_hidden=[45, 19], batch=19,
+                              **over)
+    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
+    assert n_bad == 0, msg
+    for bad in (dict(wl, bands=wl["rows"] + 1), dict(wl, bands=9), dict(wl, trainer="nes")):
+        assert L.lipz_workspace_bytes(L.config_from_dict(bad), wl["data"]["n"]) == 0
+
+
 def test_invalid_dcgan_shapes_are_rejected():
     wl = synth.small_workload("celeba_dcgan_4x4", img=(48, 48, 3), x_dim=48 * 48 * 3)
     assert L.lipz_workspace_bytes(L.config_from_dict(wl), 100) == 0
