@@ -362,7 +362,10 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
     const int tpp = ceil_div(p.M, ph.tile_rows) * p.tiles_n;
     if (tpp != prev_tpp) {
       // a new group; the problem lists built here have at most 2 shapes per phase
-      if (ph.grp.n == GEMM_MAX_GROUPS) abort();
+      if (ph.grp.n == GEMM_MAX_GROUPS) {  // a plan this library builds never gets here
+        g->plan_ok = false;
+        break;
+      }
       ph.grp.first_tile[ph.grp.n] = tiles;
       ph.grp.first_prob[ph.grp.n] = (int)k;
       ph.grp.tiles_per_prob[ph.grp.n] = tpp;
@@ -855,6 +858,11 @@ lipz_grid* plan_grid(const lipz_config* cfg, int64_t n_samples, char* base, cons
   if (g->dc) dc_build(g);
   else build_tables(g);
   carve(g, base, total);
+  if (!g->plan_ok || (g->dc && !dc_plan_ok(g->dc))) {
+    dc_delete(g->dc);
+    delete g;
+    return nullptr;
+  }
   return g;
 }
 

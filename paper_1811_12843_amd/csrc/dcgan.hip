@@ -402,6 +402,7 @@ double conv_bytes(const ConvProb& p) {
 
 struct DcPlan {
   DcNet G, D;
+  bool plan_ok = true;  // false if a phase exceeded the launch descriptor's shape groups
   int n = 0, img_log = 0, ic = 0;
   // training (per cell)
   float *z = nullptr, *Xtr = nullptr, *gdimg = nullptr;
@@ -521,6 +522,8 @@ DcPlan* dc_new(const lipz_config* c) {
   return p;
 }
 
+bool dc_plan_ok(const DcPlan* p) { return p->plan_ok; }
+
 void dc_delete(DcPlan* p) { delete p; }
 
 void dc_carve(lipz_grid* g, Carver& cv) {
@@ -614,7 +617,10 @@ int add_conv_phase(DcPlan& P, const std::vector<ConvProb>& ps) {
     if (p.mode != CONV_WG) p.splits = 1;
     const int tpp = p.tiles_m * p.tiles_n * p.splits;
     if (tpp != prev) {
-      if (ph.grp.n == GEMM_MAX_GROUPS) abort();
+      if (ph.grp.n == GEMM_MAX_GROUPS) {  // a plan this library builds never gets here
+        P.plan_ok = false;
+        break;
+      }
       if (ph.grp.n > 0) blocks += round8(ph.grp.real_tiles[ph.grp.n - 1]);
       ph.grp.first_block[ph.grp.n] = blocks;
       ph.grp.first_prob[ph.grp.n] = (int)k;

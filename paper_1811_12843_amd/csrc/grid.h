@@ -158,6 +158,7 @@ struct lipz_grid {
   int elite_state = 0;  // 1: evaluated; 2: selected after that evaluation (training allowed)
   int32_t elite_gen = -1;
 
+  bool plan_ok = true;  // false if a phase exceeded the launch descriptor's shape groups
   bool fitness_valid = false;
   lipz_status sticky = LIPZ_OK;
   std::string last_err;
@@ -204,6 +205,7 @@ DcPlan* dc_new(const lipz_config* c);
 void dc_delete(DcPlan* p);
 void dc_carve(lipz_grid* g, Carver& cv);
 void dc_build(lipz_grid* g);
+bool dc_plan_ok(const DcPlan* p);
 void dc_carve_tables(lipz_grid* g, Carver& cv);
 hipError_t dc_upload_tables(lipz_grid* g, hipStream_t s);
 hipError_t dc_init_params(lipz_grid* g, const StateBuf& S, hipStream_t s);
