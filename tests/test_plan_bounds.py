@@ -91,6 +91,18 @@ def test_band_plans_stay_in_bounds(over):
         assert L.lipz_workspace_bytes(L.config_from_dict(bad), wl["data"]["n"]) == 0
 
 
+@pytest.mark.parametrize("over", [
+    dict(rows=1, cols=1, z_dim=1, x_dim=1, g_hidden=[1], d_hidden=[1], batch=1, data=dict(n=64)),
+    dict(rows=2, cols=2, z_dim=5, x_dim=29, g_hidden=[17, 9, 33, 70], d_hidden=[45, 3, 19, 66], batch=13),
+    dict(rows=1, cols=2, z_dim=6, x_dim=40, g_hidden=[24], d_hidden=[20], batch=2048, data=dict(n=5000)),
+])
+def test_edge_plans_stay_in_bounds(over):
+    """One-wide networks and a batch of one, four hidden layers, the largest batch."""
+    wl = synth.small_workload("mnist_mlp_3x3", **over)
+    n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
+    assert n_bad == 0, msg
+
+
 def test_invalid_dcgan_shapes_are_rejected():
     wl = synth.small_workload("celeba_dcgan_4x4", img=(48, 48, 3), x_dim=48 * 48 * 3)
     assert L.lipz_workspace_bytes(L.config_from_dict(wl), 100) == 0
