@@ -1350,29 +1350,11 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   return LIPZ_OK;
 }
 
-lipz_status lipz_run_generations(lipz_grid* g, int32_t gen0, int32_t n_gens, int32_t n_steps) {
-  lipz_status st = pre_call(g);
-  if (st) return st;
-  if (gen0 < 0 || n_gens < 0 || (int64_t)gen0 + n_gens > 65536)
-    return fail(g, LIPZ_E_INVAL, "generations must lie in [0, 65535]");
-  if (n_steps < 0 || n_steps > 65535) return fail(g, LIPZ_E_INVAL, "n_steps must be in [0, 65535]");
-  if (g->n_bands < 2) {  // one batch: the entry points in order
-    for (int i = 0; i < n_gens; ++i) {
-      const int gen = gen0 + i;
-      if ((st = lipz_eval_neighborhoods(g, gen, nullptr, nullptr, nullptr, nullptr))) return st;
-      if ((st = lipz_select_replace(g, gen, nullptr, nullptr, nullptr))) return st;
-      if ((st = lipz_train_step(g, gen, 0, n_steps, nullptr))) return st;
-      if (g->cfg.elitism && (st = lipz_elitist_replace(g, gen, nullptr, nullptr, nullptr))) return st;
-      if (g->cfg.mix_enable && (st = lipz_mixture_update(g, gen, nullptr, nullptr, nullptr))) return st;
-    }
-    return LIPZ_OK;
-  }
+// The generations of lipz_run_generations on the row bands' streams (the
+// caller forks before and joins after, also when this stops on an error).
+static lipz_status enq_band_generations(lipz_grid* g, int gen0, int n_gens, int n_steps) {
   const int nb = g->n_bands, sp = g->s;
-  hipStream_t s = g->stream;
-  // fork: every band waits for the work already on the caller's stream
-  if ((st = check_hip(g, hipEventRecord(g->fork_ev, s), "fork"))) return st;
-  for (int b = 1; b < nb; ++b)
-    if ((st = check_hip(g, hipStreamWaitEvent(g->gstream[b], g->fork_ev, 0), "fork"))) return st;
+  lipz_status st;
   for (int i = 0; i < n_gens; ++i) {
     const int gen = gen0 + i, par = g->cur;
     HeadArgs hd, hg;
@@ -1449,12 +1431,42 @@ lipz_status lipz_run_generations(lipz_grid* g, int32_t gen0, int32_t n_gens, int
     }
     g->cur = 1 - par;
   }
-  // join: the caller's stream waits for every band
+  return LIPZ_OK;
+}
+
+lipz_status lipz_run_generations(lipz_grid* g, int32_t gen0, int32_t n_gens, int32_t n_steps) {
+  lipz_status st = pre_call(g);
+  if (st) return st;
+  if (gen0 < 0 || n_gens < 0 || (int64_t)gen0 + n_gens > 65536)
+    return fail(g, LIPZ_E_INVAL, "generations must lie in [0, 65535]");
+  if (n_steps < 0 || n_steps > 65535) return fail(g, LIPZ_E_INVAL, "n_steps must be in [0, 65535]");
+  if (g->n_bands < 2) {  // one batch: the entry points in order
+    for (int i = 0; i < n_gens; ++i) {
+      const int gen = gen0 + i;
+      if ((st = lipz_eval_neighborhoods(g, gen, nullptr, nullptr, nullptr, nullptr))) return st;
+      if ((st = lipz_select_replace(g, gen, nullptr, nullptr, nullptr))) return st;
+      if ((st = lipz_train_step(g, gen, 0, n_steps, nullptr))) return st;
+      if (g->cfg.elitism && (st = lipz_elitist_replace(g, gen, nullptr, nullptr, nullptr))) return st;
+      if (g->cfg.mix_enable && (st = lipz_mixture_update(g, gen, nullptr, nullptr, nullptr))) return st;
+    }
+    return LIPZ_OK;
+  }
+  const int nb = g->n_bands;
+  hipStream_t s = g->stream;
+  // fork: every band waits for the work already on the caller's stream
+  if ((st = check_hip(g, hipEventRecord(g->fork_ev, s), "fork"))) return st;
   for (int b = 1; b < nb; ++b)
-    if ((st = check_hip(g, hipStreamWaitEvent(s, g->band_ev[b], 0), "join"))) return st;
+    if ((st = check_hip(g, hipStreamWaitEvent(g->gstream[b], g->fork_ev, 0), "fork"))) return st;
+  st = enq_band_generations(g, gen0, n_gens, n_steps);
+  // join: the caller's stream waits for everything enqueued on the bands
+  for (int b = 1; b < nb; ++b) {
+    lipz_status sj = check_hip(g, hipEventRecord(g->join_ev[b], g->gstream[b]), "join");
+    if (!sj) sj = check_hip(g, hipStreamWaitEvent(s, g->join_ev[b], 0), "join");
+    if (!st) st = sj;
+  }
   g->fitness_valid = false;
   g->elite_state = 0;
-  return LIPZ_OK;
+  return st;
 }
 
 lipz_status lipz_mixture_update(lipz_grid* g, int32_t gen, float* d_w, float* d_score,
