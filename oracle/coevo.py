@@ -139,8 +139,6 @@ class Setup:
         self.loss = wl.get("loss", "bce")
         if self.loss not in ("bce", "wasserstein"):
             raise ValueError(f"unknown loss {self.loss!r}")
-        if self.loss == "wasserstein" and wl["net"] != "mlp":
-            raise ValueError("the Wasserstein trainer is defined for the MLP workloads")
         self.clip = float(wl.get("wgan_clip", 0.01))
         self.trainer = wl.get("trainer", "gradient")
         if self.trainer not in ("gradient", "nes", "es"):

@@ -39,6 +39,9 @@ WORKLOADS = {
     "dc32_3x3": lambda: _wl(rows=3, cols=3, img=(32, 32, 3), x_dim=3072, z_dim=12, g_hidden=[64, 32, 16],
                             d_hidden=[16, 32, 64], batch=6, lr0_g=2e-3, lr0_d=2e-3,
                             data=dict(n=512, h=32, w=32)),
+    # generators ranked by their own non-saturating loss (fitness_mode 1)
+    "dc16_2x2_fm1": lambda: _wl(rows=2, cols=2, img=(16, 16, 3), x_dim=768, z_dim=8, g_hidden=[32, 16],
+                                d_hidden=[16, 32], batch=5, fitness_mode=1, data=dict(n=512, h=16, w=16)),
 }
 _CACHE = {}
 

@@ -231,9 +231,13 @@ def test_bce_closed_form_at_half():
     assert np.allclose(Lg, math.log(2), rtol=0, atol=1e-15)
 
 
-def test_one_by_one_grid_is_plain_gan_training():
-    """On a 1x1 torus a generation is textbook alternating GAN training."""
-    wl = _small_wl(rows=1, cols=1, lr_mutation=0, steps=3, lr0_g=2e-3, lr0_d=2e-3)
+@pytest.mark.parametrize("loss", ["bce", "wasserstein"])
+def test_one_by_one_grid_is_plain_gan_training(loss):
+    """On a 1x1 torus a generation is textbook alternating GAN training (for
+    the Wasserstein trainer: critic loss mean D(fake) - mean D(real), the
+    critic clamped after its step, generator loss -mean D(fake))."""
+    wl = _small_wl(rows=1, cols=1, lr_mutation=0, steps=3, lr0_g=2e-3, lr0_d=2e-3, loss=loss, wgan_clip=0.05)
+    wgan = loss == "wasserstein"
     data = synth.make_dataset(wl["data"])
     S = coevo.Setup(wl, len(data))
     st = coevo.create(S)
@@ -252,12 +256,15 @@ def test_one_by_one_grid_is_plain_gan_training():
         xf = _torch_net(S.Gnet.arch, Gp, z, slope)
         ar = _torch_net(S.Dnet.arch, Dp, x, slope)
         af = _torch_net(S.Dnet.arch, Dp, xf.detach(), slope)
-        ld = bce(ar, torch.ones_like(ar)) + bce(af, torch.zeros_like(af))
+        ld = af.mean() - ar.mean() if wgan else bce(ar, torch.ones_like(ar)) + bce(af, torch.zeros_like(af))
         od.zero_grad()
         ld.backward()
         od.step()
+        if wgan:
+            with torch.no_grad():
+                Dp.clamp_(-0.05, 0.05)
         af2 = _torch_net(S.Dnet.arch, Dp, xf, slope)
-        lg = bce(af2, torch.ones_like(af2))
+        lg = -af2.mean() if wgan else bce(af2, torch.ones_like(af2))
         og.zero_grad()
         lg.backward()
         og.step()
@@ -265,3 +272,18 @@ def test_one_by_one_grid_is_plain_gan_training():
         assert np.isclose(rec["losses"][s, 0, 1], lg.item(), rtol=1e-10)
     assert np.allclose(new.Gp[0], Gp.detach().numpy(), rtol=1e-9, atol=1e-12)
     assert np.allclose(new.Dp[0], Dp.detach().numpy(), rtol=1e-9, atol=1e-12)
+
+
+def test_wasserstein_constant_critic_closed_form():
+    """A critic whose weights are all zero outputs its output bias b for every
+    image: the critic loss is exactly 0 and the generator loss exactly -b."""
+    wl = _small_wl(loss="wasserstein")
+    data = synth.make_dataset(wl["data"])
+    S = coevo.Setup(wl, len(data))
+    st = coevo.create(S)
+    last = S.Dnet.arch.layers[-1]
+    st.Dp[...] = 0.0
+    st.Dp[:, last["off_b"]] = 0.37
+    L, Lg, fg, fd = coevo.evaluate(S, st, data, 0)
+    assert np.all(L == 0.0) and np.all(Lg == -0.37)
+    assert np.all(fd == 0.0)
