@@ -62,10 +62,8 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
     if (c->nes_pairs < 1 || c->nes_pairs > 64) return "nes_pairs must be in [1, 64]";
     if (!(c->nes_sigma > 0.f && c->nes_sigma < 1e30f)) return "nes_sigma must be a positive finite scale";
   }
-  if (c->loss_kind == LIPZ_LOSS_WASSERSTEIN) {
-    if (c->net != LIPZ_NET_MLP) return "the Wasserstein trainer is implemented for the MLP networks";
-    if (!(c->wgan_clip > 0.f && c->wgan_clip < 1e30f)) return "wgan_clip must be a positive finite bound";
-  }
+  if (c->loss_kind == LIPZ_LOSS_WASSERSTEIN && !(c->wgan_clip > 0.f && c->wgan_clip < 1e30f))
+    return "wgan_clip must be a positive finite bound";
   if (!(c->beta1 >= 0.f && c->beta1 < 1.f && c->beta2 >= 0.f && c->beta2 < 1.f && c->eps > 0.f))
     return "bad Adam constants";
   if (!(c->lr0_g >= 0.f && c->lr0_d >= 0.f)) return "learning rates must be >= 0";

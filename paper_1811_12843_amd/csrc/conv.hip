@@ -537,12 +537,14 @@ __global__ __launch_bounds__(NT, 2) void conv_kernel(const ConvProb* __restrict_
 // gradient element in split order and takes the Adam step of the parameter.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void adam_at(float* p, float* m, float* v, float g, float lr, float bc1, float bc2,
-                                        const AdamConsts& ac) {
+                                        const AdamConsts& ac, float clip = 0.f) {
   const float mm = ac.beta1 * *m + ac.one_minus_beta1 * g;
   const float vv = ac.beta2 * *v + ac.one_minus_beta2 * g * g;
   *m = mm;
   *v = vv;
-  *p = *p - lr * (mm / bc1) / (sqrtf(vv / bc2) + ac.eps);
+  float q = *p - lr * (mm / bc1) / (sqrtf(vv / bc2) + ac.eps);
+  if (clip > 0.f) q = q > clip ? clip : (q < -clip ? -clip : q);  // keeps NaN
+  *p = q;
 }
 
 // Grid (x, problem): the Adam bias corrections are computed once per thread,
@@ -556,7 +558,7 @@ __global__ void reduce_adam_kernel(const RedProb* __restrict__ probs, int step_l
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < R.n; e += (int64_t)gridDim.x * blockDim.x) {
     float g = 0.f;
     for (int s = 0; s < R.splits; ++s) g += R.part[(int64_t)s * R.split_stride + e];
-    adam_at(R.p + e, R.m + e, R.v + e, g, lr, bc1, bc2, ac);
+    adam_at(R.p + e, R.m + e, R.v + e, g, lr, bc1, bc2, ac, R.clip);
   }
 }
 

@@ -738,6 +738,8 @@ BnProb bn_prob(const float* x, float* y, int64_t rows, int ch, float* part, floa
 
 void dc_build(lipz_grid* g) {
   DcPlan& P = *g->dc;
+  // the Wasserstein critic's parameters are clipped after every update
+  const float d_clip = g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN ? g->cfg.wgan_clip : 0.f;
   P.conv_h.clear();
   P.bn_h.clear();
   P.red_h.clear();
@@ -873,6 +875,8 @@ void dc_build(lipz_grid* g) {
         p.lr = S.Dlr + c;
         p.t = S.Dt + c;
         p.epi = EPI_ADAM;
+        p.clip = d_clip;
+        if (g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN) p.gscale = 1.f / (float)B;  // dL/da stored as exact +-1
         ps.push_back(p);
       }
       gemm(ps);
@@ -915,6 +919,7 @@ void dc_build(lipz_grid* g) {
           r.v = S.Dv + o;
           r.lr = S.Dlr + c;
           r.t = S.Dt + c;
+          r.clip = d_clip;
           rs.push_back(r);
         }
       ops.push_back({DC_REDUCE, add_red_op(P, rs)});
@@ -1251,7 +1256,7 @@ lipz_status dc_eval(lipz_grid* g, int gen) {
   ha.C = C;
   ha.nn = LIPZ_SLOTS;
   ha.rmean = nullptr;
-  ha.loss_kind = LIPZ_LOSS_BCE;
+  ha.loss_kind = g->cfg.loss_kind;
   return check_hip(g, launch_head_eval(ha, s), "eval head");
 }
 
@@ -1277,6 +1282,7 @@ lipz_status dc_train(lipz_grid* g, int gen, int step0, int n_steps, float* d_los
   hd.C = C;
   hd.hidden_act = P.D.L[n - 1].act;
   hd.slope = g->slope;
+  hd.loss_kind = g->cfg.loss_kind;
   HeadArgs hg = hd;
   hg.part = P.part_g;
   hg.act = P.dyg[n - 1];

@@ -320,6 +320,7 @@ struct RedProb {
   float* v;
   const float* lr;
   const int32_t* t;
+  float clip;              // > 0: clip every updated parameter to [-clip, clip] (the Wasserstein critic)
 };
 hipError_t launch_reduce_adam(const RedProb* d_probs, int n_probs, int64_t max_n, int step_local, AdamConsts ac,
                               hipStream_t s);

@@ -69,11 +69,12 @@ def test_workspace_sizing_and_validation():
     c = L.config_from_dict(w)
     c.loss_kind = 2
     assert L.lipz_workspace_bytes(c, 60000) == 0
-    # the Wasserstein trainer: same buffers as the BCE one; MLP networks only
+    # the Wasserstein trainer: same buffers as the BCE one, for both network kinds
     assert L.lipz_workspace_bytes(L.config_from_dict(dict(w, loss="wasserstein")), 60000) == base
     assert L.lipz_workspace_bytes(L.config_from_dict(synth.workload("mnist_mlp_4x4_wgan")), 60000) > 0
-    d = dict(synth.workload("celeba_dcgan_4x4"), loss="wasserstein")
-    assert L.lipz_workspace_bytes(L.config_from_dict(d), 1000) == 0
+    d = synth.workload("celeba_dcgan_4x4")
+    assert L.lipz_workspace_bytes(L.config_from_dict(dict(d, loss="wasserstein")), 1000) == \
+        L.lipz_workspace_bytes(L.config_from_dict(d), 1000) > 0
     # the NES trainer: its Q = 2 nes_pairs + 1 parameter sets per role and cell add to the workspace
     nes = synth.workload("mnist_mlp_3x3_nes")
     assert L.lipz_workspace_bytes(L.config_from_dict(nes), 60000) > base

@@ -39,6 +39,10 @@ WORKLOADS = {
     "dc32_3x3": lambda: _wl(rows=3, cols=3, img=(32, 32, 3), x_dim=3072, z_dim=12, g_hidden=[64, 32, 16],
                             d_hidden=[16, 32, 64], batch=6, lr0_g=2e-3, lr0_d=2e-3,
                             data=dict(n=512, h=32, w=32)),
+    # the Wasserstein trainer on the convolutional critic
+    "dc16_2x2_wgan": lambda: _wl(rows=2, cols=2, img=(16, 16, 3), x_dim=768, z_dim=8, g_hidden=[32, 16],
+                                 d_hidden=[16, 32], batch=5, lr0_g=2e-3, lr0_d=2e-3, loss="wasserstein",
+                                 wgan_clip=0.05, data=dict(n=512, h=16, w=16)),
     # generators ranked by their own non-saturating loss (fitness_mode 1)
     "dc16_2x2_fm1": lambda: _wl(rows=2, cols=2, img=(16, 16, 3), x_dim=768, z_dim=8, g_hidden=[32, 16],
                                 d_hidden=[16, 32], batch=5, fitness_mode=1, data=dict(n=512, h=16, w=16)),
@@ -123,10 +127,12 @@ def test_eval_matches_oracle(key):
         for gen in (0, 2):
             Lm, Lg, fg, fd = gg.eval(gen)
             oL, oLg, ofg, ofd = coevo.evaluate(S, st, data, gen)
+            # the Wasserstein losses are differences of two means: an absolute term beside the relative one
+            atol = RTOL * 1e-2 if wl.get("loss") == "wasserstein" else 0.0
             for a, b in ((Lm, oL), (Lg, oLg), (fg, ofg), (fd, ofd)):
                 err = np.max(np.abs(a - b) / np.abs(b))
                 print(f"  gen {gen}: max rel err {err:.2e}")
-                assert np.all(np.abs(a - b) <= RTOL * np.abs(b)), err
+                assert np.all(np.abs(a - b) <= RTOL * np.abs(b) + atol), err
             if wl["rows"] == 2 and wl["cols"] == 2:
                 assert np.array_equal(Lm[:, 1], Lm[:, 2]) and np.array_equal(Lm[:, :, 3], Lm[:, :, 4])
 
@@ -153,6 +159,39 @@ def test_train_step_matches_oracle(key, steps):
                              net.arch)
             print(f"  {p}: params rel {e:.2e} ({where}), updates rel {du:.2e} ({wdu})")
             assert e <= 1e-3 and du <= 5e-2
+
+
+def test_wasserstein_train_step_matches_oracle():
+    """One step of the Wasserstein trainer on the convolutional critic from an
+    identical state: the critic loss before any update (1e-4 plus an absolute
+    1e-6), the generator loss on the GPU's own updated critic (teacher forcing,
+    as for the MLP critic: Adam's first steps move a weight by about lr
+    whatever its gradient, so near-zero gradients of the other sign in fp32
+    shift the loss by ~1e-5), the critic inside its clip, parameters per
+    section 1e-3."""
+    wl, data, S = _setup("dc16_2x2_wgan")
+    st = _warm_state(S, data)
+    gen, step = 1, 4
+    _print_case("dcgan wgan train", key="dc16_2x2_wgan")
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        gl = gg.train(gen, step, 1)[0]
+        got = gg.get_state()
+    ref = st.copy()
+    ol = coevo.train_step(S, ref, data, gen, step)
+    assert np.all(np.abs(gl[:, 0] - ol[:, 0]) <= RTOL * np.abs(ol[:, 0]) + 1e-6)
+    lg = np.zeros(S.C)
+    for c in range(S.C):
+        _, _, z = coevo.sample(S, data, c, gen, step + 1)
+        a = coevo.d_logits(S, got.Dp[c], coevo.g_forward(S, st.Gp[c], z)[1])[1]
+        lg[c] = coevo.pair_losses(S, a, a)[1]
+    assert np.all(np.abs(gl[:, 1] - lg) <= RTOL * np.abs(lg) + 1e-6)
+    assert np.all(np.abs(got.Dp) <= np.float32(0.05))
+    assert np.array_equal(got.Gt, ref.Gt) and np.array_equal(got.Dt, ref.Dt)
+    for p, net in (("G", S.Gnet), ("D", S.Dnet)):
+        e, where = _worst(getattr(got, p + "p"), getattr(ref, p + "p"), net.arch)
+        print(f"  {p}: params rel {e:.2e} ({where})")
+        assert e <= 1e-3
 
 
 def test_select_replace_copies_individuals_bit_exactly():
