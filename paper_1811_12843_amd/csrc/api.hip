@@ -81,8 +81,7 @@ std::string validate(const lipz_config* c, int64_t n_samples, Net* Gn, Net* Dn) 
   if (c->pop_size > 1 && c->mix_enable) return "the mixture step needs pop_size 1";
   if (c->bands < 0 || c->bands > LIPZ_MAX_BANDS || (c->bands > 1 && c->bands > c->rows))
     return "bands must be in [0, 8] and at most rows";
-  if (c->bands > 1 && (c->net != LIPZ_NET_MLP || c->trainer != LIPZ_TRAINER_GRADIENT))
-    return "row bands are implemented for the MLP networks and the gradient trainer";
+  if (c->bands > 1 && c->net != LIPZ_NET_MLP) return "row bands are implemented for the MLP networks";
   if ((int64_t)c->rows * c->cols * c->pop_size > 4096) return "grid size x pop_size out of range";
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31) - 1) return "n_samples must be in [1, 2^31)";
   if (c->net == LIPZ_NET_DCGAN) return dc_validate(c, Gn, Dn);
@@ -438,19 +437,19 @@ void setup_groups(lipz_grid* g) {
 // discriminator's Q parameter sets, each D forward over the 2B rows, their
 // losses, the estimate + Adam; then the generator's Q sets, each G forward,
 // the updated D over all Q B generated rows, their losses, estimate + Adam.
-void build_nes_ops(lipz_grid* g) {
-  const int C = g->U, B = g->B, zd = g->zd, xd = g->xd, Q = g->nes_q;  // C: training units
+// Training units u0 .. u1 - 1 of state buffer par.
+void build_nes_ops_range(lipz_grid* g, int par, int u0, int u1, std::vector<Op>& ops) {
+  const int B = g->B, zd = g->zd, xd = g->xd, Q = g->nes_q;
   const Net &G = g->G, &D = g->D;
   const int LG = G.nl, LD = D.nl;
   const size_t sG = G.stride, sD = D.stride;
-  for (int par = 0; par < 2; ++par) {
+  {
     const StateBuf& S = g->st[par];
-    std::vector<Op>& ops = g->nes_ops[par];
     ops.clear();
     ops.push_back({OP_SAMPLE, -1});
     for (int l = 0; l < LG; ++l) {
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c) {
+      for (int c = u0; c < u1; ++c) {
         const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
         float* y = l + 1 < LG ? g->h[l] + (size_t)c * B * G.fo[l]
                               : g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd;
@@ -461,7 +460,7 @@ void build_nes_ops(lipz_grid* g) {
     ops.push_back({OP_NES_PERTURB, LIPZ_ROLE_D});
     for (int l = 0; l + 1 < LD; ++l) {
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c)
+      for (int c = u0; c < u1; ++c)
         for (int q = 0; q < Q; ++q) {
           const size_t cq = (size_t)c * Q + q;
           const float* W = q + 1 < Q ? g->nes_pd + ((size_t)c * (Q - 1) + q) * sD : S.Dp + c * sD;
@@ -478,7 +477,7 @@ void build_nes_ops(lipz_grid* g) {
     ops.push_back({OP_NES_PERTURB, LIPZ_ROLE_G});
     for (int l = 0; l < LG; ++l) {
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c)
+      for (int c = u0; c < u1; ++c)
         for (int q = 0; q < Q; ++q) {
           const size_t cq = (size_t)c * Q + q;
           const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->nes_hq[l - 1] + cq * B * G.fi[l];
@@ -490,7 +489,7 @@ void build_nes_ops(lipz_grid* g) {
     }
     for (int l = 0; l + 1 < LD; ++l) {
       std::vector<GemmProb> ps;
-      for (int c = 0; c < C; ++c) {
+      for (int c = u0; c < u1; ++c) {
         const float* x = l == 0 ? g->nes_xq + (size_t)c * Q * B * xd : g->nes_agq[l - 1] + (size_t)c * Q * B * D.fi[l];
         GemmProb p = fwd_prob(x, Q * B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
                               g->nes_agq[l] + (size_t)c * Q * B * D.fo[l], D.act[l]);
@@ -502,6 +501,14 @@ void build_nes_ops(lipz_grid* g) {
     }
     ops.push_back({OP_NES_HEAD, LIPZ_ROLE_G});
     ops.push_back({OP_NES_UPDATE, LIPZ_ROLE_G});
+  }
+}
+
+void build_nes_ops(lipz_grid* g) {
+  for (int par = 0; par < 2; ++par) {
+    build_nes_ops_range(g, par, 0, g->U, g->nes_ops[par]);
+    for (int b = 0; b < g->n_bands; ++b)
+      build_nes_ops_range(g, par, g->band_c0[b] * g->s, g->band_c0[b + 1] * g->s, g->nes_band_ops[par][b]);
   }
 }
 
@@ -1077,6 +1084,72 @@ lipz_status enq_train_group_step(lipz_grid* g, int gen, int par, int grp, int k,
   return LIPZ_OK;
 }
 
+// The gradient-free trainers' per-role arguments for state buffer par.
+void nes_args(lipz_grid* g, int gen, int par, NesArgs* na) {
+  const StateBuf& S = g->st[par];
+  for (int role = 0; role < 2; ++role) {
+    NesArgs& a = na[role];
+    memset(&a, 0, sizeof(a));
+    const bool d = role == LIPZ_ROLE_D;
+    a.p = d ? S.Dp : S.Gp;
+    a.m = d ? S.Dm : S.Gm;
+    a.v = d ? S.Dv : S.Gv;
+    a.lr = d ? S.Dlr : S.Glr;
+    a.t = d ? S.Dt : S.Gt;
+    a.sets = d ? g->nes_pd : g->nes_pg;
+    a.eps = g->nes_eps;
+    a.eps_stride = g->nes_eps_stride;
+    a.part = d ? g->nes_part_d : g->nes_part_g;
+    a.fit = d ? g->nes_fd : g->nes_fg;
+    a.stride = d ? g->D.stride : g->G.stride;
+    a.P = d ? g->D.P : g->G.P;
+    a.n = g->cfg.nes_pairs;
+    a.tn = g->tn;
+    a.B = g->B;
+    a.c0 = 0;
+    a.C = g->U;
+    a.role = role;
+    a.loss_kind = g->cfg.loss_kind;
+    a.sigma = g->cfg.nes_sigma;
+    a.clip = (d && g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN) ? g->cfg.wgan_clip : 0.f;
+    a.key = g->key;
+    a.gen = (uint32_t)gen;
+    a.tag = d ? LIPZ_TAG_NES_D : LIPZ_TAG_NES_G;
+    a.ac = g->ac;
+  }
+}
+
+// Gradient-free step k (training step `step`) of training units u0 .. u0 + nu - 1
+// with their plan `ops`.
+lipz_status enq_nes_step(lipz_grid* g, int gen, const std::vector<Op>& ops, const NesArgs* na, int u0, int nu,
+                         int k, int step, float* d_losses, hipStream_t s) {
+  const bool es = g->cfg.trainer == LIPZ_TRAINER_ES;
+  const int B = g->B;
+  lipz_status st;
+  for (const Op& op : ops) {
+    hipError_t e = hipSuccess;
+    NesArgs a = op.kind >= OP_NES_PERTURB ? na[op.phase] : na[0];
+    a.c0 = u0;
+    a.C = nu;
+    a.sf = (uint32_t)(step + 1);
+    a.step_local = k;
+    a.losses = d_losses ? d_losses + (size_t)k * g->U * 2 : nullptr;
+    switch (op.kind) {
+      case OP_SAMPLE:
+        e = launch_sample(g->data, g->N, g->xd, g->zd, B, u0, nu, g->key, (uint32_t)gen, (uint32_t)(step + 1),
+                          g->Xtr, (int64_t)2 * B * g->xd, g->z, (int64_t)B * g->zd, s);
+        break;
+      case OP_GEMM: e = run_gemm_phase(g, op.phase, k, s); break;
+      case OP_NES_PERTURB: e = launch_nes_perturb(a, s); break;
+      case OP_NES_HEAD: e = launch_nes_head(a, s); break;
+      case OP_NES_UPDATE: e = es ? launch_es_select(a, s) : launch_nes_update(a, s); break;
+      default: e = hipErrorInvalidValue; break;
+    }
+    if ((st = check_hip(g, e, es ? "ES step" : "NES step"))) return st;
+  }
+  return LIPZ_OK;
+}
+
 }  // namespace lipz
 
 extern "C" {
@@ -1267,59 +1340,10 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   HeadArgs hd, hg;
   train_heads(g, par, &hd, &hg);
   if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
-    const bool es = g->cfg.trainer == LIPZ_TRAINER_ES;
     NesArgs na[2];
-    for (int role = 0; role < 2; ++role) {
-      NesArgs& a = na[role];
-      memset(&a, 0, sizeof(a));
-      const bool d = role == LIPZ_ROLE_D;
-      a.p = d ? S.Dp : S.Gp;
-      a.m = d ? S.Dm : S.Gm;
-      a.v = d ? S.Dv : S.Gv;
-      a.lr = d ? S.Dlr : S.Glr;
-      a.t = d ? S.Dt : S.Gt;
-      a.sets = d ? g->nes_pd : g->nes_pg;
-      a.eps = g->nes_eps;
-      a.eps_stride = g->nes_eps_stride;
-      a.part = d ? g->nes_part_d : g->nes_part_g;
-      a.fit = d ? g->nes_fd : g->nes_fg;
-      a.stride = d ? g->D.stride : g->G.stride;
-      a.P = d ? g->D.P : g->G.P;
-      a.n = g->cfg.nes_pairs;
-      a.tn = g->tn;
-      a.B = B;
-      a.C = C;
-      a.role = role;
-      a.loss_kind = g->cfg.loss_kind;
-      a.sigma = g->cfg.nes_sigma;
-      a.clip = (d && g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN) ? g->cfg.wgan_clip : 0.f;
-      a.key = g->key;
-      a.gen = (uint32_t)gen;
-      a.tag = d ? LIPZ_TAG_NES_D : LIPZ_TAG_NES_G;
-      a.ac = g->ac;
-    }
-    for (int k = 0; k < n_steps; ++k) {
-      const int step = step0 + k;
-      for (const Op& op : g->nes_ops[par]) {
-        hipError_t e = hipSuccess;
-        NesArgs a = op.kind >= OP_NES_PERTURB ? na[op.phase] : na[0];
-        a.sf = (uint32_t)(step + 1);
-        a.step_local = k;
-        a.losses = d_losses ? d_losses + (size_t)k * C * 2 : nullptr;
-        switch (op.kind) {
-          case OP_SAMPLE:
-            e = launch_sample(g->data, g->N, g->xd, g->zd, B, 0, C, g->key, (uint32_t)gen, (uint32_t)(step + 1),
-                              g->Xtr, (int64_t)2 * B * g->xd, g->z, (int64_t)B * g->zd, s);
-            break;
-          case OP_GEMM: e = run_gemm_phase(g, op.phase, k, s); break;
-          case OP_NES_PERTURB: e = launch_nes_perturb(a, s); break;
-          case OP_NES_HEAD: e = launch_nes_head(a, s); break;
-          case OP_NES_UPDATE: e = es ? launch_es_select(a, s) : launch_nes_update(a, s); break;
-          default: e = hipErrorInvalidValue; break;
-        }
-        if ((st = check_hip(g, e, es ? "ES step" : "NES step"))) return st;
-      }
-    }
+    nes_args(g, gen, par, na);
+    for (int k = 0; k < n_steps; ++k)
+      if ((st = enq_nes_step(g, gen, g->nes_ops[par], na, 0, C, k, step0 + k, d_losses, s))) return st;
     hipError_t e = launch_add_i32(S.Gt, C, n_steps, s);
     if (e == hipSuccess) e = launch_add_i32(S.Dt, C, n_steps, s);
     if ((st = check_hip(g, e, "step count"))) return st;
@@ -1371,9 +1395,18 @@ static lipz_status enq_band_generations(lipz_grid* g, int gen0, int n_gens, int 
       if ((st = enq_select(g, gen, par, c0, nc, nullptr, nullptr, nullptr, bs))) return st;
     }
     // training, step by step across the bands so every stream has work early
+    NesArgs na[2];
+    if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) nes_args(g, gen, 1 - par, na);
     for (int k = 0; k < n_steps; ++k)
-      for (int b = 0; b < nb; ++b)
-        if ((st = enq_train_group_step(g, gen, 1 - par, b, k, k, nullptr, hd, hg, g->gstream[b]))) return st;
+      for (int b = 0; b < nb; ++b) {
+        if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
+          const int u0 = g->band_c0[b] * sp, nu = g->band_c0[b + 1] * sp - u0;
+          if ((st = enq_nes_step(g, gen, g->nes_band_ops[1 - par][b], na, u0, nu, k, k, nullptr, g->gstream[b])))
+            return st;
+        } else if ((st = enq_train_group_step(g, gen, 1 - par, b, k, k, nullptr, hd, hg, g->gstream[b]))) {
+          return st;
+        }
+      }
     for (int b = 0; b < nb; ++b) {
       hipStream_t bs = g->gstream[b];
       const int c0 = g->band_c0[b], nc = g->band_c0[b + 1] - c0;

@@ -183,6 +183,7 @@ struct lipz_grid {
   float *nes_agq[LIPZ_MAX_HIDDEN] = {}, *nes_part_g = nullptr;        // D on the Q B generated rows
   float *nes_fd = nullptr, *nes_fg = nullptr;                         // losses per set [C][Q]
   std::vector<Op> nes_ops[2];
+  std::vector<Op> nes_band_ops[2][LIPZ_MAX_GROUPS];  // the same per row band
 };
 
 namespace lipz {

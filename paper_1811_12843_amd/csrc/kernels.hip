@@ -227,7 +227,7 @@ __global__ __launch_bounds__(NT) void head_eval_kernel(EvalHeadArgs A) {
 // the sets theta + sigma eps_k and theta - sigma eps_k.  n P < 2^31.
 __global__ __launch_bounds__(NT) void nes_perturb_kernel(NesArgs A) {
   __shared__ float4 zs4[NT];
-  const int c = blockIdx.y;
+  const int c = A.c0 + blockIdx.y;
   const uint32_t P = (uint32_t)A.P, total = (uint32_t)A.n * P;
   const uint32_t b0 = blockIdx.x * NT, b = b0 + threadIdx.x;
   if (4u * b < total) {
@@ -263,7 +263,7 @@ __global__ __launch_bounds__(NT) void nes_perturb_kernel(NesArgs A) {
 // D role: rows [x; G(z)] (2B); G role: the B rows generated by set q.
 __global__ __launch_bounds__(NT) void nes_head_kernel(NesArgs A) {
   __shared__ float red[4];
-  const int q = blockIdx.x, c = blockIdx.y, Q = 2 * A.n + 1;
+  const int q = blockIdx.x, c = A.c0 + blockIdx.y, Q = 2 * A.n + 1;
   const bool d_role = A.role == LIPZ_ROLE_D;
   const int rows = d_role ? 2 * A.B : A.B;
   const float* part = A.part + ((int64_t)c * Q + q) * rows * A.tn;
@@ -285,7 +285,7 @@ __global__ __launch_bounds__(NT) void nes_head_kernel(NesArgs A) {
 // bias-corrected Adam step of parameter e (and the clip, when set)
 __global__ __launch_bounds__(NT) void nes_update_kernel(NesArgs A) {
   __shared__ float bc[2];
-  const int c = blockIdx.y, Q = 2 * A.n + 1;
+  const int c = A.c0 + blockIdx.y, Q = 2 * A.n + 1;
   const AdamConsts& ac = A.ac;
   if (threadIdx.x == 0) {
     const int tt = A.t[c] + A.step_local + 1;
@@ -326,7 +326,7 @@ __global__ __launch_bounds__(NT) void nes_update_kernel(NesArgs A) {
 // critic clip, on whichever set was kept.
 __global__ __launch_bounds__(NT) void es_select_kernel(NesArgs A) {
   __shared__ int win;
-  const int c = blockIdx.y, parent = 2 * A.n;
+  const int c = A.c0 + blockIdx.y, parent = 2 * A.n;
   if (threadIdx.x == 0) {
     const float* f = A.fit + c * (parent + 1);
     int q = 0;

@@ -444,7 +444,7 @@ struct NesArgs {
   float* fit;            // [C][Q] loss of each set
   float* losses;         // [C][2] slice of this step, or null
   int64_t stride, P, eps_stride;
-  int n, tn, B, C;
+  int n, tn, B, c0, C;   // training units c0 .. c0 + C - 1
   int role;              // LIPZ_ROLE_G / LIPZ_ROLE_D
   int loss_kind;
   float sigma, clip;     // clip > 0: clip the updated parameters (Wasserstein critic)

@@ -34,6 +34,9 @@ CASES = {
     # the 4x4 grid with the mixture step, in 2 and 4 bands (its ES waits for the neighbour bands' moments)
     "mnist_4x4_mix_b2": dict(rows=4, cols=4, bands=2, batch=32, mix_enable=1, mix_samples=300, data=dict(n=4000)),
     "ragged_6x2_mix_b3": dict(RAGGED, rows=6, cols=2, bands=3, mix_enable=1, mix_samples=130, mix_feat_dim=24),
+    # the gradient-free trainers
+    "ragged_8x3_b4_nes": dict(RAGGED, rows=8, cols=3, bands=4, trainer="nes", nes_pairs=3),
+    "ragged_6x2_b3_es_s2": dict(RAGGED, rows=6, cols=2, bands=3, trainer="es", nes_pairs=2, pop_size=2, elitism=1),
 }
 
 

@@ -87,7 +87,11 @@ def test_band_plans_stay_in_bounds(over):
                               **over)
     n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), wl["data"]["n"])
     assert n_bad == 0, msg
-    for bad in (dict(wl, bands=wl["rows"] + 1), dict(wl, bands=9), dict(wl, trainer="nes")):
+    for trainer in ("nes", "es"):
+        n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(dict(wl, trainer=trainer, nes_pairs=3)),
+                                             wl["data"]["n"])
+        assert n_bad == 0, msg
+    for bad in (dict(wl, bands=wl["rows"] + 1), dict(wl, bands=9)):
         assert L.lipz_workspace_bytes(L.config_from_dict(bad), wl["data"]["n"]) == 0
 
 
