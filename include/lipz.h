@@ -273,7 +273,8 @@ lipz_status lipz_elitist_replace(lipz_grid* g, int32_t gen, int32_t* d_src, floa
  * n_steps) and (elitism = 1) lipz_elitist_replace, and, with mix_enable,
  * lipz_mixture_update, with the same results bit for bit.
  *
- * bands >= 2 (MLP networks, gradient trainer, no mixture step): the paper's
+ * bands >= 2 (MLP networks, every trainer, with or without the mixture
+ * step, whose ES also waits for the neighbour bands' moments): the paper's
  * cells run asynchronously (Section 3, step 1 and its Figure 1), and this is
  * that scheduling on one device.  The grid's rows are split into `bands` row
  * bands, each on its own stream, and nothing waits for the whole grid: a
