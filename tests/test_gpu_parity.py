@@ -358,6 +358,59 @@ def test_generation_wasserstein_3x3_short():
     _generation_parity("mnist_3x3_wgan", steps=5)
 
 
+@pytest.mark.parametrize("key", ["mnist_3x3", "mnist_4x4_mix"])
+def test_generation_full_length_each_step(key):
+    """A whole generation at the workload's own length (100 training steps):
+    evaluation and selection, then every training step on the GPU from the
+    state the GPU reached, the oracle taking the same step from that state;
+    per step losses 1e-4, parameters 1e-3 and their updates 5e-2; then the
+    mixture update from the GPU's final state.
+
+    Left to run free for 100 steps the two sides part by more than 1e-3 (the
+    4x4 grid: 5e-3 in D's parameters), because the GAN dynamics amplify every
+    rounding: the oracle parts nearly as far from a copy of itself whose state
+    is rounded to fp32 after each step (the 4x4 grid: 1.7e-3 in G's
+    parameters).  So the steps are compared from a shared state."""
+    wl, data, S = _setup(key)
+    st = _warm_state(S, data, steps=1)
+    gen = 2
+    _print_case("generation-each-step", key=key, steps=wl["steps"])
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        gg.eval(gen)
+        _, _, ofg, ofd = coevo.evaluate(S, st, data, gen)
+        gsel, _ = gg.select(gen)
+        check_selection(S, gsel, ofg, ofd, gen)
+        ref, _ = coevo.select_replace(S, st, ofg, ofd, gen, forced=gsel)
+        cur = gg.get_state()
+        for f in ("Gp", "Gm", "Gv", "Dp", "Dm", "Dv", "Gt", "Dt"):
+            assert np.array_equal(getattr(cur, f), getattr(ref, f)), f
+        worst = dict(loss=0.0, G=0.0, D=0.0, dG=0.0, dD=0.0)
+        for s in range(wl["steps"]):
+            gl = gg.train(gen, s, 1)[0]
+            nxt = gg.get_state()
+            ref = cur.copy()
+            ol = coevo.train_step(S, ref, data, gen, s)
+            e = float(np.max(np.abs(gl - ol) / np.abs(ol)))
+            assert e <= RTOL, (s, e)
+            worst["loss"] = max(worst["loss"], e)
+            assert np.array_equal(nxt.Gt, ref.Gt) and np.array_equal(nxt.Dt, ref.Dt)
+            for p, sizes in (("G", S.g_sizes), ("D", S.d_sizes)):
+                e = per_tensor_rel(getattr(nxt, p + "p"), getattr(ref, p + "p"), sizes)
+                du = per_tensor_rel(getattr(nxt, p + "p") - getattr(cur, p + "p"),
+                                    getattr(ref, p + "p") - getattr(cur, p + "p"), sizes)
+                assert e <= 1e-3 and du <= 5e-2, (s, p, e, du)
+                worst[p], worst["d" + p] = max(worst[p], e), max(worst["d" + p], du)
+            cur = nxt
+        print("  worst over the steps: " + ", ".join(f"{k} {v:.2e}" for k, v in worst.items()))
+        if wl["mix_enable"]:
+            stats = mixture.real_stats(S, data)
+            w, sc, acc = gg.mixture(gen)
+            ow, osc, oacc = mixture.update(S, cur, stats, gen)
+            assert np.all(np.abs(sc - osc) <= 1e-3 * np.abs(osc))
+            assert np.all(np.abs(w - ow) <= 1e-5)
+
+
 @pytest.mark.parametrize("key", ["ragged_2x3", "mnist_4x4_mix"])
 def test_mixture_matches_oracle(key):
     wl, data, S = _setup(key)
