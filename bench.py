@@ -226,7 +226,7 @@ def main():
         print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n}), flush=True)
         return
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU; the grid is not sharded across GPUs "
+        print("bench.py: the library runs a grid on one GPU; it is not sharded across GPUs "
               "(--gpus must be 1)", file=sys.stderr)
         sys.exit(2)
 
