@@ -196,6 +196,46 @@ def cpu_baseline(wl, data, budget_s=20.0):
             "pair_evals_per_s": S.C * S.n * S.n / t_eval}
 
 
+def mfma_ceiling(torch, L, n=8192, reps=6):
+    """The fp32 matrix-core rate that one large square product reaches on this
+    GPU: torch.matmul (the vendor BLAS, fp32 without reduced-precision inputs)
+    and this library's grouped GEMM on the same n x n x n problem (through its
+    single-problem test entry point).  Both in TFLOP/s, HIP events."""
+    torch.backends.cuda.matmul.allow_tf32 = False
+    g = torch.Generator(device="cuda").manual_seed(0)
+    a = torch.randn(n, n, device="cuda", generator=g)
+    b = torch.randn(n, n, device="cuda", generator=g)
+    c = torch.empty(n, n, device="cuda")
+    flop = 2.0 * n * n * n
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        e1.synchronize()
+        return flop * reps / (e0.elapsed_time(e1) * 1e-3) / 1e12
+
+    vendor = timed(lambda: torch.matmul(a, b, out=c))
+    # the vendor product's precision: a 256 x 256 corner against fp64 (fp32
+    # inputs give ~1e-6 here; reduced-precision inputs would give ~1e-3)
+    ref = a[:256].double() @ b[:, :256].double()
+    vendor_err = float((c[:256, :256].double() - ref).norm() / ref.norm())
+    desc = torch.zeros(256, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def own():
+        L.lipz_test_gemm(stream, desc.data_ptr(), n, n, n, a.data_ptr(), n, 0, -1, b.data_ptr(), n, 0,
+                         c.data_ptr(), n, 0, 0)
+
+    ours = timed(own)
+    del a, b, c
+    return {"shape": [n, n, n], "vendor_tflops": vendor, "vendor_rel_err": vendor_err, "own_gemm_tflops": ours}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -208,6 +248,8 @@ def main():
                          "uniformly, so the work per step does not depend on it)")
     ap.add_argument("--eval-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the large-GEMM measurement of the fp32 matrix-core ceiling")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--bands", type=int, default=0,
                     help="run the timed generations with lipz_run_generations on this many row bands "
@@ -353,9 +395,14 @@ def main():
                      "algorithmic_bytes_per_launch": gemm_bytes / max(launches, 1),
                      "instrumented_ms_per_step": inst_ms},
     }
+    L.lipz_grid_destroy(g)
+    if not args.no_ceiling:
+        ceil = mfma_ceiling(torch, L)
+        ceil["gen_frac_of_vendor"] = f_gen / (ms_per_gen * 1e-3) / (ceil["vendor_tflops"] * 1e12)
+        ceil["gemm_frac_of_vendor"] = achieved / (ceil["vendor_tflops"] * 1e12)
+        out["mfma_ceiling"] = ceil
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, data_np, args.cpu_budget)
-    L.lipz_grid_destroy(g)
     print(json.dumps(out), flush=True)
 
 
