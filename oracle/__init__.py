@@ -28,5 +28,15 @@ torch.optim.Adam, brute-force tournament enumeration, the 1x1-grid reduction
 to plain alternating GAN training, Frechet-distance closed forms, and, for
 NES, exactness on quadratics and convergence to the backpropagated gradient;
 for ES, the selection rule on hand-made losses, brute-force scoring of every
-candidate with torch networks and the elitist invariant.
+candidate with torch networks and the elitist invariant; for sub-populations,
+uniform tournament draws over ordered tuples, members that train exactly like
+the cells of a wider grid, an evaluation that scores every pair of the
+neighbourhood population, and the elitist truncation on hand-made fitness
+lists.
+
+Parity unpinned: trajectories over many steps or generations at workload
+scale.  The paper prints no worked values for them, and the GAN dynamics
+amplify any rounding (a run differing from another by one fp32 rounding of
+its start state ends 7e-4 apart after 100 steps), so they are compared with
+the GPU only step by step from shared states.
 """
