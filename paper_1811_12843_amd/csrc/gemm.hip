@@ -584,8 +584,9 @@ __device__ __forceinline__ void mfma_frag(const Frag<BM>& F, v4f (&acc)[Tile<BM>
 }
 
 // One slice: write registers R (slice it) to LDS stage (as, bs), barrier,
-// start the loads of slice it + NS into R, then the MFMAs of the slice with
-// the LDS reads of k block kb + 1 issued ahead of the MFMAs of block kb.
+// start the loads of slice it + NS into R, then the MFMAs of the slice's two
+// 16-deep k blocks, with the LDS reads of the second block issued ahead of
+// the MFMAs of the first.
 template <int BM, int AT, int BT, int NS>
 __device__ __forceinline__ void fast_slice(const GemmProb& P, __amdgpu_buffer_rsrc_t ra,
                                            __amdgpu_buffer_rsrc_t rb, int m0, int n0, int it, int n_it,
@@ -599,19 +600,19 @@ __device__ __forceinline__ void fast_slice(const GemmProb& P, __amdgpu_buffer_rs
   fast_store<BM, AT, BT>(P, m0, P.K - it * BK, tid, R, as, bs);
   __syncthreads();
   if (it + NS < n_it) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, (it + NS) * BK, tid, R);
+  // A wave whose rows all lie past M, or a 16-deep k block wholly past K
+  // (zeros in both operands), has no MFMA work: skip it (wave-uniform).
+  static_assert(BK == 32, "the k-block skip is written for two 16-deep blocks per slice");
+  if (m0 + wm >= P.M) return;
+  const bool two = P.K - it * BK > 16;
   Frag<BM> F0, F1;
   read_frag<BM, AT, BT>(as, bs, 0, wm, wn, li, lg, F0);
-#pragma unroll
-  for (int kb = 0; kb < BK / 16; kb += 2) {
-    read_frag<BM, AT, BT>(as, bs, kb + 1, wm, wn, li, lg, F1);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_frag<BM>(F0, acc);
-    __builtin_amdgcn_sched_barrier(0);
-    if (kb + 2 < BK / 16) read_frag<BM, AT, BT>(as, bs, kb + 2, wm, wn, li, lg, F0);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_frag<BM>(F1, acc);
-    __builtin_amdgcn_sched_barrier(0);
-  }
+  if (two) read_frag<BM, AT, BT>(as, bs, 1, wm, wn, li, lg, F1);
+  __builtin_amdgcn_sched_barrier(0);
+  mfma_frag<BM>(F0, acc);
+  __builtin_amdgcn_sched_barrier(0);
+  if (two) mfma_frag<BM>(F1, acc);
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // K loop: NS register sets hold the loads of the next NS slices; the loop is
@@ -753,13 +754,16 @@ __device__ __forceinline__ void wave_mma(const GemmProb& P, int m0, int kb, int 
       }
     }
   }
+  // a 16-row block wholly past M has no MFMA work (uniform); each
+  // accumulator still takes its four k steps in order
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
+  for (int i = 0; i < BM / 16; ++i)
+    if (i == 0 || m0 + 16 * i < P.M)
 #pragma unroll
-    for (int i = 0; i < BM / 16; ++i)
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(F.a[i][s], F.b[j][s], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(F.a[i][s], F.b[j][s], acc[i][j], 0, 0, 0);
 }
 
 template <int BM, int AT, int BT, bool ONES>
