@@ -486,6 +486,7 @@ def test_determinism_bitwise():
     assert np.array_equal(outs[0][3], outs[1][3])
 
 
+@pytest.mark.filterwarnings("ignore:invalid value encountered in logaddexp:RuntimeWarning")
 def test_nonfinite_individual_loses_and_is_flagged():
     """A collapsed (NaN) discriminator sorts as +inf and is replaced by a
     neighbour's winner; the sticky non-finite flag is reported by lipz_sync."""
