@@ -52,6 +52,7 @@ WORKLOADS = {
                                                                  rows=1, cols=3, batch=70)),
     "mnist_3x3": lambda: _workload("mnist_mlp_3x3"),
     "mnist_4x4_mix": lambda: _workload("mnist_mlp_4x4_mix"),
+    "mnist_8x8": lambda: _workload("mnist_mlp_8x8"),
     # generators ranked by their own non-saturating loss (fitness_mode 1)
     "mnist_3x3_fm1": lambda: _workload("mnist_mlp_3x3", fitness_mode=1),
     # the Wasserstein trainer: linear critic, clipped critic weights
@@ -358,8 +359,8 @@ def test_generation_wasserstein_3x3_short():
     _generation_parity("mnist_3x3_wgan", steps=5)
 
 
-@pytest.mark.parametrize("key", ["mnist_3x3", "mnist_4x4_mix"])
-def test_generation_full_length_each_step(key):
+@pytest.mark.parametrize("key,n_steps", [("mnist_3x3", None), ("mnist_4x4_mix", None), ("mnist_8x8", 12)])
+def test_generation_full_length_each_step(key, n_steps):
     """A whole generation at the workload's own length (100 training steps):
     evaluation and selection, then every training step on the GPU from the
     state the GPU reached, the oracle taking the same step from that state;
@@ -370,11 +371,13 @@ def test_generation_full_length_each_step(key):
     4x4 grid: 5e-3 in D's parameters), because the GAN dynamics amplify every
     rounding: the oracle parts nearly as far from a copy of itself whose state
     is rounded to fp32 after each step (the 4x4 grid: 1.7e-3 in G's
-    parameters).  So the steps are compared from a shared state."""
+    parameters).  So the steps are compared from a shared state.  The 8x8
+    grid (64 cells) runs the first 12 steps of its generation."""
     wl, data, S = _setup(key)
     st = _warm_state(S, data, steps=1)
     gen = 2
-    _print_case("generation-each-step", key=key, steps=wl["steps"])
+    steps = n_steps or wl["steps"]
+    _print_case("generation-each-step", key=key, steps=steps)
     with GpuGrid(wl, data) as gg:
         gg.set_state(st)
         gg.eval(gen)
@@ -386,7 +389,7 @@ def test_generation_full_length_each_step(key):
         for f in ("Gp", "Gm", "Gv", "Dp", "Dm", "Dv", "Gt", "Dt"):
             assert np.array_equal(getattr(cur, f), getattr(ref, f)), f
         worst = dict(loss=0.0, G=0.0, D=0.0, dG=0.0, dD=0.0)
-        for s in range(wl["steps"]):
+        for s in range(steps):
             gl = gg.train(gen, s, 1)[0]
             nxt = gg.get_state()
             ref = cur.copy()
