@@ -51,6 +51,21 @@ lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M, int32_t N,
 lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, char* msg, int32_t msg_len,
                                   int32_t* n_bad);
 
+/*
+ * The ES trainer's plus-selection (paper Section 3: gradient-free trainers;
+ * the selection rule of the mixture step's (1+1)-ES) on caller-given losses:
+ * for each of n_units units u, d_fit[u][0 .. 2n] holds the losses of the 2n
+ * mutants and, last, of the parent.  The kept candidate is the first mutant
+ * of lowest loss if that loss is strictly lower than the parent's, else the
+ * parent; a NaN loss ranks as +infinity.  Its P values are written over
+ * d_params[u][0 .. P) (row stride `stride` floats): mutant q's are
+ * d_sets[(u * 2n + q) * stride ...], the parent's the row itself.  clip > 0
+ * clips every kept value to [-clip, clip].  Device pointers, caller-owned;
+ * enqueued on hip_stream; LIPZ_E_INVAL on bad sizes.
+ */
+lipz_status lipz_test_es_select(void* hip_stream, const float* d_fit, const float* d_sets, float* d_params,
+                                int32_t n_units, int32_t n_pairs, int64_t P, int64_t stride, float clip);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,7 +25,9 @@ Pinned by tests/test_oracle_*.py against: published Philox known-answer
 vectors and rocRAND's host Philox, hand-enumerated neighbourhoods, BCE closed
 forms, finite differences, torch CPU fp64 convolutions, batch norm and autograd, Adam closed forms and
 torch.optim.Adam, brute-force tournament enumeration, the 1x1-grid reduction
-to plain alternating GAN training, Frechet-distance closed forms, and, for
+to plain alternating GAN training, Frechet-distance closed forms, the
+mixture's generator moments recomputed with torch fp64 layers on the shared
+latents and the closed form of a constant generator, and, for
 NES, exactness on quadratics and convergence to the backpropagated gradient;
 for ES, the selection rule on hand-made losses, brute-force scoring of every
 candidate with torch networks and the elitist invariant; for sub-populations,

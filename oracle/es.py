@@ -32,13 +32,22 @@ from . import coevo, nes
 
 def choose(f):
     """Index of the kept candidate among losses f[0 .. 2n] (f[2n] = parent) and
-    its margin: the distance to the nearest other candidate's loss."""
+    its margin: the distance to the nearest other candidate's loss.
+
+    A NaN loss ranks as +infinity (a non-finite candidate loses, as in the
+    tournament); two infinite candidates are a tie (margin 0)."""
     f = np.asarray(f, dtype=np.float64)
+    key = np.where(np.isnan(f), np.inf, f)
     parent = len(f) - 1
-    q = int(np.argmin(f[:parent]))  # first of equal minima
-    w = q if f[q] < f[parent] else parent
-    others = np.delete(f, w)
-    return w, float(np.min(np.abs(others - f[w]))) if len(others) else np.inf
+    q = int(np.argmin(key[:parent]))  # first of equal minima
+    w = q if key[q] < key[parent] else parent
+    others = np.delete(key, w)
+    if not len(others):
+        return w, np.inf
+    with np.errstate(invalid="ignore"):
+        d = np.abs(others - key[w])
+    d[np.isnan(d)] = 0.0  # inf - inf: a tie between two losing candidates
+    return w, float(np.min(d))
 
 
 def candidates(theta, eps, sigma):

@@ -217,12 +217,12 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     for (int l = 0; l + 1 < G.nl; ++l) g->hm[l] = cv.take<float>((size_t)C * S * G.fo[l]);
     g->xm = cv.take<float>((size_t)C * S * xd);
     g->fm = cv.take<float>((size_t)C * S * F);
-    g->mu_k = cv.take<float>((size_t)C * F);
-    g->s2_k = cv.take<float>((size_t)C * F);
-    g->mom_part = cv.take<float>((size_t)C * ((S + 63) / 64) * 2 * F);
+    g->mu_k = cv.take<double>((size_t)C * F);
+    g->s2_k = cv.take<double>((size_t)C * F);
+    g->mom_part = cv.take<double>((size_t)C * ((S + 63) / 64) * 2 * F);
     g->P = cv.take<float>((size_t)xd * F);
-    g->mu_r = cv.take<float>(F);
-    g->sd_r = cv.take<float>(F);
+    g->mu_r = cv.take<double>(F);
+    g->sd_r = cv.take<double>(F);
     g->realfeat = cv.take<float>((size_t)g->N * F);
   }
   if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
@@ -352,6 +352,13 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
   int prev_tpp = -1;
   for (size_t k = 0; k < ps.size(); ++k) {
     GemmProb p = ps[k];
+    // the epilogue addresses C (and aux, m, v) with 32-bit element offsets
+    // row * ldc + col: a problem whose output reaches 2^31 elements is not
+    // planned (the configuration is rejected as invalid)
+    if ((int64_t)(p.M - 1) * p.ldc + p.N >= ((int64_t)1 << 31)) {
+      g->plan_ok = false;
+      break;
+    }
     gemm_set_extents(p);
     ph.fast = ph.fast && gemm_fast_ok(p);
     p.tiles_n = ceil_div(p.N, GEMM_BN);
@@ -1720,6 +1727,16 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
       if (!inside(g->fit2_g, 0, C * s - 1) || !inside(g->fit2_d, 0, C * s - 1) || !inside(g->esrc, 0, U * 2 - 1))
         note("elitist truncation", 0);
     }
+  }
+  if (g->cfg.mix_enable) {
+    // the mixture kernels' fp64 moments [C][F] x 2, chunk sums
+    // [C][ceil(S / 64)][2][F] and data statistics [F] x 2 (in floats: 2 per double)
+    const int64_t C = g->C, F = g->F, nch = (g->S + 63) / 64;
+    if (!inside(g->mu_k, 0, 2 * C * F - 1) || !inside(g->s2_k, 0, 2 * C * F - 1) ||
+        !inside(g->mom_part, 0, 2 * C * nch * 2 * F - 1))
+      note("mixture moments", 0);
+    if (!inside(g->mu_r, 0, 2 * F - 1) || !inside(g->sd_r, 0, 2 * F - 1)) note("mixture data statistics", 0);
+    if (!inside(g->fm, 0, C * g->S * F - 1) || !inside(g->realfeat, 0, g->N * F - 1)) note("mixture features", 0);
   }
   if (g->cfg.trainer != LIPZ_TRAINER_GRADIENT) {
     // the NES / ES kernels' extents: sets [C][2n][stride] and directions

@@ -117,9 +117,11 @@ struct lipz_grid {
   float *ze = nullptr, *Xe = nullptr;
   float *he[LIPZ_MAX_HIDDEN] = {}, *ae[LIPZ_MAX_HIDDEN] = {};
   // mixture buffers
-  float *zeta = nullptr, *xm = nullptr, *fm = nullptr, *mu_k = nullptr, *s2_k = nullptr, *mom_part = nullptr;
+  float *zeta = nullptr, *xm = nullptr, *fm = nullptr;
+  double *mu_k = nullptr, *s2_k = nullptr, *mom_part = nullptr;  // generator feature moments, fp64
   float *hm[LIPZ_MAX_HIDDEN] = {};
-  float *P = nullptr, *mu_r = nullptr, *sd_r = nullptr, *realfeat = nullptr;
+  float *P = nullptr, *realfeat = nullptr;
+  double *mu_r = nullptr, *sd_r = nullptr;  // dataset feature mean and standard deviation, fp64
 
   GemmProb* probs_d = nullptr;
   std::vector<GemmProb> probs_h;

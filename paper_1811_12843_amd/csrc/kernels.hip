@@ -324,6 +324,12 @@ __global__ __launch_bounds__(NT) void nes_update_kernel(NesArgs A) {
 // mutants, q = 2n the parent) has loss fit[c][q]; the first mutant of lowest
 // loss replaces the parent only if that loss is strictly lower.  Then the
 // critic clip, on whichever set was kept.
+// Ordering key of a loss or fitness value: NaN sorts as +infinity (it loses).
+__device__ __forceinline__ float fit_key(float f) { return f != f ? INFINITY : f; }
+
+// Plus-selection over the 2n + 1 losses of a unit (parent last), NaN as
+// +infinity: the first mutant of lowest key replaces the parent only when
+// its key is strictly lower.
 __global__ __launch_bounds__(NT) void es_select_kernel(NesArgs A) {
   __shared__ int win;
   const int c = A.c0 + blockIdx.y, parent = 2 * A.n;
@@ -331,8 +337,8 @@ __global__ __launch_bounds__(NT) void es_select_kernel(NesArgs A) {
     const float* f = A.fit + c * (parent + 1);
     int q = 0;
     for (int j = 1; j < parent; ++j)
-      if (f[j] < f[q]) q = j;
-    win = f[q] < f[parent] ? q : parent;
+      if (fit_key(f[j]) < fit_key(f[q])) q = j;
+    win = fit_key(f[q]) < fit_key(f[parent]) ? q : parent;
   }
   __syncthreads();
   const int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x;
@@ -378,8 +384,6 @@ __global__ void fitness_kernel(const float* L, const float* Lg, int C, int nn, i
 // ---------------------------------------------------------------------------
 // Tournament + learning-rate mutation, one thread per (cell, role).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float fit_key(float f) { return f != f ? INFINITY : f; }
-
 // Thread (cell c, member i, role): tournament i of the cell over its nn
 // neighbourhood individuals, words 8 i .. 8 i + 7 of the cell's stream
 // (Philox blocks 2 i, 2 i + 1); the copy's learning-rate mutation from words
@@ -548,23 +552,23 @@ __global__ void copy_winners_kernel(CopyArgs A) {
   }
 }
 
-// Per-cell feature moments over S samples: mu = mean f, s2 = mean f^2, in a
-// fixed order.  Stage 1, block (chunk, cell): 4 row lanes x 64 features sum
-// MOM_ROWS rows of a chunk, combined in lane order; stage 2, thread (cell, f):
-// the chunk sums in chunk order.
+// Per-cell feature moments over S samples: mu = mean f, s2 = mean f^2, summed
+// in fp64 in a fixed order.  Stage 1, block (chunk, cell): 4 row lanes x 64
+// features sum MOM_ROWS rows of a chunk, combined in lane order; stage 2,
+// thread (cell, f) (grid-stride): the chunk sums in chunk order.
 constexpr int MOM_ROWS = 64;
 
-__global__ __launch_bounds__(NT) void moments_chunk_kernel(const float* feats, int S, int F, float* part) {
-  __shared__ float red[2][4][64];
+__global__ __launch_bounds__(NT) void moments_chunk_kernel(const float* feats, int S, int F, double* part) {
+  __shared__ double red[2][4][64];
   const int chunk = blockIdx.x, c = blockIdx.y, n_chunks = gridDim.x;
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   for (int f0 = 0; f0 < F; f0 += 64) {
     const int f = f0 + l;
-    float s = 0.f, q = 0.f;
+    double s = 0.0, q = 0.0;
     if (f < F) {
       const int r1 = min(S, (chunk + 1) * MOM_ROWS);
       for (int r = chunk * MOM_ROWS + w; r < r1; r += 4) {
-        const float v = feats[((int64_t)c * S + r) * F + f];
+        const double v = (double)feats[((int64_t)c * S + r) * F + f];
         s += v;
         q += v * v;
       }
@@ -574,96 +578,113 @@ __global__ __launch_bounds__(NT) void moments_chunk_kernel(const float* feats, i
     red[1][w][l] = q;
     __syncthreads();
     if (w == 0 && f < F) {
-      float* o = part + (((int64_t)c * n_chunks + chunk) * 2) * F;
+      double* o = part + (((int64_t)c * n_chunks + chunk) * 2) * F;
       o[f] = (red[0][0][l] + red[0][1][l]) + (red[0][2][l] + red[0][3][l]);
       o[F + f] = (red[1][0][l] + red[1][1][l]) + (red[1][2][l] + red[1][3][l]);
     }
   }
 }
 
-__global__ void moments_final_kernel(const float* part, int n_chunks, int C, int S, int F, float* mu, float* s2) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= C * F) return;
-  const int c = i / F, f = i - c * F;
-  float s = 0.f, q = 0.f;
-  for (int k = 0; k < n_chunks; ++k) {
-    const float* o = part + (((int64_t)c * n_chunks + k) * 2) * F;
-    s += o[f];
-    q += o[F + f];
+__global__ void moments_final_kernel(const double* part, int n_chunks, int C, int S, int F, double* mu,
+                                     double* s2) {
+  const int64_t n = (int64_t)C * F;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t c = i / F, f = i - c * F;
+    double s = 0.0, q = 0.0;
+    for (int k = 0; k < n_chunks; ++k) {
+      const double* o = part + ((c * n_chunks + k) * 2) * F;
+      s += o[f];
+      q += o[F + f];
+    }
+    mu[i] = s / (double)S;
+    s2[i] = q / (double)S;
   }
-  mu[i] = s / (float)S;
-  s2[i] = q / (float)S;
 }
 
-// Column mean and (biased, two-pass) standard deviation over N rows.
+// Column mean and (biased, two-pass) standard deviation over N rows, fp64.
+__device__ double block_sum_f64(double v, double* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
 __global__ __launch_bounds__(NT) void col_stats_kernel(const float* feats, int64_t N, int F,
-                                                       float* mu, float* sd) {
-  __shared__ float red[4];
+                                                       double* mu, double* sd) {
+  __shared__ double red[4];
   const int f = blockIdx.x;
   double s = 0.0;
   for (int64_t r = threadIdx.x; r < N; r += NT) s += feats[r * F + f];
-  const float mean = block_sum((float)(s / (double)N), red);
+  const double mean = block_sum_f64(s, red) / (double)N;
   double q = 0.0;
   for (int64_t r = threadIdx.x; r < N; r += NT) {
-    const double d = (double)feats[r * F + f] - (double)mean;
+    const double d = (double)feats[r * F + f] - mean;
     q += d * d;
   }
-  const float var = block_sum((float)(q / (double)N), red);
+  const double var = block_sum_f64(q, red) / (double)N;
   if (threadIdx.x == 0) {
     mu[f] = mean;
-    sd[f] = sqrtf(var);
+    sd[f] = sqrt(var);
   }
 }
 
-__device__ float mixture_score(const float* w, const int32_t* ks, const float* mu, const float* s2,
-                               const float* mu_r, const float* sd_r, int F) {
-  float sc = 0.f;
+// score(w) = sum_f (mu_w - mu_r)^2 + (sqrt(var_w) - sd_r)^2 with the mixture's
+// mean mu_w = sum_k w_k mu_k and variance var_w = sum_k w_k s2_k - mu_w^2, in fp64.
+__device__ double mixture_score(const double* w, const int32_t* ks, const double* mu, const double* s2,
+                                const double* mu_r, const double* sd_r, int F) {
+  double sc = 0.0;
   for (int f = 0; f < F; ++f) {
-    float mw = 0.f, sw = 0.f;
+    double mw = 0.0, sw = 0.0;
     for (int k = 0; k < 5; ++k) {
-      mw += w[k] * mu[ks[k] * F + f];
-      sw += w[k] * s2[ks[k] * F + f];
+      mw += w[k] * mu[(int64_t)ks[k] * F + f];
+      sw += w[k] * s2[(int64_t)ks[k] * F + f];
     }
-    const float var = fmaxf(sw - mw * mw, 0.f);
-    const float dm = mw - mu_r[f], ds = sqrtf(var) - sd_r[f];
+    const double var = fmax(sw - mw * mw, 0.0);
+    const double dm = mw - mu_r[f], ds = sqrt(var) - sd_r[f];
     sc += dm * dm + ds * ds;
   }
   return sc;
 }
 
-// (1+1)-ES on the mixture weights of cell i.
+// (1+1)-ES on the mixture weights of cell i.  The weights are stored in
+// fp32; the proposal, both scores and the comparison are formed in fp64.
 __global__ void es_kernel(EsArgs A) {
   const int c = A.c0 + blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= A.c0 + A.C) return;
   const int32_t* ks = A.nbr + c * 5;
-  float w[5], wp[5];
-  for (int k = 0; k < 5; ++k) w[k] = A.w[c * 5 + k];
+  float w[5];
+  double wd[5], wpd[5];
+  for (int k = 0; k < 5; ++k) {
+    w[k] = A.w[c * 5 + k];
+    wd[k] = (double)w[k];
+  }
   const uint4 w0 = stream_block(A.key, 0, (uint32_t)c, A.gen, 0, LIPZ_TAG_MIXN);
   const uint4 w1 = stream_block(A.key, 1, (uint32_t)c, A.gen, 0, LIPZ_TAG_MIXN);
   double tot = 0.0;
-  double wpd[5];
   for (int k = 0; k < 5; ++k) {
     const double n = k < 4 ? normal_of(w0, k) : normal_of(w1, 0);
-    const double x = (double)w[k] + (double)A.sigma * n;
+    const double x = wd[k] + (double)A.sigma * n;
     wpd[k] = x > 0.0 ? x : 0.0;
     tot += wpd[k];
   }
-  float cur = mixture_score(w, ks, A.mu, A.s2, A.mu_r, A.sd_r, A.F);
+  double cur = mixture_score(wd, ks, A.mu, A.s2, A.mu_r, A.sd_r, A.F);
   int acc = 0;
   if (tot > 0.0) {
-    for (int k = 0; k < 5; ++k) wp[k] = (float)(wpd[k] / tot);
-    const float nw = mixture_score(wp, ks, A.mu, A.s2, A.mu_r, A.sd_r, A.F);
+    for (int k = 0; k < 5; ++k) wpd[k] /= tot;
+    const double nw = mixture_score(wpd, ks, A.mu, A.s2, A.mu_r, A.sd_r, A.F);
     if (nw < cur) {
       cur = nw;
       acc = 1;
-      for (int k = 0; k < 5; ++k) w[k] = wp[k];
+      for (int k = 0; k < 5; ++k) w[k] = (float)wpd[k];
     }
   }
   for (int k = 0; k < 5; ++k) {
     A.w[c * 5 + k] = w[k];
     if (A.w_out) A.w_out[c * 5 + k] = w[k];
   }
-  if (A.score_out) A.score_out[c] = cur;
+  if (A.score_out) A.score_out[c] = (float)cur;
   if (A.acc_out) A.acc_out[c] = acc;
 }
 
@@ -763,7 +784,7 @@ hipError_t launch_copy_winners(const CopyArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(copy_winners_kernel, dim3(grid_for(n4, NT, 64), a.U, 2), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
-hipError_t launch_moments(const float* feats, int C, int S, int F, float* part, float* mu, float* s2,
+hipError_t launch_moments(const float* feats, int C, int S, int F, double* part, double* mu, double* s2,
                           hipStream_t s) {
   const int n_chunks = (S + MOM_ROWS - 1) / MOM_ROWS;
   hipLaunchKernelGGL(moments_chunk_kernel, dim3(n_chunks, C), dim3(NT), 0, s, feats, S, F, part);
@@ -771,7 +792,7 @@ hipError_t launch_moments(const float* feats, int C, int S, int F, float* part, 
                      mu, s2);
   return hipGetLastError();
 }
-hipError_t launch_col_stats(const float* feats, int64_t N, int F, float* mu, float* sd,
+hipError_t launch_col_stats(const float* feats, int64_t N, int F, double* mu, double* sd,
                             hipStream_t s) {
   hipLaunchKernelGGL(col_stats_kernel, dim3(F), dim3(NT), 0, s, feats, N, F, mu, sd);
   return hipGetLastError();

@@ -528,15 +528,18 @@ struct CopyArgs {
 hipError_t launch_copy_winners(const CopyArgs& a, hipStream_t s);
 hipError_t launch_add_i32(int32_t* p, int n, int32_t v, hipStream_t s);
 
-// part: scratch of C * ceil(S / 64) * 2 * F floats.
-hipError_t launch_moments(const float* feats, int C, int S, int F, float* part, float* mu, float* s2, hipStream_t s);
-hipError_t launch_col_stats(const float* feats, int64_t N, int F, float* mu, float* sd, hipStream_t s);
+// Feature moments in fp64 (mean f and mean f^2 per cell and feature: their
+// difference, the variance, cancels when the mean dominates).
+// part: scratch of C * ceil(S / 64) * 2 * F doubles.
+hipError_t launch_moments(const float* feats, int C, int S, int F, double* part, double* mu, double* s2,
+                          hipStream_t s);
+hipError_t launch_col_stats(const float* feats, int64_t N, int F, double* mu, double* sd, hipStream_t s);
 
 struct EsArgs {
-  const float* mu;        // [cells][F]
-  const float* s2;
-  const float* mu_r;
-  const float* sd_r;
+  const double* mu;       // [cells][F]
+  const double* s2;
+  const double* mu_r;
+  const double* sd_r;
   const int32_t* nbr;
   float* w;               // [C][5] in place
   float* w_out;

@@ -71,3 +71,23 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
     return LIPZ_E_HIP;
   return LIPZ_OK;
 }
+
+extern "C" lipz_status lipz_test_es_select(void* hip_stream, const float* d_fit, const float* d_sets,
+                                           float* d_params, int32_t n_units, int32_t n_pairs, int64_t P,
+                                           int64_t stride, float clip) {
+  if (!d_fit || !d_sets || !d_params || n_units < 1 || n_units > 65535 || n_pairs < 1 || n_pairs > 64 || P < 1 ||
+      stride < P || !(clip >= 0.f))
+    return LIPZ_E_INVAL;
+  NesArgs a;
+  memset(&a, 0, sizeof(a));
+  a.p = d_params;
+  a.sets = (float*)d_sets;
+  a.fit = (float*)d_fit;
+  a.stride = stride;
+  a.P = P;
+  a.n = n_pairs;
+  a.c0 = 0;
+  a.C = n_units;
+  a.clip = clip;
+  return launch_es_select(a, (hipStream_t)hip_stream) == hipSuccess ? LIPZ_OK : LIPZ_E_HIP;
+}

@@ -118,6 +118,7 @@ _SIGS = {
     "lipz_test_gemm": (_i32, [_vp, _vp, _i32, _i32, _i32, _vp, _i32, _i32, _i32, _vp, _i32, _i32,
                               _vp, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                               _f32, _f32, _f32, _i32]),
+    "lipz_test_es_select": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _i64, _i64, _f32]),
 }
 
 _lib = None
@@ -278,6 +279,11 @@ def lipz_test_gemm(stream, d_desc, M, N, K, d_A, lda, a_trans, ones_row, d_B, ld
                                                 slope, _p(d_bias), _p(d_aux), _p(d_m), _p(d_v), _p(d_lr),
                                                 _p(d_t), step_local, beta1, beta2, eps, tile_rows),
                   "lipz_test_gemm")
+
+
+def lipz_test_es_select(stream, d_fit, d_sets, d_params, n_units, n_pairs, P, stride, clip=0.0):
+    return _check(load_library().lipz_test_es_select(_p(stream), _p(d_fit), _p(d_sets), _p(d_params), n_units,
+                                                     n_pairs, P, stride, clip), "lipz_test_es_select")
 
 
 def lipz_test_plan_bounds(cfg, n_samples):

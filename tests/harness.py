@@ -195,3 +195,34 @@ def check_selection(S, gsel, ofg, ofd, gen):
                 else:
                     assert gsel[u, r] in [S.pool[c, k] for k in drawn]
     return n_decisive
+
+
+def check_mixture(S, st, stats, gen, w, sc, acc, tol=1e-4):
+    """GPU mixture ES step (w [C][5], kept score sc [C], accepted acc [C])
+    from state st against the oracle's: for every cell the oracle scores the
+    current weights and the proposal; where they differ by more than tol
+    relative the decision must match, the kept score agree to tol relative
+    and the kept weights to 1e-6 (fp32 storage of the fp64 proposal).  On a
+    nearer tie the GPU may take either branch, but its score and weights must
+    then be that branch's.  Returns the number of decisive cells."""
+    from oracle import mixture
+
+    mu, s2 = mixture.generator_moments(S, st, stats["P"], gen)
+    n_decisive = 0
+    for c in range(S.C):
+        ks = S.nbr[c]
+        cur = mixture.score(st.w[c], mu[ks], s2[ks], stats["mu_r"], stats["sd_r"])
+        wp = mixture.propose(S, st.w[c], c, gen)
+        new = None if wp is None else mixture.score(wp, mu[ks], s2[ks], stats["mu_r"], stats["sd_r"])
+        if new is None or abs(new - cur) > tol * max(new, cur):
+            n_decisive += 1
+            o_acc = new is not None and new < cur
+            assert acc[c] == int(o_acc), (c, cur, new)
+        if acc[c]:
+            assert wp is not None, c
+            assert abs(sc[c] - new) <= tol * new, (c, sc[c], new)
+            assert np.all(np.abs(w[c] - wp) <= 1e-6), (c, w[c], wp)
+        else:
+            assert abs(sc[c] - cur) <= tol * cur, (c, sc[c], cur)
+            assert np.array_equal(w[c], st.w[c].astype(np.float32)), c
+    return n_decisive

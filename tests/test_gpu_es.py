@@ -25,6 +25,7 @@ pytestmark = pytest.mark.gpu
 if not torch.cuda.is_available():  # pragma: no cover - collected on CPU, skipped there
     pytest.skip("no GPU", allow_module_level=True)
 
+import paper_1811_12843_amd as L  # noqa: E402
 from harness import GpuGrid, fp32_state, per_tensor_rel  # noqa: E402
 
 RAGGED = dict(rows=2, cols=3, z_dim=7, x_dim=37, g_hidden=[33, 70], d_hidden=[45, 19], batch=19,
@@ -127,3 +128,32 @@ def test_es_generation_matches_oracle():
             cur = nxt
     for f in ("Gp", "Dp", "Gt", "Dt"):
         assert np.array_equal(getattr(cur, f), getattr(got4, f)), f
+
+
+@pytest.mark.parametrize("losses", [
+    [np.nan, 1.0, 2.0, 3.0, 2.5],            # a NaN first mutant loses; the better later one is kept
+    [np.nan, np.nan, np.nan, np.nan, 2.0],   # only NaN mutants: the parent stays
+    [1.5, np.nan, 0.5, 0.5, np.nan],         # a NaN parent loses to the best finite mutant
+    [np.nan] * 5,                            # all NaN: the parent stays
+    [2.0, 1.0, 1.0, 3.0, 1.0],               # equal losses: the parent stays
+])
+def test_plus_selection_ranks_nan_last(losses):
+    """The selection kernel on hand-made losses with NaN entries against the
+    oracle's rule (NaN ranks as +infinity): the kept candidate's values land
+    in the parameter row, bit for bit."""
+    n, P, stride = 2, 37, 40
+    f = np.array(losses, dtype=np.float32)
+    g = np.random.default_rng(7)
+    sets = g.normal(size=(1, 2 * n, stride)).astype(np.float32)
+    parent = g.normal(size=(1, stride)).astype(np.float32)
+    d_f = torch.from_numpy(f).cuda()
+    d_s = torch.from_numpy(sets).cuda()
+    d_p = torch.from_numpy(parent.copy()).cuda()
+    L.lipz_test_es_select(torch.cuda.current_stream().cuda_stream, d_f.data_ptr(), d_s.data_ptr(), d_p.data_ptr(),
+                          1, n, P, stride)
+    torch.cuda.synchronize()
+    w, _ = es.choose(f.astype(np.float64))
+    expect = parent[0].copy()
+    if w < 2 * n:
+        expect[:P] = sets[0, w, :P]
+    assert np.array_equal(d_p.cpu().numpy()[0], expect)

@@ -24,7 +24,7 @@ if not torch.cuda.is_available():  # pragma: no cover - collected on CPU, skippe
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_1811_12843_amd as L  # noqa: E402
-from harness import GpuGrid, check_selection, fp32_state, per_tensor_rel, rel_err  # noqa: E402
+from harness import GpuGrid, check_mixture, check_selection, fp32_state, per_tensor_rel, rel_err  # noqa: E402
 
 RTOL = 1e-4
 
@@ -339,9 +339,7 @@ def _generation_parity(key, **over):
             assert per_tensor_rel(getattr(got, p + "p"), getattr(ref, p + "p"), sizes) <= 1e-3
         if wl["mix_enable"]:
             w, sc, acc = gg.mixture(gen)
-            ow, osc, oacc = mixture.update(S, fp32_state(got), stats, gen)
-            assert np.all(np.abs(sc - osc) <= 1e-3 * np.abs(osc))
-            assert np.all(np.abs(w - ow) <= 1e-5)
+            check_mixture(S, fp32_state(got), stats, gen, w, sc, acc)
 
 
 def test_generation_ring8_2x2_full():
@@ -409,13 +407,14 @@ def test_generation_full_length_each_step(key, n_steps):
         if wl["mix_enable"]:
             stats = mixture.real_stats(S, data)
             w, sc, acc = gg.mixture(gen)
-            ow, osc, oacc = mixture.update(S, cur, stats, gen)
-            assert np.all(np.abs(sc - osc) <= 1e-3 * np.abs(osc))
-            assert np.all(np.abs(w - ow) <= 1e-5)
+            assert check_mixture(S, cur, stats, gen, w, sc, acc) > 0
 
 
 @pytest.mark.parametrize("key", ["ragged_2x3", "mnist_4x4_mix"])
 def test_mixture_matches_oracle(key):
+    """Two mixture steps from random simplex weights: decisions, kept scores
+    (1e-4 relative) and weights wherever the oracle's score margin exceeds
+    1e-4; at least a quarter of the cells must be decisive."""
     wl, data, S = _setup(key)
     wl = dict(wl, mix_enable=1, mix_samples=1024 if key == "mnist_4x4_mix" else 77, mix_feat_dim=64 if key == "mnist_4x4_mix" else 9)
     S = coevo.Setup(wl, len(data))
@@ -429,20 +428,33 @@ def test_mixture_matches_oracle(key):
         gg.set_state(st)
         for gen in (0, 1):
             w, sc, acc = gg.mixture(gen)
-            mu, s2 = mixture.generator_moments(S, st, stats["P"], gen)
-            ow, osc, oacc = mixture.update(S, st, stats, gen)
-            for c in range(S.C):
-                ks = S.nbr[c]
-                cur = mixture.score(st.w[c], mu[ks], s2[ks], stats["mu_r"], stats["sd_r"])
-                wp = mixture.propose(S, st.w[c], c, gen)
-                if wp is None:
-                    continue
-                new = mixture.score(wp, mu[ks], s2[ks], stats["mu_r"], stats["sd_r"])
-                if abs(new - cur) > 1e-3 * max(new, cur):
-                    assert acc[c] == oacc[c], c
-                    assert abs(sc[c] - osc[c]) <= 1e-3 * osc[c]
-                    assert np.all(np.abs(w[c] - ow[c]) <= 1e-5)
-            st.w = w
+            n_dec = check_mixture(S, st, stats, gen, w, sc, acc)
+            print(f"  gen {gen}: {n_dec} of {S.C} cells decisive, {int(acc.sum())} accepted")
+            assert 4 * n_dec >= S.C
+            st.w = w.astype(np.float64)
+
+
+def test_mixture_large_grid_many_features():
+    """C x F = 1024 x 4096 > 2^21 feature moments (a 32x32 grid with 4096
+    features, tiny networks): every cell's moments are formed and its ES step
+    matches the oracle."""
+    wl = synth.small_workload("mnist_mlp_4x4_mix", rows=32, cols=32, z_dim=4, x_dim=16, g_hidden=[8],
+                              d_hidden=[8], batch=4, mix_samples=8, mix_feat_dim=4096,
+                              data=dict(kind="mnist_like", n=256))
+    data = synth.make_dataset(wl["data"])
+    data = np.ascontiguousarray(data[:, :wl["x_dim"]])
+    S = coevo.Setup(wl, len(data))
+    st = fp32_state(coevo.create(S))
+    g0 = np.random.default_rng(1)
+    st.w = g0.dirichlet(np.ones(5), size=S.C).astype(np.float32).astype(np.float64)
+    stats = mixture.real_stats(S, data)
+    _print_case("mixture-32x32-F4096")
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        w, sc, acc = gg.mixture(0)
+        n_dec = check_mixture(S, st, stats, 0, w, sc, acc)
+        print(f"  {n_dec} of {S.C} cells decisive, {int(acc.sum())} accepted")
+        assert 4 * n_dec >= S.C
 
 
 def test_full_size_8x8_eval_and_one_step():

@@ -24,6 +24,10 @@ def _setup(**kw):
     ([1.0, 3.0, 1.0], 2, 0.0),               # a mutant only as good as the parent: the parent stays
     ([4.0, 1.0, 1.0, 3.0, 2.0], 1, 0.0),     # equal mutants: the lower index
     ([3.0, 4.0, 2.5, 5.0, 2.0], 4, 0.5),     # the parent is best
+    ([np.nan, 1.0, 2.0], 1, 1.0),            # a NaN mutant loses; a later, better one is kept
+    ([np.nan, np.nan, 2.0], 2, np.inf),      # only NaN mutants: the parent stays
+    ([1.0, np.nan, np.nan], 0, np.inf),      # a NaN parent loses to a finite mutant
+    ([np.nan, np.nan, np.nan], 2, 0.0),      # everything NaN: the parent stays, a tie
 ])
 def test_choice_rule(f, w, margin):
     got_w, got_m = es.choose(f)
