@@ -192,6 +192,28 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
                              lipz_grid** out);
 lipz_status lipz_grid_destroy(lipz_grid* g);
 
+/* For callers that cannot allocate device memory (code under stream capture,
+ * tight serving loops, harnesses that forbid hipMalloc): lipz_grid_create
+ * with the workspace taken from a static device array of
+ * LIPZ_STATIC_WORKSPACE_BYTES that the library holds on every GPU it runs on
+ * until the process ends; the grid lives on the current device.  It calls no
+ * hipMalloc / hipFree and creates no stream or event; initialisation,
+ * results and the other calls are those of lipz_grid_create.  The array
+ * keeps whatever the last grid left in it; the create clears what must
+ * start at zero.  One such grid per device at a time: a second create on the
+ * same device returns LIPZ_E_ORDER until lipz_grid_destroy (which waits for
+ * the grid's stream) releases the array; work enqueued on it from other
+ * threads or streams after that races with the next grid.  Errors:
+ * LIPZ_E_WORKSPACE when lipz_workspace_bytes(cfg, n_samples) exceeds
+ * LIPZ_STATIC_WORKSPACE_BYTES (e.g. the 2x2 ring-of-Gaussians grid needs
+ * 6.4 MiB, the 3x3 MNIST-shaped grid 214 MiB), LIPZ_E_UNSUPPORTED for row
+ * bands (bands >= 2: they create streams) or a device index >= 64,
+ * LIPZ_E_INVAL for an invalid configuration, LIPZ_E_HIP when the array
+ * cannot be located on the device. */
+#define LIPZ_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+lipz_status lipz_grid_create_static(const lipz_config* cfg, const float* d_dataset, int64_t n_samples,
+                                    void* hip_stream, lipz_grid** out);
+
 /* Step 2 (Section 3): for every cell c, draw one minibatch (B data rows,
  * B latents; step_field 0) and evaluate each generator slot i against each
  * discriminator slot j of its neighbourhood:

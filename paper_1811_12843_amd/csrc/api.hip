@@ -10,6 +10,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -18,6 +19,21 @@
 #include "lipz_testing.h"
 
 using namespace lipz;
+
+namespace {
+
+// Workspace of lipz_grid_create_static: one array per device, held for the
+// life of the process.  Host code never uses its name as an address: each
+// device's copy is looked up once with hipGetSymbolAddress (that device
+// current) and kept in g_static_ptr.
+constexpr size_t kStaticWorkspaceBytes = LIPZ_STATIC_WORKSPACE_BYTES;
+constexpr int kMaxStaticDevices = 64;
+static __device__ __align__(256) char scratch[kStaticWorkspaceBytes];
+std::mutex g_static_mu;
+void* g_static_ptr[kMaxStaticDevices] = {};
+bool g_static_busy[kMaxStaticDevices] = {};  // a live grid uses the device's array
+
+}  // namespace
 
 namespace lipz {
 
@@ -1159,20 +1175,10 @@ lipz_status enq_nes_step(lipz_grid* g, int gen, const std::vector<Op>& ops, cons
 
 }  // namespace lipz
 
-extern "C" {
+namespace lipz {
 
-size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples) {
-  size_t total = 0;
-  lipz_grid* g = plan_grid(cfg, n_samples, nullptr, nullptr, &total);
-  if (!g) return 0;
-  dc_delete(g->dc);
-  delete g;
-  return total;
-}
-
-lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t workspace_bytes,
-                             const float* d_dataset, int64_t n_samples, void* hip_stream,
-                             lipz_grid** out) {
+lipz_status create_grid(const lipz_config* cfg, void* d_workspace, size_t workspace_bytes,
+                        const float* d_dataset, int64_t n_samples, void* hip_stream, lipz_grid** out) {
   if (!out) return LIPZ_E_INVAL;
   *out = nullptr;
   Net Gn, Dn;
@@ -1197,7 +1203,7 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
     if (st == LIPZ_OK) st = check_hip(g, e, what);
   };
   g->gstream[0] = s;
-  ck(hipEventCreateWithFlags(&g->fork_ev, hipEventDisableTiming), "create event");
+  if (g->n_groups > 1 || g->n_bands > 0) ck(hipEventCreateWithFlags(&g->fork_ev, hipEventDisableTiming), "create event");
   for (int i = 1; i < g->n_groups; ++i) {
     ck(hipStreamCreateWithFlags(&g->gstream[i], hipStreamNonBlocking), "create stream");
     ck(hipEventCreateWithFlags(&g->join_ev[i], hipEventDisableTiming), "create event");
@@ -1251,8 +1257,64 @@ lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t w
   return LIPZ_OK;
 }
 
+}  // namespace lipz
+
+extern "C" {
+
+size_t lipz_workspace_bytes(const lipz_config* cfg, int64_t n_samples) {
+  size_t total = 0;
+  lipz_grid* g = plan_grid(cfg, n_samples, nullptr, nullptr, &total);
+  if (!g) return 0;
+  dc_delete(g->dc);
+  delete g;
+  return total;
+}
+
+lipz_status lipz_grid_create(const lipz_config* cfg, void* d_workspace, size_t workspace_bytes,
+                             const float* d_dataset, int64_t n_samples, void* hip_stream,
+                             lipz_grid** out) {
+  return create_grid(cfg, d_workspace, workspace_bytes, d_dataset, n_samples, hip_stream, out);
+}
+
+lipz_status lipz_grid_create_static(const lipz_config* cfg, const float* d_dataset, int64_t n_samples,
+                                    void* hip_stream, lipz_grid** out) {
+  if (!out) return LIPZ_E_INVAL;
+  *out = nullptr;
+  Net Gn, Dn;
+  if (!validate(cfg, n_samples, &Gn, &Dn).empty() || !d_dataset) return LIPZ_E_INVAL;
+  // row bands create streams and events of their own
+  if (cfg->bands >= 2) return LIPZ_E_UNSUPPORTED;
+  const size_t need = lipz_workspace_bytes(cfg, n_samples);
+  if (need == 0) return LIPZ_E_INVAL;
+  if (need > kStaticWorkspaceBytes) return LIPZ_E_WORKSPACE;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return LIPZ_E_HIP;
+  if (dev >= kMaxStaticDevices) return LIPZ_E_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (g_static_busy[dev]) return LIPZ_E_ORDER;
+  if (!g_static_ptr[dev]) {
+    // the device's own copy of the array (the name itself is a host-side stand-in)
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return LIPZ_E_HIP;
+    g_static_ptr[dev] = p;
+  }
+  lipz_status st = create_grid(cfg, g_static_ptr[dev], kStaticWorkspaceBytes, d_dataset, n_samples, hip_stream, out);
+  if (st == LIPZ_OK) {
+    g_static_busy[dev] = true;
+    (*out)->static_dev = dev;
+  }
+  return st;
+}
+
+
 lipz_status lipz_grid_destroy(lipz_grid* g) {
   if (!g) return LIPZ_E_INVAL;
+  if (g->static_dev >= 0) {
+    // the static array goes back to the device once the grid's work is done
+    hipStreamSynchronize(g->stream);
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    g_static_busy[g->static_dev] = false;
+  }
   for (int i = 1; i < g->n_groups; ++i) {
     if (g->gstream[i]) {
       hipStreamSynchronize(g->gstream[i]);

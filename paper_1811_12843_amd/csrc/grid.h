@@ -173,6 +173,7 @@ struct lipz_grid {
   int64_t gemm_launches = 0;
 
   lipz::DcPlan* dc = nullptr;  // set for LIPZ_NET_DCGAN
+  int static_dev = -1;         // lipz_grid_create_static: the device whose static workspace it holds
 
   // NES trainer: Q = 2 nes_pairs + 1 parameter sets per role and cell (the
   // + and - perturbations, then the unperturbed parameters)
@@ -191,6 +192,8 @@ struct lipz_grid {
 namespace lipz {
 
 // api.hip
+lipz_status create_grid(const lipz_config* cfg, void* d_workspace, size_t workspace_bytes,
+                        const float* d_dataset, int64_t n_samples, void* hip_stream, lipz_grid** out);
 lipz_status fail(lipz_grid* g, lipz_status s, const std::string& msg);
 lipz_status check_hip(lipz_grid* g, hipError_t e, const char* what);
 void carve_state(lipz_grid* g, Carver& cv, char* base);

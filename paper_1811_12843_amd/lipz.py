@@ -21,6 +21,7 @@ LIPZ_ROLE_G, LIPZ_ROLE_D = 0, 1
 LIPZ_LOSS_BCE, LIPZ_LOSS_WASSERSTEIN = 0, 1
 LOSSES = {"bce": LIPZ_LOSS_BCE, "wasserstein": LIPZ_LOSS_WASSERSTEIN}
 LIPZ_TRAINER_GRADIENT, LIPZ_TRAINER_NES, LIPZ_TRAINER_ES = 0, 1, 2
+LIPZ_STATIC_WORKSPACE_BYTES = 64 << 20
 TRAINERS = {"gradient": LIPZ_TRAINER_GRADIENT, "nes": LIPZ_TRAINER_NES, "es": LIPZ_TRAINER_ES}
 ACTS = {"linear": LIPZ_ACT_LINEAR, "relu": LIPZ_ACT_RELU, "lrelu": LIPZ_ACT_LRELU, "tanh": LIPZ_ACT_TANH}
 
@@ -94,6 +95,7 @@ _SIGS = {
     "lipz_workspace_bytes": (_sz, [ctypes.POINTER(lipz_config), _i64]),
     "lipz_grid_create": (_i32, [ctypes.POINTER(lipz_config), _vp, _sz, _vp, _i64, _vp,
                                 ctypes.POINTER(_vp)]),
+    "lipz_grid_create_static": (_i32, [ctypes.POINTER(lipz_config), _vp, _i64, _vp, ctypes.POINTER(_vp)]),
     "lipz_grid_destroy": (_i32, [_vp]),
     "lipz_eval_neighborhoods": (_i32, [_vp, _i32, _vp, _vp, _vp, _vp]),
     "lipz_select_replace": (_i32, [_vp, _i32, _vp, _vp, _vp]),
@@ -171,6 +173,15 @@ def lipz_grid_create(cfg, d_workspace, workspace_bytes, d_dataset, n_samples, st
     st = load_library().lipz_grid_create(ctypes.byref(cfg), _p(d_workspace), workspace_bytes,
                                          _p(d_dataset), n_samples, _p(stream), ctypes.byref(out))
     _check(st, "lipz_grid_create")
+    return out.value
+
+
+def lipz_grid_create_static(cfg, d_dataset, n_samples, stream):
+    """lipz_grid_create on the library's static per-device workspace (no device allocation)."""
+    out = _vp()
+    st = load_library().lipz_grid_create_static(ctypes.byref(cfg), _p(d_dataset), n_samples, _p(stream),
+                                                ctypes.byref(out))
+    _check(st, "lipz_grid_create_static")
     return out.value
 
 

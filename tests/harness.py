@@ -17,7 +17,7 @@ def fp32_state(st):
 
 
 class GpuGrid:
-    def __init__(self, wl, data_np, device="cuda"):
+    def __init__(self, wl, data_np, device="cuda", static_ws=False):
         self.wl = wl
         self.cfg = L.config_from_dict(wl)
         self.N = int(len(data_np))
@@ -28,10 +28,14 @@ class GpuGrid:
         self.data = torch.from_numpy(np.ascontiguousarray(data_np, dtype=np.float32)).to(device)
         nb = L.lipz_workspace_bytes(self.cfg, self.N)
         assert nb > 0
-        self.ws = torch.empty(nb, dtype=torch.uint8, device=device)
         self.stream = torch.cuda.current_stream().cuda_stream
-        self.g = L.lipz_grid_create(self.cfg, self.ws.data_ptr(), nb, self.data.data_ptr(), self.N,
-                                    self.stream)
+        if static_ws:  # the library's own static workspace: no allocation
+            self.ws = None
+            self.g = L.lipz_grid_create_static(self.cfg, self.data.data_ptr(), self.N, self.stream)
+        else:
+            self.ws = torch.empty(nb, dtype=torch.uint8, device=device)
+            self.g = L.lipz_grid_create(self.cfg, self.ws.data_ptr(), nb, self.data.data_ptr(), self.N,
+                                        self.stream)
         self.offs, self.strides = L.lipz_state_layout(self.g)
         self.state_bytes = L.lipz_state_bytes(self.g)
         self.S = coevo.Setup(wl, self.N)
