@@ -236,19 +236,29 @@ def evaluate(S, st, data, gen):
     L = np.zeros((C, n, n))
     Lg = np.zeros((C, n, n))
     for c in range(C):
-        _, x, z = sample(S, data, c, gen, 0)
-        fakes = [g_forward(S, st.Gp[S.pool[c, i]], z)[1] for i in range(n)]
-        for j in range(n):
-            dp = st.Dp[S.pool[c, j]]
-            a_r = d_logits(S, dp, x)[1]
-            for i in range(n):
-                L[c, i, j], Lg[c, i, j] = pair_losses(S, a_r, d_logits(S, dp, fakes[i])[1])
+        L[c], Lg[c] = evaluate_cell(S, st, data, gen, c)
     fit_d = L.mean(axis=1)
     if S.wl["fitness_mode"] == 0:
         fit_g = -L.mean(axis=2)
     else:
         fit_g = Lg.mean(axis=2)
     return L, Lg, fit_g, fit_d
+
+
+def evaluate_cell(S, st, data, gen, c):
+    """The n x n pair losses (L, Lg) of cell c's neighbourhood on its
+    evaluation minibatch (one cell of evaluate)."""
+    n = S.n
+    L = np.zeros((n, n))
+    Lg = np.zeros((n, n))
+    _, x, z = sample(S, data, c, gen, 0)
+    fakes = [g_forward(S, st.Gp[S.pool[c, i]], z)[1] for i in range(n)]
+    for j in range(n):
+        dp = st.Dp[S.pool[c, j]]
+        a_r = d_logits(S, dp, x)[1]
+        for i in range(n):
+            L[i, j], Lg[i, j] = pair_losses(S, a_r, d_logits(S, dp, fakes[i])[1])
+    return L, Lg
 
 
 def tournament_draw(S, cell, gen, tag, member=0):
@@ -330,27 +340,34 @@ def train_step(S, st, data, gen, step):
     """Step 3 (training part): one discriminator and one generator Adam step for
     every training unit (individual pair) c, in place.  Returns losses[U, 2] =
     (L_D, L_G) before the updates."""
-    B = S.B
     losses = np.zeros((S.U, 2))
     for c in range(S.U):
-        _, x, z = sample(S, data, c, gen, step + 1)
-        gcache, xf = g_forward(S, st.Gp[c], z)
-        # discriminator step on real and detached fake
-        cache_r, a_r = d_logits(S, st.Dp[c], x)
-        cache_f, a_f = d_logits(S, st.Dp[c], xf)
-        losses[c, 0] = pair_losses(S, a_r, a_f)[0]
-        d_r, d_f = d_loss_grads(S, a_r, a_f)
-        g_r, _ = S.Dnet.backward(st.Dp[c], cache_r, d_r)
-        g_f, _ = S.Dnet.backward(st.Dp[c], cache_f, d_f)
-        st.Dt[c] = adam(S, st.Dp[c], st.Dm[c], st.Dv[c], st.Dt[c], st.Dlr[c], g_r + g_f)
-        if S.loss == "wasserstein":
-            np.clip(st.Dp[c], -S.clip, S.clip, out=st.Dp[c])
-        # generator step (non-saturating) against the updated discriminator, same z
-        cache2, a2 = d_logits(S, st.Dp[c], xf)
-        losses[c, 1] = pair_losses(S, a2, a2)[1]
-        _, dxf = S.Dnet.backward(st.Dp[c], cache2, g_loss_grad(S, a2), want_input_grad=True)
-        gG, _ = S.Gnet.backward(st.Gp[c], gcache, dxf)
-        st.Gt[c] = adam(S, st.Gp[c], st.Gm[c], st.Gv[c], st.Gt[c], st.Glr[c], gG)
+        losses[c] = train_unit(S, st, data, gen, step, c)
+    return losses
+
+
+def train_unit(S, st, data, gen, step, c):
+    """Training step `step` of unit c alone (one iteration of train_step), in
+    place on st's row c; returns (L_D, L_G) before the updates."""
+    losses = np.zeros(2)
+    _, x, z = sample(S, data, c, gen, step + 1)
+    gcache, xf = g_forward(S, st.Gp[c], z)
+    # discriminator step on real and detached fake
+    cache_r, a_r = d_logits(S, st.Dp[c], x)
+    cache_f, a_f = d_logits(S, st.Dp[c], xf)
+    losses[0] = pair_losses(S, a_r, a_f)[0]
+    d_r, d_f = d_loss_grads(S, a_r, a_f)
+    g_r, _ = S.Dnet.backward(st.Dp[c], cache_r, d_r)
+    g_f, _ = S.Dnet.backward(st.Dp[c], cache_f, d_f)
+    st.Dt[c] = adam(S, st.Dp[c], st.Dm[c], st.Dv[c], st.Dt[c], st.Dlr[c], g_r + g_f)
+    if S.loss == "wasserstein":
+        np.clip(st.Dp[c], -S.clip, S.clip, out=st.Dp[c])
+    # generator step (non-saturating) against the updated discriminator, same z
+    cache2, a2 = d_logits(S, st.Dp[c], xf)
+    losses[1] = pair_losses(S, a2, a2)[1]
+    _, dxf = S.Dnet.backward(st.Dp[c], cache2, g_loss_grad(S, a2), want_input_grad=True)
+    gG, _ = S.Gnet.backward(st.Gp[c], gcache, dxf)
+    st.Gt[c] = adam(S, st.Gp[c], st.Gm[c], st.Gv[c], st.Gt[c], st.Glr[c], gG)
     return losses
 
 

@@ -1,15 +1,23 @@
 """The row-band executor (lipz_run_generations with bands >= 2, the paper's
-asynchronous cells scheduled by neighbour readiness) against the one-batch
-schedule: the same generations give the same state bit for bit.
+asynchronous cells scheduled by neighbour readiness) against the oracle and
+against the one-batch schedule: the same generations give the same state bit
+for bit.
 
-The one-batch schedule is itself checked against the oracle call by call
-(tests/test_gpu_parity.py, tests/test_gpu_subpop.py); here it is also checked
-against the entry points called one by one.
+Against the oracle: one banded generation from a state loaded on both sides.
+Its selections are read back from a banded run without training steps (each
+cell's individuals are then bit-exact copies of their sources); the
+tournaments must agree with the oracle's where decisive, and the oracle
+replays them.  After evaluation, selection, the training steps and the
+mixture step: parameters 1e-3 per tensor, step counts bit-exact, learning
+rates 1e-6, mixture weights where the oracle's ES margin is decisive.  The
+one-batch schedule is also checked against the entry points called one by
+one.
 """
 import numpy as np
 import pytest
 
 import synth
+from oracle import coevo, mixture
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -18,7 +26,7 @@ if not torch.cuda.is_available():  # pragma: no cover - collected on CPU, skippe
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_1811_12843_amd as L  # noqa: E402
-from harness import GpuGrid  # noqa: E402
+from harness import GpuGrid, check_selection, fp32_state, per_tensor_rel  # noqa: E402
 
 RAGGED = dict(z_dim=7, x_dim=37, g_hidden=[33, 70], d_hidden=[45, 19], batch=19,
               data=dict(kind="mnist_like", n=3000))
@@ -80,3 +88,73 @@ def test_one_batch_matches_the_entry_points():
             b.elite(gen)
         got = b.save_blob()
     assert np.array_equal(got, ref)
+
+
+def _sources(before, after, S):
+    """Source individual of every unit and role: the row of `before` that the
+    unit's parameters in `after` copy bit for bit."""
+    sel = np.zeros((S.U, 2), dtype=np.int64)
+    for r, f in enumerate(("Gp", "Dp")):
+        a, b = getattr(after, f), getattr(before, f)
+        for u in range(S.U):
+            hits = [k for k in range(S.U) if np.array_equal(a[u], b[k])]
+            assert len(hits) == 1, (u, f, hits)
+            sel[u, r] = hits[0]
+    return sel
+
+
+@pytest.mark.parametrize("key", ["mnist_4x4_mix_b2", "ragged_8x3_b4"])
+def test_banded_generation_matches_oracle(key):
+    wl, data = _setup(key)
+    steps, gen = 3, 1
+    wl = dict(wl, steps=steps)
+    S = coevo.Setup(wl, len(data))
+    st = coevo.create(S)
+    for s in range(2):  # a trained state
+        coevo.train_step(S, st, data, 0, 60 + s)
+    st = fp32_state(st)
+    if wl["mix_enable"]:
+        st.w = np.random.default_rng(2).dirichlet(np.ones(5), size=S.C).astype(np.float32).astype(np.float64)
+    print(f"[case] banded generation vs oracle key={key}", flush=True)
+    # the banded schedule's selections: a generation without training steps
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        L.lipz_run_generations(gg.g, gen, 1, 0)
+        assert gg.sync() == L.LIPZ_OK
+        gsel = _sources(st, gg.get_state(), S)
+    _, _, ofg, ofd = coevo.evaluate(S, st, data, gen)
+    n_dec = check_selection(S, gsel, ofg, ofd, gen)
+    assert n_dec > 0
+    # the whole banded generation
+    with GpuGrid(wl, data) as gg:
+        gg.set_state(st)
+        L.lipz_run_generations(gg.g, gen, 1, steps)
+        assert gg.sync() == L.LIPZ_OK
+        got = gg.get_state()
+    ref, _ = coevo.select_replace(S, st, ofg, ofd, gen, forced=gsel)
+    for s in range(steps):
+        coevo.train_step(S, ref, data, gen, s)
+    assert np.array_equal(got.Gt, ref.Gt) and np.array_equal(got.Dt, ref.Dt)
+    assert np.all(np.abs(got.Glr - ref.Glr) <= 1e-6 * np.abs(ref.Glr))
+    assert np.all(np.abs(got.Dlr - ref.Dlr) <= 1e-6 * np.abs(ref.Dlr))
+    for p, sizes in (("G", S.g_sizes), ("D", S.d_sizes)):
+        e = per_tensor_rel(getattr(got, p + "p"), getattr(ref, p + "p"), sizes)
+        print(f"  {p}: params rel {e:.2e}")
+        assert e <= 1e-3
+    if wl["mix_enable"]:
+        stats = mixture.real_stats(S, data)
+        # the ES step scores the generators the banded run trained (shared state)
+        mu, s2 = mixture.generator_moments(S, got, stats["P"], gen)
+        n_dec = 0
+        for c in range(S.C):
+            ks = S.nbr[c]
+            cur = mixture.score(st.w[c], mu[ks], s2[ks], stats["mu_r"], stats["sd_r"])
+            wp = mixture.propose(S, st.w[c], c, gen)
+            new = None if wp is None else mixture.score(wp, mu[ks], s2[ks], stats["mu_r"], stats["sd_r"])
+            kept_old = np.array_equal(got.w[c], st.w[c])
+            if new is None or abs(new - cur) > 1e-4 * max(new, cur):
+                n_dec += 1
+                assert kept_old == (new is None or not new < cur), c
+            if not kept_old:
+                assert np.all(np.abs(got.w[c] - wp) <= 1e-6), c
+        assert 4 * n_dec >= S.C

@@ -7,7 +7,8 @@ library), with the tolerances of the MLP parity tests:
   copies, indices, counts   bit-exact
 Small grids cover several tiles, ragged tails, multi-split weight gradients
 and the element-wise (3-channel image) paths; the 64x64 test runs the 4x4
-workload's own shapes and checks sampled outputs one by one."""
+workload's own shapes and checks every output of an evaluation, a selection
+and a training step."""
 import numpy as np
 import pytest
 
@@ -21,7 +22,8 @@ if not torch.cuda.is_available():  # pragma: no cover - collected on CPU, skippe
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_1811_12843_amd as L  # noqa: E402
-from harness import GpuGrid, fp32_state, rel_err  # noqa: E402
+from harness import GpuGrid, check_selection, fp32_state, rel_err  # noqa: E402
+from oracle_pool import OraclePool  # noqa: E402
 
 RTOL = 1e-4
 
@@ -210,11 +212,14 @@ def test_select_replace_copies_individuals_bit_exactly():
             assert np.array_equal(getattr(got, f), getattr(new, f)), f
 
 
-def test_full_size_64x64_4x4_sampled():
+def test_full_size_64x64_4x4(tmp_path):
     """The 4x4 workload's shapes (64x64x3 images, G 100-512-256-128-64-3, D
-    3-64-128-256-512-1, batch 64): sampled pair losses of one evaluation and
-    cell 0's losses and parameters after one training step, each computed by
-    the oracle on its own."""
+    3-64-128-256-512-1, batch 64), every output checked: all 16 x 25 pair
+    losses L and Lg of one evaluation and the fitness of both roles (1e-4),
+    the tournaments (where decisive), the replacement (bit for bit), and one
+    training step of every cell from the shared state: losses 1e-4, every
+    parameter section 1e-3, its update 5e-2.  The oracle (about 10 TFLOP in
+    fp64) runs cell by cell in a pool of CPU worker processes."""
     wl = synth.workload("celeba_dcgan_4x4")
     wl["data"] = dict(wl["data"], n=2048)
     data = synth.make_dataset(wl["data"])
@@ -222,8 +227,12 @@ def test_full_size_64x64_4x4_sampled():
     n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(wl), len(data))
     assert n_bad == 0, msg
     st = coevo.create(S)
-    # Adam moments of a trained individual, so one step is not just lr * sign(g)
+    # a trained individual: non-zero biases and betas (a section that starts at
+    # zero would compare only its one-step update), and Adam moments, so one
+    # step is not just lr * sign(g)
     r = np.random.default_rng(3)
+    st.Gp += 0.01 * r.normal(size=st.Gp.shape)
+    st.Dp += 0.01 * r.normal(size=st.Dp.shape)
     for f in ("G", "D"):
         m = getattr(st, f + "m")
         m[...] = 1e-3 * r.normal(size=m.shape)
@@ -235,30 +244,34 @@ def test_full_size_64x64_4x4_sampled():
     with GpuGrid(wl, data) as gg:
         gg.set_state(st)
         Lm, Lg, fg, fd = gg.eval(0)
-        assert np.all(np.isfinite(Lm))
-        for c, i, j in ((0, 0, 0), (5, 2, 3), (15, 4, 1)):
-            _, x, z = coevo.sample(S, data, c, 0, 0)
-            xf = coevo.g_forward(S, st.Gp[S.nbr[c, i]], z)[1]
-            dp = st.Dp[S.nbr[c, j]]
-            ar = coevo.d_logits(S, dp, x)[1]
-            af = coevo.d_logits(S, dp, xf)[1]
-            oL = coevo.softplus(-ar).mean() + coevo.softplus(af).mean()
-            oLg = coevo.softplus(-af).mean()
-            print(f"  L[{c},{i},{j}] gpu {Lm[c, i, j]:.7f} oracle {oL:.7f}")
-            assert abs(Lm[c, i, j] - oL) <= RTOL * abs(oL)
-            assert abs(Lg[c, i, j] - oLg) <= RTOL * abs(oLg)
-        glosses = gg.train(0, 0, 1)
+        gsel, _ = gg.select(0)
+        selected = gg.get_state()
+        glosses = gg.train(0, 0, 1)[0]
         got = gg.get_state()
-    # cell 0 alone: a 1x1 grid draws the same samples (cell id 0) from the same state
-    wl1 = dict(wl, rows=1, cols=1)
-    S1 = coevo.Setup(wl1, len(data))
-    st1 = coevo.State(**{f: np.array(getattr(st, f)[:1]) for f in coevo.State.FIELDS})
-    ol = coevo.train_step(S1, st1, data, 0, 0)
-    print(f"  cell 0 losses gpu {glosses[0, 0]} oracle {ol[0]}")
-    assert np.all(np.abs(glosses[0, 0] - ol[0]) <= RTOL * np.abs(ol[0]))
+    with OraclePool(wl, data, st, tmp_path) as pool:
+        oL, oLg, ofg, ofd = pool.evaluate(0)
+    print(f"  L max rel {np.max(np.abs(Lm - oL) / np.abs(oL)):.2e}, Lg max rel {np.max(np.abs(Lg - oLg) / np.abs(oLg)):.2e}")
+    assert np.all(np.abs(Lm - oL) <= RTOL * np.abs(oL))
+    assert np.all(np.abs(Lg - oLg) <= RTOL * np.abs(oLg))
+    assert np.all(np.abs(fg - ofg) <= RTOL * np.abs(ofg))
+    assert np.all(np.abs(fd - ofd) <= RTOL * np.abs(ofd))
+    n_dec = check_selection(S, gsel, ofg, ofd, 0)
+    print(f"  {n_dec} of {2 * S.C} tournaments decisive")
+    ref, _ = coevo.select_replace(S, st, ofg, ofd, 0, forced=gsel)
+    for f in ("Gp", "Gm", "Gv", "Dp", "Dm", "Dv", "Gt", "Dt"):
+        assert np.array_equal(getattr(selected, f), getattr(ref, f)), f
+    for f in ("Glr", "Dlr"):
+        assert np.all(np.abs(getattr(selected, f) - getattr(ref, f)) <= 1e-6 * np.abs(getattr(ref, f))), f
+    del st
+    shared = selected  # the training step from the state the GPU holds after selection
+    with OraclePool(wl, data, shared, tmp_path) as pool:
+        olosses, new = pool.train_step(0, 0)
+    print(f"  losses max rel {np.max(np.abs(glosses - olosses) / np.abs(olosses)):.2e}")
+    assert np.all(np.abs(glosses - olosses) <= RTOL * np.abs(olosses))
+    assert np.array_equal(got.Gt, new.Gt) and np.array_equal(got.Dt, new.Dt)
     for p, net in (("G", S.Gnet), ("D", S.Dnet)):
-        e, where = _worst(getattr(got, p + "p")[:1], getattr(st1, p + "p"), net.arch)
-        du, wdu = _worst(getattr(got, p + "p")[:1] - getattr(st, p + "p")[:1],
-                         getattr(st1, p + "p") - getattr(st, p + "p")[:1], net.arch)
+        e, where = _worst(getattr(got, p + "p"), getattr(new, p + "p"), net.arch)
+        du, wdu = _worst(getattr(got, p + "p") - getattr(shared, p + "p"),
+                         getattr(new, p + "p") - getattr(shared, p + "p"), net.arch)
         print(f"  {p}: params rel {e:.2e} ({where}), updates rel {du:.2e} ({wdu})")
         assert e <= 1e-3 and du <= 5e-2
