@@ -14,6 +14,10 @@ Prints one JSON line:
                    traffic = HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE
                    passes stored in profiles/ (null once the GEMM source changed)
   cpu_baseline     the oracle (fp64 NumPy) on this host's cores, on a bounded sample
+  per_config       the other workloads of the benchmark (the 2x2 ring grid, the 3x3
+                   and 8x8 MNIST-shaped grids, the 64x64 DCGAN grid), one warm-up
+                   and one timed generation each: generations/s, ms/generation,
+                   mfma_frac, and the matrix-core kernels' own rate and fraction
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
@@ -236,6 +240,126 @@ def mfma_ceiling(torch, L, n=8192, reps=6):
     return {"shape": [n, n, n], "vendor_tflops": vendor, "vendor_rel_err": vendor_err, "own_gemm_tflops": ours}
 
 
+# The configurations reported beside the headline one (dataset rows; 0 = the
+# workload's own): the 2x2 ring grid, the 3x3 and 8x8 MNIST-shaped grids and
+# the 64x64 DCGAN grid on a small synthetic image set (minibatch rows are drawn
+# uniformly, so the work per step does not depend on the dataset size).
+PER_CONFIG = {"mnist_mlp_3x3": 0, "mnist_mlp_4x4_mix": 0, "mnist_mlp_8x8": 0, "ring8_mlp_2x2": 0,
+              "celeba_dcgan_4x4": 512}
+_DATA = {}
+
+
+def run_workload(L, torch, name, steps, warmup, eval_reps, data_n=0, bands=0):
+    """Time `steps` generations of workload `name` after `warmup` untimed ones,
+    the evaluation alone, and the matrix-core kernels in an instrumented pass."""
+    import synth
+
+    wl = synth.workload(name)
+    if bands:
+        wl["bands"] = bands
+    n_data = data_n or (8192 if wl["net"] == "dcgan" else wl["data"]["n"])
+    wl["data"] = dict(wl["data"], n=n_data)
+    key = json.dumps(wl["data"], sort_keys=True)
+    if key not in _DATA:
+        _DATA.clear()
+        _DATA[key] = synth.make_dataset(wl["data"])
+    data_np = _DATA[key]
+    dev = "cuda"
+    data = torch.from_numpy(data_np).to(dev)
+    cfg = L.config_from_dict(wl)
+    nb = L.lipz_workspace_bytes(cfg, len(data_np))
+    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    g = L.lipz_grid_create(cfg, ws.data_ptr(), nb, data.data_ptr(), len(data_np), stream.cuda_stream)
+    C = wl["rows"] * wl["cols"]
+    S = wl["steps"]
+
+    def generation(gen):
+        L.lipz_eval_neighborhoods(g, gen)
+        L.lipz_select_replace(g, gen)
+        L.lipz_train_step(g, gen, 0, S)
+        if wl.get("elitism", 0):
+            L.lipz_elitist_replace(g, gen)
+        if wl["mix_enable"]:
+            L.lipz_mixture_update(g, gen)
+
+    gen = 0
+    for _ in range(warmup):
+        generation(gen)
+        gen += 1
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    if bands:  # one call: the bands run ahead of each other across generations
+        L.lipz_run_generations(g, gen, steps, S)
+        gen += steps
+    else:
+        for _ in range(steps):
+            generation(gen)
+            gen += 1
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert L.lipz_sync(g) in (L.LIPZ_OK, L.LIPZ_E_NONFINITE)
+    ms_per_gen = 1e3 * elapsed / steps
+
+    # evaluation alone
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for r in range(eval_reps):
+        L.lipz_eval_neighborhoods(g, gen + r)
+    torch.cuda.synchronize()
+    t_eval = (time.perf_counter() - t0) / eval_reps
+    nbh = 5 * wl.get("pop_size", 1)
+    pair_evals = C * nbh * nbh / t_eval
+
+    # grouped-GEMM kernel timing with HIP events on the grid's stream
+    # one instrumented generation first, so the timed ones reuse its event pairs
+    L.lipz_set_gemm_timing(g, 1)
+    generation(gen)
+    gen += 1
+    L.lipz_gemm_timing(g)  # reset
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        generation(gen)
+        gen += 1
+    torch.cuda.synchronize()
+    inst_ms = 1e3 * (time.perf_counter() - t0) / steps
+    gemm_ms, launches, gemm_flops, gemm_bytes = L.lipz_gemm_timing(g)
+    L.lipz_set_gemm_timing(g, 0)
+
+    cfg_desc = {"workload": name, "grid": f"{wl['rows']}x{wl['cols']}", "cells": C,
+                "pairings_per_eval": nbh * nbh * C, "batch": wl["batch"], "steps_per_generation": S,
+                "mixture_es": bool(wl["mix_enable"]), "bands": bands}
+    if wl["net"] == "mlp":
+        cfg_desc.update(g=[wl["z_dim"]] + wl["g_hidden"] + [wl["x_dim"]], d=[wl["x_dim"]] + wl["d_hidden"] + [1])
+        data_desc = (f"synthetic (seeded MNIST-shaped blobs, {len(data_np)} x {wl['x_dim']}); "
+                     "random-init MLPs")
+        kernel = "grouped GEMM (gemm_fast_kernel + gemm_wave_kernel)"
+    else:
+        cfg_desc.update(image=list(wl["img"]), z=wl["z_dim"], g_channels=wl["g_hidden"],
+                        d_channels=wl["d_hidden"], net="dcgan")
+        data_desc = (f"synthetic (seeded colour fields + blobs, {len(data_np)} x {wl['img'][0]}x{wl['img'][1]}"
+                     f"x{wl['img'][2]} NHWC); random-init DCGAN-style conv nets")
+        kernel = "implicit-GEMM convolution (conv_kernel) + grouped GEMM"
+    f_ev, f_tr, f_mix = gemm_flops_per_generation(wl)
+    f_gen = f_ev + f_tr + f_mix
+    avg_ms = gemm_ms / max(launches, 1)
+    achieved = (gemm_flops / max(launches, 1)) / (avg_ms * 1e-3) if launches else 0.0
+    L.lipz_grid_destroy(g)
+    del ws, data
+    torch.cuda.empty_cache()
+    return {"wl": wl, "data": data_np, "data_desc": data_desc, "config": cfg_desc, "ms_per_gen": ms_per_gen,
+            "pair_evals_per_s": pair_evals, "eval_ms": t_eval * 1e3, "gflop_per_gen": f_gen / 1e9,
+            "mfma_frac": f_gen / (ms_per_gen * 1e-3) / FP32_MFMA_PEAK, "eval_mfma_frac": f_ev / t_eval / FP32_MFMA_PEAK,
+            "roofline": {"kernel": kernel, "bound": "mfma", "achieved": achieved / 1e12,
+                         "peak": FP32_MFMA_PEAK / 1e12, "unit": "TFLOP/s",
+                         "frac": achieved / FP32_MFMA_PEAK, "traffic": None,
+                         "launches": launches, "avg_launch_us": avg_ms * 1e3,
+                         "flop_per_launch": gemm_flops / max(launches, 1),
+                         "algorithmic_bytes_per_launch": gemm_bytes / max(launches, 1),
+                         "instrumented_ms_per_step": inst_ms}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -248,6 +372,8 @@ def main():
                          "uniformly, so the work per step does not depend on it)")
     ap.add_argument("--eval-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="skip the one-generation measurements of the other workloads")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the large-GEMM measurement of the fp32 matrix-core ceiling")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
@@ -272,130 +398,55 @@ def main():
               "(--gpus must be 1)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
     import paper_1811_12843_amd as L
-    import synth
 
     if not os.path.exists(L.LIB_PATH):
         from paper_1811_12843_amd import build as _b
         _b.build()
-    wl = synth.workload(args.workload)
-    if args.bands:
-        wl["bands"] = args.bands
-    n_data = args.data_n or (8192 if wl["net"] == "dcgan" else wl["data"]["n"])
-    wl["data"] = dict(wl["data"], n=n_data)
-    data_np = synth.make_dataset(wl["data"])
-    dev = "cuda"
-    data = torch.from_numpy(data_np).to(dev)
-    cfg = L.config_from_dict(wl)
-    nb = L.lipz_workspace_bytes(cfg, len(data_np))
-    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream()
-    g = L.lipz_grid_create(cfg, ws.data_ptr(), nb, data.data_ptr(), len(data_np), stream.cuda_stream)
-    C = wl["rows"] * wl["cols"]
-    S = wl["steps"]
-
-    def generation(gen):
-        L.lipz_eval_neighborhoods(g, gen)
-        L.lipz_select_replace(g, gen)
-        L.lipz_train_step(g, gen, 0, S)
-        if wl.get("elitism", 0):
-            L.lipz_elitist_replace(g, gen)
-        if wl["mix_enable"]:
-            L.lipz_mixture_update(g, gen)
-
-    gen = 0
-    for _ in range(args.warmup):
-        generation(gen)
-        gen += 1
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    if args.bands:  # one call: the bands run ahead of each other across generations
-        L.lipz_run_generations(g, gen, args.steps, S)
-        gen += args.steps
-    else:
-        for _ in range(args.steps):
-            generation(gen)
-            gen += 1
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    assert L.lipz_sync(g) in (L.LIPZ_OK, L.LIPZ_E_NONFINITE)
-    ms_per_gen = 1e3 * elapsed / args.steps
-
-    # evaluation alone
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for r in range(args.eval_reps):
-        L.lipz_eval_neighborhoods(g, gen + r)
-    torch.cuda.synchronize()
-    t_eval = (time.perf_counter() - t0) / args.eval_reps
-    nbh = 5 * wl.get("pop_size", 1)
-    pair_evals = C * nbh * nbh / t_eval
-
-    # grouped-GEMM kernel timing with HIP events on the grid's stream
-    # one instrumented generation first, so the timed ones reuse its event pairs
-    L.lipz_set_gemm_timing(g, 1)
-    generation(gen)
-    gen += 1
-    L.lipz_gemm_timing(g)  # reset
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        generation(gen)
-        gen += 1
-    torch.cuda.synchronize()
-    inst_ms = 1e3 * (time.perf_counter() - t0) / args.steps
-    gemm_ms, launches, gemm_flops, gemm_bytes = L.lipz_gemm_timing(g)
-    L.lipz_set_gemm_timing(g, 0)
-
+    r = run_workload(L, torch, args.workload, args.steps, args.warmup, args.eval_reps, args.data_n, args.bands)
+    wl, data_np = r["wl"], r["data"]
     traffic = stored_gemm_traffic(args.workload)
-    cfg_desc = {"workload": args.workload, "grid": f"{wl['rows']}x{wl['cols']}", "cells": C,
-                "pairings_per_eval": nbh * nbh * C, "batch": wl["batch"], "steps_per_generation": S,
-                "mixture_es": bool(wl["mix_enable"]), "bands": args.bands}
-    if wl["net"] == "mlp":
-        cfg_desc.update(g=[wl["z_dim"]] + wl["g_hidden"] + [wl["x_dim"]], d=[wl["x_dim"]] + wl["d_hidden"] + [1])
-        data_desc = (f"synthetic (seeded MNIST-shaped blobs, {len(data_np)} x {wl['x_dim']}); "
-                     "random-init MLPs")
-        kernel = "grouped GEMM (gemm_fast_kernel + gemm_wave_kernel)"
-    else:
-        cfg_desc.update(image=list(wl["img"]), z=wl["z_dim"], g_channels=wl["g_hidden"],
-                        d_channels=wl["d_hidden"], net="dcgan")
-        data_desc = (f"synthetic (seeded colour fields + blobs, {len(data_np)} x {wl['img'][0]}x{wl['img'][1]}"
-                     f"x{wl['img'][2]} NHWC); random-init DCGAN-style conv nets")
-        kernel = "implicit-GEMM convolution (conv_kernel) + grouped GEMM"
-    f_ev, f_tr, f_mix = gemm_flops_per_generation(wl)
-    f_gen = f_ev + f_tr + f_mix
-    avg_ms = gemm_ms / max(launches, 1)
-    achieved = (gemm_flops / max(launches, 1)) / (avg_ms * 1e-3) if launches else 0.0
     out = {
         "metric": METRIC,
-        "value": 1e3 / ms_per_gen,
+        "value": 1e3 / r["ms_per_gen"],
         "unit": "generations/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_gen,
+        "ms_per_step": r["ms_per_gen"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
-        "data": data_desc,
-        "config": cfg_desc,
-        "pair_evals_per_s": pair_evals,
-        "eval_ms": t_eval * 1e3,
-        "gemm_gflop_per_generation": f_gen / 1e9,
-        "mfma_frac": f_gen / (ms_per_gen * 1e-3) / FP32_MFMA_PEAK,
-        "eval_mfma_frac": f_ev / t_eval / FP32_MFMA_PEAK,
-        "roofline": {"kernel": kernel, "bound": "mfma", "achieved": achieved / 1e12,
-                     "peak": FP32_MFMA_PEAK / 1e12, "unit": "TFLOP/s",
-                     "frac": achieved / FP32_MFMA_PEAK, "traffic": traffic,
-                     "launches": launches, "avg_launch_us": avg_ms * 1e3,
-                     "flop_per_launch": gemm_flops / max(launches, 1),
-                     "algorithmic_bytes_per_launch": gemm_bytes / max(launches, 1),
-                     "instrumented_ms_per_step": inst_ms},
+        "data": r["data_desc"],
+        "config": r["config"],
+        "pair_evals_per_s": r["pair_evals_per_s"],
+        "eval_ms": r["eval_ms"],
+        "gemm_gflop_per_generation": r["gflop_per_gen"],
+        "mfma_frac": r["mfma_frac"],
+        "eval_mfma_frac": r["eval_mfma_frac"],
+        "roofline": dict(r["roofline"], traffic=traffic),
     }
-    L.lipz_grid_destroy(g)
+    achieved = r["roofline"]["achieved"] * 1e12
+    f_gen = r["gflop_per_gen"] * 1e9
+    ms_per_gen = r["ms_per_gen"]
+    if not args.no_per_config:
+        # every other workload of the benchmark: one warm-up and one timed
+        # generation each, the matrix-core kernels' rate from a second,
+        # instrumented generation
+        out["per_config"] = {}
+        for name in PER_CONFIG:
+            if name == args.workload:
+                continue
+            q = run_workload(L, torch, name, 1, 1, 3, PER_CONFIG[name], 0)
+            out["per_config"][name] = {
+                "generations_per_s": 1e3 / q["ms_per_gen"], "ms_per_gen": q["ms_per_gen"],
+                "pair_evals_per_s": q["pair_evals_per_s"], "gflop_per_gen": q["gflop_per_gen"],
+                "mfma_frac": q["mfma_frac"], "eval_mfma_frac": q["eval_mfma_frac"],
+                "kernel": q["roofline"]["kernel"], "kernel_tflops": q["roofline"]["achieved"],
+                "kernel_frac": q["roofline"]["frac"], "config": q["config"]}
+            del q
     if not args.no_ceiling:
         ceil = mfma_ceiling(torch, L)
         ceil["gen_frac_of_vendor"] = f_gen / (ms_per_gen * 1e-3) / (ceil["vendor_tflops"] * 1e12)
