@@ -16,7 +16,10 @@
  *          Adam step with step count t = *d_t + step_local + 1 and learning
  *          rate *d_lr on C, d_m, d_v (same indexing as C).
  * tile_rows: 32 or 64 output rows per workgroup tile, 0 = the choice the
- * library makes for a phase of this size.
+ * library makes for a phase of this size.  variant: 0 = the kernel the
+ * library runs such a phase on; 1 = the register-staged LDS kernel, 2 = the
+ * wave-split kernel (1-2 need 16-byte aligned operand rows, else
+ * LIPZ_E_INVAL).
  * d_desc: device scratch of at least 256 bytes for the problem descriptor
  * (caller-owned).  The call copies the descriptor synchronously, enqueues the
  * kernel on hip_stream and returns; LIPZ_E_INVAL on bad sizes.
@@ -36,7 +39,7 @@ lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M, int32_t N,
                            int32_t epi, int32_t act, float slope, const float* d_bias,
                            const float* d_aux, float* d_m, float* d_v, const float* d_lr,
                            const int32_t* d_t, int32_t step_local, float beta1, float beta2,
-                           float eps, int32_t tile_rows);
+                           float eps, int32_t tile_rows, int32_t variant);
 
 /*
  * Host-only check of a configuration's launch plan (no GPU, no device

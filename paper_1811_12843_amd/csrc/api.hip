@@ -362,7 +362,6 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
   ph.tile_rows = gemm_tile_rows(tiles64);
   int max_k = 0;
   for (const GemmProb& p : ps) max_k = p.K > max_k ? p.K : max_k;
-  ph.wave = gemm_wave_ok(max_k);
   int tiles = 0;
   memset(&ph.grp, 0, sizeof(ph.grp));
   int prev_tpp = -1;
@@ -398,6 +397,7 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
     g->probs_h.push_back(p);
   }
   ph.tiles = tiles;
+  ph.kernel = gemm_choose_kernel(ph.fast, max_k);
   g->phases.push_back(ph);
   return (int)g->phases.size() - 1;
 }
@@ -812,7 +812,7 @@ hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t s
   hipEvent_t e0, e1;
   hipError_t e = timing_events(g, &e0, &e1);
   if (e != hipSuccess) return e;
-  e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.fast, ph.wave, step_local,
+  e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.kernel, step_local,
                           g->slope, g->ac, stream, e0, e1);
   timing_record(g, e0, e1, ph.flops, ph.bytes);
   return e;

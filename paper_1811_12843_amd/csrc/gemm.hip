@@ -867,6 +867,7 @@ __global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(const G
       }
   epilogue<BM>(P, acc, m0, n0, tile_n, step_local, slope, ac, red);
 }
+
 }  // namespace
 
 int gemm_tile_rows(int tiles64) { return tiles64 < LIPZ_GEMM_TILE64_MIN ? 32 : 64; }
@@ -888,25 +889,31 @@ bool gemm_fast_ok(const GemmProb& p) {
 bool gemm_wave_ok(int max_k) { return LIPZ_GEMM_WAVE_SPLIT && max_k >= LIPZ_GEMM_WAVE_MIN_K; }
 
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
-                               int tile_rows, bool fast, bool wave, int step_local, float slope,
+                               int tile_rows, int kernel, int step_local, float slope,
                                AdamConsts ac, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (grp.n <= 0 || total_tiles <= 0) return hipSuccess;
   const dim3 g(total_tiles), b(NT);
   // the events (may be null) are stamped by the kernel's own dispatch packet,
   // so their difference is the kernel's execution time alone
 #define LIPZ_LAUNCH(K) hipExtLaunchKernelGGL(K, g, b, 0, s, ev_start, ev_stop, 0, d_probs, grp, step_local, slope, ac)
-  if (fast && wave) {
-    if (tile_rows == 32) LIPZ_LAUNCH(gemm_wave_kernel<32>);
-    else LIPZ_LAUNCH(gemm_wave_kernel<64>);
-  } else if (fast) {
-    if (tile_rows == 32) LIPZ_LAUNCH(gemm_fast_kernel<32>);
-    else LIPZ_LAUNCH(gemm_fast_kernel<64>);
-  } else {
-    if (tile_rows == 32) LIPZ_LAUNCH(gemm_generic_kernel<32>);
-    else LIPZ_LAUNCH(gemm_generic_kernel<64>);
+  const bool r32 = tile_rows == 32;
+  switch (kernel) {
+    case GEMM_K_WAVE:
+      if (r32) LIPZ_LAUNCH(gemm_wave_kernel<32>); else LIPZ_LAUNCH(gemm_wave_kernel<64>);
+      break;
+    case GEMM_K_FAST:
+      if (r32) LIPZ_LAUNCH(gemm_fast_kernel<32>); else LIPZ_LAUNCH(gemm_fast_kernel<64>);
+      break;
+    default:
+      if (r32) LIPZ_LAUNCH(gemm_generic_kernel<32>); else LIPZ_LAUNCH(gemm_generic_kernel<64>);
   }
 #undef LIPZ_LAUNCH
   return hipGetLastError();
+}
+
+int gemm_choose_kernel(bool fast, int max_k) {
+  if (!fast) return GEMM_K_GENERIC;
+  return gemm_wave_ok(max_k) ? GEMM_K_WAVE : GEMM_K_FAST;
 }
 
 }  // namespace lipz

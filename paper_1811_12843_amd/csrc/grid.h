@@ -59,7 +59,8 @@ struct StateBuf {
 
 struct Phase {
   int first = 0, count = 0, tiles = 0, tile_rows = 64;
-  bool fast = true, wave = false;
+  bool fast = true;             // every problem eligible for the aligned kernels
+  int kernel = GEMM_K_FAST;     // GemmKernel variant
   GemmGroups grp;
   double flops = 0.0;
   double bytes = 0.0;  // algorithmic: each operand read once, each output written once

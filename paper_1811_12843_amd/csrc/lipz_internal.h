@@ -179,12 +179,21 @@ void gemm_set_extents(GemmProb& p);
 // operands straight from L2 into registers) than on the LDS-staged kernel.
 bool gemm_wave_ok(int max_k);
 
+// Kernel variants of the grouped GEMM (gemm.hip).
+enum GemmKernel : int32_t {
+  GEMM_K_GENERIC = 0,  // any alignment, per-element bounds checks
+  GEMM_K_FAST = 1,     // register-staged LDS slices
+  GEMM_K_WAVE = 2      // split-K across the four waves, operands from L2 into registers
+};
+// The kernel a phase runs on: its problems all fast-path eligible (fast), its
+// deepest K (max_k).
+int gemm_choose_kernel(bool fast, int max_k);
+
 // Launch the grouped GEMM over the problems stored at d_probs (device),
-// covering `total_tiles` tiles of tile_rows x 64 outputs.  fast: the
-// aligned kernels (else the generic one); wave: the wave-split kernel.
-// ev_start / ev_stop (or null) are recorded around the kernel itself.
+// covering `total_tiles` tiles of tile_rows x 64 outputs on kernel variant
+// `kernel`.  ev_start / ev_stop (or null) are recorded around the kernel itself.
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
-                               int tile_rows, bool fast, bool wave, int step_local, float slope,
+                               int tile_rows, int kernel, int step_local, float slope,
                                AdamConsts ac, hipStream_t s, hipEvent_t ev_start = nullptr,
                                hipEvent_t ev_stop = nullptr);
 

@@ -13,13 +13,15 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
                                       int32_t act, float slope, const float* d_bias,
                                       const float* d_aux, float* d_m, float* d_v,
                                       const float* d_lr, const int32_t* d_t, int32_t step_local,
-                                      float beta1, float beta2, float eps, int32_t tile_rows) {
+                                      float beta1, float beta2, float eps, int32_t tile_rows,
+                                      int32_t variant) {
   if (!d_desc || !d_A || !d_B || !d_C || M < 1 || N < 1 || K < 1) return LIPZ_E_INVAL;
   if (epi < EPI_STORE || epi > EPI_ADAM || act < LIPZ_ACT_LINEAR || act > LIPZ_ACT_TANH)
     return LIPZ_E_INVAL;
   if (ones_row >= 0 && (!a_trans || ones_row != M - 1)) return LIPZ_E_INVAL;
   if (epi == EPI_DACT && !d_aux) return LIPZ_E_INVAL;
   if (tile_rows != 0 && tile_rows != 32 && tile_rows != 64) return LIPZ_E_INVAL;
+  if (variant < 0 || variant > 2) return LIPZ_E_INVAL;
   if (epi == EPI_ADAM && (!d_m || !d_v || !d_lr || !d_t)) return LIPZ_E_INVAL;
   const int a_rows = ones_row >= 0 ? ones_row : M;
   if (lda < (a_trans ? a_rows : K) || ldb < (b_trans ? K : N) || ldc < N) return LIPZ_E_INVAL;
@@ -65,7 +67,14 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
   grp.tiles_per_prob[0] = tiles;
   gemm_set_extents(p);
   if (hipMemcpy(d_desc, &p, sizeof(p), hipMemcpyHostToDevice) != hipSuccess) return LIPZ_E_HIP;
-  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, gemm_fast_ok(p), gemm_wave_ok(K),
+  // variant 0: the kernel a phase of this one problem runs on; 1 / 2: the
+  // register-staged or the wave-split kernel (aligned operands only)
+  int kernel = gemm_choose_kernel(gemm_fast_ok(p), K);
+  if (variant != 0) {
+    if (!gemm_fast_ok(p)) return LIPZ_E_INVAL;
+    kernel = variant == 1 ? GEMM_K_FAST : GEMM_K_WAVE;
+  }
+  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, kernel,
                           step_local, slope, ac,
                           (hipStream_t)hip_stream) != hipSuccess)
     return LIPZ_E_HIP;

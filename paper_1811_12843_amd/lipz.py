@@ -119,7 +119,7 @@ _SIGS = {
                                      ctypes.POINTER(_i32)]),
     "lipz_test_gemm": (_i32, [_vp, _vp, _i32, _i32, _i32, _vp, _i32, _i32, _i32, _vp, _i32, _i32,
                               _vp, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
-                              _f32, _f32, _f32, _i32]),
+                              _f32, _f32, _f32, _i32, _i32]),
     "lipz_test_es_select": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _i64, _i64, _f32]),
 }
 
@@ -284,11 +284,11 @@ def lipz_gemm_timing(g):
 
 def lipz_test_gemm(stream, d_desc, M, N, K, d_A, lda, a_trans, ones_row, d_B, ldb, b_trans, d_C, ldc,
                    epi, act, slope=0.2, d_bias=None, d_aux=None, d_m=None, d_v=None, d_lr=None,
-                   d_t=None, step_local=0, beta1=0.9, beta2=0.999, eps=1e-8, tile_rows=0):
+                   d_t=None, step_local=0, beta1=0.9, beta2=0.999, eps=1e-8, tile_rows=0, variant=0):
     return _check(load_library().lipz_test_gemm(_p(stream), _p(d_desc), M, N, K, _p(d_A), lda, a_trans,
                                                 ones_row, _p(d_B), ldb, b_trans, _p(d_C), ldc, epi, act,
                                                 slope, _p(d_bias), _p(d_aux), _p(d_m), _p(d_v), _p(d_lr),
-                                                _p(d_t), step_local, beta1, beta2, eps, tile_rows),
+                                                _p(d_t), step_local, beta1, beta2, eps, tile_rows, variant),
                   "lipz_test_gemm")
 
 

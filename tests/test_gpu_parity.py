@@ -104,13 +104,19 @@ def test_gemm_kernel_against_matmul():
     # (37, 52, 600) and (200, 256, 784) reach the wave-split kernel (K >= 512) with
     # ragged M, N and K tails; (37, 53, 19) is unaligned and takes the generic kernel
     shapes = [(1, 1, 1), (64, 64, 16), (37, 53, 19), (129, 65, 33), (100, 256, 64), (200, 256, 784),
-              (257, 784, 100), (37, 52, 600)]
+              (257, 784, 100), (37, 52, 600), (100, 96, 200), (40, 8, 1000)]
     for (M, N, K), tile_rows in [(s, tr) for s in shapes for tr in (32, 64)]:
         for a_trans in (0, 1):
             for b_trans in (0, 1):
-                for epi, act in ((0, 0), (1, 1), (1, 2), (1, 3), (2, 2), (2, 3)):
+                lda, ldb = (M if a_trans else K), (K if b_trans else N)
+                aligned = lda % 4 == 0 and ldb % 4 == 0 and not (a_trans and b_trans)
+                # variant 0: the library's choice; 1, 2: each aligned kernel (register-staged,
+                # wave-split) on the same problem
+                variants = (0, 1, 2) if aligned else (0,)
+                for variant, (epi, act) in [(v, e) for v in variants
+                                            for e in ((0, 0), (1, 1), (1, 2), (1, 3), (2, 2), (2, 3))]:
                     _print_case("gemm", M=M, N=N, K=K, at=a_trans, bt=b_trans, epi=epi, act=act,
-                                tile_rows=tile_rows)
+                                tile_rows=tile_rows, variant=variant)
                     A = g.normal(size=(M, K)).astype(np.float32)
                     Bm = g.normal(size=(K, N)).astype(np.float32)
                     bias = g.normal(size=N).astype(np.float32)
@@ -123,7 +129,8 @@ def test_gemm_kernel_against_matmul():
                     L.lipz_test_gemm(stream, desc.data_ptr(), M, N, K, dA.data_ptr(),
                                      M if a_trans else K, a_trans, -1, dB.data_ptr(),
                                      K if b_trans else N, b_trans, dC.data_ptr(), N, epi, act, 0.2,
-                                     d_bias=db.data_ptr(), d_aux=daux.data_ptr(), tile_rows=tile_rows)
+                                     d_bias=db.data_ptr(), d_aux=daux.data_ptr(), tile_rows=tile_rows,
+                                     variant=variant)
                     torch.cuda.synchronize()
                     acc = A.astype(np.float64) @ Bm.astype(np.float64)
                     scale = np.abs(A).astype(np.float64) @ np.abs(Bm).astype(np.float64)
@@ -139,7 +146,8 @@ def test_gemm_kernel_against_matmul():
                         ref = acc * d
                         scale = scale * np.abs(d)
                     out = dC.cpu().numpy()
-                    assert np.all(np.abs(out - ref) <= 3e-5 * scale + 1e-6), (M, N, K, a_trans, b_trans, epi)
+                    assert np.all(np.abs(out - ref) <= 3e-5 * scale + 1e-6), (M, N, K, a_trans, b_trans, epi,
+                                                                              variant)
 
 
 def test_gemm_weight_gradient_with_bias_row_and_adam():
@@ -148,10 +156,11 @@ def test_gemm_weight_gradient_with_bias_row_and_adam():
     dev = "cuda"
     desc = torch.zeros(256, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream().cuda_stream
-    for (rows, fi, fo), tile_rows in [(s, tr) for s in [(200, 784, 256), (100, 256, 784), (19, 37, 45),
-                                                        (64, 2, 64), (100, 64, 256), (520, 72, 36)]
-                                      for tr in (32, 64)]:
-        _print_case("wgrad_adam", rows=rows, fi=fi, fo=fo, tile_rows=tile_rows)
+    cases = [(s, tr, v) for s in [(200, 784, 256), (100, 256, 784), (19, 37, 45), (64, 2, 64), (100, 64, 256),
+                                  (520, 72, 36), (100, 256, 256)]
+             for tr in (32, 64) for v in ((0, 1, 2) if s[1] % 4 == 0 and s[2] % 4 == 0 else (0,))]
+    for (rows, fi, fo), tile_rows, variant in cases:
+        _print_case("wgrad_adam", rows=rows, fi=fi, fo=fo, tile_rows=tile_rows, variant=variant)
         X = g.normal(size=(rows, fi)).astype(np.float32)
         dY = (g.normal(size=(rows, fo)) * 1e-2).astype(np.float32)
         P0 = g.normal(size=(fi + 1, fo)).astype(np.float32)
@@ -168,7 +177,7 @@ def test_gemm_weight_gradient_with_bias_row_and_adam():
         L.lipz_test_gemm(stream, desc.data_ptr(), fi + 1, fo, rows, dX.data_ptr(), fi, 1, fi,
                          ddY.data_ptr(), fo, 0, dP.data_ptr(), fo, 3, 0, 0.2, d_m=dm.data_ptr(),
                          d_v=dv.data_ptr(), d_lr=dlr.data_ptr(), d_t=dt.data_ptr(), step_local=step_local,
-                         tile_rows=tile_rows)
+                         tile_rows=tile_rows, variant=variant)
         torch.cuda.synchronize()
         Xe = np.concatenate([X, np.ones((rows, 1), np.float32)], axis=1).astype(np.float64)
         grad = Xe.T @ dY.astype(np.float64)
