@@ -20,6 +20,10 @@
 
 using namespace lipz;
 
+#ifndef LIPZ_FUSED_HEAD
+#define LIPZ_FUSED_HEAD 1
+#endif
+
 namespace {
 
 // Workspace of lipz_grid_create_static: one array per device, held for the
@@ -204,6 +208,7 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     g->ag[l] = cv.take<float>((size_t)U * B * D.fo[l]);
     g->dDg[l] = cv.take<float>((size_t)U * B * D.fo[l]);
   }
+  if (g->fused_head) g->aS = cv.take<float>((size_t)U * 2 * B * g->aS_ld);
   // evaluation: rows [x_c; G_0(z_c); ...; G_(nn-1)(z_c)] per cell
   g->ze = cv.take<float>((size_t)C * B * zd);
   g->Xe = cv.take<float>((size_t)C * er * B * xd);
@@ -345,6 +350,11 @@ double prob_bytes(const GemmProb& p) {
   if (p.epi == EPI_DACT) b += mn;                          // read the forward output
   if (p.epi == EPI_BIAS_ACT && p.bias) b += p.N;
   if (p.dot_out) b += (double)p.M * ((p.N + GEMM_BN - 1) / GEMM_BN) + p.N;
+  if (p.epi == EPI_BIAS_ACT && p.dot_out && p.gout) b += mn;  // write w * act'
+  if (p.epi == EPI_DACT && p.rs_mode) {
+    b += (double)p.M * p.rs_tn;                                // read the partial logits
+    if (p.side) b += mn + 8.0 * p.M;                           // scaled activations, dL/da, dlout
+  }
   return 4.0 * b;
 }
 
@@ -544,6 +554,7 @@ void build_tables(lipz_grid* g) {
   const size_t sG = G.stride, sD = D.stride;
   // the Wasserstein critic's parameters are clipped after every update
   const float d_clip = g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN ? g->cfg.wgan_clip : 0.f;
+  const bool fused = g->fused_head;
   for (int par = 0; par < 2; ++par) {
     const StateBuf& S = g->st[par];
     for (int grp = 0; grp < g->n_groups; ++grp) {
@@ -569,12 +580,15 @@ void build_tables(lipz_grid* g) {
                                 : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
         GemmProb p = fwd_prob(x, 2 * B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
                               g->a[l] + (size_t)c * 2 * B * D.fo[l], D.act[l]);
-        if (l == LD - 2) p = with_head(p, S.Dp + c * sD + D.off[LD - 1], g->part_tr + (size_t)c * 2 * B * g->tn, g->tn);
+        if (l == LD - 2) {
+          p = with_head(p, S.Dp + c * sD + D.off[LD - 1], g->part_tr + (size_t)c * 2 * B * g->tn, g->tn);
+          if (fused) p.gout = g->dD[LD - 2] + (size_t)c * 2 * B * D.fo[l];
+        }
         ps.push_back(p);
       }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
     }
-    ops.push_back({OP_HEAD_D, -1});
+    if (!fused) ops.push_back({OP_HEAD_D, -1});
     // output layer of D: ([act | 1]^T dL/da) and its Adam step, as GEMM problems
     std::vector<GemmProb> head_grad;
     for (int c = cb; c < ce; ++c) {
@@ -593,48 +607,112 @@ void build_tables(lipz_grid* g) {
       if (g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN) p.gscale = 1.f / (float)B;  // dL/da stored as exact +-1
       head_grad.push_back(p);
     }
-    backward_phases(
-        g, LD - 2,
-        [&](int l, std::vector<GemmProb>* ph) {
-          for (int c = cb; c < ce; ++c)
-            ph->push_back(dgrad_prob(g->dD[l] + (size_t)c * 2 * B * D.fo[l], 2 * B,
-                                     S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
-                                     g->dD[l - 1] + (size_t)c * 2 * B * D.fi[l],
-                                     g->a[l - 1] + (size_t)c * 2 * B * D.fi[l], D.act[l - 1]));
-        },
-        [&](int l, std::vector<GemmProb>* ph) {
-          for (int c = cb; c < ce; ++c) {
-            const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
-                                    : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
-            const size_t o = c * sD + D.off[l];
-            GemmProb p = wgrad_adam_prob(x, 2 * B, D.fi[l], g->dD[l] + (size_t)c * 2 * B * D.fo[l],
-                                         D.fo[l], S.Dp + o, S.Dm + o, S.Dv + o, S.Dlr + c, S.Dt + c);
-            p.clip = d_clip;
-            ph->push_back(p);
-          }
-        },
-        &ops, head_grad);
+    auto d_dgrad = [&](int l, std::vector<GemmProb>* ph) {
+      for (int c = cb; c < ce; ++c)
+        ph->push_back(dgrad_prob(g->dD[l] + (size_t)c * 2 * B * D.fo[l], 2 * B,
+                                 S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
+                                 g->dD[l - 1] + (size_t)c * 2 * B * D.fi[l],
+                                 g->a[l - 1] + (size_t)c * 2 * B * D.fi[l], D.act[l - 1]));
+    };
+    auto d_wgrad = [&](int l, std::vector<GemmProb>* ph) {
+      for (int c = cb; c < ce; ++c) {
+        const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
+                                : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
+        const size_t o = c * sD + D.off[l];
+        GemmProb p = wgrad_adam_prob(x, 2 * B, D.fi[l], g->dD[l] + (size_t)c * 2 * B * D.fo[l],
+                                     D.fo[l], S.Dp + o, S.Dm + o, S.Dv + o, S.Dlr + c, S.Dt + c);
+        p.clip = d_clip;
+        ph->push_back(p);
+      }
+    };
+    if (!fused) {
+      backward_phases(g, LD - 2, d_dgrad, d_wgrad, &ops, head_grad);
+    } else {
+      // The loss head inside the launches: with g = w (.) act'(h) (written by the
+      // last hidden layer's forward) the head's delta of that layer is the row
+      // scaling diag(dL/da) g, so
+      //   input gradient  (diag(dL/da) g) W^T (.) act'(a) = diag(dL/da) (g W^T) (.) act'(a)
+      //   weight gradient [a | 1]^T diag(dL/da) g = [diag(dL/da) a | dL/da]^T g
+      // the first launch forms dL/da from the partial logits, the scaled
+      // activations aS and the output layer's dL/da; the next one takes both
+      // weight gradients (that layer's and the output layer's).
+      const int t = LD - 2, Hs = D.fi[t], H = D.fo[t];
+      std::vector<GemmProb> ph;
+      for (int c = cb; c < ce; ++c) {
+        GemmProb p = dgrad_prob(g->dD[t] + (size_t)c * 2 * B * H, 2 * B, S.Dp + c * sD + D.off[t], Hs, H,
+                                g->dD[t - 1] + (size_t)c * 2 * B * Hs, g->a[t - 1] + (size_t)c * 2 * B * Hs,
+                                D.act[t - 1]);
+        p.rs_part = g->part_tr + (size_t)c * 2 * B * g->tn;
+        p.rs_tn = g->tn;
+        p.rs_mode = 1;
+        p.rs_B = B;
+        p.loss_kind = g->cfg.loss_kind;
+        p.side = g->aS + (size_t)c * 2 * B * g->aS_ld;
+        p.side_ld = g->aS_ld;
+        p.dlout = g->dlbuf + (size_t)c * 2 * B * 4;
+        ph.push_back(p);
+      }
+      ops.push_back({OP_GEMM, add_phase(g, ph)});
+      std::vector<GemmProb> pending;
+      for (int c = cb; c < ce; ++c) {
+        const size_t o = c * sD + D.off[t];
+        GemmProb p = base_prob(g->aS + (size_t)c * 2 * B * g->aS_ld, g->aS_ld, 1, g->dD[t] + (size_t)c * 2 * B * H,
+                               H, 0, S.Dp + o, H, Hs + 1, H, 2 * B);
+        p.a_rows = Hs + 1;  // the dL/da column is the bias row
+        p.m = S.Dm + o;
+        p.v = S.Dv + o;
+        p.lr = S.Dlr + c;
+        p.t = S.Dt + c;
+        p.epi = EPI_ADAM;
+        p.clip = d_clip;
+        pending.push_back(p);
+      }
+      for (int l = t - 1; l >= 0; --l) {
+        std::vector<GemmProb> q;
+        if (l >= 1) d_dgrad(l, &q);
+        q.insert(q.end(), pending.begin(), pending.end());
+        pending.clear();
+        d_wgrad(l, &pending);
+        if (l == 0) q.insert(q.end(), pending.begin(), pending.end());
+        ops.push_back({OP_GEMM, add_phase(g, q)});
+      }
+    }
     // generator step: D forward on the fake rows with the updated D
     for (int l = 0; l + 1 < LD; ++l) {
       std::vector<GemmProb> ps;
+      // with the head folded in, the output layer's weight gradient + Adam
+      // (it needs the dL/da of the input-gradient launch) runs beside the
+      // first layer's forward on the fakes, before the output layer is read
+      if (fused && l == 0) ps = head_grad;
       for (int c = cb; c < ce; ++c) {
         const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd
                                 : g->ag[l - 1] + (size_t)c * B * D.fi[l];
         GemmProb p = fwd_prob(x, B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
                               g->ag[l] + (size_t)c * B * D.fo[l], D.act[l]);
-        if (l == LD - 2) p = with_head(p, S.Dp + c * sD + D.off[LD - 1], g->part_g + (size_t)c * B * g->tn, g->tn);
+        if (l == LD - 2) {
+          p = with_head(p, S.Dp + c * sD + D.off[LD - 1], g->part_g + (size_t)c * B * g->tn, g->tn);
+          if (fused) p.gout = g->dDg[LD - 2] + (size_t)c * B * D.fo[l];
+        }
         ps.push_back(p);
       }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
     }
-    ops.push_back({OP_HEAD_G, -1});
+    if (!fused) ops.push_back({OP_HEAD_G, -1});
     for (int l = LD - 2; l >= 0; --l) {
       std::vector<GemmProb> ps;
       for (int c = cb; c < ce; ++c) {
         if (l >= 1) {
-          ps.push_back(dgrad_prob(g->dDg[l] + (size_t)c * B * D.fo[l], B, S.Dp + c * sD + D.off[l],
+          GemmProb p = dgrad_prob(g->dDg[l] + (size_t)c * B * D.fo[l], B, S.Dp + c * sD + D.off[l],
                                   D.fi[l], D.fo[l], g->dDg[l - 1] + (size_t)c * B * D.fi[l],
-                                  g->ag[l - 1] + (size_t)c * B * D.fi[l], D.act[l - 1]));
+                                  g->ag[l - 1] + (size_t)c * B * D.fi[l], D.act[l - 1]);
+          if (fused && l == LD - 2) {  // the generator step's head: every row has the "real" target
+            p.rs_part = g->part_g + (size_t)c * B * g->tn;
+            p.rs_tn = g->tn;
+            p.rs_mode = 2;
+            p.rs_B = B;
+            p.loss_kind = g->cfg.loss_kind;
+          }
+          ps.push_back(p);
         } else {
           // into the generator output: delta of G's last layer
           ps.push_back(dgrad_prob(g->dDg[0] + (size_t)c * B * D.fo[0], B, S.Dp + c * sD + D.off[0],
@@ -661,6 +739,12 @@ void build_tables(lipz_grid* g) {
           }
         },
         &ops);
+    // with the head folded in, the step's losses (when asked for) come from a
+    // small kernel over the partial logits at the end of the step
+    if (fused) {
+      ops.push_back({OP_LOSS_D, -1});
+      ops.push_back({OP_LOSS_G, -1});
+    }
     }  // groups
 
     // ---- evaluation: rows [x_c; G_0(z_c); ...; G_(nn-1)(z_c)] per cell ----
@@ -856,6 +940,10 @@ lipz_grid* plan_grid(const lipz_config* cfg, int64_t n_samples, char* base, cons
     }
   } else {
     g->tn = ceil_div(Dn.fi[Dn.nl - 1], GEMM_BN);
+    // the loss head folds into the launches around it when D has two or more
+    // hidden layers (the discriminator step needs the layer below the last)
+    g->fused_head = LIPZ_FUSED_HEAD && cfg->trainer == LIPZ_TRAINER_GRADIENT && Dn.nl >= 3;
+    if (g->fused_head) g->aS_ld = (Dn.fi[Dn.nl - 2] + 4 + 3) / 4 * 4;
   }
   g->data = data;
   g->key = make_uint2((uint32_t)(cfg->seed & 0xFFFFFFFFull), (uint32_t)(cfg->seed >> 32));
@@ -1100,6 +1188,8 @@ lipz_status enq_train_group_step(lipz_grid* g, int gen, int par, int grp, int k,
       case OP_GEMM: e = run_gemm_phase(g, op.phase, k, gs); break;
       case OP_HEAD_D: e = launch_head_d(gd, gs); break;
       case OP_HEAD_G: e = launch_head_g(gg, gs); break;
+      case OP_LOSS_D: if (d_losses) e = launch_loss_d(gd, gs); break;
+      case OP_LOSS_G: if (d_losses) e = launch_loss_g(gg, gs); break;
       default: e = hipErrorInvalidValue; break;
     }
     if ((st = check_hip(g, e, "train step"))) return st;
@@ -1766,6 +1856,14 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
     if (p.dot_out && (!inside(p.dot_out, 0, (int64_t)(p.M - 1) * p.dot_ld + (p.N + GEMM_BN - 1) / GEMM_BN - 1) ||
                       !inside(p.dotw, 0, p.N - 1)))
       note("gemm dot", i);
+    // fields that share storage with others are checked under the epilogue that reads them
+    if (p.epi == EPI_BIAS_ACT && p.dot_out && p.gout && !inside(p.gout, 0, c_last)) note("gemm head factor", i);
+    if (p.epi == EPI_DACT && p.rs_mode) {
+      if (p.rs_tn < 1 || !inside(p.rs_part, 0, (int64_t)p.M * p.rs_tn - 1)) note("gemm head logits", i);
+      if (p.side && (p.side_ld < p.N + 4 || !inside(p.side, 0, (int64_t)(p.M - 1) * p.side_ld + p.N + 3) ||
+                     !inside(p.dlout, 0, (int64_t)p.M * 4 - 1)))
+        note("gemm head side outputs", i);
+    }
   }
   if (!g->dc) {
     // the sample, evaluation-head, fitness, selection and re-evaluation

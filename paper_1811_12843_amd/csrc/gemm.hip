@@ -204,6 +204,61 @@ __device__ __forceinline__ void store_slices(const GemmProb& P, int tid, const R
   }
 }
 
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* p, uint32_t bytes) {
+  // dword 3 = 0x00020000: raw 32-bit data format on gfx9-family parts
+  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float4 bload4(__amdgpu_buffer_rsrc_t r, uint32_t off_bytes) {
+  const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off_bytes, 0, 0);
+  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
+                     __uint_as_float(v[3]));
+}
+
+
+// One element through a buffer resource: the epilogues address C, the Adam
+// moments and the auxiliary operand with 32-bit element offsets from the
+// descriptor's base (no 64-bit address per element).
+constexpr uint32_t kWholeBuffer = 0x7FFFFFFFu;  // element offsets of a problem stay below 2^31 (planning checks)
+__device__ __forceinline__ float bld1(__amdgpu_buffer_rsrc_t r, uint32_t off_elems) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)(off_elems * 4u), 0, 0));
+}
+__device__ __forceinline__ void bst1(__amdgpu_buffer_rsrc_t r, uint32_t off_elems, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)(off_elems * 4u), 0, 0);
+}
+
+// The loss head's dL/da of this lane's epilogue rows (rows m0 + wm + 16 i +
+// 4 (lane / 16) + r), from the partial logits, formed as the separate head
+// kernel forms it.  With four partial sums per row (a 129..256-wide last
+// hidden layer) the loads are issued together with the epilogue's other
+// loads, so they add no round trip.
+template <int BM>
+__device__ __forceinline__ void head_rows_dl(const GemmProb& P, int m0, float (&dl)[Tile<BM>::TI][4]) {
+  using T = Tile<BM>;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * T::WM, lg = lane >> 4;
+  const float invB = 1.f / (float)P.rs_B;
+#pragma unroll
+  for (int i = 0; i < T::TI; ++i) {
+    // lane r of each 16-lane group forms row r's value, then the group shares them
+    const int row = m0 + wm + 16 * i + 4 * lg + (lane & 3);
+    const LIPZ_GLOBAL float* pr = as_global(P.rs_part) + (size_t)(row < P.M ? row : 0) * P.rs_tn;
+    float a;
+    if (P.rs_tn == 4) {  // a 129..256-wide last hidden layer: the row's four partial sums in one load
+      const float4 v = ld4(pr);
+      a = ((v.x + v.y) + v.z) + v.w;
+    } else {
+      a = 0.f;
+      for (int t = 0; t < P.rs_tn; ++t) a += pr[t];
+    }
+    const float mine = head_dl(P.loss_kind, a, P.rs_mode == 2 || row < P.rs_B, invB);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dl[i][r] = __shfl(mine, (lane & ~15) | r, 64);
+  }
+}
+
 // Epilogue shared by both kernel variants: bias + activation (optionally
 // with the per-tile partial dot product of the next 1-wide layer), the
 // activation-derivative product, or the fused Adam update; then stores.
@@ -219,7 +274,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = (wave >> 1) * T::WM, wn = (wave & 1) * 32;
   const int li = lane & 15, lg = lane >> 4;
-  LIPZ_GLOBAL float* gC = as_global(P.C);
+  const __amdgpu_buffer_rsrc_t rC = make_rsrc(P.C, kWholeBuffer);
   uint32_t off[NE];
   bool ok[NE];
 #pragma unroll
@@ -235,8 +290,8 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
         off[e] = ok[e] ? (uint32_t)(row * P.ldc + col) : 0u;
       }
   if (P.epi == EPI_ADAM) {
-    LIPZ_GLOBAL float* gM = as_global(P.m);
-    LIPZ_GLOBAL float* gV = as_global(P.v);
+    const __amdgpu_buffer_rsrc_t rM = make_rsrc(P.m, kWholeBuffer);
+    const __amdgpu_buffer_rsrc_t rV = make_rsrc(P.v, kWholeBuffer);
     const float lr = *as_global(P.lr);
     const int tt = *as_global(P.t) + step_local + 1;
     const float bc1 = (float)(1.0 - pow((double)ac.beta1, (double)tt));
@@ -244,9 +299,9 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
     float pp[NE], mm[NE], vv[NE];
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      pp[e] = gC[off[e]];
-      mm[e] = gM[off[e]];
-      vv[e] = gV[off[e]];
+      pp[e] = bld1(rC, off[e]);
+      mm[e] = bld1(rM, off[e]);
+      vv[e] = bld1(rV, off[e]);
     }
 #pragma unroll
     for (int i = 0; i < T::TI; ++i)
@@ -261,18 +316,33 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
           float p = pp[e] - lr * (m / bc1) / (sqrtf(v / bc2) + ac.eps);
           if (P.clip > 0.f) p = p > P.clip ? P.clip : (p < -P.clip ? -P.clip : p);  // keeps NaN
           if (ok[e]) {
-            gM[off[e]] = m;
-            gV[off[e]] = v;
-            gC[off[e]] = p;
+            bst1(rM, off[e], m);
+            bst1(rV, off[e], v);
+            bst1(rC, off[e], p);
           }
         }
     return;
   }
   if (P.epi == EPI_DACT) {
-    const LIPZ_GLOBAL float* gAux = as_global(P.aux);
+    const __amdgpu_buffer_rsrc_t rAux = make_rsrc(P.aux, kWholeBuffer);
     float ax[NE];
 #pragma unroll
-    for (int e = 0; e < NE; ++e) ax[e] = gAux[off[e]];
+    for (int e = 0; e < NE; ++e) ax[e] = bld1(rAux, off[e]);
+    if (P.rs_mode == 0) {
+#pragma unroll
+      for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int e = (i * 2 + j) * 4 + r;
+            if (ok[e]) bst1(rC, off[e], acc[i][j][r] * act_deriv_from_out(P.act, ax[e], slope));
+          }
+      return;
+    }
+    float dl[T::TI][4];
+    head_rows_dl<BM>(P, m0, dl);
+    LIPZ_GLOBAL float* gSide = as_global(P.side);
 #pragma unroll
     for (int i = 0; i < T::TI; ++i)
 #pragma unroll
@@ -280,8 +350,36 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = (i * 2 + j) * 4 + r;
-          if (ok[e]) gC[off[e]] = acc[i][j][r] * act_deriv_from_out(P.act, ax[e], slope);
+          if (ok[e]) {
+            bst1(rC, off[e], dl[i][r] * (acc[i][j][r] * act_deriv_from_out(P.act, ax[e], slope)));
+            if (P.side) {
+              const int row = m0 + wm + 16 * i + 4 * lg + r, col = n0 + wn + 16 * j + li;
+              gSide[(size_t)row * P.side_ld + col] = dl[i][r] * ax[e];
+            }
+          }
         }
+    // column 0 of the problem: the per-row extras
+    if (P.side && tile_n == 0 && wn == 0 && li == 0) {
+      LIPZ_GLOBAL float* gDl = as_global(P.dlout);
+#pragma unroll
+      for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m0 + wm + 16 * i + 4 * lg + r;
+          if (row < P.M) {
+            LIPZ_GLOBAL float* sr = gSide + (size_t)row * P.side_ld + P.N;
+            sr[0] = dl[i][r];
+            sr[1] = 0.f;
+            sr[2] = 0.f;
+            sr[3] = 0.f;
+            LIPZ_GLOBAL float* o = gDl + (size_t)row * 4;
+            o[0] = P.loss_kind == LIPZ_LOSS_WASSERSTEIN ? (row < P.rs_B ? -1.f : 1.f) : dl[i][r];
+            o[1] = 0.f;
+            o[2] = 0.f;
+            o[3] = 0.f;
+          }
+        }
+    }
     return;
   }
   if (P.epi != EPI_BIAS_ACT) {
@@ -292,7 +390,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = (i * 2 + j) * 4 + r;
-          if (ok[e]) gC[off[e]] = acc[i][j][r];
+          if (ok[e]) bst1(rC, off[e], acc[i][j][r]);
         }
     return;
   }
@@ -316,8 +414,9 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
         const int e = (i * 2 + j) * 4 + r;
         const float y = act_fwd(P.act, acc[i][j][r] + bias[j], slope);
         if (ok[e]) {
-          gC[off[e]] = y;
+          bst1(rC, off[e], y);
           rowdot[r] += y * dw[j];
+          if (P.gout) bst1(make_rsrc(P.gout, kWholeBuffer), off[e], dw[j] * act_deriv_from_out(P.act, y, slope));
         }
       }
     if (dot) {
@@ -443,18 +542,6 @@ __global__ __launch_bounds__(NT, 2) void gemm_generic_kernel(const GemmProb* __r
 // when the slice is written to LDS.  Loads run two slices ahead of the
 // MFMAs (two register sets, two LDS stages, one barrier per slice).
 // ---------------------------------------------------------------------------
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* p, uint32_t bytes) {
-  // dword 3 = 0x00020000: raw 32-bit data format on gfx9-family parts
-  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, (int)bytes, 0x00020000);
-}
-__device__ __forceinline__ float4 bload4(__amdgpu_buffer_rsrc_t r, uint32_t off_bytes) {
-  const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off_bytes, 0, 0);
-  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
-                     __uint_as_float(v[3]));
-}
-
 template <int BM, int AT, int BT>
 struct FastRegs {
   float4 a[Tile<BM>::A_VEC];

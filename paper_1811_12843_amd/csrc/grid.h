@@ -68,7 +68,8 @@ struct Phase {
 
 // A training-step op: a GEMM phase, or a kernel of the step; for the NES ops
 // `phase` holds the role (LIPZ_ROLE_G / LIPZ_ROLE_D).
-enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G, OP_NES_PERTURB, OP_NES_HEAD, OP_NES_UPDATE };
+enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G, OP_LOSS_D, OP_LOSS_G, OP_NES_PERTURB, OP_NES_HEAD,
+              OP_NES_UPDATE };
 struct Op {
   OpKind kind;
   int phase;
@@ -113,6 +114,12 @@ struct lipz_grid {
   float *ag[LIPZ_MAX_HIDDEN] = {}, *dDg[LIPZ_MAX_HIDDEN] = {}, *dG[LIPZ_MAX_HIDDEN + 1] = {};
   float *part_tr = nullptr, *part_g = nullptr, *part_e = nullptr;  // partial logits
   float* dlbuf = nullptr;  // D-step dL/d(logit) [C][2B][4]
+  // The loss head folded into the GEMM launches (reading 8's training step
+  // with at least two hidden layers in D): aS [U][2B][aS_ld] holds dL/da-scaled
+  // activations of the layer below D's last hidden layer, then dL/da.
+  bool fused_head = false;
+  float* aS = nullptr;
+  int aS_ld = 0;
   int tn = 1;  // column tiles of D's last hidden layer
   // evaluation buffers
   float *ze = nullptr, *Xe = nullptr;

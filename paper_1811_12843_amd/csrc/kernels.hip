@@ -110,12 +110,6 @@ __global__ void sample_kernel(const float* __restrict__ data, int64_t N, int xd,
 // ---------------------------------------------------------------------------
 constexpr int HEAD_ROWS = 32;
 
-// dL/da of one row (the mean over B rows included): BCE (sigmoid(a) - target) / B;
-// Wasserstein -1 / B for a real target, +1 / B for a fake one.
-__device__ __forceinline__ float head_dl(int loss_kind, float a, bool real_target, float invB) {
-  if (loss_kind == LIPZ_LOSS_WASSERSTEIN) return real_target ? -invB : invB;
-  return (sigmoid_f(a) - (real_target ? 1.f : 0.f)) * invB;
-}
 
 template <bool D_STEP>
 __global__ __launch_bounds__(NT) void head_kernel(HeadArgs A) {
@@ -128,7 +122,7 @@ __global__ __launch_bounds__(NT) void head_kernel(HeadArgs A) {
   const int tn = A.tn;
   const float* part = A.part + (int64_t)c * rows * tn;
   const float invB = 1.f / (float)A.B;
-  if ((int)threadIdx.x < nr) {
+  if (!A.loss_only && (int)threadIdx.x < nr) {
     const int r = r0 + threadIdx.x;
     float a = 0.f;
     for (int t = 0; t < tn; ++t) a += part[(int64_t)r * tn + t];
@@ -157,6 +151,7 @@ __global__ __launch_bounds__(NT) void head_kernel(HeadArgs A) {
     if (threadIdx.x == 0 && A.losses)
       A.losses[c * 2 + (D_STEP ? 0 : 1)] = D_STEP ? lr_ * invB + lf * invB : lr_ * invB;
   }
+  if (A.loss_only) return;
   __syncthreads();
   const int H = A.H;
   const int n = cb * 64 + (threadIdx.x & 63);
@@ -740,6 +735,18 @@ hipError_t launch_head_d(const HeadArgs& a, hipStream_t s) {
 hipError_t launch_head_g(const HeadArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(head_kernel<false>, dim3(a.C, (a.H + 63) / 64, (a.B + HEAD_ROWS - 1) / HEAD_ROWS),
                      dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_loss_d(const HeadArgs& a, hipStream_t s) {
+  HeadArgs b = a;
+  b.loss_only = 1;
+  hipLaunchKernelGGL(head_kernel<true>, dim3(a.C, 1, 1), dim3(NT), 0, s, b);
+  return hipGetLastError();
+}
+hipError_t launch_loss_g(const HeadArgs& a, hipStream_t s) {
+  HeadArgs b = a;
+  b.loss_only = 1;
+  hipLaunchKernelGGL(head_kernel<false>, dim3(a.C, 1, 1), dim3(NT), 0, s, b);
   return hipGetLastError();
 }
 hipError_t launch_nes_perturb(const NesArgs& a, hipStream_t s) {

@@ -98,6 +98,12 @@ __device__ __forceinline__ float real_term(int loss_kind, float a) {
 __device__ __forceinline__ float fake_term(int loss_kind, float a) {
   return loss_kind == LIPZ_LOSS_WASSERSTEIN ? a : softplus_f(a);
 }
+// dL/da of one row (the mean over B rows included): BCE (sigmoid(a) - target) / B;
+// Wasserstein -1 / B for a real target, +1 / B for a fake one.
+__device__ __forceinline__ float head_dl(int loss_kind, float a, bool real_target, float invB) {
+  if (loss_kind == LIPZ_LOSS_WASSERSTEIN) return real_target ? -invB : invB;
+  return (sigmoid_f(a) - (real_target ? 1.f : 0.f)) * invB;
+}
 
 // ---------------------------------------------------------------------------
 // Grouped GEMM: one launch computes many independent problems
@@ -120,15 +126,27 @@ struct GemmProb {
   float* C;
   const float* bias;
   const float* aux;
-  float* m;
-  float* v;
+  // Fields that only some epilogues use share storage (the descriptor is held
+  // in scalar registers by every workgroup, so it is kept small).
+  union {
+    float* m;          // EPI_ADAM: the first moment
+    float* gout;       // EPI_BIAS_ACT with dot_out: see the loss head below
+    float* side;       // EPI_DACT with rs_mode: see the loss head below
+  };
+  union {
+    float* v;          // EPI_ADAM: the second moment
+    float* dlout;      // EPI_DACT with side
+  };
   const float* lr;     // EPI_ADAM: the cell's learning rate
   const int32_t* t;    // EPI_ADAM: the cell's Adam step count before this call
   // EPI_BIAS_ACT only: when dot_out is set, the tile also writes
   //   dot_out[i*dot_ld + tile_n] = sum over its columns j of C[i][j] * dotw[j]
   // (+ *dot_bias in tile column 0): the next layer's 1-wide output, split
   // into per-tile partial sums that a later kernel adds in a fixed order.
-  const float* dotw;
+  union {
+    const float* dotw;
+    const float* rs_part;  // EPI_DACT with rs_mode
+  };
   const float* dot_bias;
   float* dot_out;
   int32_t M, N, K;
@@ -139,11 +157,34 @@ struct GemmProb {
   int32_t vec;         // bit 0: A rows 16-byte aligned; bit 1: B rows 16-byte aligned
   int32_t tiles_n;
   int32_t tile_begin;
-  int32_t dot_ld;
+  union {
+    int32_t dot_ld;
+    int32_t rs_tn;     // EPI_DACT with rs_mode
+  };
   uint32_t a_bytes;    // extent of A from its base: a_rows * lda (a_trans 0) or K * lda floats
   uint32_t b_bytes;    // extent of B: K * ldb (b_trans 0) or N * ldb floats
-  float clip;          // EPI_ADAM: when > 0 the updated parameter is clipped to [-clip, clip]
-  float gscale;        // EPI_ADAM: the gradient is acc * gscale (0 stands for 1: descriptors start zeroed)
+  union {
+    float clip;        // EPI_ADAM: when > 0 the updated parameter is clipped to [-clip, clip]
+    int32_t side_ld;   // EPI_DACT with side
+  };
+  union {
+    float gscale;      // EPI_ADAM: the gradient is acc * gscale (0 stands for 1: descriptors start zeroed)
+    int32_t rs_B;      // EPI_DACT with rs_mode
+  };
+  // The discriminator's loss head, folded into the launches around it (a
+  // 1-wide output layer a = h w + b over the last hidden layer h):
+  //  * EPI_BIAS_ACT with dot_out: gout (when set) receives w[j] * act'(C[i][j]),
+  //    indexed like C, so that dL/dh = (dL/da)[i] * gout[i][j];
+  //  * EPI_DACT with rs_mode != 0: the product of the input gradient takes the
+  //    per-row factor dL/da[i] of the head, formed from the partial logits
+  //    rs_part[i * rs_tn + t] (t in order) as the separate head kernel forms it:
+  //    rs_mode 1 rows i < rs_B have the "real" target, the others "fake"
+  //    (discriminator step); rs_mode 2 every row "real" (generator step).
+  //    side (when set) receives dL/da[i] * aux[i][j] (ld side_ld), and the
+  //    tiles of column 0 also write side[i * side_ld + N] = dL/da[i], zeros
+  //    at N + 1 .. N + 3, and dlout[4 i] = dL/da[i] (Wasserstein: the exact
+  //    +-1 of the separate head, scaled by 1 / rs_B later), dlout[4 i + 1 .. 3] = 0.
+  int16_t rs_mode, loss_kind;
 };
 
 struct AdamConsts {
@@ -404,6 +445,7 @@ hipError_t launch_sample(const float* data, int64_t N, int xd, int zd, int B, in
                          float* Z, int64_t z_cell_stride, hipStream_t s);
 
 struct HeadArgs {
+  int loss_only;         // only the per-cell losses (the loss head is folded into the GEMM launches)
   const float* part;     // per-tile partial logits [C][rows][tn] (bias included)
   int tn;
   const float* act;      // last hidden activations [C][rows][H] (cell stride act_cell_stride)
@@ -425,6 +467,9 @@ struct HeadArgs {
 hipError_t launch_head_d(const HeadArgs& a, hipStream_t s);
 // Generator step head: logits of B fake rows, non-saturating loss, delta.
 hipError_t launch_head_g(const HeadArgs& a, hipStream_t s);
+// The losses alone (a.losses) of the discriminator / generator step.
+hipError_t launch_loss_d(const HeadArgs& a, hipStream_t s);
+hipError_t launch_loss_g(const HeadArgs& a, hipStream_t s);
 
 struct EvalHeadArgs {
   const float* part;     // partial logits [C][nn][(1 + nn) B][tn] (bias included)
