@@ -69,6 +69,16 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
 lipz_status lipz_test_es_select(void* hip_stream, const float* d_fit, const float* d_sets, float* d_params,
                                 int32_t n_units, int32_t n_pairs, int64_t P, int64_t stride, float clip);
 
+/*
+ * Host-only: the logical tile that each of the n_blocks workgroups of a
+ * grouped GEMM launch computes (tiles[b] for block b), for a launch whose
+ * n_groups (1..4) groups of problems start at tiles first_tile[0] = 0 <
+ * first_tile[1] < ... < n_blocks.  The kernels dispatch block b to XCD b % 8
+ * and give each XCD a contiguous chunk of every group.  Caller-owned host
+ * arrays; LIPZ_E_INVAL on a bad group layout.
+ */
+lipz_status lipz_test_tile_map(int32_t n_groups, const int32_t* first_tile, int32_t n_blocks, int32_t* tiles);
+
 #ifdef __cplusplus
 }
 #endif

@@ -10,6 +10,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <new>
 #include <string>
@@ -209,6 +210,7 @@ void carve(lipz_grid* g, char* base, size_t* total) {
     g->dDg[l] = cv.take<float>((size_t)U * B * D.fo[l]);
   }
   if (g->fused_head) g->aS = cv.take<float>((size_t)U * 2 * B * g->aS_ld);
+  if (g->hp_rows) g->hpart = cv.take<float>((size_t)U * g->hp_rows * g->hp_ld);
   // evaluation: rows [x_c; G_0(z_c); ...; G_(nn-1)(z_c)] per cell
   g->ze = cv.take<float>((size_t)C * B * zd);
   g->Xe = cv.take<float>((size_t)C * er * B * xd);
@@ -349,11 +351,13 @@ double prob_bytes(const GemmProb& p) {
   else b += mn;                                            // write C
   if (p.epi == EPI_DACT) b += mn;                          // read the forward output
   if (p.epi == EPI_BIAS_ACT && p.bias) b += p.N;
-  if (p.dot_out) b += (double)p.M * ((p.N + GEMM_BN - 1) / GEMM_BN) + p.N;
+  if (p.epi == EPI_BIAS_ACT && p.dot_out) b += (double)p.M * ((p.N + GEMM_BN - 1) / GEMM_BN) + p.N;
   if (p.epi == EPI_BIAS_ACT && p.dot_out && p.gout) b += mn;  // write w * act'
   if (p.epi == EPI_DACT && p.rs_mode) {
     b += (double)p.M * p.rs_tn;                                // read the partial logits
     if (p.side) b += mn + 8.0 * p.M;                           // scaled activations, dL/da, dlout
+    if (p.rs_mode == 1 && p.hpart)                             // output layer's gradient pieces
+      b += (double)p.M * p.hp_w + (double)((p.M + 31) / 32) * (p.hp_w + 1);
   }
   return 4.0 * b;
 }
@@ -374,7 +378,7 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
   for (const GemmProb& p : ps) max_k = p.K > max_k ? p.K : max_k;
   int tiles = 0;
   memset(&ph.grp, 0, sizeof(ph.grp));
-  int prev_tpp = -1;
+  int prev_tpp = -1, prev_k = -1;
   for (size_t k = 0; k < ps.size(); ++k) {
     GemmProb p = ps[k];
     // the epilogue addresses C (and aux, m, v) with 32-bit element offsets
@@ -389,8 +393,11 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
     p.tiles_n = ceil_div(p.N, GEMM_BN);
     p.tile_begin = tiles;
     const int tpp = ceil_div(p.M, ph.tile_rows) * p.tiles_n;
-    if (tpp != prev_tpp) {
-      // a new group; the problem lists built here have at most 2 shapes per phase
+    // a new group at every change of tile count (needed) and, while groups
+    // are left, of depth K (tiles of different cost are then spread over the
+    // XCDs separately)
+    if (tpp != prev_tpp || (p.K != prev_k && ph.grp.n < GEMM_MAX_GROUPS)) {
+      // the problem lists built here have at most 3 tile counts per phase
       if (ph.grp.n == GEMM_MAX_GROUPS) {  // a plan this library builds never gets here
         g->plan_ok = false;
         break;
@@ -401,6 +408,7 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
       ++ph.grp.n;
       prev_tpp = tpp;
     }
+    prev_k = p.K;
     tiles += tpp;
     ph.flops += prob_flops(p);
     ph.bytes += prob_bytes(p);
@@ -650,9 +658,38 @@ void build_tables(lipz_grid* g) {
         p.side = g->aS + (size_t)c * 2 * B * g->aS_ld;
         p.side_ld = g->aS_ld;
         p.dlout = g->dlbuf + (size_t)c * 2 * B * 4;
+        if (g->hpart) {
+          p.hpart = g->hpart + (size_t)c * g->hp_rows * g->hp_ld;
+          p.hsrc = g->a[t] + (size_t)c * 2 * B * H;
+          p.hp_w = H;
+          p.hp_ld = g->hp_ld;
+        }
         ph.push_back(p);
       }
-      ops.push_back({OP_GEMM, add_phase(g, ph)});
+      const int dgrad_phase = add_phase(g, ph);
+      ops.push_back({OP_GEMM, dgrad_phase});
+      if (g->hpart) {
+        // the output layer's weight gradient from the per-row-tile column
+        // sums: [w | b] = 1^T hpart over the launch's row tiles (a 1-row
+        // product whose A is the all-ones row), and its Adam step
+        const int rt = ceil_div(2 * B, g->phases[dgrad_phase].tile_rows);
+        head_grad.clear();
+        for (int c = cb; c < ce; ++c) {
+          const size_t o = c * sD + D.off[LD - 1];
+          float* hp = g->hpart + (size_t)c * g->hp_rows * g->hp_ld;
+          GemmProb p = base_prob(hp, g->hp_ld, 1, hp, g->hp_ld, 0, S.Dp + o, H + 1, 1, H + 1, rt);
+          p.a_rows = 0;
+          p.ones_row = 0;
+          p.m = S.Dm + o;
+          p.v = S.Dv + o;
+          p.lr = S.Dlr + c;
+          p.t = S.Dt + c;
+          p.epi = EPI_ADAM;
+          p.clip = d_clip;
+          if (g->cfg.loss_kind == LIPZ_LOSS_WASSERSTEIN) p.gscale = 1.f / (float)B;  // sums of exact +-1
+          head_grad.push_back(p);
+        }
+      }
       std::vector<GemmProb> pending;
       for (int c = cb; c < ce; ++c) {
         const size_t o = c * sD + D.off[t];
@@ -944,6 +981,10 @@ lipz_grid* plan_grid(const lipz_config* cfg, int64_t n_samples, char* base, cons
     // hidden layers (the discriminator step needs the layer below the last)
     g->fused_head = LIPZ_FUSED_HEAD && cfg->trainer == LIPZ_TRAINER_GRADIENT && Dn.nl >= 3;
     if (g->fused_head) g->aS_ld = (Dn.fi[Dn.nl - 2] + 4 + 3) / 4 * 4;
+    if (g->fused_head && Dn.fi[Dn.nl - 1] <= Dn.fi[Dn.nl - 2]) {
+      g->hp_rows = (2 * g->B + 31) / 32;  // row tiles of the input-gradient launch (at most, 32-row tiles)
+      g->hp_ld = (Dn.fi[Dn.nl - 1] + 1 + 3) / 4 * 4;
+    }
   }
   g->data = data;
   g->key = make_uint2((uint32_t)(cfg->seed & 0xFFFFFFFFull), (uint32_t)(cfg->seed >> 32));
@@ -1853,8 +1894,9 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
       note("gemm Adam state", i);
     if (p.epi == EPI_DACT && !inside(p.aux, 0, c_last)) note("gemm aux", i);
     if (p.epi == EPI_BIAS_ACT && p.bias && !inside(p.bias, 0, p.N - 1)) note("gemm bias", i);
-    if (p.dot_out && (!inside(p.dot_out, 0, (int64_t)(p.M - 1) * p.dot_ld + (p.N + GEMM_BN - 1) / GEMM_BN - 1) ||
-                      !inside(p.dotw, 0, p.N - 1)))
+    if (p.epi == EPI_BIAS_ACT && p.dot_out &&
+        (!inside(p.dot_out, 0, (int64_t)(p.M - 1) * p.dot_ld + (p.N + GEMM_BN - 1) / GEMM_BN - 1) ||
+         !inside(p.dotw, 0, p.N - 1)))
       note("gemm dot", i);
     // fields that share storage with others are checked under the epilogue that reads them
     if (p.epi == EPI_BIAS_ACT && p.dot_out && p.gout && !inside(p.gout, 0, c_last)) note("gemm head factor", i);
@@ -1863,7 +1905,36 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
       if (p.side && (p.side_ld < p.N + 4 || !inside(p.side, 0, (int64_t)(p.M - 1) * p.side_ld + p.N + 3) ||
                      !inside(p.dlout, 0, (int64_t)p.M * 4 - 1)))
         note("gemm head side outputs", i);
+      // row tile m0 / BM (BM >= 32) of the output layer's gradient pieces
+      if (p.rs_mode == 1 && p.hpart &&
+          (p.hp_w < 1 || p.hp_w > p.N || p.hp_ld < p.hp_w + 1 ||
+           !inside(p.hpart, 0, (int64_t)((p.M - 1) / 32) * p.hp_ld + p.hp_w) ||
+           !inside(p.hsrc, 0, (int64_t)p.M * p.hp_w - 1)))
+        note("gemm head gradient pieces", i);
     }
+  }
+  // every GEMM launch's block -> tile map covers each tile exactly once and
+  // spreads each group over the 8 XCDs within one tile
+  for (size_t k = 0; k < g->phases.size(); ++k) {
+    const Phase& ph = g->phases[k];
+    std::vector<int> seen((size_t)ph.tiles, 0), per((size_t)ph.grp.n * 8, 0);
+    bool ok = ph.grp.n >= 1;
+    for (int b = 0; ok && b < ph.tiles; ++b) {
+      const int t = xcd_group_tile(b, ph.tiles, ph.grp);
+      if (t < 0 || t >= ph.tiles || seen[(size_t)t]++) {
+        ok = false;
+        break;
+      }
+      int gi = 0;
+      for (int q = 1; q < ph.grp.n; ++q)
+        if (t >= ph.grp.first_tile[q]) gi = q;
+      ++per[(size_t)gi * 8 + (b & 7)];
+    }
+    for (int gi = 0; ok && gi < ph.grp.n; ++gi) {
+      const auto mm = std::minmax_element(per.begin() + gi * 8, per.begin() + gi * 8 + 8);
+      ok = *mm.second - *mm.first <= 1;
+    }
+    if (!ok) note("gemm tile map", k);
   }
   if (!g->dc) {
     // the sample, evaluation-head, fitness, selection and re-evaluation

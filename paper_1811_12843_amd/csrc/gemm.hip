@@ -71,14 +71,6 @@ constexpr int KQ = BK / 4;    // float4 per row of a k-contiguous slice
 constexpr int NT = 256;
 constexpr int S_K = BK + 4;   // row stride of k-contiguous LDS tiles ([m][k], [n][k])
 
-// Blocks are dispatched round-robin over the 8 XCDs (block b -> XCD b % 8).
-// Give each XCD a contiguous range of logical tiles so that tiles of one
-// problem (which share A rows and B columns) meet in the same L2.
-__device__ __forceinline__ int xcd_remap(int b, int nb) {
-  const int q = nb >> 3, r = nb & 7;
-  const int x = b & 7, i = b >> 3;
-  return x * q + (x < r ? x : r) + i;
-}
 
 template <int BM>
 struct Tile {
@@ -259,6 +251,69 @@ __device__ __forceinline__ void head_rows_dl(const GemmProb& P, int m0, float (&
   }
 }
 
+// The output layer's weight gradient of the discriminator step, in pieces:
+// this tile's column sums of dL/da[i] * hsrc[i][j] over its rows (and, in
+// column 0, of dL/da[i]), summed over the lane groups and then over the two
+// waves that share the tile's columns, in a fixed order.  Rows past M and
+// columns past hp_w add nothing.
+template <int BM>
+__device__ __forceinline__ void head_partials(const GemmProb& P, const float (&dl)[Tile<BM>::TI][4], int m0,
+                                              int n0, int tile_n, float (*red)[BM]) {
+  using T = Tile<BM>;
+  __shared__ float dsum;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * T::WM, wn = (wave & 1) * 32;
+  const int li = lane & 15, lg = lane >> 4;
+  const bool wgan = P.loss_kind == LIPZ_LOSS_WASSERSTEIN;
+  const __amdgpu_buffer_rsrc_t rH = make_rsrc(P.hsrc, kWholeBuffer);
+  float hv[T::TI][2][4];
+#pragma unroll
+  for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = m0 + wm + 16 * i + 4 * lg + r, col = n0 + wn + 16 * j + li;
+        const bool in = row < P.M && col < P.hp_w;
+        const float x = bld1(rH, in ? (uint32_t)(row * P.hp_w + col) : 0u);
+        hv[i][j][r] = in ? x : 0.f;
+      }
+  float cs[2] = {0.f, 0.f}, ds = 0.f;
+#pragma unroll
+  for (int i = 0; i < T::TI; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + wm + 16 * i + 4 * lg + r;
+      const float d = row < P.M ? (wgan ? (row < P.rs_B ? -1.f : 1.f) : dl[i][r]) : 0.f;
+      ds += d;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) cs[j] += d * hv[i][j][r];
+    }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    cs[j] += __shfl_xor(cs[j], 16, 64);
+    cs[j] += __shfl_xor(cs[j], 32, 64);
+  }
+  ds += __shfl_xor(ds, 16, 64);
+  ds += __shfl_xor(ds, 32, 64);
+  if (wm != 0 && lane < 16) {
+    red[wave & 1][li] = cs[0];
+    red[wave & 1][16 + li] = cs[1];
+    if (wn == 0 && lane == 0) dsum = ds;
+  }
+  __syncthreads();
+  if (wm == 0 && lane < 16) {
+    LIPZ_GLOBAL float* o = as_global(P.hpart) + (size_t)(m0 / BM) * P.hp_ld;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wn + 16 * j + li;
+      if (col < P.hp_w) o[col] = cs[j] + red[wave & 1][16 * j + li];
+    }
+    if (tile_n == 0 && wn == 0 && lane == 0) o[P.hp_w] = ds + dsum;
+  }
+}
+
 // Epilogue shared by both kernel variants: bias + activation (optionally
 // with the per-tile partial dot product of the next 1-wide layer), the
 // activation-derivative product, or the fused Adam update; then stores.
@@ -358,6 +413,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
             }
           }
         }
+    if (P.rs_mode == 1 && P.hpart) head_partials<BM>(P, dl, m0, n0, tile_n, red);
     // column 0 of the problem: the per-row extras
     if (P.side && tile_n == 0 && wn == 0 && li == 0) {
       LIPZ_GLOBAL float* gDl = as_global(P.dlout);
@@ -454,7 +510,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_generic_kernel(const GemmProb* __r
                                                              GemmGroups grp, int step_local,
                                                              float slope, AdamConsts ac) {
   using T = Tile<BM>;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int t = xcd_group_tile(blockIdx.x, gridDim.x, grp);
   int gi = 0;
 #pragma unroll
   for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
@@ -733,7 +789,7 @@ __global__ __launch_bounds__(NT, BM == 32 ? LIPZ_GEMM_WG32 : LIPZ_GEMM_WG64) voi
                                                           GemmGroups grp, int step_local, float slope,
                                                           AdamConsts ac) {
   using T = Tile<BM>;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int t = xcd_group_tile(blockIdx.x, gridDim.x, grp);
   int gi = 0;
 #pragma unroll
   for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
@@ -899,7 +955,7 @@ __global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(const G
                                                           AdamConsts ac) {
   using T = Tile<BM>;
   constexpr int RS = BN + 4;  // row stride of the partial tiles in LDS
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int t = xcd_group_tile(blockIdx.x, gridDim.x, grp);
   int gi = 0;
 #pragma unroll
   for (int q = 1; q < GEMM_MAX_GROUPS; ++q)

@@ -120,6 +120,11 @@ struct lipz_grid {
   bool fused_head = false;
   float* aS = nullptr;
   int aS_ld = 0;
+  // ... and, when D's last hidden layer is at most as wide as the one below
+  // it, the output layer's weight gradient in per-row-tile column sums
+  // hpart [U][hp_rows][hp_ld] written by the input-gradient launch
+  float* hpart = nullptr;
+  int hp_rows = 0, hp_ld = 0;
   int tn = 1;  // column tiles of D's last hidden layer
   // evaluation buffers
   float *ze = nullptr, *Xe = nullptr;

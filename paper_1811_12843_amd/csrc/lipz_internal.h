@@ -137,8 +137,17 @@ struct GemmProb {
     float* v;          // EPI_ADAM: the second moment
     float* dlout;      // EPI_DACT with side
   };
-  const float* lr;     // EPI_ADAM: the cell's learning rate
-  const int32_t* t;    // EPI_ADAM: the cell's Adam step count before this call
+  union {
+    const float* lr;   // EPI_ADAM: the cell's learning rate
+    const float* hsrc; // EPI_DACT with hpart: see the loss head below
+  };
+  union {
+    const int32_t* t;  // EPI_ADAM: the cell's Adam step count before this call
+    struct {
+      int32_t hp_w;    // EPI_DACT with hpart: columns of hsrc (its row stride)
+      int32_t hp_ld;   // EPI_DACT with hpart: row stride of hpart
+    };
+  };
   // EPI_BIAS_ACT only: when dot_out is set, the tile also writes
   //   dot_out[i*dot_ld + tile_n] = sum over its columns j of C[i][j] * dotw[j]
   // (+ *dot_bias in tile column 0): the next layer's 1-wide output, split
@@ -148,7 +157,10 @@ struct GemmProb {
     const float* rs_part;  // EPI_DACT with rs_mode
   };
   const float* dot_bias;
-  float* dot_out;
+  union {
+    float* dot_out;
+    float* hpart;      // EPI_DACT with rs_mode 1: see the loss head below
+  };
   int32_t M, N, K;
   int32_t lda, ldb, ldc;
   int32_t a_trans, b_trans;
@@ -184,6 +196,13 @@ struct GemmProb {
   //    tiles of column 0 also write side[i * side_ld + N] = dL/da[i], zeros
   //    at N + 1 .. N + 3, and dlout[4 i] = dL/da[i] (Wasserstein: the exact
   //    +-1 of the separate head, scaled by 1 / rs_B later), dlout[4 i + 1 .. 3] = 0.
+  //  * EPI_DACT with rs_mode 1 and hpart set (hp_w <= N): the output layer's
+  //    weight gradient in per-row-tile pieces.  The tile of rows m0 .. m0+BM-1
+  //    writes, for its columns j < hp_w, hpart[(m0 / BM) * hp_ld + j] = sum
+  //    over its rows i of dL/da[i] * hsrc[i * hp_w + j] (hsrc: the last hidden
+  //    layer's activations), and the tile of column 0 also
+  //    hpart[(m0 / BM) * hp_ld + hp_w] = sum over its rows of dL/da[i]
+  //    (Wasserstein: the +-1 of dlout in both).
   int16_t rs_mode, loss_kind;
 };
 
@@ -204,6 +223,39 @@ struct GemmGroups {
   int32_t first_prob[GEMM_MAX_GROUPS];
   int32_t tiles_per_prob[GEMM_MAX_GROUPS];
 };
+
+// Blocks are dispatched round-robin over the 8 XCDs (block b -> XCD b % 8).
+// Each group of problems (tiles of one shape) is split into 8 contiguous
+// chunks, one per XCD, whose sizes differ by at most one tile (the larger
+// chunks rotate over the XCDs from group to group), and an XCD runs its
+// chunks group after group.  Tiles of one problem (which share A rows and B
+// columns) meet in the same L2, and every group is spread evenly over the
+// XCDs, so a launch that mixes short and long tiles does not pile the long
+// ones onto a few XCDs.  The per-XCD totals equal the number of blocks the
+// round-robin dispatch gives each XCD.
+__host__ __device__ inline int xcd_group_tile(int b, int nb, const GemmGroups& grp) {
+  const int x = b & 7;
+  int i = b >> 3, s = 0, t = 0;
+#pragma unroll
+  for (int g = 0; g < GEMM_MAX_GROUPS; ++g) {
+    if (g < grp.n) {
+      const int last = g + 1 == grp.n;
+      const int tg = (last ? nb : grp.first_tile[g + 1]) - grp.first_tile[g];
+      const int q = tg >> 3, r = tg & 7;
+      const int cnt = q + (((x - s) & 7) < r ? 1 : 0);
+      if (i >= 0 && (i < cnt || last)) {
+        // chunks before x that hold one extra tile: XCDs s .. s + r - 1 (mod 8)
+        const int e = s + r;
+        int ext = x > s ? (x < e ? x : e) - s : 0;
+        if (e > 8) ext += x < e - 8 ? x : e - 8;
+        t = grp.first_tile[g] + x * q + ext + i;
+      }
+      i -= cnt;
+      s = (s + r) & 7;
+    }
+  }
+  return t;
+}
 
 // Tile height (32 or 64 rows) for a phase that has `tiles64` tiles of 64x64.
 int gemm_tile_rows(int tiles64);

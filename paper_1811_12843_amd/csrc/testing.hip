@@ -100,3 +100,19 @@ extern "C" lipz_status lipz_test_es_select(void* hip_stream, const float* d_fit,
   a.clip = clip;
   return launch_es_select(a, (hipStream_t)hip_stream) == hipSuccess ? LIPZ_OK : LIPZ_E_HIP;
 }
+
+extern "C" lipz_status lipz_test_tile_map(int32_t n_groups, const int32_t* first_tile, int32_t n_blocks,
+                                          int32_t* tiles) {
+  if (n_groups < 1 || n_groups > lipz::GEMM_MAX_GROUPS || !first_tile || !tiles || n_blocks < 1 ||
+      first_tile[0] != 0)
+    return LIPZ_E_INVAL;
+  lipz::GemmGroups grp{};
+  grp.n = n_groups;
+  for (int g = 0; g < n_groups; ++g) {
+    if (g > 0 && first_tile[g] <= first_tile[g - 1]) return LIPZ_E_INVAL;
+    if (first_tile[g] >= n_blocks) return LIPZ_E_INVAL;
+    grp.first_tile[g] = first_tile[g];
+  }
+  for (int32_t b = 0; b < n_blocks; ++b) tiles[b] = lipz::xcd_group_tile(b, n_blocks, grp);
+  return LIPZ_OK;
+}

@@ -121,6 +121,7 @@ _SIGS = {
                               _vp, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                               _f32, _f32, _f32, _i32, _i32]),
     "lipz_test_es_select": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _i64, _i64, _f32]),
+    "lipz_test_tile_map": (_i32, [_i32, _vp, _i32, _vp]),
 }
 
 _lib = None
@@ -304,3 +305,11 @@ def lipz_test_plan_bounds(cfg, n_samples):
     _check(load_library().lipz_test_plan_bounds(ctypes.byref(cfg), n_samples, buf, 4096, ctypes.byref(bad)),
            "lipz_test_plan_bounds")
     return bad.value, buf.value.decode()
+
+
+def lipz_test_tile_map(first_tile, n_blocks):
+    """Logical tile of each block of a grouped GEMM launch (host only)."""
+    ft = (_i32 * len(first_tile))(*first_tile)
+    out = (_i32 * n_blocks)()
+    _check(load_library().lipz_test_tile_map(len(first_tile), ft, n_blocks, out), "lipz_test_tile_map")
+    return list(out)

@@ -129,3 +129,32 @@ def test_outputs_reaching_2_31_elements_are_rejected():
     assert L.lipz_workspace_bytes(L.config_from_dict(under), 64) > 0
     n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(under), 64)
     assert n_bad == 0, msg
+
+
+@pytest.mark.parametrize("groups,nb", [
+    ([0], 1), ([0], 7), ([0], 8), ([0], 256), ([0], 2176),
+    ([0, 144], 400),            # short tiles then long ones
+    ([0, 256], 2128), ([0, 1600], 2176), ([0, 3, 10], 13), ([0, 1, 2, 3], 4),
+    ([0, 5, 11, 30], 47), ([0, 100, 101, 350], 357),
+])
+def test_tile_map_covers_every_tile_once_and_spreads_groups(groups, nb):
+    """Block b runs on XCD b % 8.  The map is a permutation of the tiles; each
+    group's tiles on one XCD are a contiguous run, and the XCDs' shares of a
+    group differ by at most one tile."""
+    t = L.lipz_test_tile_map(groups, nb)
+    assert sorted(t) == list(range(nb))
+    bounds = groups + [nb]
+    for gi in range(len(groups)):
+        lo, hi = bounds[gi], bounds[gi + 1]
+        per = [[tt for b, tt in enumerate(t) if b % 8 == x and lo <= tt < hi] for x in range(8)]
+        sizes = [len(p) for p in per]
+        assert max(sizes) - min(sizes) <= 1, sizes
+        for p in per:  # contiguous, in block order
+            assert p == list(range(p[0], p[0] + len(p))) if p else True
+        assert sum(sizes) == hi - lo
+
+
+def test_tile_map_rejects_bad_groups():
+    for groups, nb in [([1], 4), ([0, 0], 4), ([0, 5], 5), ([0, 1, 2, 3, 4], 9), ([], 3)]:
+        with pytest.raises(RuntimeError):
+            L.lipz_test_tile_map(groups, nb)
