@@ -21,6 +21,9 @@
 
 using namespace lipz;
 
+#ifndef LIPZ_FUSED_SAMPLE
+#define LIPZ_FUSED_SAMPLE 1  // draw the next step's minibatch inside a launch of the current one
+#endif
 #ifndef LIPZ_FUSED_HEAD
 #define LIPZ_FUSED_HEAD 1
 #endif
@@ -197,6 +200,10 @@ void carve(lipz_grid* g, char* base, size_t* total) {
   // training (one unit per individual pair)
   g->z = cv.take<float>((size_t)U * B * zd);
   g->Xtr = cv.take<float>((size_t)U * 2 * B * xd);
+  if (g->fused_sample) {
+    g->z_alt = cv.take<float>((size_t)U * B * zd);
+    g->Xtr_alt = cv.take<float>((size_t)U * 2 * B * xd);
+  }
   for (int l = 0; l + 1 < G.nl; ++l) g->h[l] = cv.take<float>((size_t)U * B * G.fo[l]);
   for (int l = 0; l < G.nl; ++l) g->dG[l] = cv.take<float>((size_t)U * B * G.fo[l]);
   g->part_tr = cv.take<float>((size_t)U * 2 * B * g->tn);
@@ -565,26 +572,33 @@ void build_tables(lipz_grid* g) {
   const bool fused = g->fused_head;
   for (int par = 0; par < 2; ++par) {
     const StateBuf& S = g->st[par];
-    for (int grp = 0; grp < g->n_groups; ++grp) {
+    for (int grp = 0; grp < g->n_groups; ++grp)
+    // with the minibatch drawn one step ahead, steps alternate between two
+    // buffers of minibatch and latents: the odd steps have their own tables
+    for (int sp = 0; sp < (g->fused_sample ? 2 : 1); ++sp) {
     const int cb = g->group_c0[grp], ce = g->group_c0[grp + 1];
-    std::vector<Op>& ops = g->train_ops[par][grp];
+    std::vector<Op>& ops = sp ? g->train_ops_odd[par][grp] : g->train_ops[par][grp];
+    float* const Zb = sp ? g->z_alt : g->z;
+    float* const Xb = sp ? g->Xtr_alt : g->Xtr;
     ops.clear();
     // ---- training step ----
     ops.push_back({OP_SAMPLE, -1});
     for (int l = 0; l < LG; ++l) {
       std::vector<GemmProb> ps;
       for (int c = cb; c < ce; ++c) {
-        const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
+        const float* x = l == 0 ? Zb + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
         float* y = l + 1 < LG ? g->h[l] + (size_t)c * B * G.fo[l]
-                              : g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd;
+                              : Xb + (size_t)c * 2 * B * xd + (size_t)B * xd;
         ps.push_back(fwd_prob(x, B, S.Gp + c * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
       }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
+      // the first layer's launch also draws the next step's minibatch
+      if (l == 0 && g->fused_sample) ops.back().sample_next = 1;
     }
     for (int l = 0; l + 1 < LD; ++l) {
       std::vector<GemmProb> ps;
       for (int c = cb; c < ce; ++c) {
-        const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
+        const float* x = l == 0 ? Xb + (size_t)c * 2 * B * xd
                                 : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
         GemmProb p = fwd_prob(x, 2 * B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
                               g->a[l] + (size_t)c * 2 * B * D.fo[l], D.act[l]);
@@ -624,7 +638,7 @@ void build_tables(lipz_grid* g) {
     };
     auto d_wgrad = [&](int l, std::vector<GemmProb>* ph) {
       for (int c = cb; c < ce; ++c) {
-        const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd
+        const float* x = l == 0 ? Xb + (size_t)c * 2 * B * xd
                                 : g->a[l - 1] + (size_t)c * 2 * B * D.fi[l];
         const size_t o = c * sD + D.off[l];
         GemmProb p = wgrad_adam_prob(x, 2 * B, D.fi[l], g->dD[l] + (size_t)c * 2 * B * D.fo[l],
@@ -722,7 +736,7 @@ void build_tables(lipz_grid* g) {
       // first layer's forward on the fakes, before the output layer is read
       if (fused && l == 0) ps = head_grad;
       for (int c = cb; c < ce; ++c) {
-        const float* x = l == 0 ? g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd
+        const float* x = l == 0 ? Xb + (size_t)c * 2 * B * xd + (size_t)B * xd
                                 : g->ag[l - 1] + (size_t)c * B * D.fi[l];
         GemmProb p = fwd_prob(x, B, S.Dp + c * sD + D.off[l], D.fi[l], D.fo[l],
                               g->ag[l] + (size_t)c * B * D.fo[l], D.act[l]);
@@ -754,7 +768,7 @@ void build_tables(lipz_grid* g) {
           // into the generator output: delta of G's last layer
           ps.push_back(dgrad_prob(g->dDg[0] + (size_t)c * B * D.fo[0], B, S.Dp + c * sD + D.off[0],
                                   D.fi[0], D.fo[0], g->dG[LG - 1] + (size_t)c * B * xd,
-                                  g->Xtr + (size_t)c * 2 * B * xd + (size_t)B * xd, G.act[LG - 1]));
+                                  Xb + (size_t)c * 2 * B * xd + (size_t)B * xd, G.act[LG - 1]));
         }
       }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
@@ -769,7 +783,7 @@ void build_tables(lipz_grid* g) {
         },
         [&](int l, std::vector<GemmProb>* ph) {
           for (int c = cb; c < ce; ++c) {
-            const float* x = l == 0 ? g->z + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
+            const float* x = l == 0 ? Zb + (size_t)c * B * zd : g->h[l - 1] + (size_t)c * B * G.fi[l];
             const size_t o = c * sG + G.off[l];
             ph->push_back(wgrad_adam_prob(x, B, G.fi[l], g->dG[l] + (size_t)c * B * G.fo[l], G.fo[l],
                                           S.Gp + o, S.Gm + o, S.Gv + o, S.Glr + c, S.Gt + c));
@@ -782,7 +796,7 @@ void build_tables(lipz_grid* g) {
       ops.push_back({OP_LOSS_D, -1});
       ops.push_back({OP_LOSS_G, -1});
     }
-    }  // groups
+    }  // groups and step parities
 
     // ---- evaluation: rows [x_c; G_0(z_c); ...; G_(nn-1)(z_c)] per cell ----
     const int s = g->s, nn = g->nn, er = 1 + nn;
@@ -928,13 +942,13 @@ void timing_record(lipz_grid* g, hipEvent_t e0, hipEvent_t e1, double flops, dou
   g->ev_bytes.push_back(bytes);
 }
 
-hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t stream) {
+hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t stream, const SampleJob* job) {
   const Phase& ph = g->phases[phase];
   hipEvent_t e0, e1;
   hipError_t e = timing_events(g, &e0, &e1);
   if (e != hipSuccess) return e;
   e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.kernel, step_local,
-                          g->slope, g->ac, stream, e0, e1);
+                          g->slope, g->ac, stream, e0, e1, job);
   timing_record(g, e0, e1, ph.flops, ph.bytes);
   return e;
 }
@@ -980,6 +994,7 @@ lipz_grid* plan_grid(const lipz_config* cfg, int64_t n_samples, char* base, cons
     // the loss head folds into the launches around it when D has two or more
     // hidden layers (the discriminator step needs the layer below the last)
     g->fused_head = LIPZ_FUSED_HEAD && cfg->trainer == LIPZ_TRAINER_GRADIENT && Dn.nl >= 3;
+    g->fused_sample = LIPZ_FUSED_SAMPLE && cfg->trainer == LIPZ_TRAINER_GRADIENT;
     if (g->fused_head) g->aS_ld = (Dn.fi[Dn.nl - 2] + 4 + 3) / 4 * 4;
     if (g->fused_head && Dn.fi[Dn.nl - 1] <= Dn.fi[Dn.nl - 2]) {
       g->hp_rows = (2 * g->B + 31) / 32;  // row tiles of the input-gradient launch (at most, 32-row tiles)
@@ -1210,23 +1225,48 @@ void train_heads(lipz_grid* g, int par, HeadArgs* hd, HeadArgs* hg) {
 }
 
 // Gradient-trainer step k (training step `step`) of group grp of buffer par.
-lipz_status enq_train_group_step(lipz_grid* g, int gen, int par, int grp, int k, int step, float* d_losses,
-                                 const HeadArgs& hd, const HeadArgs& hg, hipStream_t gs) {
+// One training step of cell group grp.  first: the step's minibatch is not
+// drawn yet (the first step of a sequence); last: no further step follows,
+// so the next minibatch is not drawn.
+lipz_status enq_train_group_step(lipz_grid* g, int gen, int par, int grp, int k, int step, bool first, bool last,
+                                 float* d_losses, const HeadArgs& hd, const HeadArgs& hg, hipStream_t gs) {
   const int B = g->B;
   const int c0 = g->group_c0[grp], nc = g->group_c0[grp + 1] - c0;
   HeadArgs gd = hd, gg = hg;
   gd.c0 = gg.c0 = c0;
   gd.C = gg.C = nc;
   gd.losses = gg.losses = d_losses ? d_losses + (size_t)k * g->U * 2 : nullptr;
+  const bool odd = g->fused_sample && (step & 1);
+  // the draw of step + 1 for the other buffer pair
+  SampleJob job;
+  memset(&job, 0, sizeof(job));
+  if (g->fused_sample && !last) {
+    job.data = g->data;
+    job.N = g->N;
+    job.X = odd ? g->Xtr : g->Xtr_alt;
+    job.Z = odd ? g->z : g->z_alt;
+    job.x_stride = (int64_t)2 * B * g->xd;
+    job.z_stride = (int64_t)B * g->zd;
+    job.key = g->key;
+    job.gen = (uint32_t)gen;
+    job.sf = (uint32_t)(step + 2);
+    job.xd = g->xd;
+    job.zd = g->zd;
+    job.B = B;
+    job.u0 = c0;
+    job.blocks = nc * ((B + SAMPLE_ROWS - 1) / SAMPLE_ROWS);
+  }
   lipz_status st;
-  for (const Op& op : g->train_ops[par][grp]) {
+  for (const Op& op : odd ? g->train_ops_odd[par][grp] : g->train_ops[par][grp]) {
     hipError_t e = hipSuccess;
     switch (op.kind) {
       case OP_SAMPLE:
-        e = launch_sample(g->data, g->N, g->xd, g->zd, B, c0, nc, g->key, (uint32_t)gen, (uint32_t)(step + 1),
-                          g->Xtr, (int64_t)2 * B * g->xd, g->z, (int64_t)B * g->zd, gs);
+        if (!g->fused_sample || first)
+          e = launch_sample(g->data, g->N, g->xd, g->zd, B, c0, nc, g->key, (uint32_t)gen, (uint32_t)(step + 1),
+                            odd ? g->Xtr_alt : g->Xtr, (int64_t)2 * B * g->xd, odd ? g->z_alt : g->z,
+                            (int64_t)B * g->zd, gs);
         break;
-      case OP_GEMM: e = run_gemm_phase(g, op.phase, k, gs); break;
+      case OP_GEMM: e = run_gemm_phase(g, op.phase, k, gs, op.sample_next && job.blocks ? &job : nullptr); break;
       case OP_HEAD_D: e = launch_head_d(gd, gs); break;
       case OP_HEAD_G: e = launch_head_g(gg, gs); break;
       case OP_LOSS_D: if (d_losses) e = launch_loss_d(gd, gs); break;
@@ -1559,7 +1599,9 @@ lipz_status lipz_train_step(lipz_grid* g, int32_t gen, int32_t step0, int32_t n_
   // enqueue step by step across the groups so every stream has work early
   for (int k = 0; k < n_steps; ++k)
     for (int grp = 0; grp < g->n_groups; ++grp)
-      if ((st = enq_train_group_step(g, gen, par, grp, k, step0 + k, d_losses, hd, hg, g->gstream[grp]))) return st;
+      if ((st = enq_train_group_step(g, gen, par, grp, k, step0 + k, k == 0, k + 1 == n_steps, d_losses, hd, hg,
+                                     g->gstream[grp])))
+        return st;
   // join: the caller's stream waits for every group
   for (int i = 1; i < g->n_groups; ++i) {
     if ((st = check_hip(g, hipEventRecord(g->join_ev[i], g->gstream[i]), "join"))) return st;
@@ -1603,7 +1645,8 @@ static lipz_status enq_band_generations(lipz_grid* g, int gen0, int n_gens, int 
           const int u0 = g->band_c0[b] * sp, nu = g->band_c0[b + 1] * sp - u0;
           if ((st = enq_nes_step(g, gen, g->nes_band_ops[1 - par][b], na, u0, nu, k, k, nullptr, g->gstream[b])))
             return st;
-        } else if ((st = enq_train_group_step(g, gen, 1 - par, b, k, k, nullptr, hd, hg, g->gstream[b]))) {
+        } else if ((st = enq_train_group_step(g, gen, 1 - par, b, k, k, k == 0, k + 1 == n_steps, nullptr, hd, hg,
+                                              g->gstream[b]))) {
           return st;
         }
       }
@@ -1942,6 +1985,9 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
     const int64_t C = g->C, U = g->U, B = g->B, tn = g->tn, nn = g->nn, s = g->s, er = 1 + nn;
     if (!inside(g->Xe, 0, C * er * B * g->xd - 1) || !inside(g->ze, 0, C * B * g->zd - 1)) note("eval sample", 0);
     if (!inside(g->Xtr, 0, U * 2 * B * g->xd - 1) || !inside(g->z, 0, U * B * g->zd - 1)) note("train sample", 0);
+    if (g->fused_sample &&
+        (!inside(g->Xtr_alt, 0, U * 2 * B * g->xd - 1) || !inside(g->z_alt, 0, U * B * g->zd - 1)))
+      note("train sample, odd steps", 0);
     if (!inside(g->part_e, 0, C * nn * er * B * tn - 1)) note("eval logits", 0);
     if (!inside(g->L, 0, C * nn * nn - 1) || !inside(g->Lg, 0, C * nn * nn - 1)) note("eval losses", 0);
     if (!inside(g->fit_g, 0, C * nn - 1) || !inside(g->fit_d, 0, C * nn - 1)) note("fitness", 0);

@@ -32,6 +32,8 @@
 // MFMA 16x16x4 f32 operand layout (wave64): lane l supplies A[l % 16][l / 16]
 // and B[l / 16][l % 16]; accumulator register r of lane l is
 // D[4 (l / 16) + r][l % 16].
+#include <string.h>
+
 #include <hip/hip_ext.h>
 
 #include "lipz_internal.h"
@@ -248,6 +250,33 @@ __device__ __forceinline__ void head_rows_dl(const GemmProb& P, int m0, float (&
     const float mine = head_dl(P.loss_kind, a, P.rs_mode == 2 || row < P.rs_B, invB);
 #pragma unroll
     for (int r = 0; r < 4; ++r) dl[i][r] = __shfl(mine, (lane & ~15) | r, 64);
+  }
+}
+
+// Workgroup q of a sampling job: SAMPLE_ROWS minibatch rows of one unit,
+// drawn exactly as sample_kernel draws them.
+__device__ __forceinline__ void sample_rows(const SampleJob& sj, int q) {
+  const int per = (sj.B + SAMPLE_ROWS - 1) / SAMPLE_ROWS;
+  const int u = sj.u0 + q / per, b0 = (q % per) * SAMPLE_ROWS;
+  const int nr = sj.B - b0 < SAMPLE_ROWS ? sj.B - b0 : SAMPLE_ROWS;
+  const int tid = threadIdx.x;
+  for (int rr = 0; rr < nr; ++rr) {
+    const int b = b0 + rr;
+    const uint4 wi = stream_block(sj.key, (uint32_t)(b >> 2), (uint32_t)u, sj.gen, sj.sf, LIPZ_TAG_IDX);
+    const int64_t row = (int64_t)(((uint64_t)word_of(wi, b & 3) * (uint64_t)sj.N) >> 32);
+    const float* src = sj.data + row * sj.xd;
+    float* dst = sj.X + u * sj.x_stride + (int64_t)b * sj.xd;
+    if ((sj.xd & 3) == 0) {
+      for (int k = tid; k < (sj.xd >> 2); k += NT)
+        reinterpret_cast<float4*>(dst)[k] = reinterpret_cast<const float4*>(src)[k];
+    } else {
+      for (int k = tid; k < sj.xd; k += NT) dst[k] = src[k];
+    }
+  }
+  for (int k = tid; k < nr * sj.zd; k += NT) {
+    const int64_t e = (int64_t)b0 * sj.zd + k;
+    const uint4 w = stream_block(sj.key, (uint32_t)(e >> 2), (uint32_t)u, sj.gen, sj.sf, LIPZ_TAG_Z);
+    sj.Z[u * sj.z_stride + e] = (float)normal_of(w, (int)(e & 3));
   }
 }
 
@@ -508,9 +537,17 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
 template <int BM>
 __global__ __launch_bounds__(NT, 2) void gemm_generic_kernel(const GemmProb* __restrict__ probs,
                                                              GemmGroups grp, int step_local,
-                                                             float slope, AdamConsts ac) {
+                                                             float slope, AdamConsts ac, SampleJob sj) {
   using T = Tile<BM>;
-  const int t = xcd_group_tile(blockIdx.x, gridDim.x, grp);
+  // every kernel-argument line the GEMM path reads (the groups, then
+  // step_local, slope and the Adam constants) is requested before the first
+  // branch, so that the arguments arrive in one round trip
+  asm volatile("" ::"s"(grp.total), "s"(step_local));
+  if ((int)blockIdx.x >= grp.total) {
+    sample_rows(sj, (int)blockIdx.x - grp.total);
+    return;
+  }
+  const int t = xcd_group_tile(blockIdx.x, grp.total, grp);
   int gi = 0;
 #pragma unroll
   for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
@@ -787,9 +824,17 @@ __device__ __forceinline__ void fast_mainloop(const GemmProb& P, int m0, int n0,
 template <int BM>
 __global__ __launch_bounds__(NT, BM == 32 ? LIPZ_GEMM_WG32 : LIPZ_GEMM_WG64) void gemm_fast_kernel(const GemmProb* __restrict__ probs,
                                                           GemmGroups grp, int step_local, float slope,
-                                                          AdamConsts ac) {
+                                                          AdamConsts ac, SampleJob sj) {
   using T = Tile<BM>;
-  const int t = xcd_group_tile(blockIdx.x, gridDim.x, grp);
+  // every kernel-argument line the GEMM path reads (the groups, then
+  // step_local, slope and the Adam constants) is requested before the first
+  // branch, so that the arguments arrive in one round trip
+  asm volatile("" ::"s"(grp.total), "s"(step_local));
+  if ((int)blockIdx.x >= grp.total) {
+    sample_rows(sj, (int)blockIdx.x - grp.total);
+    return;
+  }
+  const int t = xcd_group_tile(blockIdx.x, grp.total, grp);
   int gi = 0;
 #pragma unroll
   for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
@@ -952,10 +997,18 @@ __device__ __forceinline__ void wave_mainloop(const GemmProb& P, int m0, int n0,
 template <int BM>
 __global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(const GemmProb* __restrict__ probs,
                                                           GemmGroups grp, int step_local, float slope,
-                                                          AdamConsts ac) {
+                                                          AdamConsts ac, SampleJob sj) {
   using T = Tile<BM>;
   constexpr int RS = BN + 4;  // row stride of the partial tiles in LDS
-  const int t = xcd_group_tile(blockIdx.x, gridDim.x, grp);
+  // every kernel-argument line the GEMM path reads (the groups, then
+  // step_local, slope and the Adam constants) is requested before the first
+  // branch, so that the arguments arrive in one round trip
+  asm volatile("" ::"s"(grp.total), "s"(step_local));
+  if ((int)blockIdx.x >= grp.total) {
+    sample_rows(sj, (int)blockIdx.x - grp.total);
+    return;
+  }
+  const int t = xcd_group_tile(blockIdx.x, grp.total, grp);
   int gi = 0;
 #pragma unroll
   for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
@@ -1033,12 +1086,18 @@ bool gemm_wave_ok(int max_k) { return LIPZ_GEMM_WAVE_SPLIT && max_k >= LIPZ_GEMM
 
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
                                int tile_rows, int kernel, int step_local, float slope,
-                               AdamConsts ac, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                               AdamConsts ac, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop,
+                               const SampleJob* job) {
   if (grp.n <= 0 || total_tiles <= 0) return hipSuccess;
-  const dim3 g(total_tiles), b(NT);
+  SampleJob sj;
+  memset(&sj, 0, sizeof(sj));
+  if (job) sj = *job;
+  GemmGroups gg = grp;
+  gg.total = total_tiles;
+  const dim3 g(total_tiles + sj.blocks), b(NT);
   // the events (may be null) are stamped by the kernel's own dispatch packet,
   // so their difference is the kernel's execution time alone
-#define LIPZ_LAUNCH(K) hipExtLaunchKernelGGL(K, g, b, 0, s, ev_start, ev_stop, 0, d_probs, grp, step_local, slope, ac)
+#define LIPZ_LAUNCH(K) hipExtLaunchKernelGGL(K, g, b, 0, s, ev_start, ev_stop, 0, d_probs, gg, step_local, slope, ac, sj)
   const bool r32 = tile_rows == 32;
   switch (kernel) {
     case GEMM_K_WAVE:

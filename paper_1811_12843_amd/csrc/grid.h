@@ -73,6 +73,7 @@ enum OpKind { OP_SAMPLE, OP_GEMM, OP_HEAD_D, OP_HEAD_G, OP_LOSS_D, OP_LOSS_G, OP
 struct Op {
   OpKind kind;
   int phase;
+  int sample_next = 0;  // OP_GEMM: the launch also draws the next step's minibatch
 };
 
 struct DcPlan;  // the convolutional networks' plan (dcgan.hip)
@@ -110,6 +111,10 @@ struct lipz_grid {
   float *L = nullptr, *Lg = nullptr, *fit_g = nullptr, *fit_d = nullptr;
   // training buffers
   float *z = nullptr, *Xtr = nullptr;
+  // The gradient trainer draws step k + 1's minibatch inside step k's first
+  // launch: steps alternate between (z, Xtr) (even) and (z_alt, Xtr_alt) (odd).
+  bool fused_sample = false;
+  float *z_alt = nullptr, *Xtr_alt = nullptr;
   float *h[LIPZ_MAX_HIDDEN] = {}, *a[LIPZ_MAX_HIDDEN] = {}, *dD[LIPZ_MAX_HIDDEN] = {};
   float *ag[LIPZ_MAX_HIDDEN] = {}, *dDg[LIPZ_MAX_HIDDEN] = {}, *dG[LIPZ_MAX_HIDDEN + 1] = {};
   float *part_tr = nullptr, *part_g = nullptr, *part_e = nullptr;  // partial logits
@@ -147,6 +152,7 @@ struct lipz_grid {
   hipStream_t gstream[LIPZ_MAX_GROUPS] = {};
   hipEvent_t fork_ev = nullptr, join_ev[LIPZ_MAX_GROUPS] = {};
   std::vector<Op> train_ops[2][LIPZ_MAX_GROUPS];
+  std::vector<Op> train_ops_odd[2][LIPZ_MAX_GROUPS];  // odd steps when fused_sample
   // Row bands of lipz_run_generations (config bands >= 2): band b holds cells
   // band_c0[b] .. band_c0[b + 1] - 1 (whole rows); the training groups are
   // the bands' individuals, and each band has its own evaluation and
@@ -213,7 +219,8 @@ void carve_state(lipz_grid* g, Carver& cv, char* base);
 GemmProb base_prob(const float* A, int lda, int a_trans, const float* Bm, int ldb, int b_trans, float* C, int ldc,
                    int M, int N, int K);
 int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps);
-hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t stream);
+hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t stream,
+                          const SampleJob* job = nullptr);
 hipError_t timing_events(lipz_grid* g, hipEvent_t* e0, hipEvent_t* e1);
 void timing_record(lipz_grid* g, hipEvent_t e0, hipEvent_t e1, double flops, double bytes);
 int ceil_div(int a, int b);

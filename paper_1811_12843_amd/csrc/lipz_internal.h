@@ -219,6 +219,7 @@ constexpr int GEMM_MAX_GROUPS = 4;
 // first_prob[g] + (tile - first_tile[g]) / tiles_per_prob[g].
 struct GemmGroups {
   int32_t n;
+  int32_t total;  // GEMM tiles of the launch (set at launch); workgroups past them run its SampleJob
   int32_t first_tile[GEMM_MAX_GROUPS];
   int32_t first_prob[GEMM_MAX_GROUPS];
   int32_t tiles_per_prob[GEMM_MAX_GROUPS];
@@ -282,13 +283,32 @@ enum GemmKernel : int32_t {
 // deepest K (max_k).
 int gemm_choose_kernel(bool fast, int max_k);
 
+// A training minibatch drawn by extra workgroups of a GEMM launch (the
+// draws of sample_kernel, written to other buffers than the launch's GEMMs
+// read): units u0 .. u0 + units - 1, B rows each; workgroup q (of
+// `blocks` = units * ceil(B / SAMPLE_ROWS)) takes rows SAMPLE_ROWS * (q %
+// ceil(B / SAMPLE_ROWS)) .. of unit u0 + q / ceil(B / SAMPLE_ROWS): data row
+// floor(w N / 2^32) of stream (u, gen, sf, IDX) to X[u][b][:] and latent row
+// z[u][b][:] from stream (u, gen, sf, Z).  blocks == 0: no sampling.
+constexpr int SAMPLE_ROWS = 4;
+struct SampleJob {
+  const float* data;
+  float* X;
+  float* Z;
+  int64_t N, x_stride, z_stride;  // dataset rows; per-unit strides of X and Z (floats)
+  uint2 key;
+  uint32_t gen, sf;
+  int32_t xd, zd, B, u0, blocks;
+};
+
 // Launch the grouped GEMM over the problems stored at d_probs (device),
 // covering `total_tiles` tiles of tile_rows x 64 outputs on kernel variant
-// `kernel`.  ev_start / ev_stop (or null) are recorded around the kernel itself.
+// `kernel`, plus the sampling workgroups of *job (may be null).
+// ev_start / ev_stop (or null) are recorded around the kernel itself.
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
                                int tile_rows, int kernel, int step_local, float slope,
                                AdamConsts ac, hipStream_t s, hipEvent_t ev_start = nullptr,
-                               hipEvent_t ev_stop = nullptr);
+                               hipEvent_t ev_stop = nullptr, const SampleJob* job = nullptr);
 
 // ---------------------------------------------------------------------------
 // Convolutions as implicit GEMMs (conv.hip)
