@@ -592,8 +592,6 @@ void build_tables(lipz_grid* g) {
         ps.push_back(fwd_prob(x, B, S.Gp + c * sG + G.off[l], G.fi[l], G.fo[l], y, G.act[l]));
       }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
-      // the first layer's launch also draws the next step's minibatch
-      if (l == 0 && g->fused_sample) ops.back().sample_next = 1;
     }
     for (int l = 0; l + 1 < LD; ++l) {
       std::vector<GemmProb> ps;
@@ -772,6 +770,9 @@ void build_tables(lipz_grid* g) {
         }
       }
       ops.push_back({OP_GEMM, add_phase(g, ps)});
+      // this launch (832 tiles at the 4x4 grid's shapes, about 450 workgroup
+      // slots free) also draws the next step's minibatch
+      if (l == 0 && g->fused_sample) ops.back().sample_next = 1;
     }
     backward_phases(
         g, LG - 1,
