@@ -107,6 +107,8 @@ __global__ void sample_kernel(const float* __restrict__ data, int64_t N, int xd,
 // cb 0 write dL/da into dlbuf[r][0] (columns 1..3 zero): the gradient of the
 // output layer, [act | 1]^T dL/da, and its Adam step run as a GEMM problem
 // of the next phase, so nothing here reads and writes w in one launch.
+// When the head is folded into the GEMM epilogues (D with two or more hidden
+// layers) the same kernel runs with loss_only: grid (C, 1, 1), the loss alone.
 // ---------------------------------------------------------------------------
 constexpr int HEAD_ROWS = 32;
 
