@@ -555,3 +555,37 @@ def test_call_order_and_argument_errors():
             L.lipz_select_replace(gg.g, 0)
         assert e.value.status == L.LIPZ_E_ORDER
         assert gg.sync() == L.LIPZ_OK
+
+
+@pytest.mark.parametrize("key", ["ring8_2x2", "ragged_2x3", "mnist_4x4_mix"])
+def test_train_calls_split_anywhere_give_the_same_state(key):
+    """Steps 3..9 of a generation in one call, in calls of 1, 2, 3 and 1 steps,
+    in calls of 2 and 5 steps without the loss output: the state after them
+    is bit for bit the same.  A step's minibatch is drawn by the call's first
+    launch (the call's first step) or, one step ahead, inside a launch of the
+    step before, into the minibatch buffer of the step's parity; a call may
+    start at an odd or an even step."""
+    wl, data, S = _setup(key)
+    st = _warm_state(S, data, steps=1)
+    gen = 2
+    _print_case("train-split", key=key)
+    with GpuGrid(wl, data) as gg:
+        blobs = []
+        for plan, with_losses in (([(3, 7)], True), ([(3, 1), (4, 2), (6, 3), (9, 1)], True),
+                                  ([(3, 2), (5, 5)], False)):
+            gg.set_state(st)
+            for step0, n in plan:
+                if with_losses:
+                    gg.train(gen, step0, n)
+                else:
+                    L.lipz_train_step(gg.g, gen, step0, n, None)
+                    gg.sync()
+            blobs.append(gg.save_blob())
+        assert not np.array_equal(blobs[0], _blob_of(gg, st))
+        for b in blobs[1:]:
+            assert np.array_equal(b, blobs[0])
+
+
+def _blob_of(gg, st):
+    gg.set_state(st)
+    return gg.save_blob()
