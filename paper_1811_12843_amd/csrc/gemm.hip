@@ -214,12 +214,19 @@ __device__ __forceinline__ float4 bload4(__amdgpu_buffer_rsrc_t r, uint32_t off_
 // One element through a buffer resource: the epilogues address C, the Adam
 // moments and the auxiliary operand with 32-bit element offsets from the
 // descriptor's base (no 64-bit address per element).
+//
+// Every store of the GEMM kernels is a device-scope store (cache policy sc1):
+// it is written through the XCD's L2 towards memory, where the next launch
+// reads it from whichever XCD its tiles run on.  Write-back stores leave the
+// lines dirty in L2 until the writeback at the end of the kernel, which the
+// next dependent launch waits for.
 constexpr uint32_t kWholeBuffer = 0x7FFFFFFFu;  // element offsets of a problem stay below 2^31 (planning checks)
+constexpr int kStoreDevice = 16;                // buffer-store cache policy: sc1 (device scope)
 __device__ __forceinline__ float bld1(__amdgpu_buffer_rsrc_t r, uint32_t off_elems) {
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)(off_elems * 4u), 0, 0));
 }
 __device__ __forceinline__ void bst1(__amdgpu_buffer_rsrc_t r, uint32_t off_elems, float v) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)(off_elems * 4u), 0, 0);
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)(off_elems * 4u), 0, kStoreDevice);
 }
 
 // The loss head's dL/da of this lane's epilogue rows (rows m0 + wm + 16 i +
@@ -265,18 +272,23 @@ __device__ __forceinline__ void sample_rows(const SampleJob& sj, int q) {
     const uint4 wi = stream_block(sj.key, (uint32_t)(b >> 2), (uint32_t)u, sj.gen, sj.sf, LIPZ_TAG_IDX);
     const int64_t row = (int64_t)(((uint64_t)word_of(wi, b & 3) * (uint64_t)sj.N) >> 32);
     const float* src = sj.data + row * sj.xd;
-    float* dst = sj.X + u * sj.x_stride + (int64_t)b * sj.xd;
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(sj.X + u * sj.x_stride + (int64_t)b * sj.xd, kWholeBuffer);
     if ((sj.xd & 3) == 0) {
-      for (int k = tid; k < (sj.xd >> 2); k += NT)
-        reinterpret_cast<float4*>(dst)[k] = reinterpret_cast<const float4*>(src)[k];
+      for (int k = tid; k < (sj.xd >> 2); k += NT) {
+        const float4 v = reinterpret_cast<const float4*>(src)[k];
+        __builtin_amdgcn_raw_buffer_store_b128(
+            v4u{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)}, rd,
+            k * 16, 0, kStoreDevice);
+      }
     } else {
-      for (int k = tid; k < sj.xd; k += NT) dst[k] = src[k];
+      for (int k = tid; k < sj.xd; k += NT) bst1(rd, (uint32_t)k, src[k]);
     }
   }
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(sj.Z + u * sj.z_stride + (int64_t)b0 * sj.zd, kWholeBuffer);
   for (int k = tid; k < nr * sj.zd; k += NT) {
     const int64_t e = (int64_t)b0 * sj.zd + k;
     const uint4 w = stream_block(sj.key, (uint32_t)(e >> 2), (uint32_t)u, sj.gen, sj.sf, LIPZ_TAG_Z);
-    sj.Z[u * sj.z_stride + e] = (float)normal_of(w, (int)(e & 3));
+    bst1(rz, (uint32_t)k, (float)normal_of(w, (int)(e & 3)));
   }
 }
 
@@ -333,13 +345,13 @@ __device__ __forceinline__ void head_partials(const GemmProb& P, const float (&d
   }
   __syncthreads();
   if (wm == 0 && lane < 16) {
-    LIPZ_GLOBAL float* o = as_global(P.hpart) + (size_t)(m0 / BM) * P.hp_ld;
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(P.hpart + (size_t)(m0 / BM) * P.hp_ld, kWholeBuffer);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int col = n0 + wn + 16 * j + li;
-      if (col < P.hp_w) o[col] = cs[j] + red[wave & 1][16 * j + li];
+      if (col < P.hp_w) bst1(ro, (uint32_t)col, cs[j] + red[wave & 1][16 * j + li]);
     }
-    if (tile_n == 0 && wn == 0 && lane == 0) o[P.hp_w] = ds + dsum;
+    if (tile_n == 0 && wn == 0 && lane == 0) bst1(ro, (uint32_t)P.hp_w, ds + dsum);
   }
 }
 
