@@ -388,10 +388,11 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
   int prev_tpp = -1, prev_k = -1;
   for (size_t k = 0; k < ps.size(); ++k) {
     GemmProb p = ps[k];
-    // the epilogue addresses C (and aux, m, v) with 32-bit element offsets
-    // row * ldc + col: a problem whose output reaches 2^31 elements is not
-    // planned (the configuration is rejected as invalid)
-    if ((int64_t)(p.M - 1) * p.ldc + p.N >= ((int64_t)1 << 31)) {
+    // the epilogue addresses C (and aux, m, v) through buffer resources with
+    // 32-bit byte offsets 4 (row * ldc + col) below 2^31: a problem whose
+    // output reaches 2^29 elements (2 GiB) is not planned (the configuration
+    // is rejected as invalid)
+    if ((int64_t)(p.M - 1) * p.ldc + p.N >= ((int64_t)1 << 29)) {
       g->plan_ok = false;
       break;
     }
@@ -1933,6 +1934,7 @@ lipz_status lipz_test_plan_bounds(const lipz_config* cfg, int64_t n_samples, cha
     if (!inside(p.A, 0, a_last)) note("gemm A", i);
     if (!inside(p.B, 0, b_last)) note("gemm B", i);
     if (!inside(p.C, 0, c_last)) note("gemm C", i);
+    if (c_last >= ((int64_t)1 << 29)) note("gemm C byte offset", i);
     if (p.epi == EPI_ADAM && (!inside(p.m, 0, c_last) || !inside(p.v, 0, c_last) || !inside(p.lr, 0, 0) ||
                               !inside(p.t, 0, 0)))
       note("gemm Adam state", i);

@@ -215,11 +215,14 @@ __device__ __forceinline__ float4 bload4(__amdgpu_buffer_rsrc_t r, uint32_t off_
 // moments and the auxiliary operand with 32-bit element offsets from the
 // descriptor's base (no 64-bit address per element).
 //
-// Every store of the GEMM kernels is a device-scope store (cache policy sc1):
-// it is written through the XCD's L2 towards memory, where the next launch
-// reads it from whichever XCD its tiles run on.  Write-back stores leave the
-// lines dirty in L2 until the writeback at the end of the kernel, which the
-// next dependent launch waits for.
+// The epilogues' element stores (outputs, Adam's p, m, v), the head
+// partials and the minibatch rows are device-scope stores (cache policy
+// sc1): written through the XCD's L2 towards memory, where the next launch
+// reads them from whichever XCD its tiles run on.  Write-back stores leave
+// the lines dirty in L2 until the writeback at the end of the kernel, which
+// the next dependent launch waits for.  (The per-row side outputs of the
+// folded loss head stay write-back stores: as relaxed device-scope atomic
+// stores, the only pointer form of sc1, they made the step slower.)
 constexpr uint32_t kWholeBuffer = 0x7FFFFFFFu;  // element offsets of a problem stay below 2^31 (planning checks)
 constexpr int kStoreDevice = 16;                // buffer-store cache policy: sc1 (device scope)
 __device__ __forceinline__ float bld1(__amdgpu_buffer_rsrc_t r, uint32_t off_elems) {

@@ -116,16 +116,18 @@ def test_invalid_dcgan_shapes_are_rejected():
     assert L.lipz_workspace_bytes(L.config_from_dict(wl), 100) == 0
 
 
-def test_outputs_reaching_2_31_elements_are_rejected():
-    """The GEMM epilogue addresses its output with 32-bit element offsets:
-    a batch of 2048 rows of 2^20 generated values (2^31 elements in one
-    problem's output) is not planned; one row fewer is."""
+def test_outputs_reaching_2_29_elements_are_rejected():
+    """The GEMM epilogue addresses its output through buffer resources with
+    32-bit byte offsets below 2^31: a batch of 512 rows of 2^20 generated
+    values (2^29 elements, 2 GiB, in one problem's output) is not planned;
+    one row fewer is."""
     base = dict(rows=1, cols=1, z_dim=4, x_dim=1 << 20, g_hidden=[8], d_hidden=[8], data=dict(n=64))
-    over = synth.small_workload("mnist_mlp_3x3", batch=2048, **base)
-    assert L.lipz_workspace_bytes(L.config_from_dict(over), 64) == 0
-    with pytest.raises(RuntimeError):
-        L.lipz_test_plan_bounds(L.config_from_dict(over), 64)
-    under = synth.small_workload("mnist_mlp_3x3", batch=2047, **base)
+    for batch in (512, 2048):
+        over = synth.small_workload("mnist_mlp_3x3", batch=batch, **base)
+        assert L.lipz_workspace_bytes(L.config_from_dict(over), 64) == 0
+        with pytest.raises(RuntimeError):
+            L.lipz_test_plan_bounds(L.config_from_dict(over), 64)
+    under = synth.small_workload("mnist_mlp_3x3", batch=511, **base)
     assert L.lipz_workspace_bytes(L.config_from_dict(under), 64) > 0
     n_bad, msg = L.lipz_test_plan_bounds(L.config_from_dict(under), 64)
     assert n_bad == 0, msg
