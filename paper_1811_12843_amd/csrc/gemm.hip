@@ -220,9 +220,9 @@ __device__ __forceinline__ float4 bload4(__amdgpu_buffer_rsrc_t r, uint32_t off_
 // sc1): written through the XCD's L2 towards memory, where the next launch
 // reads them from whichever XCD its tiles run on.  Write-back stores leave
 // the lines dirty in L2 until the writeback at the end of the kernel, which
-// the next dependent launch waits for.  (The per-row side outputs of the
-// folded loss head stay write-back stores: as relaxed device-scope atomic
-// stores, the only pointer form of sc1, they made the step slower.)
+// the next dependent launch waits for.  (The folded loss head's per-row side
+// outputs and partial dot products stay write-back stores: made
+// device-scope, the step was no faster.)
 constexpr uint32_t kWholeBuffer = 0x7FFFFFFFu;  // element offsets of a problem stay below 2^31 (planning checks)
 constexpr int kStoreDevice = 16;                // buffer-store cache policy: sc1 (device scope)
 __device__ __forceinline__ float bld1(__amdgpu_buffer_rsrc_t r, uint32_t off_elems) {
