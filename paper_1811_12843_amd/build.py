@@ -17,6 +17,9 @@ HIPCC_FLAGS = [
     "--offload-arch=gfx950",
     # keep packed-fp32 instructions out of the generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # the first 14 words of kernel arguments arrive preloaded in scalar
+    # registers (the GEMM kernels' descriptor pointer, tile groups and step)
+    "-mllvm", "-amdgpu-kernarg-preload-count=14",
     "-Wno-unused-command-line-argument",
 ]
 

@@ -388,6 +388,8 @@ int add_phase(lipz_grid* g, const std::vector<GemmProb>& ps) {
   int prev_tpp = -1, prev_k = -1;
   for (size_t k = 0; k < ps.size(); ++k) {
     GemmProb p = ps[k];
+    p.slope = g->slope;
+    p.ac = g->ac;
     // the epilogue addresses C (and aux, m, v) through buffer resources with
     // 32-bit byte offsets 4 (row * ldc + col) below 2^31: a problem whose
     // output reaches 2^29 elements (2 GiB) is not planned (the configuration
@@ -949,8 +951,8 @@ hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t s
   hipEvent_t e0, e1;
   hipError_t e = timing_events(g, &e0, &e1);
   if (e != hipSuccess) return e;
-  e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.kernel, step_local,
-                          g->slope, g->ac, stream, e0, e1, job);
+  e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.kernel, step_local, stream,
+                          e0, e1, job);
   timing_record(g, e0, e1, ph.flops, ph.bytes);
   return e;
 }

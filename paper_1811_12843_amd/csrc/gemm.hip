@@ -358,6 +358,43 @@ __device__ __forceinline__ void head_partials(const GemmProb& P, const float (&d
   }
 }
 
+// Kernel arguments of the three GEMM kernels.  The descriptor pointer, the
+// tile groups of the launch and the step index come first, as 14 scalar
+// words that the hardware preloads into scalar registers (the library is
+// built with -mllvm -amdgpu-kernarg-preload-count=14), so that a GEMM
+// workgroup's first memory access is its problem descriptor; only the
+// sampling workgroups read their SampleJob from kernel-argument memory.
+// Group q of the launch: tiles first_tile[q] .. (first_tile[q + 1] or
+// total) - 1, problems first_prob[q] on, tiles_per_prob[q] tiles each;
+// first_tile[0] = first_prob[0] = 0, and a group past the launch's last one
+// has first_tile = total.
+#define LIPZ_GEMM_ARGS                                                                              \
+  const GemmProb *__restrict__ probs, int32_t g_total, int32_t g_ft1, int32_t g_ft2, int32_t g_ft3, \
+      int32_t g_fp1, int32_t g_fp2, int32_t g_fp3, int32_t g_tp0, int32_t g_tp1, int32_t g_tp2,     \
+      int32_t g_tp3, int32_t step_local, SampleJob sj
+#define LIPZ_GEMM_GROUPS g_total, g_ft1, g_ft2, g_ft3, g_fp1, g_fp2, g_fp3, g_tp0, g_tp1, g_tp2, g_tp3
+
+// This workgroup's problem (index pi into the launch's descriptors) and tile
+// of it (lt), from the XCD-balanced block-to-tile map.  No array is indexed
+// at run time, so the groups stay in scalar registers.
+__device__ __forceinline__ void locate_tile(int total, int ft1, int ft2, int ft3, int fp1, int fp2, int fp3, int tp0,
+                                            int tp1, int tp2, int tp3, int& pi, int& lt) {
+  GemmGroups grp;
+  grp.n = 1 + (ft1 < total) + (ft2 < total) + (ft3 < total);
+  grp.total = total;
+  grp.first_tile[0] = 0;
+  grp.first_tile[1] = ft1;
+  grp.first_tile[2] = ft2;
+  grp.first_tile[3] = ft3;
+  const int t = xcd_group_tile(blockIdx.x, total, grp);
+  int ft = 0, fp = 0, tp = tp0;
+  if (t >= ft1) ft = ft1, fp = fp1, tp = tp1;
+  if (t >= ft2) ft = ft2, fp = fp2, tp = tp2;
+  if (t >= ft3) ft = ft3, fp = fp3, tp = tp3;
+  pi = fp + (t - ft) / tp;
+  lt = (t - ft) % tp;
+}
+
 // Epilogue shared by both kernel variants: bias + activation (optionally
 // with the per-tile partial dot product of the next 1-wide layer), the
 // activation-derivative product, or the fused Adam update; then stores.
@@ -365,14 +402,14 @@ __device__ __forceinline__ void head_partials(const GemmProb& P, const float (&d
 // latencies overlap (out-of-range elements read element 0 and are dropped).
 template <int BM>
 __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>::TI][2], int m0, int n0,
-                                         int tile_n, int step_local, float slope, const AdamConsts& ac,
-                                         float (*red)[BM]) {
+                                         int tile_n, int step_local, float (*red)[BM]) {
   using T = Tile<BM>;
   constexpr int NE = T::TI * 2 * 4;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = (wave >> 1) * T::WM, wn = (wave & 1) * 32;
   const int li = lane & 15, lg = lane >> 4;
+  const float slope = P.slope;
   const __amdgpu_buffer_rsrc_t rC = make_rsrc(P.C, kWholeBuffer);
   uint32_t off[NE];
   bool ok[NE];
@@ -389,6 +426,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
         off[e] = ok[e] ? (uint32_t)(row * P.ldc + col) : 0u;
       }
   if (P.epi == EPI_ADAM) {
+    const AdamConsts& ac = P.ac;
     const __amdgpu_buffer_rsrc_t rM = make_rsrc(P.m, kWholeBuffer);
     const __amdgpu_buffer_rsrc_t rV = make_rsrc(P.v, kWholeBuffer);
     const float lr = *as_global(P.lr);
@@ -550,26 +588,14 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
 // Generic variant: any alignment, per-element bounds checks.  Used for
 // phases whose rows are not 16-byte aligned (tiny widths such as 2-D data).
 template <int BM>
-__global__ __launch_bounds__(NT, 2) void gemm_generic_kernel(const GemmProb* __restrict__ probs,
-                                                             GemmGroups grp, int step_local,
-                                                             float slope, AdamConsts ac, SampleJob sj) {
+__global__ __launch_bounds__(NT, 2) void gemm_generic_kernel(LIPZ_GEMM_ARGS) {
   using T = Tile<BM>;
-  // every kernel-argument line the GEMM path reads (the groups, then
-  // step_local, slope and the Adam constants) is requested before the first
-  // branch, so that the arguments arrive in one round trip
-  asm volatile("" ::"s"(grp.total), "s"(step_local));
-  if ((int)blockIdx.x >= grp.total) {
-    sample_rows(sj, (int)blockIdx.x - grp.total);
+  if ((int)blockIdx.x >= g_total) {
+    sample_rows(sj, (int)blockIdx.x - g_total);
     return;
   }
-  const int t = xcd_group_tile(blockIdx.x, grp.total, grp);
-  int gi = 0;
-#pragma unroll
-  for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
-    if (q < grp.n && t >= grp.first_tile[q]) gi = q;
-  const int rel = t - grp.first_tile[gi];
-  const int pi = grp.first_prob[gi] + rel / grp.tiles_per_prob[gi];
-  const int lt = rel % grp.tiles_per_prob[gi];
+  int pi, lt;
+  locate_tile(LIPZ_GEMM_GROUPS, pi, lt);
   const GemmProb P = probs[pi];
   const int tile_n = lt % P.tiles_n;
   const int m0 = (lt / P.tiles_n) * BM;
@@ -638,7 +664,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_generic_kernel(const GemmProb* __r
     __syncthreads();
   }
 
-  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, slope, ac, red);
+  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -837,26 +863,14 @@ __device__ __forceinline__ void fast_mainloop(const GemmProb& P, int m0, int n0,
 }
 
 template <int BM>
-__global__ __launch_bounds__(NT, BM == 32 ? LIPZ_GEMM_WG32 : LIPZ_GEMM_WG64) void gemm_fast_kernel(const GemmProb* __restrict__ probs,
-                                                          GemmGroups grp, int step_local, float slope,
-                                                          AdamConsts ac, SampleJob sj) {
+__global__ __launch_bounds__(NT, BM == 32 ? LIPZ_GEMM_WG32 : LIPZ_GEMM_WG64) void gemm_fast_kernel(LIPZ_GEMM_ARGS) {
   using T = Tile<BM>;
-  // every kernel-argument line the GEMM path reads (the groups, then
-  // step_local, slope and the Adam constants) is requested before the first
-  // branch, so that the arguments arrive in one round trip
-  asm volatile("" ::"s"(grp.total), "s"(step_local));
-  if ((int)blockIdx.x >= grp.total) {
-    sample_rows(sj, (int)blockIdx.x - grp.total);
+  if ((int)blockIdx.x >= g_total) {
+    sample_rows(sj, (int)blockIdx.x - g_total);
     return;
   }
-  const int t = xcd_group_tile(blockIdx.x, grp.total, grp);
-  int gi = 0;
-#pragma unroll
-  for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
-    if (q < grp.n && t >= grp.first_tile[q]) gi = q;
-  const int rel = t - grp.first_tile[gi];
-  const int pi = grp.first_prob[gi] + rel / grp.tiles_per_prob[gi];
-  const int lt = rel % grp.tiles_per_prob[gi];
+  int pi, lt;
+  locate_tile(LIPZ_GEMM_GROUPS, pi, lt);
   const GemmProb P = probs[pi];
   const int tile_n = lt % P.tiles_n;
   const int m0 = (lt / P.tiles_n) * BM;
@@ -874,7 +888,7 @@ __global__ __launch_bounds__(NT, BM == 32 ? LIPZ_GEMM_WG32 : LIPZ_GEMM_WG64) voi
   if (P.a_trans) fast_mainloop<BM, 1, 0>(P, m0, n0, As, Bs, acc);
   else if (P.b_trans) fast_mainloop<BM, 0, 1>(P, m0, n0, As, Bs, acc);
   else fast_mainloop<BM, 0, 0>(P, m0, n0, As, Bs, acc);
-  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, slope, ac, red);
+  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -1010,27 +1024,15 @@ __device__ __forceinline__ void wave_mainloop(const GemmProb& P, int m0, int n0,
 }
 
 template <int BM>
-__global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(const GemmProb* __restrict__ probs,
-                                                          GemmGroups grp, int step_local, float slope,
-                                                          AdamConsts ac, SampleJob sj) {
+__global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(LIPZ_GEMM_ARGS) {
   using T = Tile<BM>;
   constexpr int RS = BN + 4;  // row stride of the partial tiles in LDS
-  // every kernel-argument line the GEMM path reads (the groups, then
-  // step_local, slope and the Adam constants) is requested before the first
-  // branch, so that the arguments arrive in one round trip
-  asm volatile("" ::"s"(grp.total), "s"(step_local));
-  if ((int)blockIdx.x >= grp.total) {
-    sample_rows(sj, (int)blockIdx.x - grp.total);
+  if ((int)blockIdx.x >= g_total) {
+    sample_rows(sj, (int)blockIdx.x - g_total);
     return;
   }
-  const int t = xcd_group_tile(blockIdx.x, grp.total, grp);
-  int gi = 0;
-#pragma unroll
-  for (int q = 1; q < GEMM_MAX_GROUPS; ++q)
-    if (q < grp.n && t >= grp.first_tile[q]) gi = q;
-  const int rel = t - grp.first_tile[gi];
-  const int pi = grp.first_prob[gi] + rel / grp.tiles_per_prob[gi];
-  const int lt = rel % grp.tiles_per_prob[gi];
+  int pi, lt;
+  locate_tile(LIPZ_GEMM_GROUPS, pi, lt);
   const GemmProb P = probs[pi];
   const int tile_n = lt % P.tiles_n;
   const int m0 = (lt / P.tiles_n) * BM;
@@ -1076,7 +1078,7 @@ __global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(const G
         const int o = (wm + 16 * i + 4 * lg + r) * RS + wn + 16 * j + li;
         acc[i][j][r] = (part[0][o] + part[1][o]) + (part[2][o] + part[3][o]);
       }
-  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, slope, ac, red);
+  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, red);
 }
 
 }  // namespace
@@ -1100,8 +1102,8 @@ bool gemm_fast_ok(const GemmProb& p) {
 bool gemm_wave_ok(int max_k) { return LIPZ_GEMM_WAVE_SPLIT && max_k >= LIPZ_GEMM_WAVE_MIN_K; }
 
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
-                               int tile_rows, int kernel, int step_local, float slope,
-                               AdamConsts ac, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop,
+                               int tile_rows, int kernel, int step_local, hipStream_t s, hipEvent_t ev_start,
+                               hipEvent_t ev_stop,
                                const SampleJob* job) {
   if (grp.n <= 0 || total_tiles <= 0) return hipSuccess;
   SampleJob sj;
@@ -1112,7 +1114,18 @@ hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, i
   const dim3 g(total_tiles + sj.blocks), b(NT);
   // the events (may be null) are stamped by the kernel's own dispatch packet,
   // so their difference is the kernel's execution time alone
-#define LIPZ_LAUNCH(K) hipExtLaunchKernelGGL(K, g, b, 0, s, ev_start, ev_stop, 0, d_probs, gg, step_local, slope, ac, sj)
+  // the groups as the kernels take them (see LIPZ_GEMM_ARGS)
+  if (gg.n > GEMM_MAX_GROUPS || gg.first_tile[0] != 0 || gg.first_prob[0] != 0) return hipErrorInvalidValue;
+  int ft[GEMM_MAX_GROUPS], fp[GEMM_MAX_GROUPS];
+  for (int q = 0; q < GEMM_MAX_GROUPS; ++q) {
+    ft[q] = q < gg.n ? gg.first_tile[q] : total_tiles;
+    fp[q] = q < gg.n ? gg.first_prob[q] : 0;
+    if (q > 0 && q < gg.n && !(ft[q - 1] < ft[q] && ft[q] < total_tiles)) return hipErrorInvalidValue;
+  }
+#define LIPZ_LAUNCH(K)                                                                                          \
+  hipExtLaunchKernelGGL(K, g, b, 0, s, ev_start, ev_stop, 0, d_probs, total_tiles, ft[1], ft[2], ft[3], fp[1], \
+                        fp[2], fp[3], gg.tiles_per_prob[0], gg.tiles_per_prob[1], gg.tiles_per_prob[2],       \
+                        gg.tiles_per_prob[3], step_local, sj)
   const bool r32 = tile_rows == 32;
   switch (kernel) {
     case GEMM_K_WAVE:

@@ -120,6 +120,10 @@ enum Epi : int32_t {
   EPI_ADAM = 3       // acc is the gradient of parameter C[i][j]; Adam update of C, m, v
 };
 
+struct AdamConsts {
+  float beta1, beta2, one_minus_beta1, one_minus_beta2, eps;
+};
+
 struct GemmProb {
   const float* A;
   const float* B;
@@ -204,10 +208,11 @@ struct GemmProb {
   //    hpart[(m0 / BM) * hp_ld + hp_w] = sum over its rows of dL/da[i]
   //    (Wasserstein: the +-1 of dlout in both).
   int16_t rs_mode, loss_kind;
-};
-
-struct AdamConsts {
-  float beta1, beta2, one_minus_beta1, one_minus_beta2, eps;
+  // The grid's constants of the epilogues, the same in every descriptor:
+  // the leaky-ReLU slope and Adam's constants.  Carried here so that a GEMM
+  // workgroup reads nothing from kernel-argument memory.
+  float slope;
+  AdamConsts ac;
 };
 
 constexpr int GEMM_BN = 64;
@@ -306,8 +311,7 @@ struct SampleJob {
 // `kernel`, plus the sampling workgroups of *job (may be null).
 // ev_start / ev_stop (or null) are recorded around the kernel itself.
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
-                               int tile_rows, int kernel, int step_local, float slope,
-                               AdamConsts ac, hipStream_t s, hipEvent_t ev_start = nullptr,
+                               int tile_rows, int kernel, int step_local, hipStream_t s, hipEvent_t ev_start = nullptr,
                                hipEvent_t ev_stop = nullptr, const SampleJob* job = nullptr);
 
 // ---------------------------------------------------------------------------

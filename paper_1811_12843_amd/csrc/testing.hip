@@ -15,6 +15,7 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
                                       const float* d_lr, const int32_t* d_t, int32_t step_local,
                                       float beta1, float beta2, float eps, int32_t tile_rows,
                                       int32_t variant) {
+  static_assert(sizeof(GemmProb) <= 256, "the caller's descriptor scratch is 256 bytes");
   if (!d_desc || !d_A || !d_B || !d_C || M < 1 || N < 1 || K < 1) return LIPZ_E_INVAL;
   if (epi < EPI_STORE || epi > EPI_ADAM || act < LIPZ_ACT_LINEAR || act > LIPZ_ACT_TANH)
     return LIPZ_E_INVAL;
@@ -54,13 +55,12 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
   p.tile_begin = 0;
   if (tile_rows == 0) tile_rows = gemm_tile_rows(((M + 63) / 64) * p.tiles_n);
   const int tiles = ((M + tile_rows - 1) / tile_rows) * p.tiles_n;
-  if (hipMemcpy(d_desc, &p, sizeof(p), hipMemcpyHostToDevice) != hipSuccess) return LIPZ_E_HIP;
-  AdamConsts ac;
-  ac.beta1 = beta1;
-  ac.beta2 = beta2;
-  ac.one_minus_beta1 = (float)(1.0 - (double)beta1);
-  ac.one_minus_beta2 = (float)(1.0 - (double)beta2);
-  ac.eps = eps;
+  p.slope = slope;
+  p.ac.beta1 = beta1;
+  p.ac.beta2 = beta2;
+  p.ac.one_minus_beta1 = (float)(1.0 - (double)beta1);
+  p.ac.one_minus_beta2 = (float)(1.0 - (double)beta2);
+  p.ac.eps = eps;
   GemmGroups grp;
   memset(&grp, 0, sizeof(grp));
   grp.n = 1;
@@ -74,8 +74,7 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
     if (!gemm_fast_ok(p)) return LIPZ_E_INVAL;
     kernel = variant == 1 ? GEMM_K_FAST : GEMM_K_WAVE;
   }
-  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, kernel,
-                          step_local, slope, ac,
+  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, kernel, step_local,
                           (hipStream_t)hip_stream) != hipSuccess)
     return LIPZ_E_HIP;
   return LIPZ_OK;
