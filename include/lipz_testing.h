@@ -19,7 +19,9 @@
  * library makes for a phase of this size.  variant: 0 = the kernel the
  * library runs such a phase on; 1 = the register-staged LDS kernel, 2 = the
  * wave-split kernel (1-2 need 16-byte aligned operand rows, else
- * LIPZ_E_INVAL).
+ * LIPZ_E_INVAL); plus 4: the kernel's write-back stores instead of its
+ * device-scope ones (the store policy of grids whose state exceeds 128 MB;
+ * the results are the same).  Other values: LIPZ_E_INVAL.
  * d_desc: device scratch of at least 256 bytes for the problem descriptor
  * (caller-owned).  The call copies the descriptor synchronously, enqueues the
  * kernel on hip_stream and returns; LIPZ_E_INVAL on bad sizes.

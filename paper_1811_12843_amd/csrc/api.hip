@@ -164,6 +164,7 @@ void carve_state(lipz_grid* g, Carver& cv, char* base) {
     cv.off = align_up(cv.off, kAlign);
     so[11] = (int64_t)(cv.off - start);
     g->state_bytes = (size_t)so[11];
+    g->gemm_wt = g->state_bytes <= ((size_t)128 << 20);
     g->st[b] = sb;
   }
 }
@@ -951,8 +952,8 @@ hipError_t run_gemm_phase(lipz_grid* g, int phase, int step_local, hipStream_t s
   hipEvent_t e0, e1;
   hipError_t e = timing_events(g, &e0, &e1);
   if (e != hipSuccess) return e;
-  e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.kernel, step_local, stream,
-                          e0, e1, job);
+  e = launch_gemm_grouped(g->probs_d + ph.first, ph.grp, ph.tiles, ph.tile_rows, ph.kernel, step_local, g->gemm_wt,
+                          stream, e0, e1, job);
   timing_record(g, e0, e1, ph.flops, ph.bytes);
   return e;
 }

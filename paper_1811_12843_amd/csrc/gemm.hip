@@ -215,21 +215,22 @@ __device__ __forceinline__ float4 bload4(__amdgpu_buffer_rsrc_t r, uint32_t off_
 // moments and the auxiliary operand with 32-bit element offsets from the
 // descriptor's base (no 64-bit address per element).
 //
-// The epilogues' element stores (outputs, Adam's p, m, v), the head
+// Store policy (WT, a template parameter of the kernels, chosen per grid).
+// With WT the epilogues' element stores (outputs, Adam's p, m, v), the head
 // partials and the minibatch rows are device-scope stores (cache policy
-// sc1): written through the XCD's L2 towards memory, where the next launch
-// reads them from whichever XCD its tiles run on.  Write-back stores leave
-// the lines dirty in L2 until the writeback at the end of the kernel, which
-// the next dependent launch waits for.  (The folded loss head's per-row side
-// outputs and partial dot products stay write-back stores: made
-// device-scope, the step was no faster.)
+// sc1): written through the XCD's L2 towards memory, so that the next
+// dependent launch, which reads them from whichever XCD its tiles run on,
+// does not wait for an end-of-kernel writeback of dirty L2 lines.  Without
+// it they are write-back stores.  (The folded loss head's per-row side
+// outputs and partial dot products are write-back stores in either case.)
 constexpr uint32_t kWholeBuffer = 0x7FFFFFFFu;  // element offsets of a problem stay below 2^31 (planning checks)
 constexpr int kStoreDevice = 16;                // buffer-store cache policy: sc1 (device scope)
 __device__ __forceinline__ float bld1(__amdgpu_buffer_rsrc_t r, uint32_t off_elems) {
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)(off_elems * 4u), 0, 0));
 }
+template <bool WT>
 __device__ __forceinline__ void bst1(__amdgpu_buffer_rsrc_t r, uint32_t off_elems, float v) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)(off_elems * 4u), 0, kStoreDevice);
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)(off_elems * 4u), 0, WT ? kStoreDevice : 0);
 }
 
 // The loss head's dL/da of this lane's epilogue rows (rows m0 + wm + 16 i +
@@ -265,6 +266,7 @@ __device__ __forceinline__ void head_rows_dl(const GemmProb& P, int m0, float (&
 
 // Workgroup q of a sampling job: SAMPLE_ROWS minibatch rows of one unit,
 // drawn exactly as sample_kernel draws them.
+template <bool WT>
 __device__ __forceinline__ void sample_rows(const SampleJob& sj, int q) {
   const int per = (sj.B + SAMPLE_ROWS - 1) / SAMPLE_ROWS;
   const int u = sj.u0 + q / per, b0 = (q % per) * SAMPLE_ROWS;
@@ -281,17 +283,17 @@ __device__ __forceinline__ void sample_rows(const SampleJob& sj, int q) {
         const float4 v = reinterpret_cast<const float4*>(src)[k];
         __builtin_amdgcn_raw_buffer_store_b128(
             v4u{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)}, rd,
-            k * 16, 0, kStoreDevice);
+            k * 16, 0, WT ? kStoreDevice : 0);
       }
     } else {
-      for (int k = tid; k < sj.xd; k += NT) bst1(rd, (uint32_t)k, src[k]);
+      for (int k = tid; k < sj.xd; k += NT) bst1<WT>(rd, (uint32_t)k, src[k]);
     }
   }
   const __amdgpu_buffer_rsrc_t rz = make_rsrc(sj.Z + u * sj.z_stride + (int64_t)b0 * sj.zd, kWholeBuffer);
   for (int k = tid; k < nr * sj.zd; k += NT) {
     const int64_t e = (int64_t)b0 * sj.zd + k;
     const uint4 w = stream_block(sj.key, (uint32_t)(e >> 2), (uint32_t)u, sj.gen, sj.sf, LIPZ_TAG_Z);
-    bst1(rz, (uint32_t)k, (float)normal_of(w, (int)(e & 3)));
+    bst1<WT>(rz, (uint32_t)k, (float)normal_of(w, (int)(e & 3)));
   }
 }
 
@@ -300,7 +302,7 @@ __device__ __forceinline__ void sample_rows(const SampleJob& sj, int q) {
 // column 0, of dL/da[i]), summed over the lane groups and then over the two
 // waves that share the tile's columns, in a fixed order.  Rows past M and
 // columns past hp_w add nothing.
-template <int BM>
+template <int BM, bool WT>
 __device__ __forceinline__ void head_partials(const GemmProb& P, const float (&dl)[Tile<BM>::TI][4], int m0,
                                               int n0, int tile_n, float (*red)[BM]) {
   using T = Tile<BM>;
@@ -352,9 +354,9 @@ __device__ __forceinline__ void head_partials(const GemmProb& P, const float (&d
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int col = n0 + wn + 16 * j + li;
-      if (col < P.hp_w) bst1(ro, (uint32_t)col, cs[j] + red[wave & 1][16 * j + li]);
+      if (col < P.hp_w) bst1<WT>(ro, (uint32_t)col, cs[j] + red[wave & 1][16 * j + li]);
     }
-    if (tile_n == 0 && wn == 0 && lane == 0) bst1(ro, (uint32_t)P.hp_w, ds + dsum);
+    if (tile_n == 0 && wn == 0 && lane == 0) bst1<WT>(ro, (uint32_t)P.hp_w, ds + dsum);
   }
 }
 
@@ -400,7 +402,7 @@ __device__ __forceinline__ void locate_tile(int total, int ft1, int ft2, int ft3
 // activation-derivative product, or the fused Adam update; then stores.
 // All of a lane's loads are issued before any of them is used, so their
 // latencies overlap (out-of-range elements read element 0 and are dropped).
-template <int BM>
+template <int BM, bool WT>
 __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>::TI][2], int m0, int n0,
                                          int tile_n, int step_local, float (*red)[BM]) {
   using T = Tile<BM>;
@@ -453,9 +455,9 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
           float p = pp[e] - lr * (m / bc1) / (sqrtf(v / bc2) + ac.eps);
           if (P.clip > 0.f) p = p > P.clip ? P.clip : (p < -P.clip ? -P.clip : p);  // keeps NaN
           if (ok[e]) {
-            bst1(rM, off[e], m);
-            bst1(rV, off[e], v);
-            bst1(rC, off[e], p);
+            bst1<WT>(rM, off[e], m);
+            bst1<WT>(rV, off[e], v);
+            bst1<WT>(rC, off[e], p);
           }
         }
     return;
@@ -473,7 +475,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int e = (i * 2 + j) * 4 + r;
-            if (ok[e]) bst1(rC, off[e], acc[i][j][r] * act_deriv_from_out(P.act, ax[e], slope));
+            if (ok[e]) bst1<WT>(rC, off[e], acc[i][j][r] * act_deriv_from_out(P.act, ax[e], slope));
           }
       return;
     }
@@ -488,14 +490,14 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
         for (int r = 0; r < 4; ++r) {
           const int e = (i * 2 + j) * 4 + r;
           if (ok[e]) {
-            bst1(rC, off[e], dl[i][r] * (acc[i][j][r] * act_deriv_from_out(P.act, ax[e], slope)));
+            bst1<WT>(rC, off[e], dl[i][r] * (acc[i][j][r] * act_deriv_from_out(P.act, ax[e], slope)));
             if (P.side) {
               const int row = m0 + wm + 16 * i + 4 * lg + r, col = n0 + wn + 16 * j + li;
               gSide[(size_t)row * P.side_ld + col] = dl[i][r] * ax[e];
             }
           }
         }
-    if (P.rs_mode == 1 && P.hpart) head_partials<BM>(P, dl, m0, n0, tile_n, red);
+    if (P.rs_mode == 1 && P.hpart) head_partials<BM, WT>(P, dl, m0, n0, tile_n, red);
     // column 0 of the problem: the per-row extras
     if (P.side && tile_n == 0 && wn == 0 && li == 0) {
       LIPZ_GLOBAL float* gDl = as_global(P.dlout);
@@ -528,7 +530,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = (i * 2 + j) * 4 + r;
-          if (ok[e]) bst1(rC, off[e], acc[i][j][r]);
+          if (ok[e]) bst1<WT>(rC, off[e], acc[i][j][r]);
         }
     return;
   }
@@ -552,9 +554,9 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
         const int e = (i * 2 + j) * 4 + r;
         const float y = act_fwd(P.act, acc[i][j][r] + bias[j], slope);
         if (ok[e]) {
-          bst1(rC, off[e], y);
+          bst1<WT>(rC, off[e], y);
           rowdot[r] += y * dw[j];
-          if (P.gout) bst1(make_rsrc(P.gout, kWholeBuffer), off[e], dw[j] * act_deriv_from_out(P.act, y, slope));
+          if (P.gout) bst1<WT>(make_rsrc(P.gout, kWholeBuffer), off[e], dw[j] * act_deriv_from_out(P.act, y, slope));
         }
       }
     if (dot) {
@@ -587,11 +589,11 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, v4f (&acc)[Tile<BM>:
 
 // Generic variant: any alignment, per-element bounds checks.  Used for
 // phases whose rows are not 16-byte aligned (tiny widths such as 2-D data).
-template <int BM>
+template <int BM, bool WT>
 __global__ __launch_bounds__(NT, 2) void gemm_generic_kernel(LIPZ_GEMM_ARGS) {
   using T = Tile<BM>;
   if ((int)blockIdx.x >= g_total) {
-    sample_rows(sj, (int)blockIdx.x - g_total);
+    sample_rows<WT>(sj, (int)blockIdx.x - g_total);
     return;
   }
   int pi, lt;
@@ -664,7 +666,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_generic_kernel(LIPZ_GEMM_ARGS) {
     __syncthreads();
   }
 
-  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, red);
+  epilogue<BM, WT>(P, acc, m0, n0, tile_n, step_local, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -862,11 +864,11 @@ __device__ __forceinline__ void fast_mainloop(const GemmProb& P, int m0, int n0,
   }
 }
 
-template <int BM>
+template <int BM, bool WT>
 __global__ __launch_bounds__(NT, BM == 32 ? LIPZ_GEMM_WG32 : LIPZ_GEMM_WG64) void gemm_fast_kernel(LIPZ_GEMM_ARGS) {
   using T = Tile<BM>;
   if ((int)blockIdx.x >= g_total) {
-    sample_rows(sj, (int)blockIdx.x - g_total);
+    sample_rows<WT>(sj, (int)blockIdx.x - g_total);
     return;
   }
   int pi, lt;
@@ -888,7 +890,7 @@ __global__ __launch_bounds__(NT, BM == 32 ? LIPZ_GEMM_WG32 : LIPZ_GEMM_WG64) voi
   if (P.a_trans) fast_mainloop<BM, 1, 0>(P, m0, n0, As, Bs, acc);
   else if (P.b_trans) fast_mainloop<BM, 0, 1>(P, m0, n0, As, Bs, acc);
   else fast_mainloop<BM, 0, 0>(P, m0, n0, As, Bs, acc);
-  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, red);
+  epilogue<BM, WT>(P, acc, m0, n0, tile_n, step_local, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -1023,12 +1025,12 @@ __device__ __forceinline__ void wave_mainloop(const GemmProb& P, int m0, int n0,
   }
 }
 
-template <int BM>
+template <int BM, bool WT>
 __global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(LIPZ_GEMM_ARGS) {
   using T = Tile<BM>;
   constexpr int RS = BN + 4;  // row stride of the partial tiles in LDS
   if ((int)blockIdx.x >= g_total) {
-    sample_rows(sj, (int)blockIdx.x - g_total);
+    sample_rows<WT>(sj, (int)blockIdx.x - g_total);
     return;
   }
   int pi, lt;
@@ -1078,7 +1080,7 @@ __global__ __launch_bounds__(NT, BM == 32 ? 2 : 1) void gemm_wave_kernel(LIPZ_GE
         const int o = (wm + 16 * i + 4 * lg + r) * RS + wn + 16 * j + li;
         acc[i][j][r] = (part[0][o] + part[1][o]) + (part[2][o] + part[3][o]);
       }
-  epilogue<BM>(P, acc, m0, n0, tile_n, step_local, red);
+  epilogue<BM, WT>(P, acc, m0, n0, tile_n, step_local, red);
 }
 
 }  // namespace
@@ -1102,41 +1104,41 @@ bool gemm_fast_ok(const GemmProb& p) {
 bool gemm_wave_ok(int max_k) { return LIPZ_GEMM_WAVE_SPLIT && max_k >= LIPZ_GEMM_WAVE_MIN_K; }
 
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
-                               int tile_rows, int kernel, int step_local, hipStream_t s, hipEvent_t ev_start,
-                               hipEvent_t ev_stop,
-                               const SampleJob* job) {
+                               int tile_rows, int kernel, int step_local, bool write_through, hipStream_t s,
+                               hipEvent_t ev_start, hipEvent_t ev_stop, const SampleJob* job) {
   if (grp.n <= 0 || total_tiles <= 0) return hipSuccess;
   SampleJob sj;
   memset(&sj, 0, sizeof(sj));
   if (job) sj = *job;
-  GemmGroups gg = grp;
-  gg.total = total_tiles;
+  // the groups as the kernels take them (see LIPZ_GEMM_ARGS)
+  if (grp.n > GEMM_MAX_GROUPS || grp.first_tile[0] != 0 || grp.first_prob[0] != 0) return hipErrorInvalidValue;
+  int ft[GEMM_MAX_GROUPS], fp[GEMM_MAX_GROUPS];
+  for (int q = 0; q < GEMM_MAX_GROUPS; ++q) {
+    ft[q] = q < grp.n ? grp.first_tile[q] : total_tiles;
+    fp[q] = q < grp.n ? grp.first_prob[q] : 0;
+    if (q > 0 && q < grp.n && !(ft[q - 1] < ft[q] && ft[q] < total_tiles)) return hipErrorInvalidValue;
+  }
   const dim3 g(total_tiles + sj.blocks), b(NT);
   // the events (may be null) are stamped by the kernel's own dispatch packet,
   // so their difference is the kernel's execution time alone
-  // the groups as the kernels take them (see LIPZ_GEMM_ARGS)
-  if (gg.n > GEMM_MAX_GROUPS || gg.first_tile[0] != 0 || gg.first_prob[0] != 0) return hipErrorInvalidValue;
-  int ft[GEMM_MAX_GROUPS], fp[GEMM_MAX_GROUPS];
-  for (int q = 0; q < GEMM_MAX_GROUPS; ++q) {
-    ft[q] = q < gg.n ? gg.first_tile[q] : total_tiles;
-    fp[q] = q < gg.n ? gg.first_prob[q] : 0;
-    if (q > 0 && q < gg.n && !(ft[q - 1] < ft[q] && ft[q] < total_tiles)) return hipErrorInvalidValue;
-  }
 #define LIPZ_LAUNCH(K)                                                                                          \
   hipExtLaunchKernelGGL(K, g, b, 0, s, ev_start, ev_stop, 0, d_probs, total_tiles, ft[1], ft[2], ft[3], fp[1], \
-                        fp[2], fp[3], gg.tiles_per_prob[0], gg.tiles_per_prob[1], gg.tiles_per_prob[2],       \
-                        gg.tiles_per_prob[3], step_local, sj)
+                        fp[2], fp[3], grp.tiles_per_prob[0], grp.tiles_per_prob[1], grp.tiles_per_prob[2],    \
+                        grp.tiles_per_prob[3], step_local, sj)
+#define LIPZ_LAUNCH_WT(KN, BMV) \
+  if (write_through) LIPZ_LAUNCH((KN<BMV, true>)); else LIPZ_LAUNCH((KN<BMV, false>))
   const bool r32 = tile_rows == 32;
   switch (kernel) {
     case GEMM_K_WAVE:
-      if (r32) LIPZ_LAUNCH(gemm_wave_kernel<32>); else LIPZ_LAUNCH(gemm_wave_kernel<64>);
+      if (r32) { LIPZ_LAUNCH_WT(gemm_wave_kernel, 32); } else { LIPZ_LAUNCH_WT(gemm_wave_kernel, 64); }
       break;
     case GEMM_K_FAST:
-      if (r32) LIPZ_LAUNCH(gemm_fast_kernel<32>); else LIPZ_LAUNCH(gemm_fast_kernel<64>);
+      if (r32) { LIPZ_LAUNCH_WT(gemm_fast_kernel, 32); } else { LIPZ_LAUNCH_WT(gemm_fast_kernel, 64); }
       break;
     default:
-      if (r32) LIPZ_LAUNCH(gemm_generic_kernel<32>); else LIPZ_LAUNCH(gemm_generic_kernel<64>);
+      if (r32) { LIPZ_LAUNCH_WT(gemm_generic_kernel, 32); } else { LIPZ_LAUNCH_WT(gemm_generic_kernel, 64); }
   }
+#undef LIPZ_LAUNCH_WT
 #undef LIPZ_LAUNCH
   return hipGetLastError();
 }

@@ -100,6 +100,12 @@ struct lipz_grid {
   uint2 key;
   float slope = 0.f;
   AdamConsts ac;
+  // GEMM launches store write-through (device scope) when the grid's state
+  // (parameters and Adam moments of every individual) is at most 128 MB,
+  // half the 256 MB last-level cache: measured faster for such grids (4x4
+  // and 3x3 MNIST-shaped), slower for larger ones (4x4 with two individuals
+  // per cell, 8x8), which store write-back.
+  bool gemm_wt = false;
 
   StateBuf st[2];
   int cur = 0;

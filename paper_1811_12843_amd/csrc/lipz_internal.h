@@ -308,11 +308,12 @@ struct SampleJob {
 
 // Launch the grouped GEMM over the problems stored at d_probs (device),
 // covering `total_tiles` tiles of tile_rows x 64 outputs on kernel variant
-// `kernel`, plus the sampling workgroups of *job (may be null).
+// `kernel`, plus the sampling workgroups of *job (may be null).  With
+// write_through the kernels' stores are device-scope (written through L2).
 // ev_start / ev_stop (or null) are recorded around the kernel itself.
 hipError_t launch_gemm_grouped(const GemmProb* d_probs, const GemmGroups& grp, int total_tiles,
-                               int tile_rows, int kernel, int step_local, hipStream_t s, hipEvent_t ev_start = nullptr,
-                               hipEvent_t ev_stop = nullptr, const SampleJob* job = nullptr);
+                               int tile_rows, int kernel, int step_local, bool write_through, hipStream_t s,
+                               hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const SampleJob* job = nullptr);
 
 // ---------------------------------------------------------------------------
 // Convolutions as implicit GEMMs (conv.hip)

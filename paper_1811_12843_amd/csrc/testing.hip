@@ -22,7 +22,7 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
   if (ones_row >= 0 && (!a_trans || ones_row != M - 1)) return LIPZ_E_INVAL;
   if (epi == EPI_DACT && !d_aux) return LIPZ_E_INVAL;
   if (tile_rows != 0 && tile_rows != 32 && tile_rows != 64) return LIPZ_E_INVAL;
-  if (variant < 0 || variant > 2) return LIPZ_E_INVAL;
+  if (variant < 0 || variant > 6 || (variant & 3) == 3) return LIPZ_E_INVAL;
   if (epi == EPI_ADAM && (!d_m || !d_v || !d_lr || !d_t)) return LIPZ_E_INVAL;
   const int a_rows = ones_row >= 0 ? ones_row : M;
   if (lda < (a_trans ? a_rows : K) || ldb < (b_trans ? K : N) || ldc < N) return LIPZ_E_INVAL;
@@ -67,14 +67,16 @@ extern "C" lipz_status lipz_test_gemm(void* hip_stream, void* d_desc, int32_t M,
   grp.tiles_per_prob[0] = tiles;
   gemm_set_extents(p);
   if (hipMemcpy(d_desc, &p, sizeof(p), hipMemcpyHostToDevice) != hipSuccess) return LIPZ_E_HIP;
-  // variant 0: the kernel a phase of this one problem runs on; 1 / 2: the
-  // register-staged or the wave-split kernel (aligned operands only)
+  // variant & 3 = 0: the kernel a phase of this one problem runs on; 1 / 2:
+  // the register-staged or the wave-split kernel (aligned operands only);
+  // variant & 4: write-back stores (else device-scope)
+  const int kv = variant & 3;
   int kernel = gemm_choose_kernel(gemm_fast_ok(p), K);
-  if (variant != 0) {
+  if (kv != 0) {
     if (!gemm_fast_ok(p)) return LIPZ_E_INVAL;
-    kernel = variant == 1 ? GEMM_K_FAST : GEMM_K_WAVE;
+    kernel = kv == 1 ? GEMM_K_FAST : GEMM_K_WAVE;
   }
-  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, kernel, step_local,
+  if (launch_gemm_grouped((const GemmProb*)d_desc, grp, tiles, tile_rows, kernel, step_local, (variant & 4) == 0,
                           (hipStream_t)hip_stream) != hipSuccess)
     return LIPZ_E_HIP;
   return LIPZ_OK;

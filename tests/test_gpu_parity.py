@@ -111,8 +111,8 @@ def test_gemm_kernel_against_matmul():
                 lda, ldb = (M if a_trans else K), (K if b_trans else N)
                 aligned = lda % 4 == 0 and ldb % 4 == 0 and not (a_trans and b_trans)
                 # variant 0: the library's choice; 1, 2: each aligned kernel (register-staged,
-                # wave-split) on the same problem
-                variants = (0, 1, 2) if aligned else (0,)
+                # wave-split) on the same problem; + 4: the same with write-back stores
+                variants = (0, 1, 2, 4, 5, 6) if aligned else (0, 4)
                 for variant, (epi, act) in [(v, e) for v in variants
                                             for e in ((0, 0), (1, 1), (1, 2), (1, 3), (2, 2), (2, 3))]:
                     _print_case("gemm", M=M, N=N, K=K, at=a_trans, bt=b_trans, epi=epi, act=act,
@@ -158,7 +158,7 @@ def test_gemm_weight_gradient_with_bias_row_and_adam():
     stream = torch.cuda.current_stream().cuda_stream
     cases = [(s, tr, v) for s in [(200, 784, 256), (100, 256, 784), (19, 37, 45), (64, 2, 64), (100, 64, 256),
                                   (520, 72, 36), (100, 256, 256)]
-             for tr in (32, 64) for v in ((0, 1, 2) if s[1] % 4 == 0 and s[2] % 4 == 0 else (0,))]
+             for tr in (32, 64) for v in ((0, 1, 2, 4, 5, 6) if s[1] % 4 == 0 and s[2] % 4 == 0 else (0, 4))]
     for (rows, fi, fo), tile_rows, variant in cases:
         _print_case("wgrad_adam", rows=rows, fi=fi, fo=fo, tile_rows=tile_rows, variant=variant)
         X = g.normal(size=(rows, fi)).astype(np.float32)
