@@ -810,7 +810,7 @@ __device__ __forceinline__ void mfma_frag(const Frag<BM>& F, v4f (&acc)[Tile<BM>
 // start the loads of slice it + NS into R, then the MFMAs of the slice's two
 // 16-deep k blocks, with the LDS reads of the second block issued ahead of
 // the MFMAs of the first.
-template <int BM, int AT, int BT, int NS>
+template <int BM, int AT, int BT, int NS, bool LOAD_ALWAYS>
 __device__ __forceinline__ void fast_slice(const GemmProb& P, __amdgpu_buffer_rsrc_t ra,
                                            __amdgpu_buffer_rsrc_t rb, int m0, int n0, int it, int n_it,
                                            FastRegs<BM, AT, BT>& R, float* as, float* bs,
@@ -822,7 +822,7 @@ __device__ __forceinline__ void fast_slice(const GemmProb& P, __amdgpu_buffer_rs
   const int li = lane & 15, lg = lane >> 4;
   fast_store<BM, AT, BT>(P, m0, P.K - it * BK, tid, R, as, bs);
   __syncthreads();
-  if (it + NS < n_it) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, (it + NS) * BK, tid, R);
+  if (LOAD_ALWAYS || it + NS < n_it) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, (it + NS) * BK, tid, R);
   // A wave whose rows all lie past M, or a 16-deep k block wholly past K
   // (zeros in both operands), has no MFMA work: skip it (wave-uniform).
   static_assert(BK == 32, "the k-block skip is written for two 16-deep blocks per slice");
@@ -840,7 +840,10 @@ __device__ __forceinline__ void fast_slice(const GemmProb& P, __amdgpu_buffer_rs
 
 // K loop: NS register sets hold the loads of the next NS slices; the loop is
 // unrolled by NS so each set (and each of the two LDS stages) has a fixed
-// role and the compiler can count outstanding loads exactly.
+// role.  Its steady state issues every prefetch without a branch, so the
+// compiler counts the outstanding loads exactly and a slice's stores wait
+// for that slice's loads only (with a branch around the prefetch, the stores
+// also waited for the loads of the slices after it).
 template <int BM, int AT, int BT>
 __device__ __forceinline__ void fast_mainloop(const GemmProb& P, int m0, int n0, float* As0,
                                               float* Bs0, v4f (&acc)[Tile<BM>::TI][2]) {
@@ -852,15 +855,27 @@ __device__ __forceinline__ void fast_mainloop(const GemmProb& P, int m0, int n0,
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(P.B, P.b_bytes);
   FastRegs<BM, AT, BT> R[NS];
   const int n_it = (P.K + BK - 1) / BK;
+  // the first NS slices' loads, all issued (past K they read zeros or
+  // data the K-tail selects drop), so that the steady-state loop below
+  // starts from the same outstanding loads on every path
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
-    if (s < n_it) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, s * BK, tid, R[s]);
-  for (int it = 0; it < n_it; it += NS) {
+  for (int s = 0; s < NS; ++s) fast_load<BM, AT, BT>(P, ra, rb, m0, n0, s * BK, tid, R[s]);
+  int it = 0;
+  // steady state: every slice's prefetch is needed, no branch on the loads,
+  // so each store waits for its own slice's loads and no later ones
+  for (; it + 2 * NS <= n_it; it += NS) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      fast_slice<BM, AT, BT, NS, true>(P, ra, rb, m0, n0, it + s, n_it, R[s], As0 + (s & 1) * T::A_FLOATS,
+                                       Bs0 + (s & 1) * T::B_FLOATS, acc);
+  }
+  // the last NS .. 2 NS - 1 slices
+  for (; it < n_it; it += NS) {
 #pragma unroll
     for (int s = 0; s < NS; ++s)
       if (it + s < n_it)
-        fast_slice<BM, AT, BT, NS>(P, ra, rb, m0, n0, it + s, n_it, R[s], As0 + (s & 1) * T::A_FLOATS,
-                                   Bs0 + (s & 1) * T::B_FLOATS, acc);
+        fast_slice<BM, AT, BT, NS, false>(P, ra, rb, m0, n0, it + s, n_it, R[s], As0 + (s & 1) * T::A_FLOATS,
+                                          Bs0 + (s & 1) * T::B_FLOATS, acc);
   }
 }
 
