@@ -1012,9 +1012,11 @@ __device__ __forceinline__ void wave_mainloop(const GemmProb& P, int m0, int n0,
   const int nkb = (P.K + 15) / 16;                          // k blocks of the problem
   const int mine = nkb > wave ? (nkb - wave + 3) / 4 : 0;   // blocks wave, wave + 4, ...
   WFrag<BM> F[PD];
+  // every prologue load issued (past the wave's blocks they read zeros or
+  // values no MFMA uses), so that the steady-state loop below starts from
+  // the same outstanding loads on every path
 #pragma unroll
-  for (int p = 0; p < PD; ++p)
-    if (p < mine) wave_load<BM, AT, BT>(P, ra, rb, m0, n0, 16 * (wave + 4 * p), li, lg, F[p]);
+  for (int p = 0; p < PD; ++p) wave_load<BM, AT, BT>(P, ra, rb, m0, n0, 16 * (wave + 4 * p), li, lg, F[p]);
   // steady state: every block full, every prefetch needed, no branches on
   // the loads, so the compiler can count outstanding loads exactly
   int q = 0;
