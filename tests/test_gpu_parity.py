@@ -102,9 +102,13 @@ def test_gemm_kernel_against_matmul():
     desc = torch.zeros(256, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream().cuda_stream
     # (37, 52, 600) and (200, 256, 784) reach the wave-split kernel (K >= 512) with
-    # ragged M, N and K tails; (37, 53, 19) is unaligned and takes the generic kernel
+    # ragged M, N and K tails; (37, 53, 19) is unaligned and takes the generic kernel.
+    # The depths give the register-staged kernel 1 to 32 slices of 32 (its K loop
+    # drains 1, 2 or 3 slices, with and without a steady-state pass before) and
+    # the wave-split kernel (variants 2, 6) waves with 0 to 16 k blocks of 16,
+    # a partial last block among them
     shapes = [(1, 1, 1), (64, 64, 16), (37, 53, 19), (129, 65, 33), (100, 256, 64), (200, 256, 784),
-              (257, 784, 100), (37, 52, 600), (100, 96, 200), (40, 8, 1000)]
+              (257, 784, 100), (37, 52, 600), (100, 96, 200), (40, 8, 1000), (44, 72, 96), (36, 132, 148)]
     for (M, N, K), tile_rows in [(s, tr) for s in shapes for tr in (32, 64)]:
         for a_trans in (0, 1):
             for b_trans in (0, 1):
