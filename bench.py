@@ -96,18 +96,24 @@ def gemm_flops_per_generation(wl):
 
 
 def gemm_source_digest():
-    """SHA-256 of the GEMM kernels' source: gemm.hip and the part of
+    """SHA-256 of the GEMM kernels' code: gemm.hip and the part of
     lipz_internal.h up to the declaration of launch_gemm_grouped (the device
     helpers and the GEMM's descriptor types; the rest of the header declares
-    other kernels)."""
+    other kernels), with comments and whitespace removed, so that a change
+    of wording alone keeps counters taken from the same code valid."""
     import hashlib
+    import re
     csrc = os.path.join(ROOT, "paper_1811_12843_amd", "csrc")
     with open(os.path.join(csrc, "gemm.hip"), "rb") as f:
         gemm = f.read()
     with open(os.path.join(csrc, "lipz_internal.h"), "rb") as f:
         head = f.read()
     cut = head.index(b";", head.index(b"hipError_t launch_gemm_grouped(")) + 1
-    return hashlib.sha256(gemm + head[:cut]).hexdigest()
+    code = gemm + b"\n" + head[:cut]
+    code = re.sub(rb"/\*.*?\*/", b" ", code, flags=re.S)   # block comments
+    code = re.sub(rb"//[^\n]*", b"", code)                  # line comments
+    code = re.sub(rb"\s+", b"", code)
+    return hashlib.sha256(code).hexdigest()
 
 
 def stored_gemm_traffic(workload):

@@ -3,8 +3,14 @@
 // phase of a generation: each cell's networks are small (M = 100..600 rows,
 // K = 64..784), so they are only worth a GPU when all of them run side by side.
 // Problems of one launch are described in device memory (GemmProb) and grouped
-// by shape (GemmGroups, kernel arguments); blockIdx is remapped so that the
-// tiles of one problem land on one XCD and share its L2.
+// by shape and depth (GemmGroups, passed as scalar kernel arguments that the
+// hardware preloads); blockIdx is remapped so that each group is split into
+// eight contiguous shares, one per XCD: the tiles of one problem share an L2
+// and the long tiles of a launch are spread over every XCD.
+//
+// Stores: a template parameter WT selects device-scope (write-through) buffer
+// stores for the epilogues' outputs, or write-back; the library picks one per
+// grid, by the size of its state.
 //
 // Tiling: a 256-thread workgroup (4 wave64) owns a BM x 64 output tile
 // (BM = 32 or 64).  Three kernels share the tile and the epilogue:
