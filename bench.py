@@ -252,6 +252,9 @@ def mfma_ceiling(torch, L, n=8192, reps=6):
 # uniformly, so the work per step does not depend on the dataset size).
 PER_CONFIG = {"mnist_mlp_3x3": 0, "mnist_mlp_4x4_mix": 0, "mnist_mlp_8x8": 0, "ring8_mlp_2x2": 0,
               "celeba_dcgan_4x4": 512}
+# workloads whose asynchronous row-band schedule (same results bit for bit)
+# is also timed in the per-workload block, with its band count
+PER_CONFIG_BANDS = {"mnist_mlp_8x8": 4}
 _DATA = {}
 
 
@@ -453,6 +456,14 @@ def main():
                 "kernel": q["roofline"]["kernel"], "kernel_tflops": q["roofline"]["achieved"],
                 "kernel_frac": q["roofline"]["frac"], "config": q["config"]}
             del q
+            if name in PER_CONFIG_BANDS:
+                # the generation rate only: with the bands' launches overlapping on
+                # several streams, per-launch kernel times do not add up to a rate
+                qb = run_workload(L, torch, name, 1, 1, 1, PER_CONFIG[name], PER_CONFIG_BANDS[name])
+                out["per_config"][name]["row_bands"] = {
+                    "bands": PER_CONFIG_BANDS[name], "generations_per_s": 1e3 / qb["ms_per_gen"],
+                    "ms_per_gen": qb["ms_per_gen"], "mfma_frac": qb["mfma_frac"]}
+                del qb
     if not args.no_ceiling:
         ceil = mfma_ceiling(torch, L)
         ceil["gen_frac_of_vendor"] = f_gen / (ms_per_gen * 1e-3) / (ceil["vendor_tflops"] * 1e12)
